@@ -1,0 +1,54 @@
+"""MoE layer output with SwiGLU experts (oracle side), in float64.
+
+Section 2.1: y = sum_i g_i(x) E_i(x) over the routed experts (the shared-expert
+term is not part of this layer).  Each expert is a SwiGLU FFN in nn.Linear
+[out, in] layout:  E(x) = W2 (silu(W1 x) * (W3 x)),  silu(z) = z / (1 + e^-z),
+W1, W3 in R^{f x d}, W2 in R^{d x f}.  Inputs are bf16 bit patterns (exact in
+float64); nothing is rounded until the caller compares.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def bf16_to_f64(bits) -> np.ndarray:
+    b = np.asarray(bits, dtype=np.uint16)
+    return (b.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def silu(z):
+    return z / (1.0 + np.exp(-z))
+
+
+def expert_ffn(x, w1_bits, w3_bits, w2_bits) -> np.ndarray:
+    """SwiGLU expert applied to the rows of x (float64 [t,d]) -> float64 [t,d]."""
+    W1 = bf16_to_f64(w1_bits)
+    W3 = bf16_to_f64(w3_bits)
+    W2 = bf16_to_f64(w2_bits)
+    a = x @ W1.T
+    b = x @ W3.T
+    return (silu(a) * b) @ W2.T
+
+
+def moe_forward(x_bits, ids, w, expert, rows=None) -> np.ndarray:
+    """y[i] = sum_r w[i,r] * E_{ids[i,r]}(x_i) for the tokens in ``rows`` (default: all).
+
+    ``expert(e)`` returns the bf16 bit arrays (w1 [f,d], w3 [f,d], w2 [d,f]) of expert e.
+    Returns float64 [len(rows), d].
+    """
+    X = bf16_to_f64(x_bits)
+    ids = np.asarray(ids)
+    w = np.asarray(w, dtype=np.float64)
+    rows = list(range(X.shape[0])) if rows is None else [int(i) for i in rows]
+    y = np.zeros((len(rows), X.shape[1]), dtype=np.float64)
+    by_expert: dict[int, list[tuple[int, int]]] = {}
+    for p, i in enumerate(rows):
+        for r in range(ids.shape[1]):
+            by_expert.setdefault(int(ids[i, r]), []).append((p, r))
+    for e in sorted(by_expert):
+        pairs = by_expert[e]
+        w1, w3, w2 = expert(e)
+        out = expert_ffn(X[[rows[p] for p, _ in pairs]], w1, w3, w2)
+        for q, (p, r) in enumerate(pairs):
+            y[p] += w[rows[p], r] * out[q]
+    return y

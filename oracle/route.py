@@ -1,0 +1,274 @@
+"""Expert selection and routing (oracle side).
+
+Follows, step by step:
+* Section 2.2 -- top-k gating: the k largest logits of a token, gates given by a
+  softmax renormalised over those k;
+* Section 3.2, Eq. (2) -- per-layer proxy: the score of expert j is the sum over
+  the batch of its gates, s_j = sum_i g_ij;
+* Section 3.4, Algorithm 1 -- greedy selection, here with the fixed budget the
+  paper says it uses in practice instead of the threshold;
+* Section 3.4, Algorithm 2 -- warm-up S_0 (top-k0 of every token), greedy
+  selection, refinement (each token routed to its top-k inside the set);
+* Section 4.1, Eqs. (3)-(4), Algorithms 3 and 4 -- per-request warm-up plus the
+  m_r best experts of each request by its own score, union over requests, then
+  the batch-level greedy and the same refinement.
+
+Readings of what the paper leaves open (each one is listed with its reason in
+the design notes of the repository):
+* gates for the scores are the top-k-sparse renormalised gates of Section 2.2
+  ("topk" mode, default); "dense" mode uses the softmax over all N experts;
+* refinement ranks a token's experts by its logits (monotone in the softmax);
+* ranking key everywhere is (value descending, expert index ascending); logits
+  are canonicalised with h + 0.0 so that -0.0 and +0.0 compare equal;
+* budget "total": |S| <= M (requires M >= k); budget "extra": M experts are
+  added beyond the warm-up set (beyond the union of the per-request sets in the
+  hierarchical case), which is how the paper's tables use m_l;
+* candidates: in "topk" mode only experts some token (some token of the
+  request, for per-request picks) has in its top-k; in "dense" mode all experts
+  (none when the batch is empty);
+* the effective set size is clamped up to k so that every token keeps exactly k
+  experts; if the starting set is larger than a total budget it is cut by
+  priority (warm-up first, then per-request picks), score descending, index
+  ascending;
+* batch scores are always the sum over all tokens in ascending token order, so
+  the hierarchical scores of Eq. (4) equal the flat ones bit for bit.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+from .numerics import F32, seq_sum, softmax_dense, softmax_ranked
+
+TOTAL = "total"
+EXTRA = "extra"
+TOPK = "topk"
+DENSE = "dense"
+
+
+@dataclass
+class Routing:
+    sel_mask: np.ndarray          # uint8 [N], 1 = expert in S
+    ids: np.ndarray               # int32 [T,k], rank order
+    w: np.ndarray                 # fp32 [T,k]
+    scores: np.ndarray            # fp32 [N], batch scores s_j
+    vanilla_ids: np.ndarray       # int32 [T,k], plain top-k
+    vanilla_gates: np.ndarray     # fp32 [T,k]
+    n_vanilla_union: int
+    n_warmup: int
+    budget_eff: int
+    extra: dict = field(default_factory=dict)
+
+    @property
+    def sel_list(self) -> list[int]:
+        return [int(j) for j in np.flatnonzero(self.sel_mask)]
+
+    @property
+    def n_selected(self) -> int:
+        return int(self.sel_mask.sum())
+
+    @property
+    def n_active(self) -> int:
+        return len(set(int(e) for e in self.ids.reshape(-1)))
+
+
+# ----------------------------------------------------------------------------- ranking
+
+def canonical(h) -> np.ndarray:
+    """fp32 logits with -0.0 mapped to +0.0; rejects NaN and infinities."""
+    h = np.asarray(h, dtype=F32)
+    if not np.all(np.isfinite(h)):
+        raise ValueError("logits must be finite")
+    return (h + F32(0.0)).astype(F32)
+
+
+def ranked(h_row, allowed=None) -> list[int]:
+    """Experts in rank order (logit descending, index ascending), optionally restricted."""
+    js = range(len(h_row)) if allowed is None else allowed
+    return sorted((int(j) for j in js), key=lambda j: (-float(h_row[j]), j))
+
+
+# ----------------------------------------------------------------------------- gates and scores
+
+def vanilla_gating(h, k: int):
+    """Section 2.2: per token the top-k experts (rank order) and their renormalised gates."""
+    T = h.shape[0]
+    ids = np.zeros((T, k), dtype=np.int32)
+    gates = np.zeros((T, k), dtype=F32)
+    for i in range(T):
+        top = ranked(h[i])[:k]
+        ids[i] = top
+        gates[i] = softmax_ranked(h[i, top])
+    return ids, gates
+
+
+def gate_matrix(h, ids, gates, score_mode: str) -> np.ndarray:
+    """G[T,N] fp32: the gates g_ij that enter the scores (zeros outside the top-k in topk mode)."""
+    T, N = h.shape
+    G = np.zeros((T, N), dtype=F32)
+    for i in range(T):
+        if score_mode == TOPK:
+            G[i, ids[i]] = gates[i]
+        elif score_mode == DENSE:
+            G[i] = softmax_dense(h[i])
+        else:
+            raise ValueError(score_mode)
+    return G
+
+
+def scores_over(G, tokens) -> np.ndarray:
+    """s_j = sum over the given tokens of g_ij, added one token at a time in the given order."""
+    s = np.zeros(G.shape[1], dtype=F32)
+    for i in tokens:
+        s = (s + G[i]).astype(F32)
+    return s
+
+
+# ----------------------------------------------------------------------------- greedy
+
+def greedy_select(scores, start, budget: int, candidates, priority=None) -> set[int]:
+    """Algorithm 1 with a fixed budget: grow ``start`` by the best remaining candidate.
+
+    If ``start`` already holds more than ``budget`` experts it is cut to the first
+    ``budget`` under (priority ascending, score descending, index ascending).
+    """
+    start = set(int(j) for j in start)
+    if len(start) > budget:
+        pri = priority or {}
+        keep = sorted(start, key=lambda j: (pri.get(j, 0), -float(scores[j]), j))[:budget]
+        return set(keep)
+    S = set(start)
+    while len(S) < budget:
+        rest = [int(e) for e in candidates if int(e) not in S]
+        if not rest:
+            break
+        e_star = max(rest, key=lambda e: (float(scores[e]), -e))   # argmax, lowest index on ties
+        S.add(e_star)
+    return S
+
+
+def _effective_budget(base: int, n_cand: int, k: int) -> int:
+    return max(min(base, n_cand), min(k, n_cand))
+
+
+def _check(h, k, k0, M, budget_mode, score_mode):
+    T, N = h.shape
+    if not 1 <= k <= N:
+        raise ValueError("need 1 <= k <= N")
+    if not 0 <= k0 <= k:
+        raise ValueError("need 0 <= k0 <= k")
+    if M < 0:
+        raise ValueError("need M >= 0")
+    if budget_mode == TOTAL and M < k:
+        raise ValueError("a total budget must be >= k")
+    if budget_mode not in (TOTAL, EXTRA) or score_mode not in (TOPK, DENSE):
+        raise ValueError("unknown mode")
+
+
+# ----------------------------------------------------------------------------- refinement
+
+def refine(h, S, k: int):
+    """Route every token to its top-k experts inside S, gates renormalised over those k."""
+    T = h.shape[0]
+    allowed = sorted(S)
+    ids = np.zeros((T, k), dtype=np.int32)
+    w = np.zeros((T, k), dtype=F32)
+    for i in range(T):
+        top = ranked(h[i], allowed)[:k]
+        ids[i] = top
+        w[i] = softmax_ranked(h[i, top])
+    return ids, w
+
+
+# ----------------------------------------------------------------------------- Algorithm 2
+
+def route(h, k: int, k0: int, M: int, budget_mode: str = TOTAL,
+          score_mode: str = TOPK) -> Routing:
+    """Batch-aware expert selection for one layer (Algorithm 2)."""
+    h = canonical(h)
+    _check(h, k, k0, M, budget_mode, score_mode)
+    T, N = h.shape
+    vids, vg = vanilla_gating(h, k)
+    G = gate_matrix(h, vids, vg, score_mode)
+    s = scores_over(G, range(T))
+
+    union = set(int(e) for e in vids.reshape(-1))
+    S0 = set(int(e) for e in vids[:, :k0].reshape(-1))            # warm-up
+    if T == 0:
+        cand = set()
+    else:
+        cand = union if score_mode == TOPK else set(range(N))
+    base = M if budget_mode == TOTAL else len(S0) + M
+    m_eff = _effective_budget(base, len(cand), k)
+
+    S = greedy_select(s, S0, m_eff, sorted(cand))
+    ids, w = refine(h, S, k)
+    mask = np.zeros(N, dtype=np.uint8)
+    mask[sorted(S)] = 1
+    return Routing(mask, ids, w, s, vids, vg, len(union), len(S0), m_eff)
+
+
+# ----------------------------------------------------------------------------- Algorithms 3 + 4
+
+def check_offsets(offsets, T: int) -> list[int]:
+    o = [int(v) for v in offsets]
+    if len(o) < 1 or o[0] != 0 or o[-1] != T or any(b <= a for a, b in zip(o, o[1:])):
+        raise ValueError("request offsets must satisfy 0 = o_0 < o_1 < ... < o_R = T")
+    return o
+
+
+def per_request_select(h, G, vids, tokens, k0: int, m_r: int, score_mode: str):
+    """Algorithm 3 for one request: (S_0(r), added experts) with the request's own scores."""
+    N = h.shape[1]
+    S0_r = set(int(e) for i in tokens for e in vids[i, :k0])
+    s_r = scores_over(G, tokens)
+    if score_mode == TOPK:
+        pool = set(int(e) for i in tokens for e in vids[i])
+    else:
+        pool = set(range(N))
+    rest = sorted(pool - S0_r, key=lambda j: (-float(s_r[j]), j))
+    return S0_r, set(rest[:m_r])
+
+
+def select_hier(h, offsets, k: int, k0: int, m_r: int, M: int,
+                budget_mode: str = TOTAL, score_mode: str = TOPK) -> Routing:
+    """Speculative-decoding-aware selection (Algorithm 4 calling Algorithm 3 per request)."""
+    h = canonical(h)
+    _check(h, k, k0, M, budget_mode, score_mode)
+    if m_r < 0:
+        raise ValueError("need m_r >= 0")
+    T, N = h.shape
+    o = check_offsets(offsets, T)
+    vids, vg = vanilla_gating(h, k)
+    G = gate_matrix(h, vids, vg, score_mode)
+    s = scores_over(G, range(T))                                   # Eq. (4) == flat score
+
+    S0 = set()
+    added = set()
+    for r in range(len(o) - 1):
+        S0_r, add_r = per_request_select(h, G, vids, range(o[r], o[r + 1]), k0, m_r, score_mode)
+        S0 |= S0_r
+        added |= add_r
+    S_batch = S0 | added                                           # union of the S_r
+    union = set(int(e) for e in vids.reshape(-1))
+    if T == 0:
+        cand = set()
+    else:
+        cand = union if score_mode == TOPK else set(range(N))
+    base = M if budget_mode == TOTAL else len(S_batch) + M
+    m_eff = _effective_budget(base, len(cand), k)
+
+    priority = {j: (0 if j in S0 else 1) for j in S_batch}
+    S = greedy_select(s, S_batch, m_eff, sorted(cand), priority)
+    ids, w = refine(h, S, k)
+    mask = np.zeros(N, dtype=np.uint8)
+    mask[sorted(S)] = 1
+    return Routing(mask, ids, w, s, vids, vg, len(union), len(S0), m_eff,
+                   extra=dict(per_request_union=len(S_batch), tier1=len(added - S0)))
+
+
+def vanilla(h, k: int) -> Routing:
+    """Plain top-k routing expressed as Algorithm 2 with every candidate kept."""
+    N = np.asarray(h).shape[1]
+    return route(h, k, 0, N, EXTRA, TOPK)

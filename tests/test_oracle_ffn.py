@@ -1,0 +1,87 @@
+"""Pins of the oracle's MoE layer output (Section 2.1, SwiGLU experts)."""
+import math
+
+import numpy as np
+import torch
+
+import workloads as W
+from oracle import ffn as O
+from oracle import route as R
+
+
+def f32_to_bf16_bits(a):
+    """Exact bf16 patterns of values that are already bf16-representable."""
+    b = np.asarray(a, np.float32).view(np.uint32)
+    assert np.all((b & 0xFFFF) == 0)
+    return (b >> 16).astype(np.uint16)
+
+
+def test_bf16_to_f64_exact():
+    vals = np.array([0.0, -0.0, 1.0, -2.5, 0.0078125, 3.0e38, -1.1754944e-38], np.float32)
+    t = torch.tensor(vals).to(torch.bfloat16)
+    bits = t.view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(O.bf16_to_f64(bits), t.to(torch.float64).numpy())
+
+
+def test_silu():
+    assert O.silu(0.0) == 0.0
+    assert abs(O.silu(30.0) - 30.0) < 1e-10
+    assert abs(O.silu(-30.0)) < 1e-10
+    assert abs(O.silu(1.0) - 1.0 / (1.0 + math.exp(-1.0))) < 1e-15
+
+
+def _perm_expert(rng, d, f):
+    """W1/W3 rows pick one input component, W2 rows pick one hidden component."""
+    p1, p3 = rng.integers(0, d, f), rng.integers(0, d, f)
+    s2 = rng.integers(0, f, d)
+    a = rng.choice([0.5, 1.0, -2.0, 0.25], f)
+    b = rng.choice([1.0, -0.5, 2.0], f)
+    c = rng.choice([1.0, -1.0, 0.75], d)
+    W1 = np.zeros((f, d), np.float32)
+    W3 = np.zeros((f, d), np.float32)
+    W2 = np.zeros((d, f), np.float32)
+    W1[np.arange(f), p1] = a
+    W3[np.arange(f), p3] = b
+    W2[np.arange(d), s2] = c
+    closed = lambda x: c * (lambda z: z / (1 + np.exp(-z)))(a[s2] * x[p1[s2]]) * (b[s2] * x[p3[s2]])
+    return (f32_to_bf16_bits(W1), f32_to_bf16_bits(W3), f32_to_bf16_bits(W2)), closed
+
+
+def test_closed_form_permutation_experts():
+    """E(x)_n = c_n silu(a_s x_p1(s)) b_s x_p3(s), s = s2(n): catches a transposed operand."""
+    rng = np.random.default_rng(0)
+    d, f, N, T, k = 12, 20, 5, 6, 2
+    experts, closed = zip(*[_perm_expert(rng, d, f) for _ in range(N)])
+    x = rng.choice([0.5, -1.0, 1.5, 2.0, -0.25], (T, d)).astype(np.float32)
+    xb = f32_to_bf16_bits(x)
+    ids = np.array([rng.choice(N, k, replace=False) for _ in range(T)], np.int32)
+    w = rng.random((T, k)).astype(np.float32)
+    y = O.moe_forward(xb, ids, w, lambda e: experts[e])
+    for i in range(T):
+        ref = sum(float(w[i, r]) * closed[ids[i, r]](x[i].astype(np.float64)) for r in range(k))
+        assert np.allclose(y[i], ref, rtol=1e-13, atol=1e-13)
+
+
+def test_dense_gate_formulation_on_tiny_workload():
+    """y = sum over ALL experts of G[:, e] * E_e(X) with a dense gate matrix (zeros elsewhere)."""
+    c = W.CONFIGS["tiny"]
+    h, _ = W.make_logits(c, 0)
+    r = R.route(h, c["k"], 1, c["M"])
+    x = W.bf16_bits(W.activations(c["T"], c["d"], 0))
+    ws = [tuple(W.bf16_bits(W.expert_matrix(e, m, c["d"], c["f"], 0)) for m in ("w1", "w3", "w2"))
+          for e in range(c["N"])]
+    y = O.moe_forward(x, r.ids, r.w, lambda e: ws[e])
+    G = np.zeros((c["T"], c["N"]))
+    for i in range(c["T"]):
+        G[i, r.ids[i]] = r.w[i]
+    X = O.bf16_to_f64(x)
+    dense = np.zeros_like(y)
+    for e in range(c["N"]):
+        W1, W3, W2 = (O.bf16_to_f64(m) for m in ws[e])
+        a = np.einsum("fd,td->tf", W1, X)
+        b = np.einsum("fd,td->tf", W3, X)
+        dense += G[:, e:e + 1] * np.einsum("df,tf->td", W2, a / (1 + np.exp(-a)) * b)
+    assert np.allclose(y, dense, rtol=1e-12, atol=1e-14)
+    # a subset of rows gives the same rows
+    sub = O.moe_forward(x, r.ids, r.w, lambda e: ws[e], rows=[5, 1])
+    assert np.allclose(sub, y[[5, 1]], rtol=1e-12, atol=1e-15)
