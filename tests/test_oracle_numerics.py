@@ -89,6 +89,21 @@ def test_softmax_ranked_single_and_ties():
     assert g[0] == F32(1.0) and g[1] == F32(0.0)
 
 
+def test_softmax_sums_in_the_stated_order():
+    """Convention pin: the denominator is summed in rank order (ranked) / index order (dense).
+
+    With e_0 = 1 and two terms e in (2^-25, 2^-24): left to right 1 + e rounds back to 1
+    twice, so Z = 1 and g_0 = 1 exactly; summing the small terms first gives Z = 1 + 2^-23.
+    """
+    x = F32(-16.64)
+    e = float(exp_ref(x))
+    assert 2.0 ** -25 < e < 2.0 ** -24
+    g = softmax_ranked([F32(0.0), x, x])
+    assert g[0] == F32(1.0)
+    gd = softmax_dense([x, x, F32(0.0)])          # index order: small terms first
+    assert gd[2] == F32(1.0) / F32(1.0 + 2.0 ** -23) and gd[2] < F32(1.0)
+
+
 def test_softmax_dense_matches_float64():
     rng = np.random.default_rng(7)
     for N in (8, 16, 128, 256):
