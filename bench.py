@@ -1,0 +1,233 @@
+#!/usr/bin/env python3
+"""Benchmark of the XShare MoE layer on one MI355X.
+
+One step = the whole layer for one decode batch: router scoring, batch selection,
+refinement, permutation, the SwiGLU expert GEMMs of the selected experts and the combine
+(one call of xshare_moe_forward).  Workload: DeepSeek-R1-shaped routed-expert layer,
+N=256 experts, k=8, d_model=7168, d_ffn=2048, T=32 tokens, total budget M=48, warm-up
+k0=1; logits from 8 domain centroids (seeded), x ~ N(0,1), weights ~ N(0,0.02), bf16.
+All inputs are resident in HBM before timing; steps rotate over several batches so each
+step selects its own experts.  Prints one JSON line.
+
+    python bench.py [--gpus 1] [--steps 50] [--warmup 5]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "MoE-layer µs/batch + HBM GB/s (N=256,k=8,B=32); experts activated/batch"
+HBM_PEAK_GBS = 8000.0
+PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "gate_up_ds_t32_m48_counters.json")
+FFN_SOURCE = os.path.join(ROOT, "paper_2602_07265_amd", "csrc", "ffn.hip")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--batches", type=int, default=8, help="distinct seeded batches rotated over")
+    ap.add_argument("--budget", type=int, default=48)
+    ap.add_argument("--tokens", type=int, default=32)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-vanilla", action="store_true")
+    return ap.parse_args()
+
+
+def gate_up_bytes(n_active, T, k, d, f):
+    """Algorithmic HBM bytes of one gate/up launch: W1, W3 of every active expert, x, H."""
+    return n_active * 2 * f * d * 2 + T * d * 2 + T * k * f * 2
+
+
+def layer_bytes(n_active, T, N, d, f):
+    """Algorithmic HBM bytes of one layer call: active experts' weights, x, logits, y."""
+    return n_active * 3 * f * d * 2 + T * d * 2 + T * N * 4 + T * d * 2
+
+
+def counters_traffic(n_launch_bytes):
+    """HBM bytes per gate/up launch from committed rocprofv3 counters, if still current."""
+    try:
+        prof = json.load(open(PROFILE_COUNTERS))
+    except (OSError, ValueError):
+        return None
+    src = hashlib.sha256(open(FFN_SOURCE, "rb").read()).hexdigest()
+    if prof.get("ffn_source_sha256") != src:
+        return None
+    return prof.get("traffic_bytes_per_launch")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (single-GPU XShare layer); got --gpus {args.gpus}",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import workloads as W
+    from paper_2602_07265_amd import xshare as X
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    X.lib()
+    dev = "cuda:0"
+    cfg = dict(W.CONFIGS["ds_t32"])
+    T, N, k, d, f = args.tokens, cfg["N"], cfg["k"], cfg["d"], cfg["f"]
+    M, k0 = args.budget, cfg["k0"]
+    nb = args.batches
+
+    print(f"[bench] generating DS-R1 layer weights ({N * 3 * d * f * 2 / 1e9:.1f} GB)", file=sys.stderr,
+          flush=True)
+    w1, w3, w2 = W.expert_weights(N, d, f, 0, dev)
+    logits = [torch.from_numpy(W.logits_domains(T, N, cfg["Q"], s)).to(dev) for s in range(nb)]
+    xs = [W.activations(T, d, s, dev) for s in range(nb)]
+    p = X.params(N, k, k0, M, "total")
+    pv = X.params(N, k, 0, N, "extra")          # vanilla top-k: S = U on the same kernels
+    ws = torch.empty(X.moe_workspace_bytes(T, d, f, p), dtype=torch.uint8, device=dev)
+    y = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+
+    # per-batch routing statistics (deterministic per batch)
+    stats = []
+    for b in range(nb):
+        r = X.moe_forward(xs[b], logits[b], w1, w3, w2, k, k0, M, "total", y=y, workspace=ws)
+        rv = X.moe_forward(xs[b], logits[b], w1, w3, w2, k, 0, N, "extra", y=y, workspace=ws)
+        stats.append((X.stats_dict(r["stats"]), X.stats_dict(rv["stats"])))
+    act = [s[0]["n_active"] for s in stats]
+    act_v = [s[1]["n_active"] for s in stats]
+
+    stream = torch.cuda.current_stream()
+    nev = X.N_STAGE_EVENTS
+
+    def run(steps, mode, timed):
+        evs = [[X.HipEvent() for _ in range(nev)] for _ in range(steps)] if timed else None
+        for s in range(steps):
+            b = s % nb
+            if mode == "xshare":
+                X.moe_forward(xs[b], logits[b], w1, w3, w2, k, k0, M, "total", y=y, workspace=ws,
+                              routing_out=False, stage_events=evs[s] if timed else None)
+            else:
+                X.moe_forward(xs[b], logits[b], w1, w3, w2, k, 0, N, "extra", y=y, workspace=ws,
+                              routing_out=False, stage_events=evs[s] if timed else None)
+        return evs
+
+    print(f"[bench] warmup {args.warmup} + {args.steps} timed steps", file=sys.stderr, flush=True)
+    run(args.warmup, "xshare", False)
+    torch.cuda.synchronize()
+    t0, t1 = X.HipEvent(), X.HipEvent()
+    wall0 = time.perf_counter()
+    t0.record(stream)
+    evs = run(args.steps, "xshare", True)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = t0.elapsed_ms(t1)
+    ms_step = total_ms / args.steps
+    stage_ms = {name: float(np.mean([e[i].elapsed_ms(e[i + 1]) for e in evs]))
+                for i, name in enumerate(X.STAGES)}
+    gu_ms = np.array([e[1].elapsed_ms(e[2]) for e in evs])
+    gu_bytes = np.array([gate_up_bytes(act[s % nb], T, k, d, f) for s in range(args.steps)])
+    lay_bytes = np.array([layer_bytes(act[s % nb], T, N, d, f) for s in range(args.steps)])
+
+    vanilla = None
+    if not args.no_vanilla:
+        run(args.warmup, "vanilla", False)
+        torch.cuda.synchronize()
+        v0, v1 = X.HipEvent(), X.HipEvent()
+        v0.record(stream)
+        run(args.steps, "vanilla", False)
+        v1.record(stream)
+        torch.cuda.synchronize()
+        vanilla = v0.elapsed_ms(v1) / args.steps
+
+    gbs = float(lay_bytes.mean()) / (ms_step * 1e-3) / 1e9
+    gu_achieved = float(gu_bytes.mean()) / (float(gu_ms.mean()) * 1e-3) / 1e9
+    traffic = counters_traffic(float(gu_bytes.mean()))
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(W, xs[0], logits[0], w1, w3, w2, T, N, k, k0, M, d, f)
+
+    out = {
+        "metric": METRIC,
+        "value": round(gbs, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"deepseek_r1_routed_moe_T{T}_N{N}_k{k}_d{d}_f{f}_M{M}_k0{k0}",
+                   "tokens": T, "n_experts": N, "top_k": k, "d_model": d, "d_ffn": f,
+                   "budget": M, "budget_mode": "total", "warmup_k0": k0,
+                   "logits": "8 domain centroids N(0,1.5) + N(0,0.5)", "batches_rotated": nb},
+        "us_per_batch": round(ms_step * 1e3, 2),
+        "tokens_per_s": round(T / (ms_step * 1e-3), 1),
+        "experts_activated": round(float(np.mean(act)), 2),
+        "experts_vanilla": round(float(np.mean(act_v)), 2),
+        "vanilla_us_per_batch": None if vanilla is None else round(vanilla * 1e3, 2),
+        "speedup_vs_vanilla": None if vanilla is None else round(vanilla / ms_step, 3),
+        "layer_frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+        "stages_us": {kk: round(v * 1e3, 2) for kk, v in stage_ms.items()},
+        "roofline": {"kernel": "gate_up_kernel", "bound": "hbm", "achieved": round(gu_achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gu_achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic, "algorithmic_bytes": round(float(gu_bytes.mean())),
+                     "avg_launch_us": round(float(gu_ms.mean()) * 1e3, 2)},
+        "cpu_baseline": cpu,
+        "wall_s_timed": round(wall, 3),
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(W, x, logits, w1, w3, w2, T, N, k, k0, M, d, f):
+    """The oracle on the host cores: routing of the whole batch plus the float64 FFN of the
+    experts used by the first token, scaled to the batch's active experts."""
+    import numpy as np
+
+    from oracle import ffn as OF
+    from oracle import route as OR
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    h = logits.cpu().numpy()
+    xb = W.bf16_bits(x)
+    print("[bench] cpu baseline: oracle route + FFN sample", file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    r = OR.route(h, k, k0, M)
+    t_route = time.perf_counter() - t0
+    rows = [0]
+    used = sorted(set(int(e) for e in r.ids[rows].reshape(-1)))
+    cache = {e: tuple(W.bf16_bits(m[e]) for m in (w1, w3, w2)) for e in used}
+    t0 = time.perf_counter()
+    OF.moe_forward(xb, r.ids, r.w, lambda e: cache[e], rows)
+    t_ffn = time.perf_counter() - t0
+    n_active = r.n_active
+    t_batch = t_route + t_ffn * n_active / len(used)
+    bytes_batch = layer_bytes(n_active, T, N, d, f)
+    return {"value": round(bytes_batch / t_batch / 1e9, 3), "unit": "GB/s",
+            "us_per_batch": round(t_batch * 1e6, 1), "cores": int(cores), "kind": "oracle",
+            "sample": f"oracle routing of the full batch ({t_route:.2f} s) + float64 SwiGLU of "
+                      f"token 0's {len(used)} experts ({t_ffn:.2f} s), scaled to the batch's "
+                      f"{n_active} active experts"}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,179 @@
+/*
+ * xshare.h -- C ABI of the XShare batch-level MoE layer for AMD Instinct MI355X (gfx950).
+ *
+ * XShare (arXiv 2602.07265) picks ONE shared expert set S for a whole decode batch by
+ * maximising the total gating score of the selected experts under a budget (Section 3.2,
+ * Eq. (2); greedy is optimal by Proposition 3.1 / Corollary 3.2), then routes every token to
+ * its top-k experts inside S (Algorithm 2), so that only the weights of experts in S are
+ * read.  For speculative-decoding batches the set is built per request first and then
+ * completed at batch level (Section 4.1, Algorithms 3 and 4).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - All array arguments are DEVICE pointers owned by the caller; the parameter structs are
+ *   HOST pointers read during the call only.  The library never allocates, frees or keeps a
+ *   pointer after returning; scratch memory comes from the caller's workspace `ws`
+ *   (size from the matching *_workspace_bytes function, 256-byte aligned).
+ * - Calls are asynchronous and stream-ordered on `stream` (a hipStream_t; NULL = the
+ *   default stream).  Outputs are valid once the stream has reached the end of the call.
+ *   Nothing is copied back to the host and the stream is never synchronised.
+ * - Host-checkable errors are returned before anything is enqueued: XSHARE_EINVAL for an
+ *   invalid argument, XSHARE_EUNSUPPORTED for a valid size outside the kernels' limits,
+ *   XSHARE_EWORKSPACE when ws_bytes is too small.  XSHARE_EHIP reports a failed launch.
+ * - Logits must be finite; NaN or infinity is not detected on the device and gives
+ *   unspecified (but memory-safe) results.
+ * - Selection is deterministic and bit-identical to the fp32 recipe documented below:
+ *   logits are canonicalised with h + 0.0 (so -0.0 == +0.0); every ranking uses the key
+ *   (value descending, expert index ascending); gates are the softmax over a token's k
+ *   chosen logits (Section 2.2) computed as e_r = exp(h_r - h_0) with a fixed fp32
+ *   exponential (Cody-Waite reduction by ln 2, degree-7 Taylor polynomial, no fused
+ *   multiply-add, 0 below -80), Z summed left to right in rank order, g_r = e_r / Z
+ *   correctly rounded; batch scores s_j = sum_i g_ij are summed in ascending token order.
+ *
+ * Limits: 1 <= N <= 1024, 1 <= k <= min(N, 32), 0 <= T <= 4096, T*k <= 8192;
+ * d and f multiples of 32 (xshare_moe_forward).
+ */
+#ifndef XSHARE_H
+#define XSHARE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  XSHARE_OK = 0,
+  XSHARE_EINVAL = 1,        /* invalid argument: range, null pointer, alignment, offsets   */
+  XSHARE_EUNSUPPORTED = 2,  /* valid, but outside the limits listed above                  */
+  XSHARE_EWORKSPACE = 3,    /* ws is NULL or ws_bytes < the required workspace size         */
+  XSHARE_EHIP = 4           /* a HIP launch failed (hipGetLastError after enqueue)          */
+} xshare_status;
+
+/* How `budget` is read (the paper uses both readings of m_l).                             */
+enum {
+  XSHARE_BUDGET_TOTAL = 0,  /* |S| <= budget; requires budget >= k                          */
+  XSHARE_BUDGET_EXTRA = 1   /* budget experts are added beyond the warm-up set (flat) or     *
+                             * beyond the union of the per-request sets (hierarchical), as   *
+                             * in the paper's (m_l, k0) settings of Section 6                */
+};
+
+/* Which gates g_ij enter the scores s_j = sum_i g_ij (Eq. (2)).                            */
+enum {
+  XSHARE_SCORE_TOPK = 0,    /* top-k-sparse renormalised gates of Section 2.2 (default);    *
+                             * candidates are the experts some token has in its top-k        */
+  XSHARE_SCORE_DENSE = 1    /* softmax over all N experts (max-shifted, summed in index     *
+                             * order); every expert is a candidate                           */
+};
+
+typedef struct {
+  int32_t n_experts;          /* N: routed experts of the layer                             */
+  int32_t top_k;              /* k: experts per token (Section 2.2)                         */
+  int32_t warmup_k0;          /* k0: top-k0 of every token always enters S (0 <= k0 <= k)   */
+  int32_t budget;             /* M: see XSHARE_BUDGET_*                                    */
+  int32_t budget_mode;        /* XSHARE_BUDGET_TOTAL or XSHARE_BUDGET_EXTRA                 */
+  int32_t score_mode;         /* XSHARE_SCORE_TOPK or XSHARE_SCORE_DENSE                    */
+  int32_t per_request_budget; /* m_r (Algorithm 3); read by the hierarchical calls only     */
+} xshare_route_params;
+
+/* Per-call statistics, written to DEVICE memory by the kernels.                          */
+typedef struct {
+  int32_t n_selected;       /* |S|                                                        */
+  int32_t n_active;         /* experts with at least one routed token (weights streamed)   */
+  int32_t n_vanilla_union;  /* |U|, U = union of every token's plain top-k (Section 3.1)    */
+  int32_t n_warmup;         /* |S_0|, S_0 = union of every token's top-k0                   */
+  int32_t n_start;          /* size of the set the batch greedy starts from: |S_0| (flat),  *
+                             * |union_r S_r| (hierarchical)                                 */
+  int32_t budget_eff;       /* effective set size the greedy fills to (clamped to [k, |C|]) */
+  int32_t reserved[2];
+} xshare_stats;
+
+/* Workspace for xshare_route / xshare_select_hier with T tokens (bytes, 256-aligned).    */
+size_t xshare_route_workspace_bytes(int32_t T, const xshare_route_params* params);
+
+/* Workspace for xshare_moe_forward (includes the routing workspace).                     */
+size_t xshare_moe_workspace_bytes(int32_t T, int32_t d, int32_t f,
+                                  const xshare_route_params* params);
+
+/*
+ * xshare_route -- batch-aware expert selection for one layer (Algorithm 2, Section 3.4).
+ *
+ *   logits    [T, N] fp32 row-major: router logits h = W_g x of the batch (Section 2.2).
+ *   T         number of tokens in the batch (0 allowed: S is empty).
+ *   sel_mask  out [N] uint8: 1 if expert j is in S, else 0.
+ *   topk_ids  out [T, k] int32: token i's top-k experts inside S, rank order (refinement).
+ *   topk_w    out [T, k] fp32: their gates, softmax renormalised over those k.
+ *   stats     out, nullable: one xshare_stats.
+ *
+ * Steps: warm-up S_0 = union of top-k0; budgeted greedy on s_j (Algorithm 1 with the
+ * fixed budget of Section 3.4; a warm-up set larger than a total budget is cut by score);
+ * refinement.
+ */
+xshare_status xshare_route(const float* logits, int32_t T, const xshare_route_params* params,
+                           uint8_t* sel_mask, int32_t* topk_ids, float* topk_w,
+                           xshare_stats* stats, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * xshare_select_hier -- speculative-decoding-aware selection (Algorithms 3 and 4, Section 4.1).
+ *
+ *   req_offsets  [R + 1] int32, DEVICE: request r owns tokens [o_r, o_{r+1});
+ *                must satisfy 0 = o_0 < o_1 < ... < o_R = T (not checked on the device:
+ *                pass host_offsets to have them validated before launch).
+ *   host_offsets nullable HOST copy of req_offsets, validated when given.
+ *   R            number of requests (0 only with T == 0).
+ *   Other arguments as xshare_route; params->per_request_budget is m_r.
+ *
+ * Per request r: S_r = S_0(r) plus the m_r best remaining experts of r by the request's own
+ * score (Eq. (3)); then S = GreedySelect over the batch score (Eq. (4)) starting from the
+ * union of the S_r (warm-up experts first when a total budget cuts it); refinement.
+ */
+xshare_status xshare_select_hier(const float* logits, int32_t T, const int32_t* req_offsets,
+                                 const int32_t* host_offsets, int32_t R,
+                                 const xshare_route_params* params, uint8_t* sel_mask,
+                                 int32_t* topk_ids, float* topk_w, xshare_stats* stats,
+                                 void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Stage boundaries recorded by xshare_moe_forward when stage_events is given.            */
+#define XSHARE_N_STAGE_EVENTS 5  /* start | route | gate-up GEMM | down GEMM | combine end */
+
+/*
+ * xshare_moe_forward -- the whole routed-expert MoE layer for one decode batch.
+ *
+ *   x        [T, d] bf16 (uint16 bit patterns) row-major: token hidden states.
+ *   logits   [T, N] fp32: router logits.
+ *   w1, w3   [N, f, d] bf16: gate and up projections of every expert, nn.Linear [out, in].
+ *   w2       [N, d, f] bf16: down projections.
+ *   req_offsets/host_offsets/R: as xshare_select_hier, or req_offsets == NULL for the flat
+ *            selection of xshare_route.
+ *   y        out [T, d] bf16: y_i = sum_r w_ir * E_{e_ir}(x_i) with the refined routing
+ *            (Section 2.1 without the shared-expert term), E(x) = W2 (silu(W1 x) * (W3 x)),
+ *            fp32 accumulation, rounded to bf16 (nearest even) once at the end.
+ *   sel_mask, topk_ids, topk_w, stats: nullable copies of the routing outputs.
+ *   stage_events: nullable; XSHARE_N_STAGE_EVENTS hipEvent_t handles created by the caller,
+ *            recorded on `stream` at the stage boundaries (profiling).
+ *
+ * Only the weights of experts that receive at least one token are read, each once per
+ * (up to) 32 tokens routed to it.  Pointers x, w1, w3, w2 and y must be 16-byte aligned.
+ */
+xshare_status xshare_moe_forward(const uint16_t* x, const float* logits, int32_t T, int32_t d,
+                                 int32_t f, const uint16_t* w1, const uint16_t* w3,
+                                 const uint16_t* w2, const xshare_route_params* params,
+                                 const int32_t* req_offsets, const int32_t* host_offsets,
+                                 int32_t R, uint16_t* y, uint8_t* sel_mask, int32_t* topk_ids,
+                                 float* topk_w, xshare_stats* stats, void* ws, size_t ws_bytes,
+                                 void* const* stage_events, hipStream_t stream);
+
+/* Static description of a status code (never NULL).                                      */
+const char* xshare_status_string(int32_t status);
+
+/* Library version, e.g. "0.1.0".                                                         */
+const char* xshare_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* XSHARE_H */

@@ -1,0 +1,9 @@
+"""XShare batch-level MoE layer (arXiv 2602.07265) for AMD Instinct MI355X (gfx950).
+
+The computation lives in hand-written HIP kernels behind the C ABI of include/xshare.h
+(libxshare.so, built in-tree by ``paper_2602_07265_amd.build``); ``xshare`` is the Python
+binding with the same entry points.
+"""
+from .xshare import (HipEvent, XShareError, lib, moe_forward, moe_workspace_bytes, params,  # noqa: F401
+                     route, route_workspace_bytes, select_hier, stats_dict, status_string,
+                     version)

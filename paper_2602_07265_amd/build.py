@@ -1,0 +1,78 @@
+"""Builds libxshare.so (gfx950) in-tree with hipcc.
+
+    python -m paper_2602_07265_amd.build      # or build() from Python
+
+Translation units:
+* route.hip -- expert selection; -ffp-contract=off and correctly rounded fp32 division, so
+               the gate arithmetic is exactly the documented sequence of fp32 operations;
+* ffn.hip   -- expert GEMMs (bf16 MFMA) and the combine;
+* abi.hip   -- the extern "C" entry points declared in include/xshare.h.
+Every HIP compile disables packed-fp32 instruction selection.
+"""
+from __future__ import annotations
+
+import os
+import shutil
+import subprocess
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+LIB = os.path.join(PKG, "libxshare.so")
+ARCH = "gfx950"
+
+COMMON = [
+    f"--offload-arch={ARCH}", "-O3", "-fPIC", "-std=c++17", "-Wall",
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-I", INCLUDE, "-I", CSRC,
+]
+UNITS = {
+    "route.hip": ["-ffp-contract=off", "-fhip-fp32-correctly-rounded-divide-sqrt",
+                  "-fno-fast-math"],
+    "ffn.hip": [],
+    "abi.hip": [],
+}
+
+
+def hipcc() -> str:
+    for cand in (shutil.which("hipcc"), "/opt/rocm/bin/hipcc"):
+        if cand and os.path.exists(cand):
+            return cand
+    raise RuntimeError("hipcc not found: install ROCm or put hipcc on PATH")
+
+
+def build(verbose: bool = False) -> str:
+    """Compiles every translation unit and links libxshare.so; returns its path."""
+    cc = hipcc()
+    objdir = os.path.join(PKG, "_build")
+    os.makedirs(objdir, exist_ok=True)
+    objs = []
+    for unit, flags in UNITS.items():
+        obj = os.path.join(objdir, unit.replace(".hip", ".o"))
+        cmd = [cc, *COMMON, *flags, "-c", os.path.join(CSRC, unit), "-o", obj]
+        _run(cmd, verbose)
+        objs.append(obj)
+    tmp = LIB + ".tmp"
+    _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs], verbose)
+    os.replace(tmp, LIB)
+    return LIB
+
+
+def _run(cmd, verbose):
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        sys.stderr.write(res.stdout + res.stderr)
+        raise RuntimeError(f"build step failed ({res.returncode}): {' '.join(cmd)}")
+    # the host pass does not know the packed-fp32 target feature; that warning is expected
+    noise = [ln for ln in (res.stdout + res.stderr).splitlines()
+             if ln.strip() and "packed-fp32-ops" not in ln and "not a recognized feature" not in ln]
+    if verbose and noise:
+        sys.stderr.write("\n".join(noise) + "\n")
+
+
+if __name__ == "__main__":
+    print(build(verbose=True))

@@ -1,0 +1,221 @@
+// Host side of the C ABI declared in include/xshare.h: argument validation (before any
+// HIP call), workspace carving and kernel launches.  No allocation, no synchronisation.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+#include "internal.h"
+#include "xshare.h"
+
+namespace {
+
+using xs::kMaxAssignments;
+using xs::kMaxExperts;
+using xs::kMaxTokens;
+using xs::kMaxTopK;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Parameter checks shared by every entry point.  `hier` enables the m_r check.
+xshare_status check_params(int32_t T, const xshare_route_params* p, bool hier) {
+  if (!p) return XSHARE_EINVAL;
+  if (T < 0 || p->n_experts < 1 || p->top_k < 1 || p->top_k > p->n_experts) return XSHARE_EINVAL;
+  if (p->warmup_k0 < 0 || p->warmup_k0 > p->top_k || p->budget < 0) return XSHARE_EINVAL;
+  if (p->budget_mode != XSHARE_BUDGET_TOTAL && p->budget_mode != XSHARE_BUDGET_EXTRA)
+    return XSHARE_EINVAL;
+  if (p->score_mode != XSHARE_SCORE_TOPK && p->score_mode != XSHARE_SCORE_DENSE)
+    return XSHARE_EINVAL;
+  if (p->budget_mode == XSHARE_BUDGET_TOTAL && p->budget < p->top_k) return XSHARE_EINVAL;
+  if (hier && p->per_request_budget < 0) return XSHARE_EINVAL;
+  if (p->n_experts > kMaxExperts || p->top_k > kMaxTopK || T > kMaxTokens ||
+      (int64_t)T * p->top_k > kMaxAssignments)
+    return XSHARE_EUNSUPPORTED;
+  return XSHARE_OK;
+}
+
+xshare_status check_offsets(int32_t T, const int32_t* req_offsets, const int32_t* host_offsets,
+                            int32_t R) {
+  if (R < 0 || R > T || (R == 0) != (T == 0)) return XSHARE_EINVAL;
+  if (R > 0 && !req_offsets) return XSHARE_EINVAL;
+  if (host_offsets) {
+    if (host_offsets[0] != 0 || host_offsets[R] != T) return XSHARE_EINVAL;
+    for (int r = 0; r < R; ++r)
+      if (host_offsets[r + 1] <= host_offsets[r]) return XSHARE_EINVAL;
+  }
+  return XSHARE_OK;
+}
+
+template <typename P>
+P* at(void* ws, size_t off) {
+  return reinterpret_cast<P*>(static_cast<char*>(ws) + off);
+}
+
+// Fills the routing arguments; outputs may be redirected to workspace scratch.
+xs::RouteArgs route_args(const float* logits, int32_t T, const xshare_route_params* p,
+                         const int32_t* req_offsets, int32_t R, uint8_t* sel_mask,
+                         int32_t* ids, float* w, xshare_stats* stats, void* ws,
+                         const xs::RouteLayout& L) {
+  xs::RouteArgs a{};
+  a.logits = logits;
+  a.T = T;
+  a.N = p->n_experts;
+  a.k = p->top_k;
+  a.k0 = p->warmup_k0;
+  a.budget = std::min(p->budget, p->n_experts);  // a larger budget selects the same set
+  a.budget_mode = p->budget_mode;
+  a.score_mode = p->score_mode;
+  a.m_r = std::min(p->per_request_budget, p->n_experts);
+  a.req_offsets = req_offsets;
+  a.R = R;
+  a.sel_mask = sel_mask;
+  a.ids = ids ? ids : at<int32_t>(ws, L.ids);
+  a.w = w ? w : at<float>(ws, L.w);
+  a.stats = reinterpret_cast<int32_t*>(stats);
+  a.offsets = at<int32_t>(ws, L.offsets);
+  a.perm = at<int32_t>(ws, L.perm);
+  a.active = at<int32_t>(ws, L.active);
+  a.counters = at<int32_t>(ws, L.counters);
+  a.dense = p->score_mode == XSHARE_SCORE_DENSE ? at<float>(ws, L.dense) : nullptr;
+  return a;
+}
+
+xshare_status route_common(const float* logits, int32_t T, const int32_t* req_offsets,
+                           const int32_t* host_offsets, int32_t R, bool hier,
+                           const xshare_route_params* p, uint8_t* sel_mask, int32_t* ids,
+                           float* w, xshare_stats* stats, void* ws, size_t ws_bytes,
+                           hipStream_t stream) {
+  xshare_status st = check_params(T, p, hier);
+  if (st != XSHARE_OK) return st;
+  if (hier) {
+    st = check_offsets(T, req_offsets, host_offsets, R);
+    if (st != XSHARE_OK) return st;
+  }
+  if (!sel_mask || (T > 0 && (!logits || !ids || !w))) return XSHARE_EINVAL;
+  const xs::RouteLayout L =
+      xs::route_layout(T, p->n_experts, p->top_k, p->score_mode == XSHARE_SCORE_DENSE);
+  if (!ws || ws_bytes < L.total) return XSHARE_EWORKSPACE;
+  const xs::RouteArgs a = route_args(logits, T, p, hier ? req_offsets : nullptr, R, sel_mask,
+                                     ids, w, stats, ws, L);
+  return xs::launch_route(a, stream) == hipSuccess ? XSHARE_OK : XSHARE_EHIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t xshare_route_workspace_bytes(int32_t T, const xshare_route_params* params) {
+  if (check_params(T, params, false) != XSHARE_OK) return 0;
+  return xs::route_layout(T, params->n_experts, params->top_k,
+                          params->score_mode == XSHARE_SCORE_DENSE)
+      .total;
+}
+
+size_t xshare_moe_workspace_bytes(int32_t T, int32_t d, int32_t f,
+                                  const xshare_route_params* params) {
+  if (check_params(T, params, false) != XSHARE_OK || d <= 0 || f <= 0) return 0;
+  return xs::ffn_layout(T, params->n_experts, params->top_k,
+                        params->score_mode == XSHARE_SCORE_DENSE, d, f)
+      .total;
+}
+
+xshare_status xshare_route(const float* logits, int32_t T, const xshare_route_params* params,
+                           uint8_t* sel_mask, int32_t* topk_ids, float* topk_w,
+                           xshare_stats* stats, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return route_common(logits, T, nullptr, nullptr, 0, false, params, sel_mask, topk_ids, topk_w,
+                      stats, ws, ws_bytes, stream);
+}
+
+xshare_status xshare_select_hier(const float* logits, int32_t T, const int32_t* req_offsets,
+                                 const int32_t* host_offsets, int32_t R,
+                                 const xshare_route_params* params, uint8_t* sel_mask,
+                                 int32_t* topk_ids, float* topk_w, xshare_stats* stats,
+                                 void* ws, size_t ws_bytes, hipStream_t stream) {
+  return route_common(logits, T, req_offsets, host_offsets, R, true, params, sel_mask, topk_ids,
+                      topk_w, stats, ws, ws_bytes, stream);
+}
+
+xshare_status xshare_moe_forward(const uint16_t* x, const float* logits, int32_t T, int32_t d,
+                                 int32_t f, const uint16_t* w1, const uint16_t* w3,
+                                 const uint16_t* w2, const xshare_route_params* params,
+                                 const int32_t* req_offsets, const int32_t* host_offsets,
+                                 int32_t R, uint16_t* y, uint8_t* sel_mask, int32_t* topk_ids,
+                                 float* topk_w, xshare_stats* stats, void* ws, size_t ws_bytes,
+                                 void* const* stage_events, hipStream_t stream) {
+  const bool hier = req_offsets != nullptr;
+  xshare_status st = check_params(T, params, hier);
+  if (st != XSHARE_OK) return st;
+  if (hier) {
+    st = check_offsets(T, req_offsets, host_offsets, R);
+    if (st != XSHARE_OK) return st;
+  }
+  if (d <= 0 || f <= 0) return XSHARE_EINVAL;
+  if (d % xs::kDimAlign != 0 || f % xs::kDimAlign != 0) return XSHARE_EUNSUPPORTED;
+  if (T > 0 && (!x || !logits || !w1 || !w3 || !w2 || !y)) return XSHARE_EINVAL;
+  if (!aligned16(x) || !aligned16(w1) || !aligned16(w3) || !aligned16(w2) || !aligned16(y))
+    return XSHARE_EINVAL;
+  const int N = params->n_experts, k = params->top_k;
+  const xs::FfnLayout L =
+      xs::ffn_layout(T, N, k, params->score_mode == XSHARE_SCORE_DENSE, d, f);
+  if (!ws || ws_bytes < L.total) return XSHARE_EWORKSPACE;
+
+  // The selection kernel always writes a mask; keep it in the workspace if not wanted.
+  uint8_t* mask = sel_mask ? sel_mask : at<uint8_t>(ws, L.route.mask);
+  auto record = [&](int s) -> bool {
+    if (!stage_events) return true;
+    return hipEventRecord(static_cast<hipEvent_t>(stage_events[s]), stream) == hipSuccess;
+  };
+  if (!record(0)) return XSHARE_EHIP;
+  const xs::RouteArgs ra = route_args(logits, T, params, hier ? req_offsets : nullptr, R, mask,
+                                      topk_ids, topk_w, stats, ws, L.route);
+  if (xs::launch_route(ra, stream) != hipSuccess || !record(1)) return XSHARE_EHIP;
+  if (T == 0) {
+    for (int s = 2; s < XSHARE_N_STAGE_EVENTS; ++s)
+      if (!record(s)) return XSHARE_EHIP;
+    return XSHARE_OK;
+  }
+
+  xs::FfnArgs fa{};
+  fa.x = x;
+  fa.w1 = w1;
+  fa.w3 = w3;
+  fa.w2 = w2;
+  fa.T = T;
+  fa.N = N;
+  fa.k = k;
+  fa.d = d;
+  fa.f = f;
+  // Active experts never exceed the selected set (<= budget under a total budget) nor the
+  // number of (token, slot) pairs; blocks beyond the device-side count exit at once.
+  int bound = std::min(N, T * k);
+  if (params->budget_mode == XSHARE_BUDGET_TOTAL) bound = std::min(bound, params->budget);
+  fa.max_active = bound;
+  fa.offsets = ra.offsets;
+  fa.perm = ra.perm;
+  fa.active = ra.active;
+  fa.counters = ra.counters;
+  fa.ids = ra.ids;
+  fa.w = ra.w;
+  fa.h = at<uint16_t>(ws, L.h);
+  fa.yslot = at<float>(ws, L.y);
+  fa.y = y;
+  if (xs::launch_gate_up(fa, stream) != hipSuccess || !record(2)) return XSHARE_EHIP;
+  if (xs::launch_down(fa, stream) != hipSuccess || !record(3)) return XSHARE_EHIP;
+  if (xs::launch_combine(fa, stream) != hipSuccess || !record(4)) return XSHARE_EHIP;
+  return XSHARE_OK;
+}
+
+const char* xshare_status_string(int32_t status) {
+  switch (status) {
+    case XSHARE_OK: return "ok";
+    case XSHARE_EINVAL: return "invalid argument";
+    case XSHARE_EUNSUPPORTED: return "unsupported size";
+    case XSHARE_EWORKSPACE: return "workspace too small";
+    case XSHARE_EHIP: return "HIP launch failed";
+    default: return "unknown status";
+  }
+}
+
+const char* xshare_version(void) { return "0.1.0"; }
+
+}  // extern "C"

@@ -1,0 +1,231 @@
+// Expert FFNs of the selected experts only (SwiGLU, nn.Linear [out, in] weights, bf16):
+//   gate/up:  H[p, :] = silu(x_i W1_e^T) * (x_i W3_e^T)      for every permuted row p = (i, r)
+//   down:     Y[i*k + r, :] = H[p, :] W2_e^T
+//   combine:  y_i = sum_r w_ir Y[i*k + r, :]  (rank order, fp32) -> bf16
+//
+// Decode batches give an expert 1..T tokens, so each weight element is used a few times:
+// the GEMMs are bound by streaming the selected experts' weights from HBM.  Each wave owns
+// 16 weight rows and the whole reduction dimension; weights go from HBM straight into the
+// B operand of v_mfma_f32_16x16x32_bf16 (lane (n, g) loads 16 contiguous bytes of row n per
+// MFMA, so a wave reads 16 rows x 32*U contiguous elements per step), tokens form the M
+// dimension (16 per tile, up to two tiles per pass), accumulation is fp32.  The next step's
+// loads are issued before the current step's MFMAs (register double buffering).
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "internal.h"
+
+namespace xs {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr int kBlock = 256;       // 4 waves
+constexpr int kWaves = kBlock / 64;
+constexpr int kCols = 16;         // weight rows (output columns) per wave
+constexpr int kTiles = 2;         // 16-token tiles per pass over the weights
+
+__device__ __forceinline__ bf16x8 load8(const uint16_t* p) {
+  return *reinterpret_cast<const bf16x8*>(p);
+}
+
+__device__ __forceinline__ floatx4 mfma(const bf16x8& a, const bf16x8& b, const floatx4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ uint16_t to_bf16(float v) {
+  uint32_t b = __float_as_uint(v);
+  b += 0x7FFFu + ((b >> 16) & 1u);  // round to nearest even
+  return (uint16_t)(b >> 16);
+}
+
+// One pass of a wave over the reduction dimension K for up to kTiles token tiles:
+// acc[m][rt] += A_rt (16 x K) * B_m^T (K x 16) for the NM weight matrices B_m.
+// `arow[rt]` points at the token row this lane feeds (any valid row for padding lanes,
+// whose output rows are discarded), `brow[m]` at the weight row of this lane's column;
+// both already offset by this lane's group position g * 8U.
+template <int U, int NM>
+__device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[kTiles], int nt,
+                                          const uint16_t* const (&brow)[NM], int K,
+                                          floatx4 (&acc)[NM][kTiles]) {
+  constexpr int KB = 32 * U;
+  bf16x8 b[NM][U], x[kTiles][U];
+#pragma unroll
+  for (int m = 0; m < NM; ++m)
+#pragma unroll
+    for (int u = 0; u < U; ++u) b[m][u] = load8(brow[m] + 8 * u);
+#pragma unroll
+  for (int rt = 0; rt < kTiles; ++rt)
+    if (rt < nt)
+#pragma unroll
+      for (int u = 0; u < U; ++u) x[rt][u] = load8(arow[rt] + 8 * u);
+
+  for (int kb = KB; kb <= K; kb += KB) {
+    bf16x8 nb[NM][U], nx[kTiles][U];
+    const bool more = kb < K;
+    if (more) {
+#pragma unroll
+      for (int m = 0; m < NM; ++m)
+#pragma unroll
+        for (int u = 0; u < U; ++u) nb[m][u] = load8(brow[m] + kb + 8 * u);
+#pragma unroll
+      for (int rt = 0; rt < kTiles; ++rt)
+        if (rt < nt)
+#pragma unroll
+          for (int u = 0; u < U; ++u) nx[rt][u] = load8(arow[rt] + kb + 8 * u);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int rt = 0; rt < kTiles; ++rt)
+        if (rt < nt)
+#pragma unroll
+          for (int m = 0; m < NM; ++m) acc[m][rt] = mfma(x[rt][u], b[m][u], acc[m][rt]);
+    if (more) {
+#pragma unroll
+      for (int m = 0; m < NM; ++m)
+#pragma unroll
+        for (int u = 0; u < U; ++u) b[m][u] = nb[m][u];
+#pragma unroll
+      for (int rt = 0; rt < kTiles; ++rt)
+#pragma unroll
+        for (int u = 0; u < U; ++u) x[rt][u] = nx[rt][u];
+    }
+  }
+}
+
+template <int U>
+__global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
+  const int slot = blockIdx.y;
+  if (slot >= a.counters[kCntActive]) return;
+  const int e = a.active[slot];
+  const int p0 = a.offsets[e];
+  const int te = a.offsets[e + 1] - p0;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int j0 = (blockIdx.x * kWaves + wave) * kCols;
+  if (j0 >= a.f) return;
+  const int n = lane & 15, g = lane >> 4;
+  const int d = a.d, f = a.f;
+  const size_t wrow = ((size_t)e * f + j0 + n) * d + (size_t)g * 8 * U;
+  const uint16_t* const brow[2] = {a.w1 + wrow, a.w3 + wrow};
+
+  for (int c0 = 0; c0 < te; c0 += 16 * kTiles) {
+    const int nt = min(kTiles, (te - c0 + 15) / 16);
+    const uint16_t* arow[kTiles];
+#pragma unroll
+    for (int rt = 0; rt < kTiles; ++rt) {
+      const int t = min(c0 + rt * 16 + n, te - 1);
+      arow[rt] = a.x + (size_t)(a.perm[p0 + t] / a.k) * d + (size_t)g * 8 * U;
+    }
+    floatx4 acc[2][kTiles];
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+#pragma unroll
+      for (int rt = 0; rt < kTiles; ++rt) acc[m][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    wave_pass<U, 2>(arow, nt, brow, d, acc);
+#pragma unroll
+    for (int rt = 0; rt < kTiles; ++rt) {
+      if (rt >= nt) break;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t = c0 + rt * 16 + 4 * g + i;
+        if (t < te) {
+          const float h1 = acc[0][rt][i], h3 = acc[1][rt][i];
+          const float hv = h1 / (1.0f + __expf(-h1)) * h3;
+          a.h[(size_t)(p0 + t) * f + j0 + n] = to_bf16(hv);
+        }
+      }
+    }
+  }
+}
+
+template <int U>
+__global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
+  const int slot = blockIdx.y;
+  if (slot >= a.counters[kCntActive]) return;
+  const int e = a.active[slot];
+  const int p0 = a.offsets[e];
+  const int te = a.offsets[e + 1] - p0;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int n0 = (blockIdx.x * kWaves + wave) * kCols;
+  if (n0 >= a.d) return;
+  const int n = lane & 15, g = lane >> 4;
+  const int d = a.d, f = a.f;
+  const uint16_t* const brow[1] = {a.w2 + ((size_t)e * d + n0 + n) * f + (size_t)g * 8 * U};
+
+  for (int c0 = 0; c0 < te; c0 += 16 * kTiles) {
+    const int nt = min(kTiles, (te - c0 + 15) / 16);
+    const uint16_t* arow[kTiles];
+#pragma unroll
+    for (int rt = 0; rt < kTiles; ++rt) {
+      const int t = min(c0 + rt * 16 + n, te - 1);
+      arow[rt] = a.h + (size_t)(p0 + t) * f + (size_t)g * 8 * U;
+    }
+    floatx4 acc[1][kTiles];
+#pragma unroll
+    for (int rt = 0; rt < kTiles; ++rt) acc[0][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    wave_pass<U, 1>(arow, nt, brow, f, acc);
+#pragma unroll
+    for (int rt = 0; rt < kTiles; ++rt) {
+      if (rt >= nt) break;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t = c0 + rt * 16 + 4 * g + i;
+        if (t < te) a.yslot[(size_t)a.perm[p0 + t] * d + n0 + n] = acc[0][rt][i];
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void combine_kernel(FfnArgs a) {
+  const int i = blockIdx.y;
+  const int c = (blockIdx.x * kBlock + threadIdx.x) * 4;
+  if (c >= a.d) return;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int r = 0; r < a.k; ++r) {
+    const int slot = i * a.k + r;
+    if (a.ids[slot] < 0) continue;
+    const float wr = a.w[slot];
+    const float4 v = *reinterpret_cast<const float4*>(a.yslot + (size_t)slot * a.d + c);
+    acc[0] += wr * v.x;
+    acc[1] += wr * v.y;
+    acc[2] += wr * v.z;
+    acc[3] += wr * v.w;
+  }
+  const uint32_t lo = (uint32_t)to_bf16(acc[0]) | ((uint32_t)to_bf16(acc[1]) << 16);
+  const uint32_t hi = (uint32_t)to_bf16(acc[2]) | ((uint32_t)to_bf16(acc[3]) << 16);
+  *reinterpret_cast<uint2*>(a.y + (size_t)i * a.d + c) = make_uint2(lo, hi);
+}
+
+int unroll_for(int K) { return (K % 128 == 0) ? 4 : (K % 64 == 0) ? 2 : 1; }
+
+}  // namespace
+
+hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
+  const dim3 grid((a.f + kWaves * kCols - 1) / (kWaves * kCols), a.max_active), block(kBlock);
+  switch (unroll_for(a.d)) {
+    case 4: hipLaunchKernelGGL(gate_up_kernel<4>, grid, block, 0, stream, a); break;
+    case 2: hipLaunchKernelGGL(gate_up_kernel<2>, grid, block, 0, stream, a); break;
+    default: hipLaunchKernelGGL(gate_up_kernel<1>, grid, block, 0, stream, a); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_down(const FfnArgs& a, hipStream_t stream) {
+  const dim3 grid((a.d + kWaves * kCols - 1) / (kWaves * kCols), a.max_active), block(kBlock);
+  switch (unroll_for(a.f)) {
+    case 4: hipLaunchKernelGGL(down_kernel<4>, grid, block, 0, stream, a); break;
+    case 2: hipLaunchKernelGGL(down_kernel<2>, grid, block, 0, stream, a); break;
+    default: hipLaunchKernelGGL(down_kernel<1>, grid, block, 0, stream, a); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_combine(const FfnArgs& a, hipStream_t stream) {
+  const dim3 grid((a.d + kBlock * 4 - 1) / (kBlock * 4), a.T), block(kBlock);
+  hipLaunchKernelGGL(combine_kernel, grid, block, 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace xs

@@ -1,0 +1,292 @@
+"""Python binding of libxshare.so (argument marshalling only).
+
+Every computation runs in the HIP kernels behind the C ABI of include/xshare.h; this module
+checks tensor devices/dtypes/shapes, carves nothing itself except the workspace tensor it
+allocates when none is passed, and forwards raw device pointers plus the current HIP stream.
+There is no fallback: if the library is not built or no GPU is present, calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libxshare.so")
+
+OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP = 0, 1, 2, 3, 4
+BUDGET = {"total": 0, "extra": 1}
+SCORE = {"topk": 0, "dense": 1}
+N_STAGE_EVENTS = 5
+STAGES = ("route", "gate_up", "down", "combine")
+
+
+class RouteParams(ctypes.Structure):
+    _fields_ = [
+        ("n_experts", ctypes.c_int32),
+        ("top_k", ctypes.c_int32),
+        ("warmup_k0", ctypes.c_int32),
+        ("budget", ctypes.c_int32),
+        ("budget_mode", ctypes.c_int32),
+        ("score_mode", ctypes.c_int32),
+        ("per_request_budget", ctypes.c_int32),
+    ]
+
+
+STATS_FIELDS = ("n_selected", "n_active", "n_vanilla_union", "n_warmup", "n_start",
+                "budget_eff")
+
+
+class XShareError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {status_string(status)} ({status})")
+        self.status = status
+
+
+_lib = None
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_SZ = ctypes.c_size_t
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libxshare.so (raises if it was not built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2602_07265_amd.build` (hipcc, gfx950)")
+        L = ctypes.CDLL(LIB_PATH)
+        L.xshare_route_workspace_bytes.argtypes = [_I32, ctypes.POINTER(RouteParams)]
+        L.xshare_route_workspace_bytes.restype = _SZ
+        L.xshare_moe_workspace_bytes.argtypes = [_I32, _I32, _I32, ctypes.POINTER(RouteParams)]
+        L.xshare_moe_workspace_bytes.restype = _SZ
+        L.xshare_route.argtypes = [_P, _I32, ctypes.POINTER(RouteParams), _P, _P, _P, _P, _P, _SZ,
+                                   _P]
+        L.xshare_route.restype = ctypes.c_int
+        L.xshare_select_hier.argtypes = [_P, _I32, _P, _P, _I32, ctypes.POINTER(RouteParams), _P,
+                                         _P, _P, _P, _P, _SZ, _P]
+        L.xshare_select_hier.restype = ctypes.c_int
+        L.xshare_moe_forward.argtypes = [_P, _P, _I32, _I32, _I32, _P, _P, _P,
+                                         ctypes.POINTER(RouteParams), _P, _P, _I32, _P, _P, _P, _P,
+                                         _P, _P, _SZ, _P, _P]
+        L.xshare_moe_forward.restype = ctypes.c_int
+        L.xshare_status_string.argtypes = [_I32]
+        L.xshare_status_string.restype = ctypes.c_char_p
+        L.xshare_version.argtypes = []
+        L.xshare_version.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().xshare_status_string(int(status)).decode()
+
+
+def version() -> str:
+    return lib().xshare_version().decode()
+
+
+def params(n_experts: int, top_k: int, warmup_k0: int, budget: int, budget_mode="total",
+           score_mode="topk", per_request_budget: int = 0) -> RouteParams:
+    return RouteParams(int(n_experts), int(top_k), int(warmup_k0), int(budget),
+                       BUDGET[budget_mode] if isinstance(budget_mode, str) else int(budget_mode),
+                       SCORE[score_mode] if isinstance(score_mode, str) else int(score_mode),
+                       int(per_request_budget))
+
+
+def route_workspace_bytes(T: int, p: RouteParams) -> int:
+    return int(lib().xshare_route_workspace_bytes(int(T), ctypes.byref(p)))
+
+
+def moe_workspace_bytes(T: int, d: int, f: int, p: RouteParams) -> int:
+    return int(lib().xshare_moe_workspace_bytes(int(T), int(d), int(f), ctypes.byref(p)))
+
+
+# ----------------------------------------------------------------------------- helpers
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dev(t, dtype, shape, name):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _check(status, what):
+    if status != OK:
+        raise XShareError(status, what)
+
+
+def stats_dict(stats: torch.Tensor) -> dict:
+    v = stats.to("cpu").tolist()
+    return dict(zip(STATS_FIELDS, v))
+
+
+def _offsets(req_offsets, device):
+    """(device int32 tensor, host int32 array pointer holder) from a list/array/tensor."""
+    if isinstance(req_offsets, torch.Tensor) and req_offsets.is_cuda:
+        dev = _dev(req_offsets, torch.int32, (req_offsets.numel(),), "req_offsets")
+        return dev, None
+    host = torch.as_tensor(list(int(v) for v in req_offsets), dtype=torch.int32)
+    return host.to(device), host
+
+
+# ----------------------------------------------------------------------------- entry points
+
+def _route_impl(logits, p, req_offsets, out, workspace, stream):
+    T, N = logits.shape
+    k = p.top_k
+    dev = logits.device
+    _dev(logits, torch.float32, (T, N), "logits")
+    if N != p.n_experts:
+        raise ValueError("logits width must equal n_experts")
+    out = dict(out or {})
+    sel = out.get("sel_mask") if out.get("sel_mask") is not None else torch.empty(N, dtype=torch.uint8, device=dev)
+    ids = out.get("ids") if out.get("ids") is not None else torch.empty((T, k), dtype=torch.int32, device=dev)
+    w = out.get("w") if out.get("w") is not None else torch.empty((T, k), dtype=torch.float32, device=dev)
+    stats = out.get("stats") if out.get("stats") is not None else torch.empty(8, dtype=torch.int32, device=dev)
+    _dev(sel, torch.uint8, (N,), "sel_mask")
+    _dev(ids, torch.int32, (T, k), "ids")
+    _dev(w, torch.float32, (T, k), "w")
+    _dev(stats, torch.int32, (8,), "stats")
+    need = route_workspace_bytes(T, p)
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    if req_offsets is None:
+        st = lib().xshare_route(_ptr(logits), T, ctypes.byref(p), _ptr(sel), _ptr(ids), _ptr(w),
+                                _ptr(stats), _ptr(workspace), workspace.numel(), _stream(stream))
+        _check(st, "xshare_route")
+    else:
+        d_off, h_off = _offsets(req_offsets, dev)
+        R = d_off.numel() - 1
+        hp = None if h_off is None else ctypes.c_void_p(h_off.data_ptr())
+        st = lib().xshare_select_hier(_ptr(logits), T, _ptr(d_off), hp, R, ctypes.byref(p),
+                                      _ptr(sel), _ptr(ids), _ptr(w), _ptr(stats), _ptr(workspace),
+                                      workspace.numel(), _stream(stream))
+        _check(st, "xshare_select_hier")
+    return dict(sel_mask=sel, ids=ids, w=w, stats=stats)
+
+
+def route(logits: torch.Tensor, top_k: int, warmup_k0: int, budget: int, budget_mode="total",
+          score_mode="topk", *, out=None, workspace=None, stream=None) -> dict:
+    """Algorithm 2 on the GPU: returns dict(sel_mask, ids, w, stats) device tensors."""
+    p = params(logits.shape[1], top_k, warmup_k0, budget, budget_mode, score_mode)
+    return _route_impl(logits, p, None, out, workspace, stream)
+
+
+def select_hier(logits: torch.Tensor, req_offsets, top_k: int, warmup_k0: int,
+                per_request_budget: int, budget: int, budget_mode="total", score_mode="topk", *,
+                out=None, workspace=None, stream=None) -> dict:
+    """Algorithms 3-4 on the GPU; req_offsets as a host sequence (validated) or device tensor."""
+    p = params(logits.shape[1], top_k, warmup_k0, budget, budget_mode, score_mode,
+               per_request_budget)
+    return _route_impl(logits, p, req_offsets, out, workspace, stream)
+
+
+def moe_forward(x: torch.Tensor, logits: torch.Tensor, w1: torch.Tensor, w3: torch.Tensor,
+                w2: torch.Tensor, top_k: int, warmup_k0: int, budget: int, budget_mode="total",
+                score_mode="topk", *, req_offsets=None, per_request_budget: int = 0,
+                y=None, routing_out=True, workspace=None, stage_events=None,
+                stream=None) -> dict:
+    """The MoE layer: returns dict(y [T,d] bf16, and sel_mask/ids/w/stats if routing_out)."""
+    T, d = x.shape
+    N = logits.shape[1]
+    f = w1.shape[1]
+    dev = x.device
+    _dev(x, torch.bfloat16, (T, d), "x")
+    _dev(logits, torch.float32, (T, N), "logits")
+    _dev(w1, torch.bfloat16, (N, f, d), "w1")
+    _dev(w3, torch.bfloat16, (N, f, d), "w3")
+    _dev(w2, torch.bfloat16, (N, d, f), "w2")
+    p = params(N, top_k, warmup_k0, budget, budget_mode, score_mode, per_request_budget)
+    if y is None:
+        y = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
+    _dev(y, torch.bfloat16, (T, d), "y")
+    res = {"y": y}
+    if routing_out:
+        res.update(sel_mask=torch.empty(N, dtype=torch.uint8, device=dev),
+                   ids=torch.empty((T, top_k), dtype=torch.int32, device=dev),
+                   w=torch.empty((T, top_k), dtype=torch.float32, device=dev),
+                   stats=torch.empty(8, dtype=torch.int32, device=dev))
+    need = moe_workspace_bytes(T, d, f, p)
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    d_off = h_off = None
+    R = 0
+    if req_offsets is not None:
+        d_off, h_off = _offsets(req_offsets, dev)
+        R = d_off.numel() - 1
+    ev = None
+    if stage_events is not None:
+        if len(stage_events) != N_STAGE_EVENTS:
+            raise ValueError(f"stage_events needs {N_STAGE_EVENTS} events")
+        ev = (ctypes.c_void_p * N_STAGE_EVENTS)(*[e.handle for e in stage_events])
+    st = lib().xshare_moe_forward(
+        _ptr(x), _ptr(logits), T, d, f, _ptr(w1), _ptr(w3), _ptr(w2), ctypes.byref(p),
+        _ptr(d_off), None if h_off is None else ctypes.c_void_p(h_off.data_ptr()), R, _ptr(y),
+        _ptr(res.get("sel_mask")), _ptr(res.get("ids")), _ptr(res.get("w")),
+        _ptr(res.get("stats")), _ptr(workspace), workspace.numel(), ev, _stream(stream))
+    _check(st, "xshare_moe_forward")
+    return res
+
+
+# ----------------------------------------------------------------------------- HIP events
+
+class HipEvent:
+    """A raw hipEvent_t (for the stage_events argument and kernel timing on any stream)."""
+    _hip = None
+
+    @classmethod
+    def _rt(cls):
+        if cls._hip is None:
+            h = ctypes.CDLL("libamdhip64.so")
+            h.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+            h.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            h.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+            h.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                              ctypes.c_void_p]
+            h.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            cls._hip = h
+        return cls._hip
+
+    def __init__(self):
+        self.handle = ctypes.c_void_p()
+        if self._rt().hipEventCreate(ctypes.byref(self.handle)) != 0:
+            raise RuntimeError("hipEventCreate failed")
+        self.handle = self.handle.value
+
+    def record(self, stream=None):
+        s = torch.cuda.current_stream() if stream is None else stream
+        if self._rt().hipEventRecord(self.handle, ctypes.c_void_p(s.cuda_stream)) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def synchronize(self):
+        self._rt().hipEventSynchronize(self.handle)
+
+    def elapsed_ms(self, later: "HipEvent") -> float:
+        out = ctypes.c_float()
+        if self._rt().hipEventElapsedTime(ctypes.byref(out), self.handle, later.handle) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(out.value)
+
+    def __del__(self):
+        try:
+            if self.handle and self._hip is not None:
+                self._hip.hipEventDestroy(self.handle)
+        except Exception:
+            pass

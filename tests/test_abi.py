@@ -1,0 +1,142 @@
+"""The C-ABI library: it loads, exports every declared symbol, and validates on the host.
+
+Every call below fails validation, so it returns before any HIP call: these tests run
+without a GPU.  Fake non-null device pointers are never dereferenced.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2602_07265_amd import xshare as X
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "xshare.h")
+FAKE = ctypes.c_void_p(1 << 20)        # 16-byte aligned, never dereferenced
+FAKE_ODD = ctypes.c_void_p((1 << 20) + 2)
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(xshare_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert {"xshare_route", "xshare_select_hier", "xshare_moe_forward"} <= set(names)
+    lib = X.lib()
+    for n in names:
+        assert hasattr(lib, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", X.LIB_PATH], capture_output=True,
+                         text=True).stdout
+    exported = set(re.findall(r" T (xshare_\w+)", out))
+    assert set(names) <= exported
+    assert X.version().count(".") == 2
+
+
+def test_status_strings():
+    assert X.status_string(0) == "ok"
+    for s in (1, 2, 3, 4):
+        assert X.status_string(s) and X.status_string(s) != "unknown status"
+    assert X.status_string(99) == "unknown status"
+
+
+def test_workspace_sizes():
+    p = X.params(256, 8, 1, 48)
+    a = X.route_workspace_bytes(32, p)
+    b = X.route_workspace_bytes(64, p)
+    assert a > 0 and a % 256 == 0 and b >= a
+    dense = X.params(256, 8, 1, 48, "total", "dense")
+    assert X.route_workspace_bytes(32, dense) >= a + 32 * 256 * 4
+    m = X.moe_workspace_bytes(32, 7168, 2048, p)
+    # H (bf16 [T k, f]) and per-slot outputs (fp32 [T k, d]) dominate
+    assert m >= a + 32 * 8 * (2048 * 2 + 7168 * 4)
+    assert X.route_workspace_bytes(0, p) > 0
+    assert X.route_workspace_bytes(32, X.params(256, 300, 1, 48)) == 0
+    assert X.moe_workspace_bytes(32, 0, 2048, p) == 0
+
+
+def _route(p, T=8, ws=FAKE, ws_bytes=1 << 30, logits=FAKE, mask=FAKE, ids=FAKE, w=FAKE):
+    return X.lib().xshare_route(logits, T, ctypes.byref(p), mask, ids, w, None, ws, ws_bytes,
+                                None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n_experts=0), X.EINVAL),
+    (dict(top_k=0), X.EINVAL),
+    (dict(top_k=17), X.EINVAL),            # k > N
+    (dict(warmup_k0=3), X.EINVAL),         # k0 > k
+    (dict(warmup_k0=-1), X.EINVAL),
+    (dict(budget=1), X.EINVAL),            # total budget < k
+    (dict(budget=-1, budget_mode=1), X.EINVAL),
+    (dict(budget_mode=2), X.EINVAL),
+    (dict(score_mode=5), X.EINVAL),
+    (dict(n_experts=2048, top_k=8, budget=64), X.EUNSUPPORTED),
+    (dict(n_experts=64, top_k=33, budget=64), X.EUNSUPPORTED),
+])
+def test_route_parameter_validation(kw, status):
+    base = dict(n_experts=16, top_k=2, warmup_k0=1, budget=8, budget_mode=0, score_mode=0,
+                per_request_budget=0)
+    base.update(kw)
+    p = X.RouteParams(*[base[f] for f, _ in X.RouteParams._fields_])
+    assert _route(p) == status
+
+
+def test_route_size_and_pointer_validation():
+    p = X.params(16, 2, 1, 8)
+    assert _route(p, T=-1) == X.EINVAL
+    assert _route(p, T=4097) == X.EUNSUPPORTED
+    assert _route(X.params(16, 4, 1, 8), T=4096) == X.EUNSUPPORTED    # T k > 8192
+    assert _route(p, logits=None) == X.EINVAL
+    assert _route(p, mask=None) == X.EINVAL
+    assert _route(p, ids=None) == X.EINVAL
+    assert _route(p, ws=None) == X.EWORKSPACE
+    assert _route(p, ws_bytes=X.route_workspace_bytes(8, p) - 1) == X.EWORKSPACE
+    assert X.lib().xshare_route(FAKE, 8, None, FAKE, FAKE, FAKE, None, FAKE, 1 << 30,
+                                None) == X.EINVAL
+
+
+def test_select_hier_offset_validation():
+    p = X.params(16, 2, 1, 8, per_request_budget=2)
+    L = X.lib()
+
+    def call(host, R, T=8, dev=FAKE, pp=p):
+        arr = None if host is None else (ctypes.c_int32 * len(host))(*host)
+        return L.xshare_select_hier(FAKE, T, dev, arr, R, ctypes.byref(pp), FAKE, FAKE, FAKE, None,
+                                    None, 0, None)
+
+    assert call([0, 4, 4, 8], 3) == X.EINVAL        # empty request
+    assert call([0, 5, 4, 8], 3) == X.EINVAL        # decreasing
+    assert call([1, 4, 8], 2) == X.EINVAL           # must start at 0
+    assert call([0, 4, 7], 2) == X.EINVAL           # must end at T
+    assert call(None, 9) == X.EINVAL                # more requests than tokens
+    assert call(None, 0) == X.EINVAL                # no request for a non-empty batch
+    assert call(None, 2, dev=None) == X.EINVAL
+    assert call([0, 4, 8], 2, pp=X.params(16, 2, 1, 8, per_request_budget=-1)) == X.EINVAL
+    assert call([0, 4, 8], 2) == X.EWORKSPACE       # valid offsets; fails on the workspace
+
+
+def test_moe_forward_validation():
+    p = X.params(16, 2, 1, 8)
+    L = X.lib()
+
+    def call(d=64, f=128, x=FAKE, y=FAKE, ws=None, T=8):
+        return L.xshare_moe_forward(x, FAKE, T, d, f, FAKE, FAKE, FAKE, ctypes.byref(p), None,
+                                    None, 0, y, None, None, None, None, ws, 1 << 30, None, None)
+
+    assert call(d=48) == X.EUNSUPPORTED
+    assert call(f=100) == X.EUNSUPPORTED
+    assert call(d=0) == X.EINVAL
+    assert call(x=None) == X.EINVAL
+    assert call(x=FAKE_ODD) == X.EINVAL             # 16-byte alignment of bf16 rows
+    assert call(y=FAKE_ODD) == X.EINVAL
+    assert call() == X.EWORKSPACE
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    with pytest.raises(ValueError):
+        X.route(torch.zeros(4, 16), 2, 1, 8)

@@ -1,0 +1,127 @@
+"""MoE layer parity on the GPU: y within 2e-2 * RMS of the float64 oracle (Section 2.1).
+
+The oracle routes independently (bit-exact routing is asserted too) and evaluates the
+SwiGLU experts in float64 from the same bf16 inputs.  Full-size layers are compared on
+sampled tokens, the oracle computing those rows one by one.
+"""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from helpers import (DEV, assert_route_equal, expert_fetcher, ffn_error, make_layer,
+                     oracle_route, say)
+from oracle import ffn as OF
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2   # max |y_gpu - y_ref| <= TOL * RMS(y_ref)
+
+
+def _run(cfg, seed, k0, M, mode="total", score="topk", rows=None, m_r=0, layer=None,
+         label=""):
+    from paper_2602_07265_amd import xshare as X
+    h, off, x, w1, w3, w2 = layer if layer is not None else make_layer(cfg, seed)
+    hier = cfg.get("logits") == "spec"
+    say(f"ffn case {label} T={cfg['T']} N={cfg['N']} d={cfg['d']} f={cfg['f']} k0={k0} M={M} "
+        f"{mode} {score}{' hier' if hier else ''}")
+    res = X.moe_forward(x, torch.from_numpy(h).to(DEV), w1, w3, w2, cfg["k"], k0, M, mode, score,
+                        req_offsets=list(off) if hier else None, per_request_budget=m_r)
+    torch.cuda.synchronize()
+    got = {k: v.cpu().numpy() for k, v in res.items() if k != "y"}
+    ref = oracle_route(h, cfg["k"], k0, M, mode, score, off if hier else None, m_r)
+    assert_route_equal(got, ref, label)
+    rows = list(range(cfg["T"])) if rows is None else rows
+    y_ref = OF.moe_forward(W.bf16_bits(x), ref.ids, ref.w, expert_fetcher(w1, w3, w2), rows)
+    y_gpu = OF.bf16_to_f64(W.bf16_bits(res["y"]))[rows]
+    err, rms = ffn_error(y_gpu, y_ref)
+    say(f"  max err / RMS = {err:.3e} (RMS {rms:.3e}), |S|={got['stats'][0]} "
+        f"active={got['stats'][1]} |U|={got['stats'][2]}")
+    assert np.all(np.isfinite(y_gpu))
+    assert err <= TOL, f"{label}: max error {err:.3e} x RMS exceeds {TOL}"
+    return res, ref
+
+
+def test_ffn_tiny_all_modes():
+    c = W.CONFIGS["tiny"]
+    for seed in range(4):
+        layer = make_layer(c, seed)
+        for k0, M, mode, score in [(1, 8, "total", "topk"), (0, 2, "total", "topk"),
+                                   (2, 0, "extra", "topk"), (1, 8, "total", "dense"),
+                                   (0, 16, "extra", "topk")]:
+            _run(c, seed, k0, M, mode, score, layer=layer, label=f"tiny/s{seed}")
+
+
+def test_ffn_ragged_shapes():
+    for T, N, k, d, f, M in [(37, 40, 4, 96, 160, 20), (1, 16, 2, 64, 32, 2),
+                             (70, 24, 3, 128, 96, 24), (5, 8, 8, 32, 64, 8)]:
+        c = dict(N=N, k=k, d=d, f=f, T=T, logits="domains", Q=3)
+        _run(c, 0, 1, M, label=f"ragged T{T} d{d} f{f}")
+
+
+def test_ffn_qwen_full():
+    c = W.CONFIGS["qwen"]
+    layer = make_layer(c, 0)
+    for M in c["M_sweep"]:
+        _run(c, 0, 1, M, layer=layer, label=f"qwen M{M}")
+    _run(c, 0, 0, c["N"], "extra", layer=layer, label="qwen vanilla")
+
+
+def test_ffn_mixtral_sampled():
+    c = W.CONFIGS["mixtral"]
+    _run(c, 0, 1, 5, rows=[0, 7, 15], label="mixtral")
+
+
+def test_ffn_deepseek_t32_sampled():
+    c = W.CONFIGS["ds_t32"]
+    layer = make_layer(c, 0)
+    for M in (24, 48):
+        _run(c, 0, 1, M, rows=[0, 13, 31], layer=layer, label=f"ds_t32 M{M}")
+    del layer
+    torch.cuda.empty_cache()
+
+
+def test_ffn_spec_hier_sampled():
+    c = W.CONFIGS["spec"]
+    _run(c, 0, 1, 64, m_r=4, rows=[0, 1, 33, 63], label="spec")
+    torch.cuda.empty_cache()
+
+
+def test_ffn_reads_only_selected_experts_and_is_deterministic():
+    """Unselected experts' weights replaced by NaN: y must not change by a single bit."""
+    from paper_2602_07265_amd import xshare as X
+    c = W.CONFIGS["qwen"]
+    h, _, x, w1, w3, w2 = make_layer(c, 1)
+    hd = torch.from_numpy(h).to(DEV)
+    say("ffn case poisoned unselected experts")
+    a = X.moe_forward(x, hd, w1, w3, w2, 8, 1, 32)
+    b = X.moe_forward(x, hd, w1, w3, w2, 8, 1, 32)
+    torch.cuda.synchronize()
+    assert torch.equal(a["y"].view(torch.int16), b["y"].view(torch.int16))
+    unused = torch.ones(c["N"], dtype=torch.bool, device=DEV)
+    unused[a["ids"].long().reshape(-1)] = False
+    nan = torch.tensor(float("nan"), dtype=torch.bfloat16, device=DEV)
+    for m in (w1, w3, w2):
+        m[unused] = nan
+    p = X.moe_forward(x, hd, w1, w3, w2, 8, 1, 32)
+    torch.cuda.synchronize()
+    assert int(unused.sum()) > 0
+    assert torch.equal(a["y"].view(torch.int16), p["y"].view(torch.int16))
+
+
+def test_ffn_empty_batch():
+    from paper_2602_07265_amd import xshare as X
+    say("ffn case empty batch")
+    x = torch.empty((0, 64), dtype=torch.bfloat16, device=DEV)
+    w1 = torch.zeros((16, 128, 64), dtype=torch.bfloat16, device=DEV)
+    w2 = torch.zeros((16, 64, 128), dtype=torch.bfloat16, device=DEV)
+    res = X.moe_forward(x, torch.empty((0, 16), device=DEV), w1, w1, w2, 2, 1, 8)
+    torch.cuda.synchronize()
+    assert res["y"].shape == (0, 64) and int(res["sel_mask"].sum()) == 0
+
+
+def test_generator_identical_on_gpu_and_cpu():
+    say("generator cpu/gpu")
+    a = W.expert_matrix(3, "w2", 96, 64, 7, "cpu")
+    b = W.expert_matrix(3, "w2", 96, 64, 7, DEV).cpu()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))

@@ -1,0 +1,131 @@
+"""Selection parity on the GPU: the HIP path must equal the oracle bit for bit.
+
+Compared on every case: the selected-set mask, each token's routed experts (rank order),
+their fp32 gates (bitwise), and the statistics |S|, |active|, |U|, |S_0|, budget_eff.
+"""
+import numpy as np
+import pytest
+
+import workloads as W
+from helpers import assert_route_equal, gpu_route, oracle_route, say
+
+pytestmark = pytest.mark.gpu
+
+F32 = np.float32
+
+
+def _case(h, k, k0, M, mode="total", score="topk", offsets=None, m_r=0, label=""):
+    say(f"route case {label} T={h.shape[0]} N={h.shape[1]} k={k} k0={k0} M={M} {mode} {score}"
+        f"{'' if offsets is None else f' hier R={len(offsets) - 1} m_r={m_r}'}")
+    got = gpu_route(h, k, k0, M, mode, score, offsets, m_r)
+    ref = oracle_route(h, k, k0, M, mode, score, offsets, m_r)
+    assert_route_equal(got, ref, label)
+    return got
+
+
+@pytest.mark.parametrize("cfg", ["tiny", "mixtral", "qwen", "ds_t8", "ds_t32", "ds_iid_t32"])
+def test_route_parity_workloads(cfg):
+    c = W.CONFIGS[cfg]
+    for seed in range(8):
+        h, _ = W.make_logits(c, seed)
+        for k0 in sorted({0, 1, min(2, c["k"])}):
+            for M in c["M_sweep"]:
+                _case(h, c["k"], k0, M, "total", "topk", label=f"{cfg}/s{seed}")
+            for m in (0, 8):
+                _case(h, c["k"], k0, m, "extra", "topk", label=f"{cfg}/s{seed}")
+
+
+@pytest.mark.parametrize("cfg", ["tiny", "qwen", "ds_t32"])
+def test_route_parity_dense_scores(cfg):
+    c = W.CONFIGS[cfg]
+    for seed in range(3):
+        h, _ = W.make_logits(c, seed)
+        for k0 in (0, 1):
+            _case(h, c["k"], k0, c["M"], "total", "dense", label=f"{cfg}/dense/s{seed}")
+            _case(h, c["k"], k0, 4, "extra", "dense", label=f"{cfg}/dense/s{seed}")
+
+
+def test_route_vanilla_mode_equals_plain_topk():
+    c = W.CONFIGS["ds_t32"]
+    h, _ = W.make_logits(c, 0)
+    got = _case(h, 8, 0, 256, "extra", label="vanilla")
+    assert got["stats"][0] == got["stats"][2]        # |S| == |U|
+
+
+def test_route_adversarial_ties_and_signed_zero():
+    rng = np.random.default_rng(0)
+    for it in range(12):
+        T, N = int(rng.integers(1, 70)), int(rng.choice([8, 16, 33, 64, 100, 256]))
+        k = int(rng.integers(1, min(N, 9) + 1))
+        h = (np.round(rng.standard_normal((T, N)) * 3) / 4).astype(F32)
+        h[rng.random(h.shape) < 0.15] = F32(-0.0)
+        h[rng.random(h.shape) < 0.15] = F32(0.0)
+        M = int(rng.integers(k, N + 1))
+        _case(h, k, int(rng.integers(0, k + 1)), M, "total", label=f"ties{it}")
+        _case(h, k, int(rng.integers(0, k + 1)), int(rng.integers(0, 6)), "extra",
+              label=f"ties{it}")
+    h = np.zeros((16, 64), F32)                       # every logit equal
+    _case(h, 4, 1, 8, label="all-equal")
+    h = np.full((16, 64), -1.0e4, F32)                # gaps far beyond the exp underflow
+    h[np.arange(16), np.arange(16) * 3] = 0.0
+    h[np.arange(16), np.arange(16) * 3 + 1] = -50.0
+    _case(h, 4, 1, 20, label="underflow")
+    _case(h, 4, 0, 6, "extra", label="underflow")
+
+
+def test_route_shapes_edges():
+    rng = np.random.default_rng(1)
+    for T, N, k, M in [(0, 16, 2, 8), (1, 256, 8, 8), (37, 200, 6, 30), (5, 1024, 32, 100),
+                       (64, 8, 2, 5), (3, 1, 1, 1), (1024, 256, 8, 96), (2048, 64, 4, 16)]:
+        h = rng.standard_normal((T, N)).astype(F32)
+        _case(h, k, min(1, k), M, "total", label=f"edge T{T} N{N}")
+        _case(h, k, min(2, k), 3, "extra", label=f"edge T{T} N{N}")
+
+
+def test_hier_parity_spec_workload():
+    c = W.CONFIGS["spec"]
+    for seed in range(6):
+        h, off = W.make_logits(c, seed)
+        for k0 in (0, 1, 2):
+            for m_r in (0, 4, 5):
+                _case(h, 8, k0, 64, "total", offsets=off, m_r=m_r, label=f"spec/s{seed}")
+                _case(h, 8, k0, 40, "total", offsets=off, m_r=m_r, label=f"spec/s{seed}")
+                _case(h, 8, k0, 0, "extra", offsets=off, m_r=m_r, label=f"spec/s{seed}")
+        _case(h, 8, 1, 64, "total", "dense", offsets=off, m_r=4, label=f"spec/dense/s{seed}")
+
+
+def test_hier_parity_ragged_groupings():
+    rng = np.random.default_rng(2)
+    for it in range(16):
+        T = int(rng.integers(1, 80))
+        R = int(rng.integers(1, T + 1))
+        cuts = np.sort(rng.choice(np.arange(1, T), R - 1, replace=False)) if R > 1 else []
+        off = [0, *[int(c) for c in cuts], T]
+        N = int(rng.choice([16, 64, 128, 256]))
+        k = int(rng.integers(1, 9))
+        h = rng.standard_normal((T, N)).astype(F32)
+        if it % 3 == 0:
+            h = (np.round(h * 2) / 4).astype(F32)
+        _case(h, k, int(rng.integers(0, k + 1)), max(k, int(rng.integers(1, N + 1))), "total",
+              offsets=off, m_r=int(rng.integers(0, 6)), label=f"ragged{it}")
+        _case(h, k, int(rng.integers(0, k + 1)), int(rng.integers(0, 5)), "extra",
+              offsets=off, m_r=int(rng.integers(0, 6)), label=f"ragged{it}")
+
+
+def test_hier_invalid_device_offsets_yield_empty_selection():
+    h = W.logits_iid(8, 16, 0)
+    say("route case invalid device offsets")
+    got = gpu_route(h, 2, 1, 8, offsets=[0, 5, 3, 8], m_r=2, device_offsets_only=True)
+    assert got["stats"][0] == -1 and got["sel_mask"].sum() == 0
+    assert np.all(got["ids"] == -1)
+
+
+def test_route_is_deterministic():
+    c = W.CONFIGS["spec"]
+    h, off = W.make_logits(c, 9)
+    say("route determinism")
+    a = gpu_route(h, 8, 1, 64, offsets=off, m_r=4)
+    for _ in range(3):
+        b = gpu_route(h, 8, 1, 64, offsets=off, m_r=4)
+        for key in a:
+            assert np.array_equal(a[key], b[key])
