@@ -2,7 +2,9 @@
 // router scoring, batch scores, greedy selection (flat Algorithm 2 or per-request +
 // batch Algorithms 3-4), refinement, and the token permutation consumed by the expert
 // GEMMs.  One workgroup of 1024 threads does all of it: the whole problem is a few
-// thousand logits and is latency-, not throughput-bound.
+// thousand logits and is latency-, not throughput-bound, so the kernel avoids LDS round
+// trips in its inner loops: wave reductions use DPP, rankings compare packed integer keys,
+// and per-token lists are scanned eight entries per LDS read.
 //
 // Numerics: this translation unit is compiled with -ffp-contract=off; every fp32 step
 // of the gates is a separate IEEE round-to-nearest operation in a fixed order, so the
@@ -20,6 +22,7 @@ namespace {
 
 constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / 64;
+constexpr uint32_t kNoEntry = 0xFFFFu;   // empty slot of the per-token lists
 
 // exp(x) for x <= 0 in fp32: n = rint(x log2 e); r = (x - n ln2_hi) - n ln2_lo with a
 // 15-bit ln2_hi (Cody-Waite: n ln2_hi is exact); p = degree-7 Taylor polynomial of e^r
@@ -48,61 +51,82 @@ __device__ __forceinline__ float exp_fixed(float x) {
   return ldexpf(p, (int)n);
 }
 
-// Ranking key: larger value first, lower expert index first on equal values.
-__device__ __forceinline__ bool better(float ha, int ja, float hb, int jb) {
-  return ha > hb || (ha == hb && ja < jb);
+// Order-preserving map of finite fp32 values to uint32 (> 0); 0 marks "no value".
+__device__ __forceinline__ uint32_t ord(float h) {
+  const uint32_t b = __float_as_uint(h);
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+__device__ __forceinline__ float unord(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
 }
 
-__device__ __forceinline__ void wave_argmax(float& h, int& j) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    const float ho = __shfl_xor(h, off, 64);
-    const int jo = __shfl_xor(j, off, 64);
-    if (better(ho, jo, h, j)) {
-      h = ho;
-      j = jo;
-    }
-  }
+template <int Ctrl, int RowMask>
+__device__ __forceinline__ uint32_t dpp(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, Ctrl, RowMask, 0xF, false);
+}
+
+// Wave-wide max / min of a uint32 with DPP (quad swaps, row mirrors, row broadcasts);
+// lane 63 ends with the result, which is returned to every lane.
+__device__ __forceinline__ uint32_t wave_max(uint32_t v) {
+  v = max(v, dpp<0xB1, 0xF>(v));   // quad_perm [1,0,3,2]
+  v = max(v, dpp<0x4E, 0xF>(v));   // quad_perm [2,3,0,1]
+  v = max(v, dpp<0x141, 0xF>(v));  // row_half_mirror
+  v = max(v, dpp<0x140, 0xF>(v));  // row_mirror
+  v = max(v, dpp<0x142, 0xA>(v));  // row_bcast:15
+  v = max(v, dpp<0x143, 0xC>(v));  // row_bcast:31
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+__device__ __forceinline__ uint32_t wave_min(uint32_t v) {
+  v = min(v, dpp<0xB1, 0xF>(v));
+  v = min(v, dpp<0x4E, 0xF>(v));
+  v = min(v, dpp<0x141, 0xF>(v));
+  v = min(v, dpp<0x140, 0xF>(v));
+  v = min(v, dpp<0x142, 0xA>(v));
+  v = min(v, dpp<0x143, 0xC>(v));
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
 __device__ __forceinline__ float lane_value(float v, int lane) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
 }
 
-// Lane l holds the logits of experts l, l+64, ..., canonicalised (h + 0.0 maps -0.0 to +0.0).
+// One round of a wave-wide selection over keys held Q per lane (expert lane + 64 q):
+// returns the expert with the largest key, lowest index on equal keys (key 0 = not
+// available), removes it from its lane, and reports its key; -1 if nothing is left.
 template <int Q>
-__device__ __forceinline__ void load_row(const float* row, int N, int lane, float (&v)[Q]) {
+__device__ __forceinline__ int wave_pick(uint32_t (&key)[Q], int lane, uint32_t& kbest) {
+  uint32_t bk = 0;
+  uint32_t bj = 0xFFFFFFFFu;
 #pragma unroll
-  for (int q = 0; q < Q; ++q) {
-    const int j = lane + 64 * q;
-    v[q] = j < N ? row[j] + 0.0f : -INFINITY;
+  for (int q = 0; q < Q; ++q)
+    if (key[q] > bk) {  // strict: the lower q (lower index) wins inside a lane
+      bk = key[q];
+      bj = (uint32_t)(lane + 64 * q);
+    }
+  kbest = wave_max(bk);
+  const uint32_t jmin = wave_min((kbest != 0 && bk == kbest) ? bj : 0xFFFFFFFFu);
+  if (jmin == 0xFFFFFFFFu) return -1;
+  if ((int)(jmin & 63) == lane) {
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+      if (q == (int)(jmin >> 6)) key[q] = 0;
   }
+  return (int)jmin;
 }
 
-// The k best entries whose bit is set in `allowed` (bit q <-> expert lane + 64 q).
-// Lane r < k receives rank r: (value, expert) or (-inf, -1) if fewer than k are allowed.
+// Top-k of the available keys; lane r < k receives rank r as (logit, expert), or
+// (-inf, -1) if fewer than k are available.
 template <int Q>
-__device__ __forceinline__ void wave_topk(const float (&v)[Q], unsigned allowed, int k, int lane,
-                                          float& my_h, int& my_j) {
-  unsigned avail = allowed;
+__device__ __forceinline__ void wave_topk(uint32_t (&key)[Q], int k, int lane, float& my_h,
+                                          int& my_j) {
   my_h = -INFINITY;
   my_j = -1;
   for (int r = 0; r < k; ++r) {
-    float bh = -INFINITY;
-    int bj = INT_MAX;
-#pragma unroll
-    for (int q = 0; q < Q; ++q) {
-      const int j = lane + 64 * q;
-      if (((avail >> q) & 1u) && better(v[q], j, bh, bj)) {
-        bh = v[q];
-        bj = j;
-      }
-    }
-    wave_argmax(bh, bj);
-    if (bj != INT_MAX && (bj & 63) == lane) avail &= ~(1u << (bj >> 6));
-    if (lane == r) {
-      my_h = bh;
-      my_j = bj == INT_MAX ? -1 : bj;
+    uint32_t kb;
+    const int jb = wave_pick<Q>(key, lane, kb);
+    if (lane == r && jb >= 0) {
+      my_h = unord(kb);
+      my_j = jb;
     }
   }
 }
@@ -115,6 +139,18 @@ __device__ __forceinline__ float ranked_gate(float my_h, int lane, int k) {
   float z = 0.0f;
   for (int r = 0; r < k; ++r) z = z + lane_value(e, r);
   return lane < k ? e / z : 0.0f;
+}
+
+// Canonicalised logits of one token as keys (h + 0.0 maps -0.0 to +0.0).
+template <int Q>
+__device__ __forceinline__ void row_keys(const float* row, int N, int lane, float (&v)[Q],
+                                         uint32_t (&key)[Q]) {
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int j = lane + 64 * q;
+    v[q] = j < N ? row[j] + 0.0f : 0.0f;
+    key[q] = j < N ? ord(v[q]) : 0u;
+  }
 }
 
 // Block-wide exclusive prefix sum of one int per thread; every thread must call it.
@@ -141,14 +177,15 @@ __device__ int block_excl_scan(int v, int* s_wsum, int& total) {
   return pre + inc - v;
 }
 
+// Per-token list entry: bits 0-9 expert, bits 10-14 rank; kNoEntry = empty.
+__device__ __forceinline__ bool entry_is(uint32_t ent, int j) { return (ent & 0x83FFu) == (uint32_t)j; }
+
 template <int Q>
 __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
-  __shared__ uint16_t s_id[kMaxAssignments];   // per (token, rank): vanilla, later refined expert
-  __shared__ float s_g[kMaxAssignments];       // per (token, rank): vanilla gate
-  __shared__ float s_score[kMaxExperts];       // batch score s_j
-  __shared__ float s_rscore[kMaxExperts];      // per-request score s^r_j
-  __shared__ uint8_t s_tier[kMaxExperts];
-  __shared__ uint8_t s_cand[kMaxExperts];
+  __shared__ __align__(16) uint16_t s_ent[kMaxAssignments];  // (token, rank) -> expert | rank
+  __shared__ float s_g[kMaxAssignments];                     // vanilla gate of that entry
+  __shared__ __align__(16) uint64_t s_key[kMaxExperts];      // greedy order key per expert
+  __shared__ uint8_t s_tier1[kMaxExperts];                   // picked by some request
   __shared__ uint8_t s_sel[kMaxExperts];
   __shared__ int s_wsum[kWaves];
   __shared__ int s_cnt[8];
@@ -160,8 +197,11 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   const bool dense = a.score_mode == 1;
   const bool hier = a.req_offsets != nullptr;
   const int TK = T * k;
+  const int TK8 = (TK + 7) & ~7;
 
   if (tid < 8) s_cnt[tid] = 0;
+  for (int j = tid; j < kMaxExperts; j += kThreads) s_tier1[j] = 0;
+  for (int p = TK + tid; p < TK8; p += kThreads) s_ent[p] = (uint16_t)kNoEntry;
   __syncthreads();
 
   // ---- request offsets must be 0 = o_0 < o_1 < ... < o_R = T (checked in parallel)
@@ -193,20 +233,17 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
     }
   }
 
-  // ---- (a) per token: plain top-k, its gates (Section 2.2); dense softmax if requested
+  // ---- (a) per token: plain top-k and its gates (Section 2.2); dense softmax if requested
   for (int i = wave; i < T; i += kWaves) {
     float v[Q];
-    load_row<Q>(a.logits + (size_t)i * N, N, lane, v);
-    unsigned all = 0;
-#pragma unroll
-    for (int q = 0; q < Q; ++q)
-      if (lane + 64 * q < N) all |= 1u << q;
+    uint32_t key[Q];
+    row_keys<Q>(a.logits + (size_t)i * N, N, lane, v, key);
     float my_h;
     int my_j;
-    wave_topk<Q>(v, all, k, lane, my_h, my_j);
+    wave_topk<Q>(key, k, lane, my_h, my_j);
     const float g = ranked_gate(my_h, lane, k);
     if (lane < k) {
-      s_id[i * k + lane] = (uint16_t)my_j;
+      s_ent[i * k + lane] = (uint16_t)(my_j < 0 ? kNoEntry : (uint32_t)((lane << 10) | my_j));
       s_g[i * k + lane] = g;
     }
     if (dense) {
@@ -227,78 +264,101 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   }
   __syncthreads();
 
-  // ---- (b) per expert: batch score, membership of U and S_0 (Eq. (2), Algorithm 2)
+  // ---- (b) per expert: batch score (ascending tokens), membership of U and S_0
   const int j = tid;
   float s = 0.0f;
   bool inU = false, inS0 = false;
   if (j < N) {
-    for (int i = 0; i < T; ++i) {
-      for (int r = 0; r < k; ++r) {
-        if (s_id[i * k + r] == j) {
+    const uint4* ents = reinterpret_cast<const uint4*>(s_ent);
+    for (int vb = 0; vb < TK8 / 8; ++vb) {
+      const uint4 e4 = ents[vb];
+      const uint32_t w4[4] = {e4.x, e4.y, e4.z, e4.w};
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint32_t ent = (w4[u >> 1] >> (16 * (u & 1))) & 0xFFFFu;
+        if (entry_is(ent, j)) {
           inU = true;
-          if (r < k0) inS0 = true;
-          if (!dense) s = s + s_g[i * k + r];
+          if ((int)((ent >> 10) & 31u) < k0) inS0 = true;
+          if (!dense) s = s + s_g[vb * 8 + u];
         }
       }
-      if (dense) s = s + a.dense[(size_t)i * N + j];
     }
+    if (dense)
+      for (int i = 0; i < T; ++i) s = s + a.dense[(size_t)i * N + j];
   }
 
-  // ---- (c) per request (Algorithm 3): S_0(r) plus the m_r best remaining experts of r
-  bool tier1 = false;
+  // ---- (c) per request (Algorithm 3), one wave per request: S_0(r) plus the m_r best
+  //      remaining experts of r under the request's own score
   if (hier && a.m_r > 0) {
-    for (int r = 0; r < a.R; ++r) {
+    for (int r = wave; r < a.R; r += kWaves) {
       const int lo = a.req_offsets[r], hi = a.req_offsets[r + 1];
-      float sr = 0.0f;
-      bool inUr = false, inS0r = false;
-      if (j < N) {
-        for (int i = lo; i < hi; ++i) {
-          for (int q = 0; q < k; ++q) {
-            if (s_id[i * k + q] == j) {
-              inUr = true;
-              if (q < k0) inS0r = true;
-              if (!dense) sr = sr + s_g[i * k + q];
-            }
+      float sr[Q];
+      unsigned inUr = 0, inS0r = 0;
+#pragma unroll
+      for (int q = 0; q < Q; ++q) sr[q] = 0.0f;
+      for (int p = lo * k; p < hi * k; ++p) {
+        const uint32_t ent = s_ent[p];
+        if (ent == kNoEntry || (int)(ent & 63u) != lane) continue;
+        const int qe = (int)((ent & 1023u) >> 6);
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+          if (q == qe) {
+            inUr |= 1u << q;
+            if ((int)((ent >> 10) & 31u) < k0) inS0r |= 1u << q;
+            if (!dense) sr[q] = sr[q] + s_g[p];
           }
-          if (dense) sr = sr + a.dense[(size_t)i * N + j];
         }
-        s_rscore[j] = sr;
-        s_cand[j] = (dense || inUr) && !inS0r;
       }
-      __syncthreads();
-      if (j < N && s_cand[j]) {
-        int rank = 0;
-        for (int jj = 0; jj < N && rank < a.m_r; ++jj)
-          if (s_cand[jj] && better(s_rscore[jj], jj, sr, j)) ++rank;
-        if (rank < a.m_r) tier1 = true;
+      if (dense)
+        for (int i = lo; i < hi; ++i)
+#pragma unroll
+          for (int q = 0; q < Q; ++q)
+            if (lane + 64 * q < N) sr[q] = sr[q] + a.dense[(size_t)i * N + lane + 64 * q];
+      uint32_t key[Q];
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        const bool cand = (lane + 64 * q < N) && (dense || ((inUr >> q) & 1u)) &&
+                          !((inS0r >> q) & 1u);
+        key[q] = cand ? ord(sr[q]) : 0u;
       }
-      __syncthreads();
+      for (int t = 0; t < a.m_r; ++t) {
+        uint32_t kb;
+        const int jb = wave_pick<Q>(key, lane, kb);
+        if (jb < 0) break;
+        if (lane == 0) s_tier1[jb] = 1;
+      }
     }
   }
+  __syncthreads();
 
   // ---- (d) batch greedy (Algorithm 1 with a fixed budget; Algorithm 4's final stage):
   //      order (tier, score desc, index asc), keep the first budget_eff candidates.
+  //      Key: (3 - tier) << 42 | ord(score) << 10 | (1023 - j); 0 = not a candidate.
   int tier = 3;
+  uint64_t mykey = 0;
   if (j < N) {
     const bool cand = dense ? (T > 0) : inU;
-    tier = inS0 ? 0 : (tier1 ? 1 : (cand ? 2 : 3));
-    s_tier[j] = (uint8_t)tier;
-    s_score[j] = s;
+    tier = inS0 ? 0 : (s_tier1[j] ? 1 : (cand ? 2 : 3));
+    if (tier < 3)
+      mykey = ((uint64_t)(3 - tier) << 42) | ((uint64_t)ord(s) << 10) | (uint64_t)(1023 - j);
     if (tier < 3) atomicAdd(&s_cnt[0], 1);
     if (tier == 0) atomicAdd(&s_cnt[1], 1);
     if (tier <= 1) atomicAdd(&s_cnt[2], 1);
     if (inU) atomicAdd(&s_cnt[3], 1);
   }
+  if (j < kMaxExperts) s_key[j] = mykey;
   __syncthreads();
   const int n_cand = s_cnt[0], n_s0 = s_cnt[1], n_start = s_cnt[2], n_u = s_cnt[3];
   const int base = a.budget_mode == 0 ? a.budget : n_start + a.budget;
   const int m_eff = max(min(base, n_cand), min(k, n_cand));
   bool sel = false;
-  if (j < N && tier < 3) {
+  if (mykey != 0) {
+    const ulonglong2* keys2 = reinterpret_cast<const ulonglong2*>(s_key);
     int rank = 0;
-    for (int jj = 0; jj < N && rank < m_eff; ++jj) {
-      const int tj = s_tier[jj];
-      if (tj < tier || (tj == tier && better(s_score[jj], jj, s, j))) ++rank;
+    const int n2 = (N + 1) >> 1;
+    for (int jj = 0; jj < n2; ++jj) {
+      const ulonglong2 kk = keys2[jj];
+      rank += (kk.x > mykey) + (kk.y > mykey);
     }
     sel = rank < m_eff;
   }
@@ -312,29 +372,36 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   // ---- (e) refinement: every token to its top-k inside S, gates renormalised (Section 3.4)
   for (int i = wave; i < T; i += kWaves) {
     float v[Q];
-    load_row<Q>(a.logits + (size_t)i * N, N, lane, v);
-    unsigned allowed = 0;
+    uint32_t key[Q];
+    row_keys<Q>(a.logits + (size_t)i * N, N, lane, v, key);
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
       const int jq = lane + 64 * q;
-      if (jq < N && s_sel[jq]) allowed |= 1u << q;
+      if (jq >= N || !s_sel[jq]) key[q] = 0;
     }
     float my_h;
     int my_j;
-    wave_topk<Q>(v, allowed, k, lane, my_h, my_j);
+    wave_topk<Q>(key, k, lane, my_h, my_j);
     const float g = ranked_gate(my_h, lane, k);
     if (lane < k) {
       a.ids[i * k + lane] = my_j;
       a.w[i * k + lane] = g;
-      s_id[i * k + lane] = (uint16_t)my_j;
+      s_ent[i * k + lane] = (uint16_t)(my_j < 0 ? kNoEntry : (uint32_t)((lane << 10) | my_j));
     }
   }
   __syncthreads();
 
   // ---- (f) permutation: rows grouped by expert (ascending), tokens ascending inside
   int cnt = 0;
-  if (j < N)
-    for (int p = 0; p < TK; ++p) cnt += s_id[p] == j;
+  if (j < N) {
+    const uint4* ents = reinterpret_cast<const uint4*>(s_ent);
+    for (int vb = 0; vb < TK8 / 8; ++vb) {
+      const uint4 e4 = ents[vb];
+      const uint32_t w4[4] = {e4.x, e4.y, e4.z, e4.w};
+#pragma unroll
+      for (int u = 0; u < 8; ++u) cnt += entry_is((w4[u >> 1] >> (16 * (u & 1))) & 0xFFFFu, j);
+    }
+  }
   int total = 0;
   const int off = block_excl_scan(cnt, s_wsum, total);
   int n_active = 0;
@@ -342,10 +409,18 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   if (j < N) {
     a.offsets[j] = off;
     if (j == N - 1) a.offsets[N] = off + cnt;
-    if (cnt > 0) a.active[arank] = j;
-    int pos = off;
-    for (int p = 0; p < TK && pos < off + cnt; ++p)
-      if (s_id[p] == j) a.perm[pos++] = p;
+    if (cnt > 0) {
+      a.active[arank] = j;
+      const uint4* ents = reinterpret_cast<const uint4*>(s_ent);
+      int pos = off;
+      for (int vb = 0; vb < TK8 / 8; ++vb) {
+        const uint4 e4 = ents[vb];
+        const uint32_t w4[4] = {e4.x, e4.y, e4.z, e4.w};
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (entry_is((w4[u >> 1] >> (16 * (u & 1))) & 0xFFFFu, j)) a.perm[pos++] = vb * 8 + u;
+      }
+    }
   }
   if (tid == 0) {
     a.counters[kCntActive] = n_active;
