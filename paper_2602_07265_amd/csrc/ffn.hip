@@ -42,10 +42,14 @@ __device__ __forceinline__ uint16_t to_bf16(float v) {
 
 // One pass of a wave over the reduction dimension K for up to kTiles token tiles:
 // acc[m][rt] += A_rt (16 x K) * B_m^T (K x 16) for the NM weight matrices B_m.
-// `arow[rt]` points at the token row this lane feeds (any valid row for padding lanes,
-// whose output rows are discarded), `brow[m]` at the weight row of this lane's column;
-// both already offset by this lane's group position g * 8U.
-template <int U, int NM>
+// `arow[rt]` points at the token row this lane feeds (a duplicate of a valid row for
+// padding lanes, whose output rows are discarded; duplicate addresses coalesce, which
+// measured faster than masking those lanes), `brow[m]` at the weight row of this lane's
+// column;
+// both already offset by this lane's group position g * 8U.  Weight loads (HBM) run one
+// step ahead; token loads (L2-resident) are issued either one step ahead too (ADBL) or
+// at the top of their own step, which halves their register footprint.
+template <int U, int NM, bool ADBL>
 __device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[kTiles], int nt,
                                           const uint16_t* const (&brow)[NM], int K,
                                           floatx4 (&acc)[NM][kTiles]) {
@@ -55,25 +59,36 @@ __device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[kTiles],
   for (int m = 0; m < NM; ++m)
 #pragma unroll
     for (int u = 0; u < U; ++u) b[m][u] = load8(brow[m] + 8 * u);
+  if (ADBL) {
 #pragma unroll
-  for (int rt = 0; rt < kTiles; ++rt)
-    if (rt < nt)
+    for (int rt = 0; rt < kTiles; ++rt)
+      if (rt < nt)
 #pragma unroll
-      for (int u = 0; u < U; ++u) x[rt][u] = load8(arow[rt] + 8 * u);
+        for (int u = 0; u < U; ++u) x[rt][u] = load8(arow[rt] + 8 * u);
+  }
 
-  for (int kb = KB; kb <= K; kb += KB) {
-    bf16x8 nb[NM][U], nx[kTiles][U];
-    const bool more = kb < K;
+  for (int kb = 0; kb < K; kb += KB) {
+    bf16x8 nb[NM][U], nx[ADBL ? kTiles : 1][U];
+    const bool more = kb + KB < K;
     if (more) {
 #pragma unroll
       for (int m = 0; m < NM; ++m)
 #pragma unroll
-        for (int u = 0; u < U; ++u) nb[m][u] = load8(brow[m] + kb + 8 * u);
+        for (int u = 0; u < U; ++u) nb[m][u] = load8(brow[m] + kb + KB + 8 * u);
+      if (ADBL) {
+#pragma unroll
+        for (int rt = 0; rt < kTiles; ++rt)
+          if (rt < nt)
+#pragma unroll
+            for (int u = 0; u < U; ++u) nx[rt][u] = load8(arow[rt] + kb + KB + 8 * u);
+      }
+    }
+    if (!ADBL) {
 #pragma unroll
       for (int rt = 0; rt < kTiles; ++rt)
         if (rt < nt)
 #pragma unroll
-          for (int u = 0; u < U; ++u) nx[rt][u] = load8(arow[rt] + kb + 8 * u);
+          for (int u = 0; u < U; ++u) x[rt][u] = load8(arow[rt] + kb + 8 * u);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u)
@@ -87,13 +102,32 @@ __device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[kTiles],
       for (int m = 0; m < NM; ++m)
 #pragma unroll
         for (int u = 0; u < U; ++u) b[m][u] = nb[m][u];
+      if (ADBL) {
 #pragma unroll
-      for (int rt = 0; rt < kTiles; ++rt)
+        for (int rt = 0; rt < kTiles; ++rt)
 #pragma unroll
-        for (int u = 0; u < U; ++u) x[rt][u] = nx[rt][u];
+          for (int u = 0; u < U; ++u) x[rt][u] = nx[ADBL ? rt : 0][u];
+      }
     }
   }
 }
+
+// Unroll (32-element k-groups per step) and token-operand buffering of the two GEMMs.
+#ifndef XS_GATE_UP_U
+#define XS_GATE_UP_U 4
+#endif
+#ifndef XS_GATE_UP_ADBL
+#define XS_GATE_UP_ADBL 1
+#endif
+#ifndef XS_DOWN_U
+#define XS_DOWN_U 8
+#endif
+#ifndef XS_DOWN_ADBL
+#define XS_DOWN_ADBL 0
+#endif
+#ifndef XS_DOWN_NM
+#define XS_DOWN_NM 2
+#endif
 
 template <int U>
 __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
@@ -123,7 +157,7 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
     for (int m = 0; m < 2; ++m)
 #pragma unroll
       for (int rt = 0; rt < kTiles; ++rt) acc[m][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    wave_pass<U, 2>(arow, nt, brow, d, acc);
+    wave_pass<U, 2, XS_GATE_UP_ADBL != 0>(arow, nt, brow, d, acc);
 #pragma unroll
     for (int rt = 0; rt < kTiles; ++rt) {
       if (rt >= nt) break;
@@ -142,17 +176,21 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
 
 template <int U>
 __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
+  constexpr int NM = XS_DOWN_NM;  // 16-row tiles of W2 per wave, sharing the token operand
   const int slot = blockIdx.y;
   if (slot >= a.counters[kCntActive]) return;
   const int e = a.active[slot];
   const int p0 = a.offsets[e];
   const int te = a.offsets[e + 1] - p0;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int n0 = (blockIdx.x * kWaves + wave) * kCols;
+  const int n0 = (blockIdx.x * kWaves + wave) * kCols * NM;
   if (n0 >= a.d) return;
   const int n = lane & 15, g = lane >> 4;
   const int d = a.d, f = a.f;
-  const uint16_t* const brow[1] = {a.w2 + ((size_t)e * d + n0 + n) * f + (size_t)g * 8 * U};
+  const uint16_t* brow[NM];
+#pragma unroll
+  for (int m = 0; m < NM; ++m)
+    brow[m] = a.w2 + ((size_t)e * d + min(n0 + 16 * m, d - 16) + n) * f + (size_t)g * 8 * U;
 
   for (int c0 = 0; c0 < te; c0 += 16 * kTiles) {
     const int nt = min(kTiles, (te - c0 + 15) / 16);
@@ -162,17 +200,24 @@ __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
       const int t = min(c0 + rt * 16 + n, te - 1);
       arow[rt] = a.h + (size_t)(p0 + t) * f + (size_t)g * 8 * U;
     }
-    floatx4 acc[1][kTiles];
+    floatx4 acc[NM][kTiles];
 #pragma unroll
-    for (int rt = 0; rt < kTiles; ++rt) acc[0][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    wave_pass<U, 1>(arow, nt, brow, f, acc);
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int rt = 0; rt < kTiles; ++rt) acc[m][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    wave_pass<U, NM, XS_DOWN_ADBL != 0>(arow, nt, brow, f, acc);
 #pragma unroll
     for (int rt = 0; rt < kTiles; ++rt) {
       if (rt >= nt) break;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int t = c0 + rt * 16 + 4 * g + i;
-        if (t < te) a.yslot[(size_t)a.perm[p0 + t] * d + n0 + n] = acc[0][rt][i];
+        if (t < te) {
+          float* yrow = a.yslot + (size_t)a.perm[p0 + t] * d;
+#pragma unroll
+          for (int m = 0; m < NM; ++m)
+            if (n0 + 16 * m < d) yrow[n0 + 16 * m + n] = acc[m][rt][i];
+        }
       }
     }
   }
@@ -198,13 +243,18 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(FfnArgs a) {
   *reinterpret_cast<uint2*>(a.y + (size_t)i * a.d + c) = make_uint2(lo, hi);
 }
 
-int unroll_for(int K) { return (K % 128 == 0) ? 4 : (K % 64 == 0) ? 2 : 1; }
+int unroll_for(int K, int want) {
+  for (int u = want; u > 1; u >>= 1)
+    if (K % (32 * u) == 0) return u;
+  return 1;
+}
 
 }  // namespace
 
 hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
   const dim3 grid((a.f + kWaves * kCols - 1) / (kWaves * kCols), a.max_active), block(kBlock);
-  switch (unroll_for(a.d)) {
+  switch (unroll_for(a.d, XS_GATE_UP_U)) {
+    case 8: hipLaunchKernelGGL(gate_up_kernel<8>, grid, block, 0, stream, a); break;
     case 4: hipLaunchKernelGGL(gate_up_kernel<4>, grid, block, 0, stream, a); break;
     case 2: hipLaunchKernelGGL(gate_up_kernel<2>, grid, block, 0, stream, a); break;
     default: hipLaunchKernelGGL(gate_up_kernel<1>, grid, block, 0, stream, a); break;
@@ -213,8 +263,10 @@ hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_down(const FfnArgs& a, hipStream_t stream) {
-  const dim3 grid((a.d + kWaves * kCols - 1) / (kWaves * kCols), a.max_active), block(kBlock);
-  switch (unroll_for(a.f)) {
+  constexpr int cols = kWaves * kCols * XS_DOWN_NM;
+  const dim3 grid((a.d + cols - 1) / cols, a.max_active), block(kBlock);
+  switch (unroll_for(a.f, XS_DOWN_U)) {
+    case 8: hipLaunchKernelGGL(down_kernel<8>, grid, block, 0, stream, a); break;
     case 4: hipLaunchKernelGGL(down_kernel<4>, grid, block, 0, stream, a); break;
     case 2: hipLaunchKernelGGL(down_kernel<2>, grid, block, 0, stream, a); break;
     default: hipLaunchKernelGGL(down_kernel<1>, grid, block, 0, stream, a); break;

@@ -1,0 +1,69 @@
+"""Workload driver for hardware-counter profiling of the expert GEMMs.
+
+    rocprofv3 --pmc FETCH_SIZE -d OUT -o fetch --output-format csv -- \
+        python -m paper_2602_07265_amd.profiling
+    rocprofv3 --pmc WRITE_SIZE -d OUT -o write --output-format csv -- \
+        python -m paper_2602_07265_amd.profiling
+
+Runs the DeepSeek-R1-shaped layer (N=256, k=8, d=7168, f=2048, T=32 tokens, total budget
+48, warm-up 1; seeded domain-centroid logits) for --calls calls over rotating batches, then
+a plain device-to-device copy of --copy-mib MiB (torch's copy kernel) --copies times.  The
+copy reads and writes a known number of bytes, so it calibrates what the counters report
+per byte.  Prints, per batch, the active experts and the algorithmic bytes of one gate/up
+launch (weights of the active experts, x, H) to compare with the counters.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--calls", type=int, default=8)
+    ap.add_argument("--batches", type=int, default=8)
+    ap.add_argument("--copy-mib", type=int, default=1024)
+    ap.add_argument("--copies", type=int, default=4)
+    ap.add_argument("--budget", type=int, default=48)
+    args = ap.parse_args()
+
+    import torch
+
+    import workloads as W
+    from paper_2602_07265_amd import xshare as X
+
+    dev = "cuda:0"
+    c = W.CONFIGS["ds_t32"]
+    T, N, k, d, f, k0, M = c["T"], c["N"], c["k"], c["d"], c["f"], c["k0"], args.budget
+    w1, w3, w2 = W.expert_weights(N, d, f, 0, dev)
+    logits = [torch.from_numpy(W.logits_domains(T, N, c["Q"], s)).to(dev) for s in range(args.batches)]
+    xs = [W.activations(T, d, s, dev) for s in range(args.batches)]
+    p = X.params(N, k, k0, M)
+    ws = torch.empty(X.moe_workspace_bytes(T, d, f, p), dtype=torch.uint8, device=dev)
+    y = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+    per_call = []
+    for s in range(args.calls):
+        b = s % args.batches
+        r = X.moe_forward(xs[b], logits[b], w1, w3, w2, k, k0, M, y=y, workspace=ws)
+        st = X.stats_dict(r["stats"])
+        per_call.append({"call": s, "n_active": st["n_active"],
+                         "gate_up_bytes": st["n_active"] * 2 * f * d * 2 + T * d * 2 + T * k * f * 2,
+                         "down_bytes": st["n_active"] * f * d * 2 + T * k * f * 2 + T * k * d * 4})
+    nbytes = args.copy_mib << 20
+    src = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(args.copies):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"workload": f"ds_t32 M={M}", "copy_bytes": nbytes, "calls": per_call}))
+
+
+if __name__ == "__main__":
+    main()
