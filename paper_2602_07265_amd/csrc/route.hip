@@ -4,7 +4,8 @@
 // GEMMs.  One workgroup of 1024 threads does all of it: the whole problem is a few
 // thousand logits and is latency-, not throughput-bound, so the kernel avoids LDS round
 // trips in its inner loops: wave reductions use DPP, rankings compare packed integer keys,
-// and per-token lists are scanned eight entries per LDS read.
+// and for decode-sized batches (T <= 64) a token bitmask per expert turns every
+// per-expert gather into popcounts.
 //
 // Numerics: this translation unit is compiled with -ffp-contract=off; every fp32 step
 // of the gates is a separate IEEE round-to-nearest operation in a fixed order, so the
@@ -93,6 +94,8 @@ __device__ __forceinline__ float lane_value(float v, int lane) {
 // One round of a wave-wide selection over keys held Q per lane (expert lane + 64 q):
 // returns the expert with the largest key, lowest index on equal keys (key 0 = not
 // available), removes it from its lane, and reports its key; -1 if nothing is left.
+// Usually one lane holds the maximum and a ballot finds it; equal maxima in several
+// lanes take a second (min-index) reduction.
 template <int Q>
 __device__ __forceinline__ int wave_pick(uint32_t (&key)[Q], int lane, uint32_t& kbest) {
   uint32_t bk = 0;
@@ -104,8 +107,13 @@ __device__ __forceinline__ int wave_pick(uint32_t (&key)[Q], int lane, uint32_t&
       bj = (uint32_t)(lane + 64 * q);
     }
   kbest = wave_max(bk);
-  const uint32_t jmin = wave_min((kbest != 0 && bk == kbest) ? bj : 0xFFFFFFFFu);
-  if (jmin == 0xFFFFFFFFu) return -1;
+  if (kbest == 0) return -1;
+  const uint64_t holders = __ballot(bk == kbest);
+  uint32_t jmin;
+  if (__popcll(holders) == 1)
+    jmin = (uint32_t)__builtin_amdgcn_readlane((int)bj, __ffsll((long long)holders) - 1);
+  else
+    jmin = wave_min(bk == kbest ? bj : 0xFFFFFFFFu);
   if ((int)(jmin & 63) == lane) {
 #pragma unroll
     for (int q = 0; q < Q; ++q)
@@ -114,17 +122,20 @@ __device__ __forceinline__ int wave_pick(uint32_t (&key)[Q], int lane, uint32_t&
   return (int)jmin;
 }
 
-// Top-k of the available keys; lane r < k receives rank r as (logit, expert), or
-// (-inf, -1) if fewer than k are available.
+// Ranks [r0, k) of the available keys; lane r receives rank r as (logit, expert), or
+// (-inf, -1) if fewer are available.  Lanes below r0 keep what they hold.
 template <int Q>
-__device__ __forceinline__ void wave_topk(uint32_t (&key)[Q], int k, int lane, float& my_h,
-                                          int& my_j) {
-  my_h = -INFINITY;
-  my_j = -1;
-  for (int r = 0; r < k; ++r) {
+__device__ __forceinline__ void wave_topk(uint32_t (&key)[Q], int r0, int k, int lane,
+                                          float& my_h, int& my_j) {
+  if (lane >= r0) {
+    my_h = -INFINITY;
+    my_j = -1;
+  }
+  for (int r = r0; r < k; ++r) {
     uint32_t kb;
     const int jb = wave_pick<Q>(key, lane, kb);
-    if (lane == r && jb >= 0) {
+    if (jb < 0) break;
+    if (lane == r) {
       my_h = unord(kb);
       my_j = jb;
     }
@@ -179,14 +190,56 @@ __device__ int block_excl_scan(int v, int* s_wsum, int& total) {
 
 // Per-token list entry: bits 0-9 expert, bits 10-14 rank; kNoEntry = empty.
 __device__ __forceinline__ bool entry_is(uint32_t ent, int j) { return (ent & 0x83FFu) == (uint32_t)j; }
+__device__ __forceinline__ uint32_t entry_at(const uint4& v, int u) {
+  const uint32_t w = u < 2 ? v.x : u < 4 ? v.y : u < 6 ? v.z : v.w;
+  return (w >> (16 * (u & 1))) & 0xFFFFu;
+}
+
+// Batches of up to this many tokens keep one token bitmask per expert, which turns the
+// per-expert gathers (scores, per-request scores, permutation) into popcounts.
+constexpr int kOccTokens = 64;
+
+__device__ __forceinline__ uint64_t below(int i) { return i >= 64 ? ~0ull : ((1ull << i) - 1ull); }
+
+// Groups the entries by expert (ascending), tokens ascending inside: s_off[e] is the start
+// of expert e's run in s_list, which holds entry indices p = i * k + r.  Needs T <= 64 and
+// s_occ zeroed; every thread must call.  Returns this thread's expert count (j = tid < N).
+__device__ int group_by_expert(const uint16_t* s_ent, uint64_t* s_occ, int* s_off,
+                               uint16_t* s_list, int* s_wsum, int TK, int k, int N, int& total) {
+  const int tid = threadIdx.x;
+  for (int p = tid; p < TK; p += kThreads) {
+    const uint32_t ent = s_ent[p];
+    if (ent != kNoEntry) atomicOr(reinterpret_cast<unsigned long long*>(&s_occ[ent & 1023u]),
+                                  1ull << (p / k));
+  }
+  __syncthreads();
+  const int cnt = tid < N ? __popcll(s_occ[tid]) : 0;
+  const int off = block_excl_scan(cnt, s_wsum, total);
+  if (tid < N) s_off[tid] = off;
+  if (tid == N - 1) s_off[N] = off + cnt;
+  __syncthreads();
+  for (int p = tid; p < TK; p += kThreads) {
+    const uint32_t ent = s_ent[p];
+    if (ent == kNoEntry) continue;
+    const int e = (int)(ent & 1023u);
+    s_list[s_off[e] + __popcll(s_occ[e] & below(p / k))] = (uint16_t)p;
+  }
+  __syncthreads();
+  return cnt;
+}
 
 template <int Q>
 __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   __shared__ __align__(16) uint16_t s_ent[kMaxAssignments];  // (token, rank) -> expert | rank
   __shared__ float s_g[kMaxAssignments];                     // vanilla gate of that entry
-  __shared__ __align__(16) uint64_t s_key[kMaxExperts];      // greedy order key per expert
+  __shared__ uint16_t s_list[kMaxAssignments];               // entries grouped by expert
+  __shared__ __align__(16) uint64_t s_occ[kMaxExperts];      // token bitmask per expert
+  __shared__ __align__(16) uint64_t s_key[kMaxExperts];      // greedy keys of the candidates
+  __shared__ int s_off[kMaxExperts + 1];
   __shared__ uint8_t s_tier1[kMaxExperts];                   // picked by some request
   __shared__ uint8_t s_sel[kMaxExperts];
+  __shared__ uint32_t s_seed[kWaves][kMaxTopK];              // refinement seeds per wave
+  __shared__ float s_seed_h[kWaves][kMaxTopK];
   __shared__ int s_wsum[kWaves];
   __shared__ int s_cnt[8];
 
@@ -196,11 +249,15 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   const int T = a.T, N = a.N, k = a.k, k0 = a.k0;
   const bool dense = a.score_mode == 1;
   const bool hier = a.req_offsets != nullptr;
+  const bool occ = T <= kOccTokens;
   const int TK = T * k;
   const int TK8 = (TK + 7) & ~7;
 
   if (tid < 8) s_cnt[tid] = 0;
-  for (int j = tid; j < kMaxExperts; j += kThreads) s_tier1[j] = 0;
+  for (int j = tid; j < kMaxExperts; j += kThreads) {
+    s_tier1[j] = 0;
+    s_occ[j] = 0;
+  }
   for (int p = TK + tid; p < TK8; p += kThreads) s_ent[p] = (uint16_t)kNoEntry;
   __syncthreads();
 
@@ -240,7 +297,7 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
     row_keys<Q>(a.logits + (size_t)i * N, N, lane, v, key);
     float my_h;
     int my_j;
-    wave_topk<Q>(key, k, lane, my_h, my_j);
+    wave_topk<Q>(key, 0, k, lane, my_h, my_j);
     const float g = ranked_gate(my_h, lane, k);
     if (lane < k) {
       s_ent[i * k + lane] = (uint16_t)(my_j < 0 ? kNoEntry : (uint32_t)((lane << 10) | my_j));
@@ -268,14 +325,25 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   const int j = tid;
   float s = 0.0f;
   bool inU = false, inS0 = false;
-  if (j < N) {
+  if (occ) {
+    int total;
+    const int cnt = group_by_expert(s_ent, s_occ, s_off, s_list, s_wsum, TK, k, N, total);
+    if (j < N) {
+      const int o = s_off[j];
+      for (int q = 0; q < cnt; ++q) {
+        const int p = s_list[o + q];
+        if (!dense) s = s + s_g[p];
+        if ((int)((s_ent[p] >> 10) & 31u) < k0) inS0 = true;
+      }
+      inU = cnt > 0;
+    }
+  } else if (j < N) {
     const uint4* ents = reinterpret_cast<const uint4*>(s_ent);
     for (int vb = 0; vb < TK8 / 8; ++vb) {
       const uint4 e4 = ents[vb];
-      const uint32_t w4[4] = {e4.x, e4.y, e4.z, e4.w};
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const uint32_t ent = (w4[u >> 1] >> (16 * (u & 1))) & 0xFFFFu;
+        const uint32_t ent = entry_at(e4, u);
         if (entry_is(ent, j)) {
           inU = true;
           if ((int)((ent >> 10) & 31u) < k0) inS0 = true;
@@ -283,9 +351,9 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
         }
       }
     }
-    if (dense)
-      for (int i = 0; i < T; ++i) s = s + a.dense[(size_t)i * N + j];
   }
+  if (dense && j < N)
+    for (int i = 0; i < T; ++i) s = s + a.dense[(size_t)i * N + j];
 
   // ---- (c) per request (Algorithm 3), one wave per request: S_0(r) plus the m_r best
   //      remaining experts of r under the request's own score
@@ -296,16 +364,34 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
       unsigned inUr = 0, inS0r = 0;
 #pragma unroll
       for (int q = 0; q < Q; ++q) sr[q] = 0.0f;
-      for (int p = lo * k; p < hi * k; ++p) {
-        const uint32_t ent = s_ent[p];
-        if (ent == kNoEntry || (int)(ent & 63u) != lane) continue;
-        const int qe = (int)((ent & 1023u) >> 6);
+      if (occ) {
+        const uint64_t range = below(hi) & ~below(lo);
 #pragma unroll
         for (int q = 0; q < Q; ++q) {
-          if (q == qe) {
-            inUr |= 1u << q;
-            if ((int)((ent >> 10) & 31u) < k0) inS0r |= 1u << q;
+          const int jq = lane + 64 * q;
+          if (jq >= N) continue;
+          const uint64_t m = s_occ[jq];
+          const int n = __popcll(m & range);
+          const int o = s_off[jq] + __popcll(m & below(lo));
+          for (int t = 0; t < n; ++t) {
+            const int p = s_list[o + t];
+            if ((int)((s_ent[p] >> 10) & 31u) < k0) inS0r |= 1u << q;
             if (!dense) sr[q] = sr[q] + s_g[p];
+          }
+          if (n > 0) inUr |= 1u << q;
+        }
+      } else {
+        for (int p = lo * k; p < hi * k; ++p) {
+          const uint32_t ent = s_ent[p];
+          if (ent == kNoEntry || (int)(ent & 63u) != lane) continue;
+          const int qe = (int)((ent & 1023u) >> 6);
+#pragma unroll
+          for (int q = 0; q < Q; ++q) {
+            if (q == qe) {
+              inUr |= 1u << q;
+              if ((int)((ent >> 10) & 31u) < k0) inS0r |= 1u << q;
+              if (!dense) sr[q] = sr[q] + s_g[p];
+            }
           }
         }
       }
@@ -333,7 +419,8 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
 
   // ---- (d) batch greedy (Algorithm 1 with a fixed budget; Algorithm 4's final stage):
   //      order (tier, score desc, index asc), keep the first budget_eff candidates.
-  //      Key: (3 - tier) << 42 | ord(score) << 10 | (1023 - j); 0 = not a candidate.
+  //      Key: (3 - tier) << 42 | ord(score) << 10 | (1023 - j); candidates are compacted
+  //      and each counts the candidates ahead of it.
   int tier = 3;
   uint64_t mykey = 0;
   if (j < N) {
@@ -341,21 +428,23 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
     tier = inS0 ? 0 : (s_tier1[j] ? 1 : (cand ? 2 : 3));
     if (tier < 3)
       mykey = ((uint64_t)(3 - tier) << 42) | ((uint64_t)ord(s) << 10) | (uint64_t)(1023 - j);
-    if (tier < 3) atomicAdd(&s_cnt[0], 1);
     if (tier == 0) atomicAdd(&s_cnt[1], 1);
     if (tier <= 1) atomicAdd(&s_cnt[2], 1);
     if (inU) atomicAdd(&s_cnt[3], 1);
   }
-  if (j < kMaxExperts) s_key[j] = mykey;
+  int n_cand = 0;
+  const int cpos = block_excl_scan(mykey != 0 ? 1 : 0, s_wsum, n_cand);
+  if (mykey != 0) s_key[cpos] = mykey;
+  if (tid == 0 && (n_cand & 1)) s_key[n_cand] = 0;
   __syncthreads();
-  const int n_cand = s_cnt[0], n_s0 = s_cnt[1], n_start = s_cnt[2], n_u = s_cnt[3];
+  const int n_s0 = s_cnt[1], n_start = s_cnt[2], n_u = s_cnt[3];
   const int base = a.budget_mode == 0 ? a.budget : n_start + a.budget;
   const int m_eff = max(min(base, n_cand), min(k, n_cand));
   bool sel = false;
   if (mykey != 0) {
     const ulonglong2* keys2 = reinterpret_cast<const ulonglong2*>(s_key);
     int rank = 0;
-    const int n2 = (N + 1) >> 1;
+    const int n2 = (n_cand + 1) >> 1;
     for (int jj = 0; jj < n2; ++jj) {
       const ulonglong2 kk = keys2[jj];
       rank += (kk.x > mykey) + (kk.y > mykey);
@@ -369,7 +458,9 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   }
   __syncthreads();
 
-  // ---- (e) refinement: every token to its top-k inside S, gates renormalised (Section 3.4)
+  // ---- (e) refinement: every token to its top-k inside S, gates renormalised (Section 3.4).
+  //      The token's plain top-k experts that are in S are its first refined ranks (in
+  //      their order); only the remaining ranks need a search.
   for (int i = wave; i < T; i += kWaves) {
     float v[Q];
     uint32_t key[Q];
@@ -379,9 +470,31 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
       const int jq = lane + 64 * q;
       if (jq >= N || !s_sel[jq]) key[q] = 0;
     }
-    float my_h;
-    int my_j;
-    wave_topk<Q>(key, k, lane, my_h, my_j);
+    const uint32_t vent = lane < k ? (uint32_t)s_ent[i * k + lane] : kNoEntry;
+    const int vid = vent == kNoEntry ? -1 : (int)(vent & 1023u);
+    const bool keep = vid >= 0 && s_sel[vid];
+    const uint64_t kept = __ballot(keep);
+    const int m = __popcll(kept);
+    if (keep) {
+      const int dst = __popcll(kept & below(lane));
+      s_seed[wave][dst] = (uint32_t)vid;
+      s_seed_h[wave][dst] = a.logits[(size_t)i * N + vid] + 0.0f;
+    }
+    for (int r = 0; r < k; ++r) {       // none of the plain top-k is searched again
+      const int vr = __builtin_amdgcn_readlane(vid, r);
+      if (vr >= 0 && (vr & 63) == lane) {
+#pragma unroll
+        for (int q = 0; q < Q; ++q)
+          if (q == (vr >> 6)) key[q] = 0;
+      }
+    }
+    float my_h = -INFINITY;
+    int my_j = -1;
+    if (lane < m) {
+      my_j = (int)s_seed[wave][lane];
+      my_h = s_seed_h[wave][lane];
+    }
+    wave_topk<Q>(key, m, k, lane, my_h, my_j);
     const float g = ranked_gate(my_h, lane, k);
     if (lane < k) {
       a.ids[i * k + lane] = my_j;
@@ -392,35 +505,42 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   __syncthreads();
 
   // ---- (f) permutation: rows grouped by expert (ascending), tokens ascending inside
-  int cnt = 0;
-  if (j < N) {
-    const uint4* ents = reinterpret_cast<const uint4*>(s_ent);
-    for (int vb = 0; vb < TK8 / 8; ++vb) {
-      const uint4 e4 = ents[vb];
-      const uint32_t w4[4] = {e4.x, e4.y, e4.z, e4.w};
+  int cnt = 0, total = 0, off = 0;
+  if (occ) {
+    for (int jj = tid; jj < kMaxExperts; jj += kThreads) s_occ[jj] = 0;
+    __syncthreads();
+    cnt = group_by_expert(s_ent, s_occ, s_off, s_list, s_wsum, TK, k, N, total);
+    if (j < N) {
+      off = s_off[j];
+      for (int q = 0; q < cnt; ++q) a.perm[off + q] = s_list[off + q];
+    }
+  } else {
+    if (j < N) {
+      const uint4* ents = reinterpret_cast<const uint4*>(s_ent);
+      for (int vb = 0; vb < TK8 / 8; ++vb) {
+        const uint4 e4 = ents[vb];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) cnt += entry_is((w4[u >> 1] >> (16 * (u & 1))) & 0xFFFFu, j);
+        for (int u = 0; u < 8; ++u) cnt += entry_is(entry_at(e4, u), j);
+      }
+    }
+    off = block_excl_scan(cnt, s_wsum, total);
+    if (j < N && cnt > 0) {
+      const uint4* ents = reinterpret_cast<const uint4*>(s_ent);
+      int pos = off;
+      for (int vb = 0; vb < TK8 / 8; ++vb) {
+        const uint4 e4 = ents[vb];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (entry_is(entry_at(e4, u), j)) a.perm[pos++] = vb * 8 + u;
+      }
     }
   }
-  int total = 0;
-  const int off = block_excl_scan(cnt, s_wsum, total);
   int n_active = 0;
   const int arank = block_excl_scan(cnt > 0 ? 1 : 0, s_wsum, n_active);
   if (j < N) {
     a.offsets[j] = off;
     if (j == N - 1) a.offsets[N] = off + cnt;
-    if (cnt > 0) {
-      a.active[arank] = j;
-      const uint4* ents = reinterpret_cast<const uint4*>(s_ent);
-      int pos = off;
-      for (int vb = 0; vb < TK8 / 8; ++vb) {
-        const uint4 e4 = ents[vb];
-        const uint32_t w4[4] = {e4.x, e4.y, e4.z, e4.w};
-#pragma unroll
-        for (int u = 0; u < 8; ++u)
-          if (entry_is((w4[u >> 1] >> (16 * (u & 1))) & 0xFFFFu, j)) a.perm[pos++] = vb * 8 + u;
-      }
-    }
+    if (cnt > 0) a.active[arank] = j;
   }
   if (tid == 0) {
     a.counters[kCntActive] = n_active;
