@@ -152,16 +152,32 @@ __device__ __forceinline__ float ranked_gate(float my_h, int lane, int k) {
   return lane < k ? e / z : 0.0f;
 }
 
-// Canonicalised logits of one token as keys (h + 0.0 maps -0.0 to +0.0).
+// Raw logits of one token, lane l holding experts l, l + 64, ...
 template <int Q>
-__device__ __forceinline__ void row_keys(const float* row, int N, int lane, float (&v)[Q],
+__device__ __forceinline__ void load_row(const float* row, int N, int lane, float (&raw)[Q]) {
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int j = lane + 64 * q;
+    raw[q] = j < N ? row[j] : 0.0f;
+  }
+}
+
+// Canonicalised logits (h + 0.0 maps -0.0 to +0.0) and their keys.
+template <int Q>
+__device__ __forceinline__ void row_keys(const float (&raw)[Q], int N, int lane, float (&v)[Q],
                                          uint32_t (&key)[Q]) {
 #pragma unroll
   for (int q = 0; q < Q; ++q) {
     const int j = lane + 64 * q;
-    v[q] = j < N ? row[j] + 0.0f : 0.0f;
+    v[q] = raw[q] + 0.0f;
     key[q] = j < N ? ord(v[q]) : 0u;
   }
+}
+
+template <int Q>
+__device__ __forceinline__ void copy_keys(uint32_t (&dst)[Q], const uint32_t (&src)[Q]) {
+#pragma unroll
+  for (int q = 0; q < Q; ++q) dst[q] = src[q];
 }
 
 // Block-wide exclusive prefix sum of one int per thread; every thread must call it.
@@ -232,6 +248,7 @@ template <int Q>
 __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   __shared__ __align__(16) uint16_t s_ent[kMaxAssignments];  // (token, rank) -> expert | rank
   __shared__ float s_g[kMaxAssignments];                     // vanilla gate of that entry
+  __shared__ float s_vh[kMaxAssignments];                    // vanilla logit of that entry
   __shared__ uint16_t s_list[kMaxAssignments];               // entries grouped by expert
   __shared__ __align__(16) uint64_t s_occ[kMaxExperts];      // token bitmask per expert
   __shared__ __align__(16) uint64_t s_key[kMaxExperts];      // greedy keys of the candidates
@@ -290,18 +307,36 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
     }
   }
 
-  // ---- (a) per token: plain top-k and its gates (Section 2.2); dense softmax if requested
-  for (int i = wave; i < T; i += kWaves) {
-    float v[Q];
+  // ---- (a) per token: plain top-k and its gates (Section 2.2); dense softmax if requested.
+  //      The next token's row is loaded while the current one is ranked; for batches of
+  //      up to two tokens per wave the keys left after the top-k (all experts but the
+  //      token's top-k) stay in registers for the refinement.
+  constexpr int kCache = 2;
+  const bool cached = T <= kCache * kWaves;
+  uint32_t kc0[Q], kc1[Q];
+  float raw_next[Q];
+  if (wave < T) load_row<Q>(a.logits + (size_t)wave * N, N, lane, raw_next);
+  for (int i = wave, it = 0; i < T; i += kWaves, ++it) {
+    float raw[Q], v[Q];
     uint32_t key[Q];
-    row_keys<Q>(a.logits + (size_t)i * N, N, lane, v, key);
+#pragma unroll
+    for (int q = 0; q < Q; ++q) raw[q] = raw_next[q];
+    if (i + kWaves < T) load_row<Q>(a.logits + (size_t)(i + kWaves) * N, N, lane, raw_next);
+    row_keys<Q>(raw, N, lane, v, key);
     float my_h;
     int my_j;
     wave_topk<Q>(key, 0, k, lane, my_h, my_j);
+    if (cached) {
+      if (it == 0)
+        copy_keys<Q>(kc0, key);
+      else
+        copy_keys<Q>(kc1, key);
+    }
     const float g = ranked_gate(my_h, lane, k);
     if (lane < k) {
       s_ent[i * k + lane] = (uint16_t)(my_j < 0 ? kNoEntry : (uint32_t)((lane << 10) | my_j));
       s_g[i * k + lane] = g;
+      s_vh[i * k + lane] = my_h;
     }
     if (dense) {
       const float m = lane_value(my_h, 0);
@@ -460,33 +495,44 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
 
   // ---- (e) refinement: every token to its top-k inside S, gates renormalised (Section 3.4).
   //      The token's plain top-k experts that are in S are its first refined ranks (in
-  //      their order); only the remaining ranks need a search.
-  for (int i = wave; i < T; i += kWaves) {
-    float v[Q];
+  //      their order); only the remaining ranks are searched, among the other experts.
+  if (!cached && wave < T) load_row<Q>(a.logits + (size_t)wave * N, N, lane, raw_next);
+  for (int i = wave, it = 0; i < T; i += kWaves, ++it) {
     uint32_t key[Q];
-    row_keys<Q>(a.logits + (size_t)i * N, N, lane, v, key);
+    const uint32_t vent = lane < k ? (uint32_t)s_ent[i * k + lane] : kNoEntry;
+    const int vid = vent == kNoEntry ? -1 : (int)(vent & 1023u);
+    if (cached) {
+      if (it == 0)
+        copy_keys<Q>(key, kc0);
+      else
+        copy_keys<Q>(key, kc1);
+    } else {
+      float raw[Q], v[Q];
+#pragma unroll
+      for (int q = 0; q < Q; ++q) raw[q] = raw_next[q];
+      if (i + kWaves < T) load_row<Q>(a.logits + (size_t)(i + kWaves) * N, N, lane, raw_next);
+      row_keys<Q>(raw, N, lane, v, key);
+      for (int r = 0; r < k; ++r) {     // the plain top-k is not searched again
+        const int vr = __builtin_amdgcn_readlane(vid, r);
+        if (vr >= 0 && (vr & 63) == lane) {
+#pragma unroll
+          for (int q = 0; q < Q; ++q)
+            if (q == (vr >> 6)) key[q] = 0;
+        }
+      }
+    }
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
       const int jq = lane + 64 * q;
       if (jq >= N || !s_sel[jq]) key[q] = 0;
     }
-    const uint32_t vent = lane < k ? (uint32_t)s_ent[i * k + lane] : kNoEntry;
-    const int vid = vent == kNoEntry ? -1 : (int)(vent & 1023u);
     const bool keep = vid >= 0 && s_sel[vid];
     const uint64_t kept = __ballot(keep);
     const int m = __popcll(kept);
     if (keep) {
       const int dst = __popcll(kept & below(lane));
       s_seed[wave][dst] = (uint32_t)vid;
-      s_seed_h[wave][dst] = a.logits[(size_t)i * N + vid] + 0.0f;
-    }
-    for (int r = 0; r < k; ++r) {       // none of the plain top-k is searched again
-      const int vr = __builtin_amdgcn_readlane(vid, r);
-      if (vr >= 0 && (vr & 63) == lane) {
-#pragma unroll
-        for (int q = 0; q < Q; ++q)
-          if (q == (vr >> 6)) key[q] = 0;
-      }
+      s_seed_h[wave][dst] = s_vh[i * k + lane];
     }
     float my_h = -INFINITY;
     int my_j = -1;
