@@ -24,6 +24,21 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "MoE-layer µs/batch + HBM GB/s (N=256,k=8,B=32); experts activated/batch"
+WORKLOAD_NAMES = {
+    "ds_t32": "deepseek_r1_routed_moe_T{T}_N{N}_k{k}_d{d}_f{f}_M{M}_k0{k0}",
+    "ds_t8": "deepseek_r1_routed_moe_T{T}_N{N}_k{k}_d{d}_f{f}_M{M}_k0{k0}",
+    "ds_iid_t8": "deepseek_r1_iid_routing_T{T}_N{N}_k{k}_d{d}_f{f}_M{M}_k0{k0}",
+    "ds_iid_t32": "deepseek_r1_iid_routing_T{T}_N{N}_k{k}_d{d}_f{f}_M{M}_k0{k0}",
+    "qwen": "qwen_moe_T{T}_N{N}_k{k}_d{d}_f{f}_M{M}_k0{k0}",
+    "mixtral": "mixtral_T{T}_N{N}_k{k}_d{d}_f{f}_M{M}_k0{k0}",
+    "tiny": "tiny_T{T}_N{N}_k{k}_d{d}_f{f}_M{M}_k0{k0}",
+    "spec": "deepseek_r1_speculative_16x4_N{N}_k{k}_d{d}_f{f}_hier_M{M}_k0{k0}_mr{m_r}",
+}
+LOGITS_RECIPE = {
+    "domains": "{Q} domain centroids N(0,1.5) + N(0,0.5)",
+    "iid": "iid N(0,1)",
+    "spec": "{Q} domains round-robin over requests, request offset N(0,1), token noise N(0,0.3)",
+}
 HBM_PEAK_GBS = 8000.0
 PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "gate_up_ds_t32_m48_counters.json")
 FFN_SOURCE = os.path.join(ROOT, "paper_2602_07265_amd", "csrc", "ffn.hip")
@@ -35,8 +50,11 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--batches", type=int, default=8, help="distinct seeded batches rotated over")
-    ap.add_argument("--budget", type=int, default=48)
-    ap.add_argument("--tokens", type=int, default=32)
+    ap.add_argument("--workload", default="ds_t32",
+                    help="ds_t32 (default; the headline), ds_t8, qwen, mixtral, spec")
+    ap.add_argument("--budget", type=int, default=None, help="total budget M (default: workload's)")
+    ap.add_argument("--replicas", type=int, default=None,
+                    help="weight copies rotated over (default: enough for >= 4 GB of weights)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-vanilla", action="store_true")
     return ap.parse_args()
@@ -82,27 +100,44 @@ def main():
         sys.exit(1)
     X.lib()
     dev = "cuda:0"
-    cfg = dict(W.CONFIGS["ds_t32"])
-    T, N, k, d, f = args.tokens, cfg["N"], cfg["k"], cfg["d"], cfg["f"]
-    M, k0 = args.budget, cfg["k0"]
+    cfg = dict(W.CONFIGS[args.workload])
+    T, N, k, d, f = cfg["T"], cfg["N"], cfg["k"], cfg["d"], cfg["f"]
+    M = cfg["M"] if args.budget is None else args.budget
+    k0, m_r = cfg["k0"], cfg.get("m_r", 0)
+    hier = cfg["logits"] == "spec"
     nb = args.batches
+    layer_gb = N * 3 * d * f * 2 / 1e9
+    # small layers would sit in the 256 MB Infinity Cache between steps: rotate weight copies
+    reps = args.replicas or max(1, min(8, int(np.ceil(4.0 / layer_gb))))
 
-    print(f"[bench] generating DS-R1 layer weights ({N * 3 * d * f * 2 / 1e9:.1f} GB)", file=sys.stderr,
-          flush=True)
+    print(f"[bench] {args.workload}: generating layer weights ({layer_gb:.2f} GB x {reps})",
+          file=sys.stderr, flush=True)
     w1, w3, w2 = W.expert_weights(N, d, f, 0, dev)
-    logits = [torch.from_numpy(W.logits_domains(T, N, cfg["Q"], s)).to(dev) for s in range(nb)]
+    wsets = [(w1, w3, w2)] + [(w1.clone(), w3.clone(), w2.clone()) for _ in range(reps - 1)]
+    made = [W.make_logits(cfg, s) for s in range(nb)]
+    logits = [torch.from_numpy(h).to(dev) for h, _ in made]
+    offs = [None if o is None else [int(v) for v in o] for _, o in made]
     xs = [W.activations(T, d, s, dev) for s in range(nb)]
     p = X.params(N, k, k0, M, "total")
     ws = torch.empty(X.moe_workspace_bytes(T, d, f, p), dtype=torch.uint8, device=dev)
     y = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
     torch.cuda.synchronize()
 
+    def call(s, mode, **kw):
+        b = s % nb
+        wa, wb, wc = wsets[s % reps]
+        if mode == "xshare":
+            return X.moe_forward(xs[b], logits[b], wa, wb, wc, k, k0, M, "total", y=y,
+                                 workspace=ws, req_offsets=offs[b] if hier else None,
+                                 per_request_budget=m_r, **kw)
+        return X.moe_forward(xs[b], logits[b], wa, wb, wc, k, 0, N, "extra", y=y, workspace=ws,
+                             **kw)
+
     # per-batch routing statistics (deterministic per batch)
     stats = []
     for b in range(nb):
-        r = X.moe_forward(xs[b], logits[b], w1, w3, w2, k, k0, M, "total", y=y, workspace=ws)
-        rv = X.moe_forward(xs[b], logits[b], w1, w3, w2, k, 0, N, "extra", y=y, workspace=ws)
-        stats.append((X.stats_dict(r["stats"]), X.stats_dict(rv["stats"])))
+        stats.append((X.stats_dict(call(b, "xshare")["stats"]),
+                      X.stats_dict(call(b, "vanilla")["stats"])))
     act = [s[0]["n_active"] for s in stats]
     act_v = [s[1]["n_active"] for s in stats]
 
@@ -112,13 +147,7 @@ def main():
     def run(steps, mode, timed):
         evs = [[X.HipEvent() for _ in range(nev)] for _ in range(steps)] if timed else None
         for s in range(steps):
-            b = s % nb
-            if mode == "xshare":
-                X.moe_forward(xs[b], logits[b], w1, w3, w2, k, k0, M, "total", y=y, workspace=ws,
-                              routing_out=False, stage_events=evs[s] if timed else None)
-            else:
-                X.moe_forward(xs[b], logits[b], w1, w3, w2, k, 0, N, "extra", y=y, workspace=ws,
-                              routing_out=False, stage_events=evs[s] if timed else None)
+            call(s, mode, routing_out=False, stage_events=evs[s] if timed else None)
         return evs
 
     print(f"[bench] warmup {args.warmup} + {args.steps} timed steps", file=sys.stderr, flush=True)
@@ -156,11 +185,13 @@ def main():
 
     gbs = float(lay_bytes.mean()) / (ms_step * 1e-3) / 1e9
     gu_achieved = float(gu_bytes.mean()) / (float(gu_ms.mean()) * 1e-3) / 1e9
-    traffic = counters_traffic()
+    # the committed counter record covers the headline workload only
+    traffic = counters_traffic() if (args.workload, M, T) == ("ds_t32", 48, 32) else None
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(W, xs, logits, w1, w3, w2, T, N, k, k0, M, d, f)
+        cpu = cpu_baseline(W, xs, logits, offs if hier else None, m_r, w1, w3, w2, T, N, k, k0, M,
+                           d, f)
 
     out = {
         "metric": METRIC,
@@ -175,10 +206,13 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": f"deepseek_r1_routed_moe_T{T}_N{N}_k{k}_d{d}_f{f}_M{M}_k0{k0}",
+        "config": {"workload": WORKLOAD_NAMES[args.workload].format(T=T, N=N, k=k, d=d, f=f, M=M,
+                                                                     k0=k0, m_r=m_r),
                    "tokens": T, "n_experts": N, "top_k": k, "d_model": d, "d_ffn": f,
                    "budget": M, "budget_mode": "total", "warmup_k0": k0,
-                   "logits": "8 domain centroids N(0,1.5) + N(0,0.5)", "batches_rotated": nb},
+                   "per_request_budget": m_r if hier else None,
+                   "logits": LOGITS_RECIPE[cfg["logits"]].format(Q=cfg.get("Q")),
+                   "batches_rotated": nb, "weight_replicas": reps},
         "us_per_batch": round(ms_step * 1e3, 2),
         "tokens_per_s": round(T / (ms_step * 1e-3), 1),
         "experts_activated": round(float(np.mean(act)), 2),
@@ -198,7 +232,7 @@ def main():
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(W, xs, logits, w1, w3, w2, T, N, k, k0, M, d, f, budget_s=10.0):
+def cpu_baseline(W, xs, logits, offs, m_r, w1, w3, w2, T, N, k, k0, M, d, f, budget_s=10.0):
     """The oracle on the host cores: routing plus the float64 SwiGLU layer of whole batches,
     over as many of the rotated batches as fit in about budget_s seconds (at least one)."""
     import numpy as np
@@ -216,7 +250,7 @@ def cpu_baseline(W, xs, logits, w1, w3, w2, T, N, k, k0, M, d, f, budget_s=10.0)
         h = logits[b].cpu().numpy()
         xb = W.bf16_bits(xs[b])
         t0 = time.perf_counter()
-        r = OR.route(h, k, k0, M)
+        r = OR.route(h, k, k0, M) if offs is None else OR.select_hier(h, offs[b], k, k0, m_r, M)
         t_route = time.perf_counter() - t0
         used = sorted(set(int(e) for e in r.ids.reshape(-1)))
         cache = {e: tuple(W.bf16_bits(m[e]) for m in (w1, w3, w2)) for e in used}   # not timed

@@ -114,8 +114,10 @@ size_t xshare_route_workspace_bytes(int32_t T, const xshare_route_params* params
 size_t xshare_moe_workspace_bytes(int32_t T, int32_t d, int32_t f,
                                   const xshare_route_params* params) {
   if (check_params(T, params, false) != XSHARE_OK || d <= 0 || f <= 0) return 0;
+  const int bound = xs::active_bound(T, params->n_experts, params->top_k, params->budget_mode,
+                                     params->budget);
   return xs::ffn_layout(T, params->n_experts, params->top_k,
-                        params->score_mode == XSHARE_SCORE_DENSE, d, f)
+                        params->score_mode == XSHARE_SCORE_DENSE, d, f, bound)
       .total;
 }
 
@@ -155,8 +157,9 @@ xshare_status xshare_moe_forward(const uint16_t* x, const float* logits, int32_t
   if (!aligned16(x) || !aligned16(w1) || !aligned16(w3) || !aligned16(w2) || !aligned16(y))
     return XSHARE_EINVAL;
   const int N = params->n_experts, k = params->top_k;
+  const int bound = xs::active_bound(T, N, k, params->budget_mode, params->budget);
   const xs::FfnLayout L =
-      xs::ffn_layout(T, N, k, params->score_mode == XSHARE_SCORE_DENSE, d, f);
+      xs::ffn_layout(T, N, k, params->score_mode == XSHARE_SCORE_DENSE, d, f, bound);
   if (!ws || ws_bytes < L.total) return XSHARE_EWORKSPACE;
 
   // The selection kernel always writes a mask; keep it in the workspace if not wanted.
@@ -187,9 +190,8 @@ xshare_status xshare_moe_forward(const uint16_t* x, const float* logits, int32_t
   fa.f = f;
   // Active experts never exceed the selected set (<= budget under a total budget) nor the
   // number of (token, slot) pairs; blocks beyond the device-side count exit at once.
-  int bound = std::min(N, T * k);
-  if (params->budget_mode == XSHARE_BUDGET_TOTAL) bound = std::min(bound, params->budget);
   fa.max_active = bound;
+  fa.splits = L.splits;
   fa.offsets = ra.offsets;
   fa.perm = ra.perm;
   fa.active = ra.active;

@@ -187,10 +187,13 @@ __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
   if (n0 >= a.d) return;
   const int n = lane & 15, g = lane >> 4;
   const int d = a.d, f = a.f;
+  const int Ks = f / a.splits;                 // this block's part of the reduction
+  const size_t k0 = (size_t)blockIdx.z * Ks + (size_t)g * 8 * U;
+  float* const ypart = a.yslot + (size_t)blockIdx.z * a.T * a.k * d;
   const uint16_t* brow[NM];
 #pragma unroll
   for (int m = 0; m < NM; ++m)
-    brow[m] = a.w2 + ((size_t)e * d + min(n0 + 16 * m, d - 16) + n) * f + (size_t)g * 8 * U;
+    brow[m] = a.w2 + ((size_t)e * d + min(n0 + 16 * m, d - 16) + n) * f + k0;
 
   for (int c0 = 0; c0 < te; c0 += 16 * kTiles) {
     const int nt = min(kTiles, (te - c0 + 15) / 16);
@@ -198,14 +201,14 @@ __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
 #pragma unroll
     for (int rt = 0; rt < kTiles; ++rt) {
       const int t = min(c0 + rt * 16 + n, te - 1);
-      arow[rt] = a.h + (size_t)(p0 + t) * f + (size_t)g * 8 * U;
+      arow[rt] = a.h + (size_t)(p0 + t) * f + k0;
     }
     floatx4 acc[NM][kTiles];
 #pragma unroll
     for (int m = 0; m < NM; ++m)
 #pragma unroll
       for (int rt = 0; rt < kTiles; ++rt) acc[m][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    wave_pass<U, NM, XS_DOWN_ADBL != 0>(arow, nt, brow, f, acc);
+    wave_pass<U, NM, XS_DOWN_ADBL != 0>(arow, nt, brow, Ks, acc);
 #pragma unroll
     for (int rt = 0; rt < kTiles; ++rt) {
       if (rt >= nt) break;
@@ -213,7 +216,7 @@ __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
       for (int i = 0; i < 4; ++i) {
         const int t = c0 + rt * 16 + 4 * g + i;
         if (t < te) {
-          float* yrow = a.yslot + (size_t)a.perm[p0 + t] * d;
+          float* yrow = ypart + (size_t)a.perm[p0 + t] * d;
 #pragma unroll
           for (int m = 0; m < NM; ++m)
             if (n0 + 16 * m < d) yrow[n0 + 16 * m + n] = acc[m][rt][i];
@@ -232,7 +235,15 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(FfnArgs a) {
     const int slot = i * a.k + r;
     if (a.ids[slot] < 0) continue;
     const float wr = a.w[slot];
-    const float4 v = *reinterpret_cast<const float4*>(a.yslot + (size_t)slot * a.d + c);
+    float4 v = *reinterpret_cast<const float4*>(a.yslot + (size_t)slot * a.d + c);
+    for (int s = 1; s < a.splits; ++s) {   // partial sums of a split reduction, in order
+      const float4 u = *reinterpret_cast<const float4*>(
+          a.yslot + ((size_t)s * a.T * a.k + slot) * a.d + c);
+      v.x += u.x;
+      v.y += u.y;
+      v.z += u.z;
+      v.w += u.w;
+    }
     acc[0] += wr * v.x;
     acc[1] += wr * v.y;
     acc[2] += wr * v.z;
@@ -264,8 +275,8 @@ hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
 
 hipError_t launch_down(const FfnArgs& a, hipStream_t stream) {
   constexpr int cols = kWaves * kCols * XS_DOWN_NM;
-  const dim3 grid((a.d + cols - 1) / cols, a.max_active), block(kBlock);
-  switch (unroll_for(a.f, XS_DOWN_U)) {
+  const dim3 grid((a.d + cols - 1) / cols, a.max_active, a.splits), block(kBlock);
+  switch (unroll_for(a.f / a.splits, XS_DOWN_U)) {
     case 8: hipLaunchKernelGGL(down_kernel<8>, grid, block, 0, stream, a); break;
     case 4: hipLaunchKernelGGL(down_kernel<4>, grid, block, 0, stream, a); break;
     case 2: hipLaunchKernelGGL(down_kernel<2>, grid, block, 0, stream, a); break;

@@ -53,20 +53,39 @@ inline RouteLayout route_layout(int T, int N, int k, bool dense) {
   return L;
 }
 
+// Upper bound on the experts that receive tokens: never more than the (token, slot) pairs,
+// and never more than a total budget.
+inline int active_bound(int T, int N, int k, int budget_mode, int budget) {
+  int b = N < T * k ? N : T * k;
+  if (budget_mode == 0 && budget < b) b = budget;
+  return b;
+}
+
+// The down GEMM splits its reduction (f) into this many parts when the active experts'
+// 32-row output tiles alone would give too few waves to keep HBM busy (few, wide experts).
+inline int down_splits(int max_active, int d, int f) {
+  const long waves = (long)max_active * (d / 32);
+  int s = 1;
+  while (s < 8 && waves * s < 2048 && f % (2 * s * 256) == 0) s *= 2;
+  return s;
+}
+
 struct FfnLayout {
   RouteLayout route;
-  size_t h;      // bf16 [T * k, f]  SwiGLU hidden rows in permuted order
-  size_t y;      // fp32 [T * k, d]  per-(token, slot) expert outputs
+  int splits;    // K-splits of the down GEMM
+  size_t h;      // bf16 [T * k, f]            SwiGLU hidden rows in permuted order
+  size_t y;      // fp32 [splits, T * k, d]    per-(token, slot) partial expert outputs
   size_t total;
 };
 
-inline FfnLayout ffn_layout(int T, int N, int k, bool dense, int d, int f) {
+inline FfnLayout ffn_layout(int T, int N, int k, bool dense, int d, int f, int max_active) {
   FfnLayout L{};
   L.route = route_layout(T, N, k, dense);
+  L.splits = down_splits(max_active, d, f);
   size_t tk = size_t(T > 0 ? T : 1) * size_t(k);
   size_t o = L.route.total;
   L.h = o; o += align256(sizeof(uint16_t) * tk * size_t(f));
-  L.y = o; o += align256(sizeof(float) * tk * size_t(d));
+  L.y = o; o += align256(sizeof(float) * size_t(L.splits) * tk * size_t(d));
   L.total = o;
   return L;
 }
@@ -96,6 +115,7 @@ struct FfnArgs {
   const uint16_t* w2;
   int T, N, k, d, f;
   int max_active;              // host bound on the number of active experts (grid size)
+  int splits;                  // K-splits of the down GEMM (partials summed in the combine)
   const int32_t* offsets;
   const int32_t* perm;
   const int32_t* active;

@@ -180,6 +180,20 @@ __device__ __forceinline__ void copy_keys(uint32_t (&dst)[Q], const uint32_t (&s
   for (int q = 0; q < Q; ++q) dst[q] = src[q];
 }
 
+// Register cache of up to C tokens' keys per wave, addressed by a run-time slot.
+template <int C, int Q>
+__device__ __forceinline__ void cache_put(uint32_t (&kc)[C][Q], int slot, const uint32_t (&key)[Q]) {
+#pragma unroll
+  for (int c = 0; c < C; ++c)
+    if (c == slot) copy_keys<Q>(kc[c], key);
+}
+template <int C, int Q>
+__device__ __forceinline__ void cache_get(const uint32_t (&kc)[C][Q], int slot, uint32_t (&key)[Q]) {
+#pragma unroll
+  for (int c = 0; c < C; ++c)
+    if (c == slot) copy_keys<Q>(key, kc[c]);
+}
+
 // Block-wide exclusive prefix sum of one int per thread; every thread must call it.
 __device__ int block_excl_scan(int v, int* s_wsum, int& total) {
   const int lane = threadIdx.x & 63;
@@ -309,11 +323,11 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
 
   // ---- (a) per token: plain top-k and its gates (Section 2.2); dense softmax if requested.
   //      The next token's row is loaded while the current one is ranked; for batches of
-  //      up to two tokens per wave the keys left after the top-k (all experts but the
+  //      up to four tokens per wave the keys left after the top-k (all experts but the
   //      token's top-k) stay in registers for the refinement.
-  constexpr int kCache = 2;
+  constexpr int kCache = 4;
   const bool cached = T <= kCache * kWaves;
-  uint32_t kc0[Q], kc1[Q];
+  uint32_t kc[kCache][Q];
   float raw_next[Q];
   if (wave < T) load_row<Q>(a.logits + (size_t)wave * N, N, lane, raw_next);
   for (int i = wave, it = 0; i < T; i += kWaves, ++it) {
@@ -326,12 +340,7 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
     float my_h;
     int my_j;
     wave_topk<Q>(key, 0, k, lane, my_h, my_j);
-    if (cached) {
-      if (it == 0)
-        copy_keys<Q>(kc0, key);
-      else
-        copy_keys<Q>(kc1, key);
-    }
+    if (cached) cache_put<kCache, Q>(kc, it, key);
     const float g = ranked_gate(my_h, lane, k);
     if (lane < k) {
       s_ent[i * k + lane] = (uint16_t)(my_j < 0 ? kNoEntry : (uint32_t)((lane << 10) | my_j));
@@ -502,10 +511,7 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
     const uint32_t vent = lane < k ? (uint32_t)s_ent[i * k + lane] : kNoEntry;
     const int vid = vent == kNoEntry ? -1 : (int)(vent & 1023u);
     if (cached) {
-      if (it == 0)
-        copy_keys<Q>(key, kc0);
-      else
-        copy_keys<Q>(key, kc1);
+      cache_get<kCache, Q>(kc, it, key);
     } else {
       float raw[Q], v[Q];
 #pragma unroll
