@@ -30,10 +30,12 @@ def expert_ffn(x, w1_bits, w3_bits, w2_bits) -> np.ndarray:
     return (silu(a) * b) @ W2.T
 
 
-def moe_forward(x_bits, ids, w, expert, rows=None) -> np.ndarray:
+def moe_forward(x_bits, ids, w, expert, rows=None, local=None) -> np.ndarray:
     """y[i] = sum_r w[i,r] * E_{ids[i,r]}(x_i) for the tokens in ``rows`` (default: all).
 
     ``expert(e)`` returns the bf16 bit arrays (w1 [f,d], w3 [f,d], w2 [d,f]) of expert e.
+    With ``local`` (a set of experts, those one GPU group hosts under expert parallelism,
+    Section 5) only the terms of those experts are summed: that group's share of y.
     Returns float64 [len(rows), d].
     """
     X = bf16_to_f64(x_bits)
@@ -44,7 +46,8 @@ def moe_forward(x_bits, ids, w, expert, rows=None) -> np.ndarray:
     by_expert: dict[int, list[tuple[int, int]]] = {}
     for p, i in enumerate(rows):
         for r in range(ids.shape[1]):
-            by_expert.setdefault(int(ids[i, r]), []).append((p, r))
+            if local is None or int(ids[i, r]) in local:
+                by_expert.setdefault(int(ids[i, r]), []).append((p, r))
     for e in sorted(by_expert):
         pairs = by_expert[e]
         w1, w3, w2 = expert(e)

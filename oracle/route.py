@@ -11,7 +11,10 @@ Follows, step by step:
   selection, refinement (each token routed to its top-k inside the set);
 * Section 4.1, Eqs. (3)-(4), Algorithms 3 and 4 -- per-request warm-up plus the
   m_r best experts of each request by its own score, union over requests, then
-  the batch-level greedy and the same refinement.
+  the batch-level greedy and the same refinement;
+* Section 5, Eq. (5), Algorithms 5 and 6 -- experts partitioned over G GPU groups;
+  after the warm-up, rounds in which every group in turn adds its best remaining
+  expert, then the same refinement.
 
 Readings of what the paper leaves open (each one is listed with its reason in
 the design notes of the repository):
@@ -31,7 +34,14 @@ the design notes of the repository):
   priority (warm-up first, then per-request picks), score descending, index
   ascending;
 * batch scores are always the sum over all tokens in ascending token order, so
-  the hierarchical scores of Eq. (4) equal the flat ones bit for bit.
+  the hierarchical scores of Eq. (4) equal the flat ones bit for bit;
+* GPU groups (Algorithm 5): the per-group budget m_g is also a cap, as in the
+  constraint of Eq. (5): a group whose load (warm-up experts included) has reached
+  m_g adds nothing more; a group with no candidate left is skipped (the argmax of
+  Algorithm 5 is over an empty set there); the loop condition |S| < m_g * G is
+  tested before each round, so a started round runs over all groups, and a round
+  that adds nothing ends the loop; the warm-up set is never cut; if fewer than k
+  experts result, the best remaining candidates are added regardless of group.
 """
 from __future__ import annotations
 
@@ -266,6 +276,85 @@ def select_hier(h, offsets, k: int, k0: int, m_r: int, M: int,
     mask[sorted(S)] = 1
     return Routing(mask, ids, w, s, vids, vg, len(union), len(S0), m_eff,
                    extra=dict(per_request_union=len(S_batch), tier1=len(added - S0)))
+
+
+# ----------------------------------------------------------------------------- Algorithms 5 + 6
+
+def contiguous_groups(N: int, G: int) -> list[int]:
+    """Expert j lives on GPU group j // (N / G) (equal contiguous blocks)."""
+    if G < 1 or N % G:
+        raise ValueError("contiguous groups need G >= 1 dividing N")
+    return [j // (N // G) for j in range(N)]
+
+
+def group_loads(S, groups, G: int) -> list[int]:
+    """Load_g(S) = |S intersected with E_g| for every group (Section 5.1)."""
+    load = [0] * G
+    for j in S:
+        load[groups[j]] += 1
+    return load
+
+
+def gpu_aware_greedy(scores, groups, G: int, m_g: int, S0, candidates) -> set[int]:
+    """Algorithm 5: starting from S_0, rounds over the groups; each group adds the
+    candidate of largest marginal gain (= its score, Proposition 3.1) among its own
+    experts not yet in S, while |S| < m_g * G at the start of a round."""
+    S = set(int(j) for j in S0)
+    load = group_loads(S, groups, G)
+    while len(S) < m_g * G:
+        added = 0
+        for g in range(G):
+            if load[g] >= m_g:                       # Eq. (5): MaxLoad(S) <= m_g
+                continue
+            rest = [int(e) for e in candidates if groups[int(e)] == g and int(e) not in S]
+            if not rest:                             # no candidate left on this group
+                continue
+            e_star = max(rest, key=lambda e: (float(scores[e]), -e))
+            S.add(e_star)
+            load[g] += 1
+            added += 1
+        if added == 0:
+            break
+    return S
+
+
+def check_groups(groups, N: int, G: int) -> list[int]:
+    gr = [int(v) for v in groups]
+    if G < 1 or len(gr) != N or any(not 0 <= v < G for v in gr):
+        raise ValueError("every expert needs a group in [0, G)")
+    return gr
+
+
+def select_ep(h, k: int, k0: int, m_g: int, groups, G: int,
+              score_mode: str = TOPK) -> Routing:
+    """Expert-parallelism-aware selection (Algorithm 6 calling Algorithm 5)."""
+    h = canonical(h)
+    _check(h, k, k0, k, TOTAL, score_mode)
+    if m_g < 0:
+        raise ValueError("need m_g >= 0")
+    T, N = h.shape
+    gr = check_groups(groups, N, G)
+    vids, vg = vanilla_gating(h, k)
+    G_mat = gate_matrix(h, vids, vg, score_mode)
+    s = scores_over(G_mat, range(T))
+
+    union = set(int(e) for e in vids.reshape(-1))
+    S0 = set(int(e) for e in vids[:, :k0].reshape(-1))            # warm-up
+    if T == 0:
+        cand = set()
+    else:
+        cand = union if score_mode == TOPK else set(range(N))
+    S = gpu_aware_greedy(s, gr, G, m_g, S0, sorted(cand))
+    if len(S) < min(k, len(cand)):                                 # every token keeps k
+        S = greedy_select(s, S, min(k, len(cand)), sorted(cand))
+    ids, w = refine(h, S, k)
+    mask = np.zeros(N, dtype=np.uint8)
+    mask[sorted(S)] = 1
+    loads = group_loads(S, gr, G)
+    vloads = group_loads(union, gr, G)
+    return Routing(mask, ids, w, s, vids, vg, len(union), len(S0), m_g * G,
+                   extra=dict(loads=loads, max_load=max(loads) if loads else 0,
+                              vanilla_loads=vloads, vanilla_max_load=max(vloads)))
 
 
 def vanilla(h, k: int) -> Routing:

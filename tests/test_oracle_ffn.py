@@ -85,3 +85,32 @@ def test_dense_gate_formulation_on_tiny_workload():
     # a subset of rows gives the same rows
     sub = O.moe_forward(x, r.ids, r.w, lambda e: ws[e], rows=[5, 1])
     assert np.allclose(sub, y[[5, 1]], rtol=1e-12, atol=1e-15)
+
+
+def test_group_shares_sum_to_the_layer():
+    """Expert parallelism: the shares of the G groups (dense formulation restricted to each
+    group's experts) add up to the whole layer output."""
+    c = W.CONFIGS["tiny"]
+    h, _ = W.make_logits(c, 2)
+    G = 4
+    groups = R.contiguous_groups(c["N"], G)
+    r = R.select_ep(h, c["k"], 1, 2, groups, G)
+    x = W.bf16_bits(W.activations(c["T"], c["d"], 2))
+    ws = [tuple(W.bf16_bits(W.expert_matrix(e, m, c["d"], c["f"], 2)) for m in ("w1", "w3", "w2"))
+          for e in range(c["N"])]
+    y = O.moe_forward(x, r.ids, r.w, lambda e: ws[e])
+    X = O.bf16_to_f64(x)
+    total = np.zeros_like(y)
+    for g in range(G):
+        mine = {e for e in range(c["N"]) if groups[e] == g}
+        share = O.moe_forward(x, r.ids, r.w, lambda e: ws[e], local=mine)
+        dense = np.zeros_like(y)
+        for e in sorted(mine):
+            W1, W3, W2 = (O.bf16_to_f64(m) for m in ws[e])
+            gate = np.array([sum(float(r.w[i, q]) for q in range(c["k"]) if r.ids[i, q] == e)
+                             for i in range(c["T"])])
+            a, b = X @ W1.T, X @ W3.T
+            dense += gate[:, None] * ((a / (1 + np.exp(-a)) * b) @ W2.T)
+        assert np.allclose(share, dense, rtol=1e-12, atol=1e-14)
+        total += share
+    assert np.allclose(total, y, rtol=1e-12, atol=1e-14)
