@@ -6,7 +6,9 @@
  * Eq. (2); greedy is optimal by Proposition 3.1 / Corollary 3.2), then routes every token to
  * its top-k experts inside S (Algorithm 2), so that only the weights of experts in S are
  * read.  For speculative-decoding batches the set is built per request first and then
- * completed at batch level (Section 4.1, Algorithms 3 and 4).
+ * completed at batch level (Section 4.1, Algorithms 3 and 4).  Under expert parallelism the
+ * experts are spread over G GPU groups and the set is grown one expert per group in turn,
+ * which bounds the most loaded group (Section 5, Eq. (5), Algorithms 5 and 6).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -56,9 +58,11 @@ typedef enum {
 /* How `budget` is read (the paper uses both readings of m_l).                             */
 enum {
   XSHARE_BUDGET_TOTAL = 0,  /* |S| <= budget; requires budget >= k                          */
-  XSHARE_BUDGET_EXTRA = 1   /* budget experts are added beyond the warm-up set (flat) or     *
+  XSHARE_BUDGET_EXTRA = 1,  /* budget experts are added beyond the warm-up set (flat) or     *
                              * beyond the union of the per-request sets (hierarchical), as   *
                              * in the paper's (m_l, k0) settings of Section 6                */
+  XSHARE_BUDGET_PER_GROUP = 2 /* budget is m_g, experts per GPU group (Algorithm 5); only    *
+                             * with an xshare_ep_layout, which in turn requires this mode    */
 };
 
 /* Which gates g_ij enter the scores s_j = sum_i g_ij (Eq. (2)).                            */
@@ -74,7 +78,7 @@ typedef struct {
   int32_t top_k;              /* k: experts per token (Section 2.2)                         */
   int32_t warmup_k0;          /* k0: top-k0 of every token always enters S (0 <= k0 <= k)   */
   int32_t budget;             /* M: see XSHARE_BUDGET_*                                    */
-  int32_t budget_mode;        /* XSHARE_BUDGET_TOTAL or XSHARE_BUDGET_EXTRA                 */
+  int32_t budget_mode;        /* XSHARE_BUDGET_TOTAL, _EXTRA or _PER_GROUP                  */
   int32_t score_mode;         /* XSHARE_SCORE_TOPK or XSHARE_SCORE_DENSE                    */
   int32_t per_request_budget; /* m_r (Algorithm 3); read by the hierarchical calls only     */
 } xshare_route_params;
@@ -82,21 +86,48 @@ typedef struct {
 /* Per-call statistics, written to DEVICE memory by the kernels.                          */
 typedef struct {
   int32_t n_selected;       /* |S|                                                        */
-  int32_t n_active;         /* experts with at least one routed token (weights streamed)   */
+  int32_t n_active;         /* experts with at least one routed token (weights streamed);  *
+                             * with a local group, only that group's experts                */
   int32_t n_vanilla_union;  /* |U|, U = union of every token's plain top-k (Section 3.1)    */
   int32_t n_warmup;         /* |S_0|, S_0 = union of every token's top-k0                   */
   int32_t n_start;          /* size of the set the batch greedy starts from: |S_0| (flat),  *
                              * |union_r S_r| (hierarchical)                                 */
-  int32_t budget_eff;       /* effective set size the greedy fills to (clamped to [k, |C|]) */
-  int32_t reserved[2];
+  int32_t budget_eff;       /* effective set size the greedy fills to (clamped to [k, |C|]); *
+                             * min(m_g * G, N) for the expert-parallel selection            */
+  int32_t max_group_load;   /* MaxLoad(S) = max_g |S on group g| (Section 5.1); 0 without   *
+                             * GPU groups                                                    */
+  int32_t reserved;
 } xshare_stats;
+
+/*
+ * Placement of the experts over G GPU groups for expert parallelism (Section 5.1): the
+ * groups partition the experts, E = E_1 u ... u E_G.
+ *
+ *   n_groups          G, 1 <= G <= N.
+ *   expert_group      DEVICE [N] int32, group of expert j in [0, G); NULL = equal contiguous
+ *                     blocks, expert j in group j / (N / G) (then G must divide N).  Entries
+ *                     outside [0, G) are detected on the device: the call then selects
+ *                     nothing, writes ids -1 and weights 0, and stats->n_selected = -1.
+ *   host_expert_group nullable HOST copy of expert_group, validated before launch when given.
+ *   local_group       xshare_moe_forward only: -1 computes the whole layer; g in [0, G)
+ *                     computes one GPU group's share, y_i = sum of w_ir * E_{e_ir}(x_i) over
+ *                     the ranks r whose expert is on group g, reading only that group's
+ *                     weights (the shares of all groups sum to the layer output).
+ */
+typedef struct {
+  int32_t n_groups;
+  int32_t local_group;
+  const int32_t* expert_group;
+  const int32_t* host_expert_group;
+} xshare_ep_layout;
 
 /* Workspace for xshare_route / xshare_select_hier with T tokens (bytes, 256-aligned).    */
 size_t xshare_route_workspace_bytes(int32_t T, const xshare_route_params* params);
 
-/* Workspace for xshare_moe_forward (includes the routing workspace).                     */
+/* Workspace for xshare_moe_forward (includes the routing workspace); `ep` as passed to   *
+ * xshare_moe_forward (nullable).  Returns 0 for invalid arguments.                        */
 size_t xshare_moe_workspace_bytes(int32_t T, int32_t d, int32_t f,
-                                  const xshare_route_params* params);
+                                  const xshare_route_params* params, const xshare_ep_layout* ep);
 
 /*
  * xshare_route -- batch-aware expert selection for one layer (Algorithm 2, Section 3.4).
@@ -120,8 +151,10 @@ xshare_status xshare_route(const float* logits, int32_t T, const xshare_route_pa
  * xshare_select_hier -- speculative-decoding-aware selection (Algorithms 3 and 4, Section 4.1).
  *
  *   req_offsets  [R + 1] int32, DEVICE: request r owns tokens [o_r, o_{r+1});
- *                must satisfy 0 = o_0 < o_1 < ... < o_R = T (not checked on the device:
- *                pass host_offsets to have them validated before launch).
+ *                must satisfy 0 = o_0 < o_1 < ... < o_R = T.  Violations are detected on
+ *                the device: the call then selects nothing, writes ids -1 and weights 0,
+ *                and stats->n_selected = -1.  Pass host_offsets to have them rejected
+ *                before launch instead.
  *   host_offsets nullable HOST copy of req_offsets, validated when given.
  *   R            number of requests (0 only with T == 0).
  *   Other arguments as xshare_route; params->per_request_budget is m_r.
@@ -136,6 +169,27 @@ xshare_status xshare_select_hier(const float* logits, int32_t T, const int32_t* 
                                  int32_t* topk_ids, float* topk_w, xshare_stats* stats,
                                  void* ws, size_t ws_bytes, hipStream_t stream);
 
+/*
+ * xshare_select_ep -- expert-parallelism-aware selection (Algorithms 5 and 6, Section 5).
+ *
+ *   ep          HOST pointer to the group layout (local_group is ignored here).
+ *   params      budget_mode must be XSHARE_BUDGET_PER_GROUP; budget is m_g >= 0.
+ *   group_load  out, nullable: DEVICE [G] int32, Load_g(S) = |S on group g|.
+ *   Other arguments as xshare_route (workspace from xshare_route_workspace_bytes).
+ *
+ * Starting from the warm-up set S_0, rounds in which every group in turn adds its best
+ * remaining candidate (score descending, index ascending), while |S| < m_g * G at the start
+ * of a round.  A group whose load (warm-up experts included) has reached m_g adds nothing
+ * more (the constraint of Eq. (5)); a group without candidates is skipped; a round that
+ * adds nothing ends the loop.  The warm-up set is never cut, so a group can exceed m_g
+ * through S_0 alone.  If fewer than k experts result, the best remaining candidates are
+ * added regardless of group, so that every token keeps k experts.  Then refinement.
+ */
+xshare_status xshare_select_ep(const float* logits, int32_t T, const xshare_route_params* params,
+                               const xshare_ep_layout* ep, uint8_t* sel_mask, int32_t* topk_ids,
+                               float* topk_w, int32_t* group_load, xshare_stats* stats,
+                               void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Stage boundaries recorded by xshare_moe_forward when stage_events is given.            */
 #define XSHARE_N_STAGE_EVENTS 5  /* start | route | gate-up GEMM | down GEMM | combine end */
 
@@ -148,6 +202,9 @@ xshare_status xshare_select_hier(const float* logits, int32_t T, const int32_t* 
  *   w2       [N, d, f] bf16: down projections.
  *   req_offsets/host_offsets/R: as xshare_select_hier, or req_offsets == NULL for the flat
  *            selection of xshare_route.
+ *   ep       nullable HOST pointer: the expert-parallel selection of xshare_select_ep and,
+ *            with ep->local_group >= 0, one group's share of y (see xshare_ep_layout).
+ *            Not combined with req_offsets (XSHARE_EUNSUPPORTED).
  *   y        out [T, d] bf16: y_i = sum_r w_ir * E_{e_ir}(x_i) with the refined routing
  *            (Section 2.1 without the shared-expert term), E(x) = W2 (silu(W1 x) * (W3 x)),
  *            fp32 accumulation, rounded to bf16 (nearest even) once at the end.
@@ -162,8 +219,9 @@ xshare_status xshare_moe_forward(const uint16_t* x, const float* logits, int32_t
                                  int32_t f, const uint16_t* w1, const uint16_t* w3,
                                  const uint16_t* w2, const xshare_route_params* params,
                                  const int32_t* req_offsets, const int32_t* host_offsets,
-                                 int32_t R, uint16_t* y, uint8_t* sel_mask, int32_t* topk_ids,
-                                 float* topk_w, xshare_stats* stats, void* ws, size_t ws_bytes,
+                                 int32_t R, const xshare_ep_layout* ep, uint16_t* y,
+                                 uint8_t* sel_mask, int32_t* topk_ids, float* topk_w,
+                                 xshare_stats* stats, void* ws, size_t ws_bytes,
                                  void* const* stage_events, hipStream_t stream);
 
 /* Static description of a status code (never NULL).                                      */

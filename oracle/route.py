@@ -352,7 +352,7 @@ def select_ep(h, k: int, k0: int, m_g: int, groups, G: int,
     mask[sorted(S)] = 1
     loads = group_loads(S, gr, G)
     vloads = group_loads(union, gr, G)
-    return Routing(mask, ids, w, s, vids, vg, len(union), len(S0), m_g * G,
+    return Routing(mask, ids, w, s, vids, vg, len(union), len(S0), min(m_g * G, N),
                    extra=dict(loads=loads, max_load=max(loads) if loads else 0,
                               vanilla_loads=vloads, vanilla_max_load=max(vloads)))
 

@@ -17,12 +17,14 @@ using xs::kMaxTopK;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-// Parameter checks shared by every entry point.  `hier` enables the m_r check.
-xshare_status check_params(int32_t T, const xshare_route_params* p, bool hier) {
+// Parameter checks shared by every entry point.  `hier` enables the m_r check; `ep` (GPU
+// groups) requires the per-group budget mode, which is valid only there.
+xshare_status check_params(int32_t T, const xshare_route_params* p, bool hier, bool ep = false) {
   if (!p) return XSHARE_EINVAL;
   if (T < 0 || p->n_experts < 1 || p->top_k < 1 || p->top_k > p->n_experts) return XSHARE_EINVAL;
   if (p->warmup_k0 < 0 || p->warmup_k0 > p->top_k || p->budget < 0) return XSHARE_EINVAL;
-  if (p->budget_mode != XSHARE_BUDGET_TOTAL && p->budget_mode != XSHARE_BUDGET_EXTRA)
+  if (ep ? p->budget_mode != XSHARE_BUDGET_PER_GROUP
+         : (p->budget_mode != XSHARE_BUDGET_TOTAL && p->budget_mode != XSHARE_BUDGET_EXTRA))
     return XSHARE_EINVAL;
   if (p->score_mode != XSHARE_SCORE_TOPK && p->score_mode != XSHARE_SCORE_DENSE)
     return XSHARE_EINVAL;
@@ -46,6 +48,43 @@ xshare_status check_offsets(int32_t T, const int32_t* req_offsets, const int32_t
   return XSHARE_OK;
 }
 
+// GPU-group layout: 1 <= G <= N; equal contiguous blocks need G | N; a host copy of the
+// map is validated; `forward` also checks the local group.
+xshare_status check_ep(int32_t N, const xshare_ep_layout* ep, bool forward) {
+  if (!ep) return XSHARE_OK;
+  const int G = ep->n_groups;
+  if (G < 1 || G > N) return XSHARE_EINVAL;
+  if (!ep->expert_group && N % G != 0) return XSHARE_EINVAL;
+  if (ep->host_expert_group)
+    for (int j = 0; j < N; ++j)
+      if (ep->host_expert_group[j] < 0 || ep->host_expert_group[j] >= G) return XSHARE_EINVAL;
+  if (forward && (ep->local_group < -1 || ep->local_group >= G)) return XSHARE_EINVAL;
+  return XSHARE_OK;
+}
+
+// Bound on the experts the expert GEMMs are launched for (grid size; blocks beyond the
+// device-side count exit at once).  Active experts never exceed the selected set (<= budget
+// under a total budget) nor the (token, slot) pairs.  One group's share also stays within
+// the group and within its load, which is at most max(m_g, |S_0 on the group|) after the
+// rounds, or at most k after a top-up to k experts; |S_0| <= T * k0.
+int layer_bound(int32_t T, const xshare_route_params* p, const xshare_ep_layout* ep) {
+  const int N = p->n_experts, k = p->top_k;
+  int b = xs::active_bound(T, N, k, p->budget_mode, p->budget);
+  if (ep && ep->local_group >= 0) {
+    int size = N;
+    if (!ep->expert_group) {
+      size = N / ep->n_groups;
+    } else if (ep->host_expert_group) {
+      size = 0;
+      for (int j = 0; j < N; ++j) size += ep->host_expert_group[j] == ep->local_group;
+    }
+    const int64_t load = std::max<int64_t>(std::max<int64_t>(p->budget, k),
+                                           (int64_t)T * p->warmup_k0);
+    b = (int)std::min<int64_t>(std::min(b, size), load);
+  }
+  return b;
+}
+
 template <typename P>
 P* at(void* ws, size_t off) {
   return reinterpret_cast<P*>(static_cast<char*>(ws) + off);
@@ -53,9 +92,9 @@ P* at(void* ws, size_t off) {
 
 // Fills the routing arguments; outputs may be redirected to workspace scratch.
 xs::RouteArgs route_args(const float* logits, int32_t T, const xshare_route_params* p,
-                         const int32_t* req_offsets, int32_t R, uint8_t* sel_mask,
-                         int32_t* ids, float* w, xshare_stats* stats, void* ws,
-                         const xs::RouteLayout& L) {
+                         const int32_t* req_offsets, int32_t R, const xshare_ep_layout* ep,
+                         int32_t* group_load, uint8_t* sel_mask, int32_t* ids, float* w,
+                         xshare_stats* stats, void* ws, const xs::RouteLayout& L) {
   xs::RouteArgs a{};
   a.logits = logits;
   a.T = T;
@@ -68,6 +107,10 @@ xs::RouteArgs route_args(const float* logits, int32_t T, const xshare_route_para
   a.m_r = std::min(p->per_request_budget, p->n_experts);
   a.req_offsets = req_offsets;
   a.R = R;
+  a.G = ep ? ep->n_groups : 0;
+  a.group = ep ? ep->expert_group : nullptr;
+  a.local_group = -1;
+  a.group_load = group_load;
   a.sel_mask = sel_mask;
   a.ids = ids ? ids : at<int32_t>(ws, L.ids);
   a.w = w ? w : at<float>(ws, L.w);
@@ -95,8 +138,8 @@ xshare_status route_common(const float* logits, int32_t T, const int32_t* req_of
   const xs::RouteLayout L =
       xs::route_layout(T, p->n_experts, p->top_k, p->score_mode == XSHARE_SCORE_DENSE);
   if (!ws || ws_bytes < L.total) return XSHARE_EWORKSPACE;
-  const xs::RouteArgs a = route_args(logits, T, p, hier ? req_offsets : nullptr, R, sel_mask,
-                                     ids, w, stats, ws, L);
+  const xs::RouteArgs a = route_args(logits, T, p, hier ? req_offsets : nullptr, R, nullptr,
+                                     nullptr, sel_mask, ids, w, stats, ws, L);
   return xs::launch_route(a, stream) == hipSuccess ? XSHARE_OK : XSHARE_EHIP;
 }
 
@@ -105,17 +148,18 @@ xshare_status route_common(const float* logits, int32_t T, const int32_t* req_of
 extern "C" {
 
 size_t xshare_route_workspace_bytes(int32_t T, const xshare_route_params* params) {
-  if (check_params(T, params, false) != XSHARE_OK) return 0;
+  const bool ep = params && params->budget_mode == XSHARE_BUDGET_PER_GROUP;
+  if (check_params(T, params, false, ep) != XSHARE_OK) return 0;
   return xs::route_layout(T, params->n_experts, params->top_k,
                           params->score_mode == XSHARE_SCORE_DENSE)
       .total;
 }
 
 size_t xshare_moe_workspace_bytes(int32_t T, int32_t d, int32_t f,
-                                  const xshare_route_params* params) {
-  if (check_params(T, params, false) != XSHARE_OK || d <= 0 || f <= 0) return 0;
-  const int bound = xs::active_bound(T, params->n_experts, params->top_k, params->budget_mode,
-                                     params->budget);
+                                  const xshare_route_params* params, const xshare_ep_layout* ep) {
+  if (check_params(T, params, false, ep != nullptr) != XSHARE_OK || d <= 0 || f <= 0) return 0;
+  if (check_ep(params->n_experts, ep, true) != XSHARE_OK) return 0;
+  const int bound = layer_bound(T, params, ep);
   return xs::ffn_layout(T, params->n_experts, params->top_k,
                         params->score_mode == XSHARE_SCORE_DENSE, d, f, bound)
       .total;
@@ -137,27 +181,49 @@ xshare_status xshare_select_hier(const float* logits, int32_t T, const int32_t* 
                       topk_w, stats, ws, ws_bytes, stream);
 }
 
+xshare_status xshare_select_ep(const float* logits, int32_t T, const xshare_route_params* params,
+                               const xshare_ep_layout* ep, uint8_t* sel_mask, int32_t* topk_ids,
+                               float* topk_w, int32_t* group_load, xshare_stats* stats,
+                               void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!ep) return XSHARE_EINVAL;
+  xshare_status st = check_params(T, params, false, true);
+  if (st != XSHARE_OK) return st;
+  st = check_ep(params->n_experts, ep, false);
+  if (st != XSHARE_OK) return st;
+  if (!sel_mask || (T > 0 && (!logits || !topk_ids || !topk_w))) return XSHARE_EINVAL;
+  const xs::RouteLayout L = xs::route_layout(T, params->n_experts, params->top_k,
+                                             params->score_mode == XSHARE_SCORE_DENSE);
+  if (!ws || ws_bytes < L.total) return XSHARE_EWORKSPACE;
+  const xs::RouteArgs a = route_args(logits, T, params, nullptr, 0, ep, group_load, sel_mask,
+                                     topk_ids, topk_w, stats, ws, L);
+  return xs::launch_route(a, stream) == hipSuccess ? XSHARE_OK : XSHARE_EHIP;
+}
+
 xshare_status xshare_moe_forward(const uint16_t* x, const float* logits, int32_t T, int32_t d,
                                  int32_t f, const uint16_t* w1, const uint16_t* w3,
                                  const uint16_t* w2, const xshare_route_params* params,
                                  const int32_t* req_offsets, const int32_t* host_offsets,
-                                 int32_t R, uint16_t* y, uint8_t* sel_mask, int32_t* topk_ids,
-                                 float* topk_w, xshare_stats* stats, void* ws, size_t ws_bytes,
+                                 int32_t R, const xshare_ep_layout* ep, uint16_t* y,
+                                 uint8_t* sel_mask, int32_t* topk_ids, float* topk_w,
+                                 xshare_stats* stats, void* ws, size_t ws_bytes,
                                  void* const* stage_events, hipStream_t stream) {
   const bool hier = req_offsets != nullptr;
-  xshare_status st = check_params(T, params, hier);
+  if (hier && ep) return XSHARE_EUNSUPPORTED;
+  xshare_status st = check_params(T, params, hier, ep != nullptr);
   if (st != XSHARE_OK) return st;
   if (hier) {
     st = check_offsets(T, req_offsets, host_offsets, R);
     if (st != XSHARE_OK) return st;
   }
+  st = check_ep(params->n_experts, ep, true);
+  if (st != XSHARE_OK) return st;
   if (d <= 0 || f <= 0) return XSHARE_EINVAL;
   if (d % xs::kDimAlign != 0 || f % xs::kDimAlign != 0) return XSHARE_EUNSUPPORTED;
   if (T > 0 && (!x || !logits || !w1 || !w3 || !w2 || !y)) return XSHARE_EINVAL;
   if (!aligned16(x) || !aligned16(w1) || !aligned16(w3) || !aligned16(w2) || !aligned16(y))
     return XSHARE_EINVAL;
   const int N = params->n_experts, k = params->top_k;
-  const int bound = xs::active_bound(T, N, k, params->budget_mode, params->budget);
+  const int bound = layer_bound(T, params, ep);
   const xs::FfnLayout L =
       xs::ffn_layout(T, N, k, params->score_mode == XSHARE_SCORE_DENSE, d, f, bound);
   if (!ws || ws_bytes < L.total) return XSHARE_EWORKSPACE;
@@ -169,8 +235,9 @@ xshare_status xshare_moe_forward(const uint16_t* x, const float* logits, int32_t
     return hipEventRecord(static_cast<hipEvent_t>(stage_events[s]), stream) == hipSuccess;
   };
   if (!record(0)) return XSHARE_EHIP;
-  const xs::RouteArgs ra = route_args(logits, T, params, hier ? req_offsets : nullptr, R, mask,
-                                      topk_ids, topk_w, stats, ws, L.route);
+  xs::RouteArgs ra = route_args(logits, T, params, hier ? req_offsets : nullptr, R, ep, nullptr,
+                                mask, topk_ids, topk_w, stats, ws, L.route);
+  if (ep) ra.local_group = ep->local_group;
   if (xs::launch_route(ra, stream) != hipSuccess || !record(1)) return XSHARE_EHIP;
   if (T == 0) {
     for (int s = 2; s < XSHARE_N_STAGE_EVENTS; ++s)
@@ -188,10 +255,11 @@ xshare_status xshare_moe_forward(const uint16_t* x, const float* logits, int32_t
   fa.k = k;
   fa.d = d;
   fa.f = f;
-  // Active experts never exceed the selected set (<= budget under a total budget) nor the
-  // number of (token, slot) pairs; blocks beyond the device-side count exit at once.
   fa.max_active = bound;
   fa.splits = L.splits;
+  fa.G = ra.G;
+  fa.group = ra.group;
+  fa.local_group = ra.local_group;
   fa.offsets = ra.offsets;
   fa.perm = ra.perm;
   fa.active = ra.active;

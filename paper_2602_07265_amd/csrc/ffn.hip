@@ -233,7 +233,10 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(FfnArgs a) {
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
   for (int r = 0; r < a.k; ++r) {
     const int slot = i * a.k + r;
-    if (a.ids[slot] < 0) continue;
+    const int e = a.ids[slot];
+    if (e < 0) continue;
+    if (a.local_group >= 0 && (a.group ? a.group[e] : e / (a.N / a.G)) != a.local_group)
+      continue;   // another GPU group's term of y_i
     const float wr = a.w[slot];
     float4 v = *reinterpret_cast<const float4*>(a.yslot + (size_t)slot * a.d + c);
     for (int s = 1; s < a.splits; ++s) {   // partial sums of a split reduction, in order

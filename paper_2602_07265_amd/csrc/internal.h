@@ -95,6 +95,10 @@ struct RouteArgs {
   int T, N, k, k0, budget, budget_mode, score_mode, m_r;
   const int32_t* req_offsets;  // nullptr: flat Algorithm 2
   int R;
+  int G;                       // GPU groups (Algorithms 5-6); 0: no groups
+  const int32_t* group;        // [N] group of each expert; nullptr: contiguous blocks of N / G
+  int local_group;             // >= 0: only this group's experts are listed as active
+  int32_t* group_load;         // nullable [G] output
   uint8_t* sel_mask;
   int32_t* ids;
   float* w;
@@ -116,6 +120,9 @@ struct FfnArgs {
   int T, N, k, d, f;
   int max_active;              // host bound on the number of active experts (grid size)
   int splits;                  // K-splits of the down GEMM (partials summed in the combine)
+  int G;                       // GPU groups, with `group` and `local_group` as in RouteArgs
+  const int32_t* group;
+  int local_group;
   const int32_t* offsets;
   const int32_t* perm;
   const int32_t* active;

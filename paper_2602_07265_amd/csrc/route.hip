@@ -273,6 +273,9 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   __shared__ float s_seed_h[kWaves][kMaxTopK];
   __shared__ int s_wsum[kWaves];
   __shared__ int s_cnt[8];
+  __shared__ int s_gload[kMaxExperts];   // GPU groups: warm-up experts per group, then |S| per group
+  __shared__ int s_gcand[kMaxExperts];   // candidates per group outside the warm-up set
+  __shared__ int s_hist[kMaxExperts];    // takeable candidates per rank inside their group
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -280,6 +283,7 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   const int T = a.T, N = a.N, k = a.k, k0 = a.k0;
   const bool dense = a.score_mode == 1;
   const bool hier = a.req_offsets != nullptr;
+  const bool ep = a.G > 0;
   const bool occ = T <= kOccTokens;
   const int TK = T * k;
   const int TK8 = (TK + 7) & ~7;
@@ -288,11 +292,15 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   for (int j = tid; j < kMaxExperts; j += kThreads) {
     s_tier1[j] = 0;
     s_occ[j] = 0;
+    s_gload[j] = 0;
+    s_gcand[j] = 0;
+    s_hist[j] = 0;
   }
   for (int p = TK + tid; p < TK8; p += kThreads) s_ent[p] = (uint16_t)kNoEntry;
   __syncthreads();
 
-  // ---- request offsets must be 0 = o_0 < o_1 < ... < o_R = T (checked in parallel)
+  // ---- request offsets must be 0 = o_0 < o_1 < ... < o_R = T and every expert's group must
+  //      lie in [0, G) (checked in parallel); otherwise the call selects nothing
   if (hier) {
     const int R = a.R;
     for (int r = tid; r < R; r += kThreads) {
@@ -300,6 +308,11 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
       if (!(lo < hi) || lo < 0 || hi > T) atomicOr(&s_cnt[7], 1);
     }
     if (tid == 0 && (a.req_offsets[0] != 0 || a.req_offsets[R] != T)) atomicOr(&s_cnt[7], 1);
+  }
+  if (ep && a.group)
+    for (int jj = tid; jj < N; jj += kThreads)
+      if (a.group[jj] < 0 || a.group[jj] >= a.G) atomicOr(&s_cnt[7], 1);
+  if (hier || (ep && a.group)) {
     __syncthreads();
     if (s_cnt[7]) {
       for (int j = tid; j < N; j += kThreads) a.sel_mask[j] = 0;
@@ -308,6 +321,8 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
         a.w[p] = 0.0f;
       }
       for (int j = tid; j <= N; j += kThreads) a.offsets[j] = 0;
+      if (a.group_load)
+        for (int g = tid; g < a.G; g += kThreads) a.group_load[g] = 0;
       if (tid == 0) {
         a.counters[kCntActive] = 0;
         a.counters[kCntSelected] = 0;
@@ -465,35 +480,128 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   //      order (tier, score desc, index asc), keep the first budget_eff candidates.
   //      Key: (3 - tier) << 42 | ord(score) << 10 | (1023 - j); candidates are compacted
   //      and each counts the candidates ahead of it.
-  int tier = 3;
-  uint64_t mykey = 0;
-  if (j < N) {
-    const bool cand = dense ? (T > 0) : inU;
-    tier = inS0 ? 0 : (s_tier1[j] ? 1 : (cand ? 2 : 3));
-    if (tier < 3)
-      mykey = ((uint64_t)(3 - tier) << 42) | ((uint64_t)ord(s) << 10) | (uint64_t)(1023 - j);
-    if (tier == 0) atomicAdd(&s_cnt[1], 1);
-    if (tier <= 1) atomicAdd(&s_cnt[2], 1);
-    if (inU) atomicAdd(&s_cnt[3], 1);
-  }
-  int n_cand = 0;
-  const int cpos = block_excl_scan(mykey != 0 ? 1 : 0, s_wsum, n_cand);
-  if (mykey != 0) s_key[cpos] = mykey;
-  if (tid == 0 && (n_cand & 1)) s_key[n_cand] = 0;
-  __syncthreads();
-  const int n_s0 = s_cnt[1], n_start = s_cnt[2], n_u = s_cnt[3];
-  const int base = a.budget_mode == 0 ? a.budget : n_start + a.budget;
-  const int m_eff = max(min(base, n_cand), min(k, n_cand));
   bool sel = false;
-  if (mykey != 0) {
-    const ulonglong2* keys2 = reinterpret_cast<const ulonglong2*>(s_key);
-    int rank = 0;
-    const int n2 = (n_cand + 1) >> 1;
-    for (int jj = 0; jj < n2; ++jj) {
-      const ulonglong2 kk = keys2[jj];
-      rank += (kk.x > mykey) + (kk.y > mykey);
+  int n_s0 = 0, n_start = 0, n_u = 0, m_eff = 0, max_load = 0;
+  if (!ep) {
+    int tier = 3;
+    uint64_t mykey = 0;
+    if (j < N) {
+      const bool cand = dense ? (T > 0) : inU;
+      tier = inS0 ? 0 : (s_tier1[j] ? 1 : (cand ? 2 : 3));
+      if (tier < 3)
+        mykey = ((uint64_t)(3 - tier) << 42) | ((uint64_t)ord(s) << 10) | (uint64_t)(1023 - j);
+      if (tier == 0) atomicAdd(&s_cnt[1], 1);
+      if (tier <= 1) atomicAdd(&s_cnt[2], 1);
+      if (inU) atomicAdd(&s_cnt[3], 1);
     }
-    sel = rank < m_eff;
+    int n_cand = 0;
+    const int cpos = block_excl_scan(mykey != 0 ? 1 : 0, s_wsum, n_cand);
+    if (mykey != 0) s_key[cpos] = mykey;
+    if (tid == 0 && (n_cand & 1)) s_key[n_cand] = 0;
+    __syncthreads();
+    n_s0 = s_cnt[1];
+    n_start = s_cnt[2];
+    n_u = s_cnt[3];
+    const int base = a.budget_mode == 0 ? a.budget : n_start + a.budget;
+    m_eff = max(min(base, n_cand), min(k, n_cand));
+    if (mykey != 0) {
+      const ulonglong2* keys2 = reinterpret_cast<const ulonglong2*>(s_key);
+      int rank = 0;
+      const int n2 = (n_cand + 1) >> 1;
+      for (int jj = 0; jj < n2; ++jj) {
+        const ulonglong2 kk = keys2[jj];
+        rank += (kk.x > mykey) + (kk.y > mykey);
+      }
+      sel = rank < m_eff;
+    }
+  } else {
+    // GPU groups (Algorithms 5 and 6).  Group g can take a_g = m_g - |S_0 on g| experts
+    // (m_g caps every group's load, Eq. (5)), one per round, best first; its candidate of
+    // rank r (score desc, index asc, among its candidates outside S_0) is taken in round
+    // r + 1 if r < a_g.  The loop stops after the fewest rounds R that bring |S| to m_g * G,
+    // or when no group can take more; so S = S_0 plus every takeable candidate of rank < R,
+    // and R follows from a prefix count of the takeable candidates by rank.
+    const int G = a.G, m_g = a.budget;
+    const int gj = j < N ? (a.group ? a.group[j] : j / (N / G)) : 0;
+    const bool cand = j < N && (dense ? (T > 0) : inU);
+    const bool pick = cand && !inS0;
+    if (j < N) {
+      if (inS0) {
+        atomicAdd(&s_gload[gj], 1);
+        atomicAdd(&s_cnt[1], 1);
+      }
+      if (pick) atomicAdd(&s_gcand[gj], 1);
+      if (inU) atomicAdd(&s_cnt[3], 1);
+      if (cand) atomicAdd(&s_cnt[5], 1);
+    }
+    // key: group << 44 | ord(score) << 10 | (1023 - j); the rank counts the group's keys above
+    const uint64_t pkey =
+        pick ? ((uint64_t)gj << 44) | ((uint64_t)ord(s) << 10) | (uint64_t)(1023 - j) : 0;
+    int n_pick = 0;
+    const int ppos = block_excl_scan(pick ? 1 : 0, s_wsum, n_pick);
+    if (pick) s_key[ppos] = pkey;
+    if (tid == 0 && (n_pick & 1)) s_key[n_pick] = 0;
+    __syncthreads();
+    int rank = 0;
+    bool takeable = false;
+    if (pick) {
+      const ulonglong2* keys2 = reinterpret_cast<const ulonglong2*>(s_key);
+      const uint64_t mine = (uint64_t)gj;
+      const int n2 = (n_pick + 1) >> 1;
+      for (int jj = 0; jj < n2; ++jj) {
+        const ulonglong2 kk = keys2[jj];
+        rank += ((kk.x >> 44) == mine && kk.x > pkey) + ((kk.y >> 44) == mine && kk.y > pkey);
+      }
+      takeable = rank < m_g - s_gload[gj];
+      if (takeable) atomicAdd(&s_hist[rank], 1);
+    }
+    __syncthreads();
+    n_s0 = s_cnt[1];
+    n_u = s_cnt[3];
+    const int n_cand = s_cnt[5];
+    const int need = m_g * G - n_s0;          // picks the rounds must reach
+    static_assert(kThreads == kMaxExperts, "one rank of s_hist per thread");
+    const int at_rank = s_hist[tid];
+    int n_take = 0;
+    const int before = block_excl_scan(at_rank, s_wsum, n_take);
+    if (need > 0 && before < need && before + at_rank >= need) s_cnt[6] = tid + 1;
+    __syncthreads();
+    const int rounds = need <= 0 ? 0 : (n_take < need ? kMaxExperts : s_cnt[6]);
+    sel = inS0 || (takeable && rank < rounds);
+    if (sel) atomicAdd(&s_cnt[2], 1);
+    __syncthreads();
+    // fewer than k experts: the best remaining candidates join regardless of group
+    const int n_loop = s_cnt[2], want = min(k, n_cand);
+    if (n_loop < want) {
+      const bool rest = cand && !sel;
+      const uint64_t fkey = rest ? ((uint64_t)ord(s) << 10) | (uint64_t)(1023 - j) : 0;
+      int n_rest = 0;
+      const int fpos = block_excl_scan(rest ? 1 : 0, s_wsum, n_rest);
+      if (rest) s_key[fpos] = fkey;
+      if (tid == 0 && (n_rest & 1)) s_key[n_rest] = 0;
+      __syncthreads();
+      if (rest) {
+        const ulonglong2* keys2 = reinterpret_cast<const ulonglong2*>(s_key);
+        int r2 = 0;
+        const int n2 = (n_rest + 1) >> 1;
+        for (int jj = 0; jj < n2; ++jj) {
+          const ulonglong2 kk = keys2[jj];
+          r2 += (kk.x > fkey) + (kk.y > fkey);
+        }
+        sel = r2 < want - n_loop;
+      }
+    }
+    // Load_g(S) and MaxLoad(S) (Section 5.1)
+    if (tid < G) s_gload[tid] = 0;
+    __syncthreads();
+    if (sel) atomicAdd(&s_gload[gj], 1);
+    __syncthreads();
+    if (tid < G) {
+      if (a.group_load) a.group_load[tid] = s_gload[tid];
+      atomicMax(&s_cnt[0], s_gload[tid]);
+    }
+    n_start = n_s0;
+    m_eff = min(m_g * G, N);
   }
   if (j < N) {
     s_sel[j] = sel;
@@ -501,6 +609,7 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
     if (sel) atomicAdd(&s_cnt[4], 1);
   }
   __syncthreads();
+  if (ep) max_load = s_cnt[0];
 
   // ---- (e) refinement: every token to its top-k inside S, gates renormalised (Section 3.4).
   //      The token's plain top-k experts that are in S are its first refined ranks (in
@@ -587,12 +696,16 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
       }
     }
   }
+  // with a local GPU group only that group's experts are listed for the expert GEMMs
+  const bool listed = j < N && cnt > 0 &&
+                      (a.local_group < 0 ||
+                       (a.group ? a.group[j] : j / (N / a.G)) == a.local_group);
   int n_active = 0;
-  const int arank = block_excl_scan(cnt > 0 ? 1 : 0, s_wsum, n_active);
+  const int arank = block_excl_scan(listed ? 1 : 0, s_wsum, n_active);
   if (j < N) {
     a.offsets[j] = off;
     if (j == N - 1) a.offsets[N] = off + cnt;
-    if (cnt > 0) a.active[arank] = j;
+    if (listed) a.active[arank] = j;
   }
   if (tid == 0) {
     a.counters[kCntActive] = n_active;
@@ -605,7 +718,7 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
       a.stats[3] = n_s0;
       a.stats[4] = n_start;
       a.stats[5] = m_eff;
-      a.stats[6] = 0;
+      a.stats[6] = max_load;
       a.stats[7] = 0;
     }
   }

@@ -16,7 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libxshare.so")
 
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP = 0, 1, 2, 3, 4
-BUDGET = {"total": 0, "extra": 1}
+BUDGET = {"total": 0, "extra": 1, "per_group": 2}
 SCORE = {"topk": 0, "dense": 1}
 N_STAGE_EVENTS = 5
 STAGES = ("route", "gate_up", "down", "combine")
@@ -34,8 +34,17 @@ class RouteParams(ctypes.Structure):
     ]
 
 
+class EpLayout(ctypes.Structure):
+    _fields_ = [
+        ("n_groups", ctypes.c_int32),
+        ("local_group", ctypes.c_int32),
+        ("expert_group", ctypes.c_void_p),
+        ("host_expert_group", ctypes.c_void_p),
+    ]
+
+
 STATS_FIELDS = ("n_selected", "n_active", "n_vanilla_union", "n_warmup", "n_start",
-                "budget_eff")
+                "budget_eff", "max_group_load")
 
 
 class XShareError(RuntimeError):
@@ -60,7 +69,8 @@ def lib() -> ctypes.CDLL:
         L = ctypes.CDLL(LIB_PATH)
         L.xshare_route_workspace_bytes.argtypes = [_I32, ctypes.POINTER(RouteParams)]
         L.xshare_route_workspace_bytes.restype = _SZ
-        L.xshare_moe_workspace_bytes.argtypes = [_I32, _I32, _I32, ctypes.POINTER(RouteParams)]
+        L.xshare_moe_workspace_bytes.argtypes = [_I32, _I32, _I32, ctypes.POINTER(RouteParams),
+                                                 ctypes.POINTER(EpLayout)]
         L.xshare_moe_workspace_bytes.restype = _SZ
         L.xshare_route.argtypes = [_P, _I32, ctypes.POINTER(RouteParams), _P, _P, _P, _P, _P, _SZ,
                                    _P]
@@ -68,9 +78,13 @@ def lib() -> ctypes.CDLL:
         L.xshare_select_hier.argtypes = [_P, _I32, _P, _P, _I32, ctypes.POINTER(RouteParams), _P,
                                          _P, _P, _P, _P, _SZ, _P]
         L.xshare_select_hier.restype = ctypes.c_int
+        L.xshare_select_ep.argtypes = [_P, _I32, ctypes.POINTER(RouteParams),
+                                       ctypes.POINTER(EpLayout), _P, _P, _P, _P, _P, _P, _SZ, _P]
+        L.xshare_select_ep.restype = ctypes.c_int
         L.xshare_moe_forward.argtypes = [_P, _P, _I32, _I32, _I32, _P, _P, _P,
-                                         ctypes.POINTER(RouteParams), _P, _P, _I32, _P, _P, _P, _P,
-                                         _P, _P, _SZ, _P, _P]
+                                         ctypes.POINTER(RouteParams), _P, _P, _I32,
+                                         ctypes.POINTER(EpLayout), _P, _P, _P, _P, _P, _P, _SZ, _P,
+                                         _P]
         L.xshare_moe_forward.restype = ctypes.c_int
         L.xshare_status_string.argtypes = [_I32]
         L.xshare_status_string.restype = ctypes.c_char_p
@@ -100,8 +114,35 @@ def route_workspace_bytes(T: int, p: RouteParams) -> int:
     return int(lib().xshare_route_workspace_bytes(int(T), ctypes.byref(p)))
 
 
-def moe_workspace_bytes(T: int, d: int, f: int, p: RouteParams) -> int:
-    return int(lib().xshare_moe_workspace_bytes(int(T), int(d), int(f), ctypes.byref(p)))
+def moe_workspace_bytes(T: int, d: int, f: int, p: RouteParams, ep=None) -> int:
+    """``ep``: an EpLayout (see ep_layout) or None."""
+    return int(lib().xshare_moe_workspace_bytes(int(T), int(d), int(f), ctypes.byref(p),
+                                                None if ep is None else ctypes.byref(ep)))
+
+
+class GroupMap:
+    """GPU groups of the experts for expert parallelism: ``groups`` None (equal contiguous
+    blocks of N / G) or a per-expert sequence / device int32 tensor of group ids."""
+
+    def __init__(self, n_groups: int, groups=None, local_group: int = -1, device="cuda"):
+        self.host = None
+        self.dev = None
+        if groups is not None:
+            if isinstance(groups, torch.Tensor) and groups.is_cuda:
+                self.dev = _dev(groups, torch.int32, (groups.numel(),), "expert_group")
+            else:
+                self.host = torch.as_tensor([int(v) for v in groups], dtype=torch.int32)
+                self.dev = self.host.to(device)
+        self.layout = EpLayout(int(n_groups), int(local_group),
+                               None if self.dev is None else self.dev.data_ptr(),
+                               None if self.host is None else self.host.data_ptr())
+
+    def with_local(self, local_group: int) -> "GroupMap":
+        g = GroupMap.__new__(GroupMap)
+        g.host, g.dev = self.host, self.dev
+        g.layout = EpLayout(self.layout.n_groups, int(local_group), self.layout.expert_group,
+                            self.layout.host_expert_group)
+        return g
 
 
 # ----------------------------------------------------------------------------- helpers
@@ -182,6 +223,35 @@ def _route_impl(logits, p, req_offsets, out, workspace, stream):
     return dict(sel_mask=sel, ids=ids, w=w, stats=stats)
 
 
+def select_ep(logits: torch.Tensor, groups: GroupMap, top_k: int, warmup_k0: int,
+              per_group_budget: int, score_mode="topk", *, out=None, workspace=None,
+              stream=None) -> dict:
+    """Algorithms 5-6 on the GPU: dict(sel_mask, ids, w, stats, group_load)."""
+    T, N = logits.shape
+    dev = logits.device
+    _dev(logits, torch.float32, (T, N), "logits")
+    p = params(N, top_k, warmup_k0, per_group_budget, "per_group", score_mode)
+    G = groups.layout.n_groups
+    out = dict(out or {})
+    sel = out.get("sel_mask") if out.get("sel_mask") is not None else torch.empty(N, dtype=torch.uint8, device=dev)
+    ids = out.get("ids") if out.get("ids") is not None else torch.empty((T, top_k), dtype=torch.int32, device=dev)
+    w = out.get("w") if out.get("w") is not None else torch.empty((T, top_k), dtype=torch.float32, device=dev)
+    stats = out.get("stats") if out.get("stats") is not None else torch.empty(8, dtype=torch.int32, device=dev)
+    load = out.get("group_load") if out.get("group_load") is not None else torch.empty(max(G, 1), dtype=torch.int32, device=dev)
+    _dev(sel, torch.uint8, (N,), "sel_mask")
+    _dev(ids, torch.int32, (T, top_k), "ids")
+    _dev(w, torch.float32, (T, top_k), "w")
+    _dev(stats, torch.int32, (8,), "stats")
+    need = route_workspace_bytes(T, p)
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    st = lib().xshare_select_ep(_ptr(logits), T, ctypes.byref(p), ctypes.byref(groups.layout),
+                                _ptr(sel), _ptr(ids), _ptr(w), _ptr(load), _ptr(stats),
+                                _ptr(workspace), workspace.numel(), _stream(stream))
+    _check(st, "xshare_select_ep")
+    return dict(sel_mask=sel, ids=ids, w=w, stats=stats, group_load=load)
+
+
 def route(logits: torch.Tensor, top_k: int, warmup_k0: int, budget: int, budget_mode="total",
           score_mode="topk", *, out=None, workspace=None, stream=None) -> dict:
     """Algorithm 2 on the GPU: returns dict(sel_mask, ids, w, stats) device tensors."""
@@ -201,9 +271,12 @@ def select_hier(logits: torch.Tensor, req_offsets, top_k: int, warmup_k0: int,
 def moe_forward(x: torch.Tensor, logits: torch.Tensor, w1: torch.Tensor, w3: torch.Tensor,
                 w2: torch.Tensor, top_k: int, warmup_k0: int, budget: int, budget_mode="total",
                 score_mode="topk", *, req_offsets=None, per_request_budget: int = 0,
-                y=None, routing_out=True, workspace=None, stage_events=None,
-                stream=None) -> dict:
-    """The MoE layer: returns dict(y [T,d] bf16, and sel_mask/ids/w/stats if routing_out)."""
+                groups: GroupMap | None = None, y=None, routing_out=True, workspace=None,
+                stage_events=None, stream=None) -> dict:
+    """The MoE layer: returns dict(y [T,d] bf16, and sel_mask/ids/w/stats if routing_out).
+
+    With ``groups`` the selection is Algorithms 5-6 (``budget`` is m_g, budget_mode is
+    ignored) and, if groups has a local group, y is that group's share of the layer."""
     T, d = x.shape
     N = logits.shape[1]
     f = w1.shape[1]
@@ -213,7 +286,10 @@ def moe_forward(x: torch.Tensor, logits: torch.Tensor, w1: torch.Tensor, w3: tor
     _dev(w1, torch.bfloat16, (N, f, d), "w1")
     _dev(w3, torch.bfloat16, (N, f, d), "w3")
     _dev(w2, torch.bfloat16, (N, d, f), "w2")
+    if groups is not None:
+        budget_mode = "per_group"
     p = params(N, top_k, warmup_k0, budget, budget_mode, score_mode, per_request_budget)
+    ep = None if groups is None else groups.layout
     if y is None:
         y = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
     _dev(y, torch.bfloat16, (T, d), "y")
@@ -223,7 +299,7 @@ def moe_forward(x: torch.Tensor, logits: torch.Tensor, w1: torch.Tensor, w3: tor
                    ids=torch.empty((T, top_k), dtype=torch.int32, device=dev),
                    w=torch.empty((T, top_k), dtype=torch.float32, device=dev),
                    stats=torch.empty(8, dtype=torch.int32, device=dev))
-    need = moe_workspace_bytes(T, d, f, p)
+    need = moe_workspace_bytes(T, d, f, p, ep)
     if workspace is None:
         workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
     d_off = h_off = None
@@ -238,7 +314,8 @@ def moe_forward(x: torch.Tensor, logits: torch.Tensor, w1: torch.Tensor, w3: tor
         ev = (ctypes.c_void_p * N_STAGE_EVENTS)(*[e.handle for e in stage_events])
     st = lib().xshare_moe_forward(
         _ptr(x), _ptr(logits), T, d, f, _ptr(w1), _ptr(w3), _ptr(w2), ctypes.byref(p),
-        _ptr(d_off), None if h_off is None else ctypes.c_void_p(h_off.data_ptr()), R, _ptr(y),
+        _ptr(d_off), None if h_off is None else ctypes.c_void_p(h_off.data_ptr()), R,
+        None if ep is None else ctypes.byref(ep), _ptr(y),
         _ptr(res.get("sel_mask")), _ptr(res.get("ids")), _ptr(res.get("w")),
         _ptr(res.get("stats")), _ptr(workspace), workspace.numel(), ev, _stream(stream))
     _check(st, "xshare_moe_forward")

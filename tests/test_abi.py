@@ -26,7 +26,8 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert {"xshare_route", "xshare_select_hier", "xshare_moe_forward"} <= set(names)
+    assert {"xshare_route", "xshare_select_hier", "xshare_select_ep",
+            "xshare_moe_forward"} <= set(names)
     lib = X.lib()
     for n in names:
         assert hasattr(lib, n), n
@@ -125,7 +126,8 @@ def test_moe_forward_validation():
 
     def call(d=64, f=128, x=FAKE, y=FAKE, ws=None, T=8):
         return L.xshare_moe_forward(x, FAKE, T, d, f, FAKE, FAKE, FAKE, ctypes.byref(p), None,
-                                    None, 0, y, None, None, None, None, ws, 1 << 30, None, None)
+                                    None, 0, None, y, None, None, None, None, ws, 1 << 30, None,
+                                    None)
 
     assert call(d=48) == X.EUNSUPPORTED
     assert call(f=100) == X.EUNSUPPORTED
@@ -140,3 +142,53 @@ def test_binding_refuses_cpu_tensors():
     import torch
     with pytest.raises(ValueError):
         X.route(torch.zeros(4, 16), 2, 1, 8)
+
+
+def _ep(G, local=-1, host=None, dev=None):
+    arr = None if host is None else (ctypes.c_int32 * len(host))(*host)
+    lay = X.EpLayout(G, local, dev, None if arr is None else ctypes.addressof(arr))
+    lay._keep = arr
+    return lay
+
+
+def test_select_ep_validation():
+    L = X.lib()
+    pg = X.params(16, 2, 1, 3, "per_group")
+
+    def call(ep, pp=pg, ws=None):
+        return L.xshare_select_ep(FAKE, 8, ctypes.byref(pp), None if ep is None else ctypes.byref(ep),
+                                  FAKE, FAKE, FAKE, None, None, ws, 0 if ws is None else 1 << 30,
+                                  None)
+
+    assert call(None) == X.EINVAL                               # the layout is required
+    assert call(_ep(4), pp=X.params(16, 2, 1, 8)) == X.EINVAL   # needs the per-group mode
+    assert call(_ep(0)) == X.EINVAL
+    assert call(_ep(17)) == X.EINVAL                            # more groups than experts
+    assert call(_ep(3)) == X.EINVAL                             # 3 does not divide 16
+    assert call(_ep(3, dev=1 << 20)) == X.EWORKSPACE            # any map on the device is fine
+    assert call(_ep(2, host=[0] * 15 + [2], dev=1 << 20)) == X.EINVAL   # group id out of range
+    assert call(_ep(2, host=[0, 1] * 8, dev=1 << 20)) == X.EWORKSPACE
+    assert call(_ep(4), pp=X.params(16, 2, 1, -1, "per_group")) == X.EINVAL
+    assert call(_ep(4)) == X.EWORKSPACE
+    # the per-group mode is refused without groups
+    assert _route(X.params(16, 2, 1, 8, "per_group")) == X.EINVAL
+
+
+def test_moe_forward_ep_validation():
+    L = X.lib()
+    pg = X.params(16, 2, 1, 3, "per_group")
+
+    def call(ep, pp=pg, offsets=None, R=0):
+        return L.xshare_moe_forward(FAKE, FAKE, 8, 64, 128, FAKE, FAKE, FAKE, ctypes.byref(pp),
+                                    offsets, None, R, None if ep is None else ctypes.byref(ep),
+                                    FAKE, None, None, None, None, None, 1 << 30, None, None)
+
+    assert call(_ep(4, local=4)) == X.EINVAL                    # local group out of range
+    assert call(_ep(4, local=-2)) == X.EINVAL
+    assert call(_ep(4, local=3)) == X.EWORKSPACE
+    assert call(_ep(4), offsets=FAKE, R=2) == X.EUNSUPPORTED    # not with request offsets
+    assert call(None, pp=pg) == X.EINVAL                        # per-group mode needs groups
+    full = X.moe_workspace_bytes(32, 7168, 2048, X.params(256, 8, 1, 5, "per_group"), _ep(8))
+    share = X.moe_workspace_bytes(32, 7168, 2048, X.params(256, 8, 1, 5, "per_group"), _ep(8, 0))
+    assert full > 0 and share > 0
+    assert X.moe_workspace_bytes(32, 7168, 2048, X.params(256, 8, 1, 5, "per_group"), None) == 0
