@@ -10,6 +10,13 @@ All inputs are resident in HBM before timing; steps rotate over several batches 
 step selects its own experts.  Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps 50] [--warmup 5]
+
+Expert parallelism (Section 5, Algorithms 5-6): ``--ep-groups G --per-group-budget m_g``
+spreads the experts over G GPU groups (equal contiguous blocks) and times, batch by
+batch, every group's share of the layer on this GPU (its experts only, partial y); the
+layer time of a batch is the slowest share (the combining collective is not included).
+Prints group loads (MaxLoad) against plain top-k routing and against the flat selection
+with the same total budget m_g * G.
 """
 from __future__ import annotations
 
@@ -27,6 +34,7 @@ METRIC = "MoE-layer µs/batch + HBM GB/s (N=256,k=8,B=32); experts activated/bat
 WORKLOAD_NAMES = {
     "ds_t32": "deepseek_r1_routed_moe_T{T}_N{N}_k{k}_d{d}_f{f}_M{M}_k0{k0}",
     "ds_t8": "deepseek_r1_routed_moe_T{T}_N{N}_k{k}_d{d}_f{f}_M{M}_k0{k0}",
+    "ds_t16": "deepseek_r1_routed_moe_T{T}_N{N}_k{k}_d{d}_f{f}_M{M}_k0{k0}",
     "ds_iid_t8": "deepseek_r1_iid_routing_T{T}_N{N}_k{k}_d{d}_f{f}_M{M}_k0{k0}",
     "ds_iid_t32": "deepseek_r1_iid_routing_T{T}_N{N}_k{k}_d{d}_f{f}_M{M}_k0{k0}",
     "qwen": "qwen_moe_T{T}_N{N}_k{k}_d{d}_f{f}_M{M}_k0{k0}",
@@ -57,6 +65,9 @@ def parse():
                     help="weight copies rotated over (default: enough for >= 4 GB of weights)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-vanilla", action="store_true")
+    ap.add_argument("--ep-groups", type=int, default=0,
+                    help="G > 0: expert-parallel selection and per-group shares")
+    ap.add_argument("--per-group-budget", type=int, default=5, help="m_g (with --ep-groups)")
     return ap.parse_args()
 
 
@@ -99,6 +110,8 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     X.lib()
+    if args.ep_groups > 0:
+        return run_ep(args, W, X, np, torch)
     dev = "cuda:0"
     cfg = dict(W.CONFIGS[args.workload])
     T, N, k, d, f = cfg["T"], cfg["N"], cfg["k"], cfg["d"], cfg["f"]
@@ -228,6 +241,109 @@ def main():
                      "avg_launch_us": round(float(gu_ms.mean()) * 1e3, 2)},
         "cpu_baseline": cpu,
         "wall_s_timed": round(wall, 3),
+    }
+    print(json.dumps(out), flush=True)
+
+
+def run_ep(args, W, X, np, torch):
+    """Expert-parallel layer: selection with GPU groups, then each group's share timed."""
+    dev = "cuda:0"
+    cfg = dict(W.CONFIGS[args.workload])
+    if cfg["logits"] == "spec":
+        raise SystemExit("--ep-groups takes a flat workload")
+    T, N, k, d, f, k0 = cfg["T"], cfg["N"], cfg["k"], cfg["d"], cfg["f"], cfg["k0"]
+    G, m_g, nb = args.ep_groups, args.per_group_budget, args.batches
+    print(f"[bench] {args.workload}: expert parallel G={G} m_g={m_g}", file=sys.stderr, flush=True)
+    w1, w3, w2 = W.expert_weights(N, d, f, 0, dev)
+    logits = [torch.from_numpy(W.make_logits(cfg, s)[0]).to(dev) for s in range(nb)]
+    xs = [W.activations(T, d, s, dev) for s in range(nb)]
+    groups = X.GroupMap(G, None, device=dev)
+    gid = torch.arange(N, device=dev) // (N // G)
+    shares = [groups.with_local(g) for g in range(G)]
+    y = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
+    p_ep = X.params(N, k, k0, m_g, "per_group")
+    p_van = X.params(N, k, 0, N, "per_group")
+    ws = torch.empty(max(X.moe_workspace_bytes(T, d, f, p, s.layout) for p in (p_ep, p_van)
+                         for s in shares), dtype=torch.uint8, device=dev)
+
+    def loads(mask):
+        return torch.bincount(gid[mask.bool()], minlength=G).cpu().tolist()
+
+    # active experts of every (batch, group) share: algorithmic bytes of the share
+    act = np.array([[X.stats_dict(X.moe_forward(xs[b], logits[b], w1, w3, w2, k, k0, m_g,
+                                                groups=shares[g], y=y, workspace=ws)["stats"])
+                     ["n_active"] for g in range(G)] for b in range(nb)])
+    rows = []
+    for b in range(nb):
+        ep = X.select_ep(logits[b], groups, k, k0, m_g)
+        flat = X.route(logits[b], k, k0, max(m_g * G, k), "total")
+        van = X.route(logits[b], k, 0, N, "extra")
+        rows.append(dict(ep=loads(ep["sel_mask"]), flat=loads(flat["sel_mask"]),
+                         van=loads(van["sel_mask"])))
+    torch.cuda.synchronize()
+
+    def timed(kk0, mg):
+        """[batch][group] microseconds of the share calls, chained events on one stream."""
+        stream = torch.cuda.current_stream()
+        for s in range(args.warmup):
+            X.moe_forward(xs[s % nb], logits[s % nb], w1, w3, w2, k, kk0, mg, groups=shares[s % G],
+                          y=y, routing_out=False, workspace=ws)
+        reps = max(1, args.steps // nb)
+        evs = [X.HipEvent() for _ in range(reps * nb * G + 1)]
+        evs[0].record(stream)
+        i = 0
+        for _ in range(reps):
+            for b in range(nb):
+                for g in range(G):
+                    X.moe_forward(xs[b], logits[b], w1, w3, w2, k, kk0, mg, groups=shares[g], y=y,
+                                  routing_out=False, workspace=ws)
+                    i += 1
+                    evs[i].record(stream)
+        torch.cuda.synchronize()
+        t = np.array([evs[j].elapsed_ms(evs[j + 1]) for j in range(len(evs) - 1)]) * 1e3
+        return t.reshape(reps, nb, G).mean(0)
+
+    t_ep = timed(k0, m_g)
+    t_van = None if args.no_vanilla else timed(0, N)
+    layer = float(t_ep.max(1).mean())
+    slow = t_ep.argmax(1)
+    share_bytes = np.array([layer_bytes(act[b, slow[b]], T, N, d, f) for b in range(nb)])
+    achieved = float(np.mean(share_bytes / (t_ep[np.arange(nb), slow] * 1e-6))) / 1e9
+    mean = lambda key, fn: round(float(np.mean([fn(r[key]) for r in rows])), 2)  # noqa: E731
+    out = {
+        "metric": f"EP MoE layer: us/batch on the slowest of G={G} GPU groups (its share of "
+                  f"the layer; collective excluded) + experts activated and MaxLoad",
+        "value": round(layer, 2),
+        "unit": "us",
+        "n_gpus": 1,
+        "steps": max(1, args.steps // nb) * nb,
+        "warmup": args.warmup,
+        "ms_per_step": round(layer / 1e3, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}_ep_G{G}_mg{m_g}_k0{k0}", "tokens": T,
+                   "n_experts": N, "top_k": k, "d_model": d, "d_ffn": f, "groups": G,
+                   "per_group_budget": m_g, "warmup_k0": k0, "placement": "contiguous blocks",
+                   "logits": LOGITS_RECIPE[cfg["logits"]].format(Q=cfg.get("Q")),
+                   "batches_rotated": nb},
+        "experts_activated": mean("ep", sum),
+        "max_group_load": mean("ep", max),
+        "vanilla_experts": mean("van", sum),
+        "vanilla_max_group_load": mean("van", max),
+        "flat_xshare_same_total_max_group_load": mean("flat", max),
+        "flat_xshare_same_total_experts": mean("flat", sum),
+        "share_us_mean": round(float(t_ep.mean()), 2),
+        "slowest_share_active_experts": round(float(np.mean(act[np.arange(nb), slow])), 2),
+        "roofline": {"kernel": "slowest group's layer share", "bound": "hbm",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "algorithmic_bytes": round(float(share_bytes.mean()))},
+        "vanilla_ep_us_per_batch": None if t_van is None else round(float(t_van.max(1).mean()), 2),
+        "speedup_vs_vanilla_ep": None if t_van is None else
+        round(float(t_van.max(1).mean()) / layer, 3),
     }
     print(json.dumps(out), flush=True)
 

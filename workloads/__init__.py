@@ -185,6 +185,8 @@ CONFIGS = {
                  logits="domains", Q=8),
     "ds_t8": dict(N=256, k=8, d=7168, f=2048, T=8, M=48, M_sweep=(24, 48, 96), k0=1,
                   logits="domains", Q=8),
+    "ds_t16": dict(N=256, k=8, d=7168, f=2048, T=16, M=48, M_sweep=(24, 48, 96), k0=1,
+                   logits="domains", Q=8),
     "ds_t32": dict(N=256, k=8, d=7168, f=2048, T=32, M=48, M_sweep=(24, 48, 96), k0=1,
                    logits="domains", Q=8),
     "ds_iid_t8": dict(N=256, k=8, d=7168, f=2048, T=8, M=48, M_sweep=(24, 48, 96), k0=1,
