@@ -85,6 +85,14 @@ int layer_bound(int32_t T, const xshare_route_params* p, const xshare_ep_layout*
   return b;
 }
 
+// Experts expected to be active, for the choice of split counts (speed only): a group's
+// share is expected to hold about m_g experts, other calls up to the bound.
+int layer_estimate(int32_t T, const xshare_route_params* p, const xshare_ep_layout* ep) {
+  const int b = layer_bound(T, p, ep);
+  if (ep && ep->local_group >= 0) return std::min(b, std::max(p->budget, 1));
+  return b;
+}
+
 template <typename P>
 P* at(void* ws, size_t off) {
   return reinterpret_cast<P*>(static_cast<char*>(ws) + off);
@@ -159,9 +167,9 @@ size_t xshare_moe_workspace_bytes(int32_t T, int32_t d, int32_t f,
                                   const xshare_route_params* params, const xshare_ep_layout* ep) {
   if (check_params(T, params, false, ep != nullptr) != XSHARE_OK || d <= 0 || f <= 0) return 0;
   if (check_ep(params->n_experts, ep, true) != XSHARE_OK) return 0;
-  const int bound = layer_bound(T, params, ep);
   return xs::ffn_layout(T, params->n_experts, params->top_k,
-                        params->score_mode == XSHARE_SCORE_DENSE, d, f, bound)
+                        params->score_mode == XSHARE_SCORE_DENSE, d, f,
+                        layer_estimate(T, params, ep))
       .total;
 }
 
@@ -224,8 +232,8 @@ xshare_status xshare_moe_forward(const uint16_t* x, const float* logits, int32_t
     return XSHARE_EINVAL;
   const int N = params->n_experts, k = params->top_k;
   const int bound = layer_bound(T, params, ep);
-  const xs::FfnLayout L =
-      xs::ffn_layout(T, N, k, params->score_mode == XSHARE_SCORE_DENSE, d, f, bound);
+  const xs::FfnLayout L = xs::ffn_layout(T, N, k, params->score_mode == XSHARE_SCORE_DENSE, d,
+                                         f, layer_estimate(T, params, ep));
   if (!ws || ws_bytes < L.total) return XSHARE_EWORKSPACE;
 
   // The selection kernel always writes a mask; keep it in the workspace if not wanted.
@@ -257,6 +265,8 @@ xshare_status xshare_moe_forward(const uint16_t* x, const float* logits, int32_t
   fa.f = f;
   fa.max_active = bound;
   fa.splits = L.splits;
+  fa.gu_splits = L.gu_splits;
+  fa.gpart = at<float>(ws, L.gpart);
   fa.G = ra.G;
   fa.group = ra.group;
   fa.local_group = ra.local_group;

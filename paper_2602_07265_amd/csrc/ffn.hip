@@ -141,8 +141,11 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
   if (j0 >= a.f) return;
   const int n = lane & 15, g = lane >> 4;
   const int d = a.d, f = a.f;
-  const size_t wrow = ((size_t)e * f + j0 + n) * d + (size_t)g * 8 * U;
+  const int Kg = d / a.gu_splits;              // this block's part of the reduction
+  const size_t k0 = (size_t)blockIdx.z * Kg + (size_t)g * 8 * U;
+  const size_t wrow = ((size_t)e * f + j0 + n) * d + k0;
   const uint16_t* const brow[2] = {a.w1 + wrow, a.w3 + wrow};
+  const size_t plane = (size_t)a.T * a.k * f;  // one fp32 partial plane [T * k, f]
 
   for (int c0 = 0; c0 < te; c0 += 16 * kTiles) {
     const int nt = min(kTiles, (te - c0 + 15) / 16);
@@ -150,14 +153,14 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
 #pragma unroll
     for (int rt = 0; rt < kTiles; ++rt) {
       const int t = min(c0 + rt * 16 + n, te - 1);
-      arow[rt] = a.x + (size_t)(a.perm[p0 + t] / a.k) * d + (size_t)g * 8 * U;
+      arow[rt] = a.x + (size_t)(a.perm[p0 + t] / a.k) * d + k0;
     }
     floatx4 acc[2][kTiles];
 #pragma unroll
     for (int m = 0; m < 2; ++m)
 #pragma unroll
       for (int rt = 0; rt < kTiles; ++rt) acc[m][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    wave_pass<U, 2, XS_GATE_UP_ADBL != 0>(arow, nt, brow, d, acc);
+    wave_pass<U, 2, XS_GATE_UP_ADBL != 0>(arow, nt, brow, Kg, acc);
 #pragma unroll
     for (int rt = 0; rt < kTiles; ++rt) {
       if (rt >= nt) break;
@@ -166,8 +169,14 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
         const int t = c0 + rt * 16 + 4 * g + i;
         if (t < te) {
           const float h1 = acc[0][rt][i], h3 = acc[1][rt][i];
-          const float hv = h1 / (1.0f + __expf(-h1)) * h3;
-          a.h[(size_t)(p0 + t) * f + j0 + n] = to_bf16(hv);
+          const size_t at = (size_t)(p0 + t) * f + j0 + n;
+          if (a.gu_splits == 1) {
+            a.h[at] = to_bf16(h1 / (1.0f + __expf(-h1)) * h3);
+          } else {
+            float* const part = a.gpart + 2 * blockIdx.z * plane;
+            part[at] = h1;
+            part[plane + at] = h3;
+          }
         }
       }
     }
@@ -226,6 +235,35 @@ __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
   }
 }
 
+// Split gate/up reduction: sums the gate and up partials in split order, then
+// H = silu(gate) * up in bf16.  One block row per hidden row (permuted order); rows whose
+// expert the GEMMs did not cover (another GPU group's) are skipped.
+__global__ __launch_bounds__(kBlock) void gate_up_finish_kernel(FfnArgs a) {
+  const int p = blockIdx.y;
+  if (p >= a.offsets[a.N]) return;
+  if (a.local_group >= 0) {
+    const int e = a.ids[a.perm[p]];
+    if ((a.group ? a.group[e] : e / (a.N / a.G)) != a.local_group) return;
+  }
+  const int c = (blockIdx.x * kBlock + threadIdx.x) * 4;
+  if (c >= a.f) return;
+  const size_t plane = (size_t)a.T * a.k * a.f;
+  const size_t at = (size_t)p * a.f + c;
+  float4 gs = *reinterpret_cast<const float4*>(a.gpart + at);
+  float4 us = *reinterpret_cast<const float4*>(a.gpart + plane + at);
+  for (int z = 1; z < a.gu_splits; ++z) {
+    const float4 gz = *reinterpret_cast<const float4*>(a.gpart + 2 * z * plane + at);
+    const float4 uz = *reinterpret_cast<const float4*>(a.gpart + (2 * z + 1) * plane + at);
+    gs.x += gz.x; gs.y += gz.y; gs.z += gz.z; gs.w += gz.w;
+    us.x += uz.x; us.y += uz.y; us.z += uz.z; us.w += uz.w;
+  }
+  const uint32_t lo = (uint32_t)to_bf16(gs.x / (1.0f + __expf(-gs.x)) * us.x) |
+                      ((uint32_t)to_bf16(gs.y / (1.0f + __expf(-gs.y)) * us.y) << 16);
+  const uint32_t hi = (uint32_t)to_bf16(gs.z / (1.0f + __expf(-gs.z)) * us.z) |
+                      ((uint32_t)to_bf16(gs.w / (1.0f + __expf(-gs.w)) * us.w) << 16);
+  *reinterpret_cast<uint2*>(a.h + at) = make_uint2(lo, hi);
+}
+
 __global__ __launch_bounds__(kBlock) void combine_kernel(FfnArgs a) {
   const int i = blockIdx.y;
   const int c = (blockIdx.x * kBlock + threadIdx.x) * 4;
@@ -266,12 +304,17 @@ int unroll_for(int K, int want) {
 }  // namespace
 
 hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
-  const dim3 grid((a.f + kWaves * kCols - 1) / (kWaves * kCols), a.max_active), block(kBlock);
-  switch (unroll_for(a.d, XS_GATE_UP_U)) {
+  const dim3 grid((a.f + kWaves * kCols - 1) / (kWaves * kCols), a.max_active, a.gu_splits),
+      block(kBlock);
+  switch (unroll_for(a.d / a.gu_splits, XS_GATE_UP_U)) {
     case 8: hipLaunchKernelGGL(gate_up_kernel<8>, grid, block, 0, stream, a); break;
     case 4: hipLaunchKernelGGL(gate_up_kernel<4>, grid, block, 0, stream, a); break;
     case 2: hipLaunchKernelGGL(gate_up_kernel<2>, grid, block, 0, stream, a); break;
     default: hipLaunchKernelGGL(gate_up_kernel<1>, grid, block, 0, stream, a); break;
+  }
+  if (a.gu_splits > 1) {
+    const dim3 fgrid((a.f + kBlock * 4 - 1) / (kBlock * 4), a.T * a.k);
+    hipLaunchKernelGGL(gate_up_finish_kernel, fgrid, block, 0, stream, a);
   }
   return hipGetLastError();
 }

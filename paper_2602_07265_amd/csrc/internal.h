@@ -61,29 +61,45 @@ inline int active_bound(int T, int N, int k, int budget_mode, int budget) {
   return b;
 }
 
-// The down GEMM splits its reduction (f) into this many parts when the active experts'
-// 32-row output tiles alone would give too few waves to keep HBM busy (few, wide experts).
-inline int down_splits(int max_active, int d, int f) {
-  const long waves = (long)max_active * (d / 32);
+// The expert GEMMs split their reduction into this many parts when the experts expected
+// to be active would give too few waves to keep HBM busy (few experts, or one GPU group's
+// share): gate/up splits d (16 output columns of W1 and W3 per wave), down splits f (32
+// output rows of W2 per wave).  Each part stays a multiple of the kernels' K step.  The
+// split count only changes speed; the grid always covers the bound on active experts.
+#ifndef XS_GATE_UP_MAX_SPLITS
+#define XS_GATE_UP_MAX_SPLITS 8
+#endif
+inline int split_for(long waves, int K, int step, int max_splits = 8) {
   int s = 1;
-  while (s < 8 && waves * s < 2048 && f % (2 * s * 256) == 0) s *= 2;
+  while (s < max_splits && waves * s < 2048 && K % (2 * s * step) == 0) s *= 2;
   return s;
+}
+inline int gate_up_splits(int est_active, int d, int f) {
+  return split_for((long)est_active * (f / 16), d, 128, XS_GATE_UP_MAX_SPLITS);
+}
+inline int down_splits(int est_active, int d, int f) {
+  return split_for((long)est_active * (d / 32), f, 128);
 }
 
 struct FfnLayout {
   RouteLayout route;
-  int splits;    // K-splits of the down GEMM
-  size_t h;      // bf16 [T * k, f]            SwiGLU hidden rows in permuted order
-  size_t y;      // fp32 [splits, T * k, d]    per-(token, slot) partial expert outputs
+  int gu_splits;  // K-splits of the gate/up GEMM
+  int splits;     // K-splits of the down GEMM
+  size_t gpart;   // fp32 [gu_splits, 2, T * k, f] gate and up partial sums (gu_splits > 1)
+  size_t h;       // bf16 [T * k, f]            SwiGLU hidden rows in permuted order
+  size_t y;       // fp32 [splits, T * k, d]    per-(token, slot) partial expert outputs
   size_t total;
 };
 
-inline FfnLayout ffn_layout(int T, int N, int k, bool dense, int d, int f, int max_active) {
+inline FfnLayout ffn_layout(int T, int N, int k, bool dense, int d, int f, int est_active) {
   FfnLayout L{};
   L.route = route_layout(T, N, k, dense);
-  L.splits = down_splits(max_active, d, f);
+  L.gu_splits = gate_up_splits(est_active, d, f);
+  L.splits = down_splits(est_active, d, f);
   size_t tk = size_t(T > 0 ? T : 1) * size_t(k);
   size_t o = L.route.total;
+  L.gpart = o;
+  if (L.gu_splits > 1) o += align256(sizeof(float) * 2 * size_t(L.gu_splits) * tk * size_t(f));
   L.h = o; o += align256(sizeof(uint16_t) * tk * size_t(f));
   L.y = o; o += align256(sizeof(float) * size_t(L.splits) * tk * size_t(d));
   L.total = o;
@@ -120,6 +136,8 @@ struct FfnArgs {
   int T, N, k, d, f;
   int max_active;              // host bound on the number of active experts (grid size)
   int splits;                  // K-splits of the down GEMM (partials summed in the combine)
+  int gu_splits;               // K-splits of the gate/up GEMM (partials summed by finish)
+  float* gpart;                // [gu_splits, 2, T * k, f] when gu_splits > 1
   int G;                       // GPU groups, with `group` and `local_group` as in RouteArgs
   const int32_t* group;
   int local_group;
@@ -134,7 +152,7 @@ struct FfnArgs {
   uint16_t* y;
 };
 
-hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream);
+hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream);  // + finish if split
 hipError_t launch_down(const FfnArgs& a, hipStream_t stream);
 hipError_t launch_combine(const FfnArgs& a, hipStream_t stream);
 

@@ -60,10 +60,11 @@ def test_ffn_ragged_shapes():
 
 
 def test_ffn_split_reduction():
-    """Few, wide experts: the down GEMM splits f into 4, 8 and 2 parts (partials summed in
-    split order before the weighted combine); the result stays within tolerance."""
+    """Few, wide experts: the down GEMM splits f into 8, 8, 4 and 2 parts and the gate/up
+    GEMM splits d into 8 and 4 parts (partials summed in split order); within tolerance."""
     for T, N, k, d, f, M in [(16, 8, 2, 128, 1024, 2), (8, 16, 2, 64, 2048, 3),
-                             (40, 12, 3, 96, 512, 12)]:
+                             (40, 12, 3, 96, 512, 12), (16, 8, 2, 1024, 256, 4),
+                             (24, 16, 4, 512, 384, 16)]:
         c = dict(N=N, k=k, d=d, f=f, T=T, logits="domains", Q=2)
         _run(c, 0, 1, M, label=f"split T{T} d{d} f{f} M{M}")
 
