@@ -129,7 +129,9 @@ __device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[kTiles],
 #define XS_DOWN_NM 2
 #endif
 
-template <int U>
+// kSplit: the block covers one part of the reduction (blockIdx.z) and writes fp32 gate and
+// up partials; otherwise it covers all of d and writes H directly.
+template <int U, bool kSplit>
 __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
   const int slot = blockIdx.y;
   if (slot >= a.counters[kCntActive]) return;
@@ -141,8 +143,8 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
   if (j0 >= a.f) return;
   const int n = lane & 15, g = lane >> 4;
   const int d = a.d, f = a.f;
-  const int Kg = d / a.gu_splits;              // this block's part of the reduction
-  const size_t k0 = (size_t)blockIdx.z * Kg + (size_t)g * 8 * U;
+  const int Kg = kSplit ? d / a.gu_splits : d;   // this block's part of the reduction
+  const size_t k0 = (kSplit ? (size_t)blockIdx.z * Kg : 0) + (size_t)g * 8 * U;
   const size_t wrow = ((size_t)e * f + j0 + n) * d + k0;
   const uint16_t* const brow[2] = {a.w1 + wrow, a.w3 + wrow};
   const size_t plane = (size_t)a.T * a.k * f;  // one fp32 partial plane [T * k, f]
@@ -170,7 +172,7 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
         if (t < te) {
           const float h1 = acc[0][rt][i], h3 = acc[1][rt][i];
           const size_t at = (size_t)(p0 + t) * f + j0 + n;
-          if (a.gu_splits == 1) {
+          if (!kSplit) {
             a.h[at] = to_bf16(h1 / (1.0f + __expf(-h1)) * h3);
           } else {
             float* const part = a.gpart + 2 * blockIdx.z * plane;
@@ -295,6 +297,14 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(FfnArgs a) {
   *reinterpret_cast<uint2*>(a.y + (size_t)i * a.d + c) = make_uint2(lo, hi);
 }
 
+template <int U>
+void launch_gu(const FfnArgs& a, bool split, dim3 grid, dim3 block, hipStream_t stream) {
+  if (split)
+    hipLaunchKernelGGL((gate_up_kernel<U, true>), grid, block, 0, stream, a);
+  else
+    hipLaunchKernelGGL((gate_up_kernel<U, false>), grid, block, 0, stream, a);
+}
+
 int unroll_for(int K, int want) {
   for (int u = want; u > 1; u >>= 1)
     if (K % (32 * u) == 0) return u;
@@ -306,13 +316,14 @@ int unroll_for(int K, int want) {
 hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
   const dim3 grid((a.f + kWaves * kCols - 1) / (kWaves * kCols), a.max_active, a.gu_splits),
       block(kBlock);
+  const bool split = a.gu_splits > 1;
   switch (unroll_for(a.d / a.gu_splits, XS_GATE_UP_U)) {
-    case 8: hipLaunchKernelGGL(gate_up_kernel<8>, grid, block, 0, stream, a); break;
-    case 4: hipLaunchKernelGGL(gate_up_kernel<4>, grid, block, 0, stream, a); break;
-    case 2: hipLaunchKernelGGL(gate_up_kernel<2>, grid, block, 0, stream, a); break;
-    default: hipLaunchKernelGGL(gate_up_kernel<1>, grid, block, 0, stream, a); break;
+    case 8: launch_gu<8>(a, split, grid, block, stream); break;
+    case 4: launch_gu<4>(a, split, grid, block, stream); break;
+    case 2: launch_gu<2>(a, split, grid, block, stream); break;
+    default: launch_gu<1>(a, split, grid, block, stream); break;
   }
-  if (a.gu_splits > 1) {
+  if (split) {
     const dim3 fgrid((a.f + kBlock * 4 - 1) / (kBlock * 4), a.T * a.k);
     hipLaunchKernelGGL(gate_up_finish_kernel, fgrid, block, 0, stream, a);
   }
