@@ -69,16 +69,35 @@ inline int active_bound(int T, int N, int k, int budget_mode, int budget) {
 #ifndef XS_GATE_UP_MAX_SPLITS
 #define XS_GATE_UP_MAX_SPLITS 8
 #endif
-inline int split_for(long waves, int K, int step, int max_splits = 8) {
+#ifndef XS_GU_SPLIT_BELOW
+#define XS_GU_SPLIT_BELOW 1024
+#endif
+#ifndef XS_GU_SPLIT_TARGET
+#define XS_GU_SPLIT_TARGET 2048
+#endif
+#ifndef XS_DN_SPLIT_BELOW
+#define XS_DN_SPLIT_BELOW 1536
+#endif
+#ifndef XS_DN_SPLIT_TARGET
+#define XS_DN_SPLIT_TARGET 4096
+#endif
+// Splits (a power of two <= max_splits) for a launch of `waves` waves: none at or above
+// `below`, else the fewest that reach `target` waves, each part a multiple of `step`.
+// Measured on MI355X: gate/up pays for its partials and the finish pass, so it splits only
+// below 1024 waves (five DeepSeek experts, 640 waves: 4 splits); down splits below 1536
+// (five experts, 1120 waves: 4 splits; Mixtral's five experts, 640 waves: 8 splits).
+inline int split_for(long waves, int K, int step, int below, int target, int max_splits = 8) {
+  if (waves >= below) return 1;
   int s = 1;
-  while (s < max_splits && waves * s < 2048 && K % (2 * s * step) == 0) s *= 2;
+  while (s < max_splits && waves * s < target && K % (2 * s * step) == 0) s *= 2;
   return s;
 }
 inline int gate_up_splits(int est_active, int d, int f) {
-  return split_for((long)est_active * (f / 16), d, 128, XS_GATE_UP_MAX_SPLITS);
+  return split_for((long)est_active * (f / 16), d, 128, XS_GU_SPLIT_BELOW, XS_GU_SPLIT_TARGET,
+                   XS_GATE_UP_MAX_SPLITS);
 }
 inline int down_splits(int est_active, int d, int f) {
-  return split_for((long)est_active * (d / 32), f, 128);
+  return split_for((long)est_active * (d / 32), f, 128, XS_DN_SPLIT_BELOW, XS_DN_SPLIT_TARGET);
 }
 
 struct FfnLayout {
