@@ -25,7 +25,12 @@ the design notes of the repository):
   are canonicalised with h + 0.0 so that -0.0 and +0.0 compare equal;
 * budget "total": |S| <= M (requires M >= k); budget "extra": M experts are
   added beyond the warm-up set (beyond the union of the per-request sets in the
-  hierarchical case), which is how the paper's tables use m_l;
+  hierarchical case), which is how the paper's tables use m_l; budget
+  "threshold": Algorithm 1's own stopping rule, add experts while
+  f(S) < tau * f(E), in fp32: f(E) sums every s_j in index order, f(S) starts
+  with the starting set in ranking order (priority, score descending, index
+  ascending) and adds each pick; tau * f(E) is one fp32 product; the starting
+  set is never cut and the loop also stops when no candidate is left;
 * candidates: in "topk" mode only experts some token (some token of the
   request, for per-request picks) has in its top-k; in "dense" mode all experts
   (none when the batch is empty);
@@ -53,6 +58,7 @@ from .numerics import F32, seq_sum, softmax_dense, softmax_ranked
 
 TOTAL = "total"
 EXTRA = "extra"
+THRESHOLD = "threshold"
 TOPK = "topk"
 DENSE = "dense"
 
@@ -158,11 +164,34 @@ def greedy_select(scores, start, budget: int, candidates, priority=None) -> set[
     return S
 
 
+def greedy_threshold(scores, start, tau: float, candidates, priority=None) -> set[int]:
+    """Algorithm 1 as printed: from ``start``, add the best remaining candidate while
+    f(S) < tau * f(E), with f(S) = sum of the scores in S (Eq. (2)) in fp32."""
+    scores = np.asarray(scores, dtype=F32)
+    f_E = F32(0.0)
+    for j in range(len(scores)):                       # f(E), index order
+        f_E = F32(f_E + scores[j])
+    target = F32(F32(tau) * f_E)
+    pri = priority or {}
+    S = set(int(j) for j in start)
+    f_S = F32(0.0)
+    for j in sorted(S, key=lambda j: (pri.get(j, 0), -float(scores[j]), j)):
+        f_S = F32(f_S + scores[j])
+    while f_S < target:
+        rest = [int(e) for e in candidates if int(e) not in S]
+        if not rest:
+            break
+        e_star = max(rest, key=lambda e: (float(scores[e]), -e))   # argmax, lowest index on ties
+        S.add(e_star)
+        f_S = F32(f_S + scores[e_star])
+    return S
+
+
 def _effective_budget(base: int, n_cand: int, k: int) -> int:
     return max(min(base, n_cand), min(k, n_cand))
 
 
-def _check(h, k, k0, M, budget_mode, score_mode):
+def _check(h, k, k0, M, budget_mode, score_mode, tau=None):
     T, N = h.shape
     if not 1 <= k <= N:
         raise ValueError("need 1 <= k <= N")
@@ -172,8 +201,10 @@ def _check(h, k, k0, M, budget_mode, score_mode):
         raise ValueError("need M >= 0")
     if budget_mode == TOTAL and M < k:
         raise ValueError("a total budget must be >= k")
-    if budget_mode not in (TOTAL, EXTRA) or score_mode not in (TOPK, DENSE):
+    if budget_mode not in (TOTAL, EXTRA, THRESHOLD) or score_mode not in (TOPK, DENSE):
         raise ValueError("unknown mode")
+    if budget_mode == THRESHOLD and (tau is None or not np.isfinite(tau) or tau < 0):
+        raise ValueError("the threshold mode needs a finite tau >= 0")
 
 
 # ----------------------------------------------------------------------------- refinement
@@ -194,10 +225,11 @@ def refine(h, S, k: int):
 # ----------------------------------------------------------------------------- Algorithm 2
 
 def route(h, k: int, k0: int, M: int, budget_mode: str = TOTAL,
-          score_mode: str = TOPK) -> Routing:
-    """Batch-aware expert selection for one layer (Algorithm 2)."""
+          score_mode: str = TOPK, tau: float | None = None) -> Routing:
+    """Batch-aware expert selection for one layer (Algorithm 2; Algorithm 1's threshold
+    rule instead of the budget with budget_mode "threshold")."""
     h = canonical(h)
-    _check(h, k, k0, M, budget_mode, score_mode)
+    _check(h, k, k0, M, budget_mode, score_mode, tau)
     T, N = h.shape
     vids, vg = vanilla_gating(h, k)
     G = gate_matrix(h, vids, vg, score_mode)
@@ -209,10 +241,14 @@ def route(h, k: int, k0: int, M: int, budget_mode: str = TOTAL,
         cand = set()
     else:
         cand = union if score_mode == TOPK else set(range(N))
-    base = M if budget_mode == TOTAL else len(S0) + M
-    m_eff = _effective_budget(base, len(cand), k)
-
-    S = greedy_select(s, S0, m_eff, sorted(cand))
+    if budget_mode == THRESHOLD:
+        S = greedy_threshold(s, S0, tau, sorted(cand))
+        m_eff = max(len(S), min(k, len(cand)))
+        S = greedy_select(s, S, m_eff, sorted(cand))               # every token keeps k
+    else:
+        base = M if budget_mode == TOTAL else len(S0) + M
+        m_eff = _effective_budget(base, len(cand), k)
+        S = greedy_select(s, S0, m_eff, sorted(cand))
     ids, w = refine(h, S, k)
     mask = np.zeros(N, dtype=np.uint8)
     mask[sorted(S)] = 1
@@ -242,10 +278,11 @@ def per_request_select(h, G, vids, tokens, k0: int, m_r: int, score_mode: str):
 
 
 def select_hier(h, offsets, k: int, k0: int, m_r: int, M: int,
-                budget_mode: str = TOTAL, score_mode: str = TOPK) -> Routing:
+                budget_mode: str = TOTAL, score_mode: str = TOPK,
+                tau: float | None = None) -> Routing:
     """Speculative-decoding-aware selection (Algorithm 4 calling Algorithm 3 per request)."""
     h = canonical(h)
-    _check(h, k, k0, M, budget_mode, score_mode)
+    _check(h, k, k0, M, budget_mode, score_mode, tau)
     if m_r < 0:
         raise ValueError("need m_r >= 0")
     T, N = h.shape
@@ -266,11 +303,15 @@ def select_hier(h, offsets, k: int, k0: int, m_r: int, M: int,
         cand = set()
     else:
         cand = union if score_mode == TOPK else set(range(N))
-    base = M if budget_mode == TOTAL else len(S_batch) + M
-    m_eff = _effective_budget(base, len(cand), k)
-
     priority = {j: (0 if j in S0 else 1) for j in S_batch}
-    S = greedy_select(s, S_batch, m_eff, sorted(cand), priority)
+    if budget_mode == THRESHOLD:
+        S = greedy_threshold(s, S_batch, tau, sorted(cand), priority)
+        m_eff = max(len(S), min(k, len(cand)))
+        S = greedy_select(s, S, m_eff, sorted(cand), priority)
+    else:
+        base = M if budget_mode == TOTAL else len(S_batch) + M
+        m_eff = _effective_budget(base, len(cand), k)
+        S = greedy_select(s, S_batch, m_eff, sorted(cand), priority)
     ids, w = refine(h, S, k)
     mask = np.zeros(N, dtype=np.uint8)
     mask[sorted(S)] = 1
