@@ -61,8 +61,11 @@ enum {
   XSHARE_BUDGET_EXTRA = 1,  /* budget experts are added beyond the warm-up set (flat) or     *
                              * beyond the union of the per-request sets (hierarchical), as   *
                              * in the paper's (m_l, k0) settings of Section 6                */
-  XSHARE_BUDGET_PER_GROUP = 2 /* budget is m_g, experts per GPU group (Algorithm 5); only    *
+  XSHARE_BUDGET_PER_GROUP = 2, /* budget is m_g, experts per GPU group (Algorithm 5); only   *
                              * with an xshare_ep_layout, which in turn requires this mode    */
+  XSHARE_BUDGET_THRESHOLD = 3 /* Algorithm 1's own rule: add experts while                   *
+                             * f(S) < threshold * f(E), f = summed batch score (Eq. (2));    *
+                             * |S| adapts to the batch; `budget` is ignored (>= 0)           */
 };
 
 /* Which gates g_ij enter the scores s_j = sum_i g_ij (Eq. (2)).                            */
@@ -81,6 +84,11 @@ typedef struct {
   int32_t budget_mode;        /* XSHARE_BUDGET_TOTAL, _EXTRA or _PER_GROUP                  */
   int32_t score_mode;         /* XSHARE_SCORE_TOPK or XSHARE_SCORE_DENSE                    */
   int32_t per_request_budget; /* m_r (Algorithm 3); read by the hierarchical calls only     */
+  float threshold;            /* tau >= 0, finite; read in XSHARE_BUDGET_THRESHOLD mode only: *
+                               * f(E) = sum of every s_j in index order, f(S) = the starting  *
+                               * set's scores in ranking order, then each added expert's, all *
+                               * fp32; the target tau * f(E) is one fp32 product; the starting *
+                               * set is never cut; tau > 1 takes every candidate              */
 } xshare_route_params;
 
 /* Per-call statistics, written to DEVICE memory by the kernels.                          */

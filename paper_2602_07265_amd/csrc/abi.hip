@@ -4,6 +4,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <cmath>
 
 #include "internal.h"
 #include "xshare.h"
@@ -24,7 +25,11 @@ xshare_status check_params(int32_t T, const xshare_route_params* p, bool hier, b
   if (T < 0 || p->n_experts < 1 || p->top_k < 1 || p->top_k > p->n_experts) return XSHARE_EINVAL;
   if (p->warmup_k0 < 0 || p->warmup_k0 > p->top_k || p->budget < 0) return XSHARE_EINVAL;
   if (ep ? p->budget_mode != XSHARE_BUDGET_PER_GROUP
-         : (p->budget_mode != XSHARE_BUDGET_TOTAL && p->budget_mode != XSHARE_BUDGET_EXTRA))
+         : (p->budget_mode != XSHARE_BUDGET_TOTAL && p->budget_mode != XSHARE_BUDGET_EXTRA &&
+            p->budget_mode != XSHARE_BUDGET_THRESHOLD))
+    return XSHARE_EINVAL;
+  if (p->budget_mode == XSHARE_BUDGET_THRESHOLD &&
+      !(std::isfinite(p->threshold) && p->threshold >= 0.0f))
     return XSHARE_EINVAL;
   if (p->score_mode != XSHARE_SCORE_TOPK && p->score_mode != XSHARE_SCORE_DENSE)
     return XSHARE_EINVAL;
@@ -113,6 +118,7 @@ xs::RouteArgs route_args(const float* logits, int32_t T, const xshare_route_para
   a.budget_mode = p->budget_mode;
   a.score_mode = p->score_mode;
   a.m_r = std::min(p->per_request_budget, p->n_experts);
+  a.tau = p->threshold;
   a.req_offsets = req_offsets;
   a.R = R;
   a.G = ep ? ep->n_groups : 0;

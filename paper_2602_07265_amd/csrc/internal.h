@@ -128,6 +128,7 @@ inline FfnLayout ffn_layout(int T, int N, int k, bool dense, int d, int f, int e
 struct RouteArgs {
   const float* logits;
   int T, N, k, k0, budget, budget_mode, score_mode, m_r;
+  float tau;                   // threshold mode (budget_mode 3)
   const int32_t* req_offsets;  // nullptr: flat Algorithm 2
   int R;
   int G;                       // GPU groups (Algorithms 5-6); 0: no groups

@@ -502,18 +502,41 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
     n_s0 = s_cnt[1];
     n_start = s_cnt[2];
     n_u = s_cnt[3];
-    const int base = a.budget_mode == 0 ? a.budget : n_start + a.budget;
-    m_eff = max(min(base, n_cand), min(k, n_cand));
+    int rank = 0;
     if (mykey != 0) {
       const ulonglong2* keys2 = reinterpret_cast<const ulonglong2*>(s_key);
-      int rank = 0;
       const int n2 = (n_cand + 1) >> 1;
       for (int jj = 0; jj < n2; ++jj) {
         const ulonglong2 kk = keys2[jj];
         rank += (kk.x > mykey) + (kk.y > mykey);
       }
-      sel = rank < m_eff;
     }
+    if (a.budget_mode == 3) {
+      // Algorithm 1's threshold rule: the starting set (ranks below n_start) and then the
+      // candidates in rank order join while f(S) < tau * f(E).  One thread replays the fp32
+      // sums in the stated order: f(E) over every expert in index order, f(S) in rank order.
+      float* const by_index = reinterpret_cast<float*>(s_gcand);
+      float* const by_rank = reinterpret_cast<float*>(s_hist);
+      if (j < N) by_index[j] = s;
+      if (mykey != 0) by_rank[rank] = s;
+      __syncthreads();
+      if (tid == 0) {
+        float f_E = 0.0f;
+        for (int jj = 0; jj < N; ++jj) f_E = f_E + by_index[jj];
+        const float target = a.tau * f_E;
+        float f_S = 0.0f;
+        for (int r = 0; r < n_start; ++r) f_S = f_S + by_rank[r];
+        int m = n_start;
+        while (m < n_cand && f_S < target) f_S = f_S + by_rank[m++];
+        s_cnt[6] = m;
+      }
+      __syncthreads();
+      m_eff = max(s_cnt[6], min(k, n_cand));
+    } else {
+      const int base = a.budget_mode == 0 ? a.budget : n_start + a.budget;
+      m_eff = max(min(base, n_cand), min(k, n_cand));
+    }
+    sel = mykey != 0 && rank < m_eff;
   } else {
     // GPU groups (Algorithms 5 and 6).  Group g can take a_g = m_g - |S_0 on g| experts
     // (m_g caps every group's load, Eq. (5)), one per round, best first; its candidate of

@@ -16,7 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libxshare.so")
 
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP = 0, 1, 2, 3, 4
-BUDGET = {"total": 0, "extra": 1, "per_group": 2}
+BUDGET = {"total": 0, "extra": 1, "per_group": 2, "threshold": 3}
 SCORE = {"topk": 0, "dense": 1}
 N_STAGE_EVENTS = 5
 STAGES = ("route", "gate_up", "down", "combine")
@@ -31,6 +31,7 @@ class RouteParams(ctypes.Structure):
         ("budget_mode", ctypes.c_int32),
         ("score_mode", ctypes.c_int32),
         ("per_request_budget", ctypes.c_int32),
+        ("threshold", ctypes.c_float),
     ]
 
 
@@ -103,11 +104,12 @@ def version() -> str:
 
 
 def params(n_experts: int, top_k: int, warmup_k0: int, budget: int, budget_mode="total",
-           score_mode="topk", per_request_budget: int = 0) -> RouteParams:
+           score_mode="topk", per_request_budget: int = 0, threshold: float = 0.0) -> RouteParams:
+    """``threshold`` is tau of the "threshold" budget mode (Algorithm 1's stopping rule)."""
     return RouteParams(int(n_experts), int(top_k), int(warmup_k0), int(budget),
                        BUDGET[budget_mode] if isinstance(budget_mode, str) else int(budget_mode),
                        SCORE[score_mode] if isinstance(score_mode, str) else int(score_mode),
-                       int(per_request_budget))
+                       int(per_request_budget), float(threshold))
 
 
 def route_workspace_bytes(T: int, p: RouteParams) -> int:
@@ -253,26 +255,26 @@ def select_ep(logits: torch.Tensor, groups: GroupMap, top_k: int, warmup_k0: int
 
 
 def route(logits: torch.Tensor, top_k: int, warmup_k0: int, budget: int, budget_mode="total",
-          score_mode="topk", *, out=None, workspace=None, stream=None) -> dict:
+          score_mode="topk", *, tau: float = 0.0, out=None, workspace=None, stream=None) -> dict:
     """Algorithm 2 on the GPU: returns dict(sel_mask, ids, w, stats) device tensors."""
-    p = params(logits.shape[1], top_k, warmup_k0, budget, budget_mode, score_mode)
+    p = params(logits.shape[1], top_k, warmup_k0, budget, budget_mode, score_mode, 0, tau)
     return _route_impl(logits, p, None, out, workspace, stream)
 
 
 def select_hier(logits: torch.Tensor, req_offsets, top_k: int, warmup_k0: int,
                 per_request_budget: int, budget: int, budget_mode="total", score_mode="topk", *,
-                out=None, workspace=None, stream=None) -> dict:
+                tau: float = 0.0, out=None, workspace=None, stream=None) -> dict:
     """Algorithms 3-4 on the GPU; req_offsets as a host sequence (validated) or device tensor."""
     p = params(logits.shape[1], top_k, warmup_k0, budget, budget_mode, score_mode,
-               per_request_budget)
+               per_request_budget, tau)
     return _route_impl(logits, p, req_offsets, out, workspace, stream)
 
 
 def moe_forward(x: torch.Tensor, logits: torch.Tensor, w1: torch.Tensor, w3: torch.Tensor,
                 w2: torch.Tensor, top_k: int, warmup_k0: int, budget: int, budget_mode="total",
                 score_mode="topk", *, req_offsets=None, per_request_budget: int = 0,
-                groups: GroupMap | None = None, y=None, routing_out=True, workspace=None,
-                stage_events=None, stream=None) -> dict:
+                groups: GroupMap | None = None, tau: float = 0.0, y=None, routing_out=True,
+                workspace=None, stage_events=None, stream=None) -> dict:
     """The MoE layer: returns dict(y [T,d] bf16, and sel_mask/ids/w/stats if routing_out).
 
     With ``groups`` the selection is Algorithms 5-6 (``budget`` is m_g, budget_mode is
@@ -288,7 +290,7 @@ def moe_forward(x: torch.Tensor, logits: torch.Tensor, w1: torch.Tensor, w3: tor
     _dev(w2, torch.bfloat16, (N, d, f), "w2")
     if groups is not None:
         budget_mode = "per_group"
-    p = params(N, top_k, warmup_k0, budget, budget_mode, score_mode, per_request_budget)
+    p = params(N, top_k, warmup_k0, budget, budget_mode, score_mode, per_request_budget, tau)
     ep = None if groups is None else groups.layout
     if y is None:
         y = torch.empty((T, d), dtype=torch.bfloat16, device=dev)

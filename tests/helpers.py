@@ -18,23 +18,24 @@ def say(*a):
 
 
 def gpu_route(h, k, k0, M, budget_mode="total", score_mode="topk", offsets=None, m_r=0,
-              device_offsets_only=False):
+              device_offsets_only=False, tau=0.0):
     from paper_2602_07265_amd import xshare as X
     hd = torch.from_numpy(np.ascontiguousarray(h)).to(DEV)
     if offsets is None:
-        res = X.route(hd, k, k0, M, budget_mode, score_mode)
+        res = X.route(hd, k, k0, M, budget_mode, score_mode, tau=tau)
     else:
         off = torch.tensor(np.asarray(offsets, np.int32), device=DEV) if device_offsets_only \
             else list(int(v) for v in offsets)
-        res = X.select_hier(hd, off, k, k0, m_r, M, budget_mode, score_mode)
+        res = X.select_hier(hd, off, k, k0, m_r, M, budget_mode, score_mode, tau=tau)
     torch.cuda.synchronize()
     return {key: v.cpu().numpy() for key, v in res.items()}
 
 
-def oracle_route(h, k, k0, M, budget_mode="total", score_mode="topk", offsets=None, m_r=0):
+def oracle_route(h, k, k0, M, budget_mode="total", score_mode="topk", offsets=None, m_r=0,
+                 tau=None):
     if offsets is None:
-        return OR.route(h, k, k0, M, budget_mode, score_mode)
-    return OR.select_hier(h, offsets, k, k0, m_r, M, budget_mode, score_mode)
+        return OR.route(h, k, k0, M, budget_mode, score_mode, tau)
+    return OR.select_hier(h, offsets, k, k0, m_r, M, budget_mode, score_mode, tau)
 
 
 def assert_route_equal(got, ref, label=""):

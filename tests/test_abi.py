@@ -73,17 +73,22 @@ def _route(p, T=8, ws=FAKE, ws_bytes=1 << 30, logits=FAKE, mask=FAKE, ids=FAKE, 
     (dict(warmup_k0=-1), X.EINVAL),
     (dict(budget=1), X.EINVAL),            # total budget < k
     (dict(budget=-1, budget_mode=1), X.EINVAL),
-    (dict(budget_mode=2), X.EINVAL),
+    (dict(budget_mode=2), X.EINVAL),       # per-group budget without groups
+    (dict(budget_mode=4), X.EINVAL),
+    (dict(budget_mode=3, threshold=-0.5), X.EINVAL),
+    (dict(budget_mode=3, threshold=float("nan")), X.EINVAL),
+    (dict(budget_mode=3, threshold=float("inf")), X.EINVAL),
+    (dict(budget_mode=3, threshold=0.8, budget=0), X.EWORKSPACE),   # valid: fails on ws
     (dict(score_mode=5), X.EINVAL),
     (dict(n_experts=2048, top_k=8, budget=64), X.EUNSUPPORTED),
     (dict(n_experts=64, top_k=33, budget=64), X.EUNSUPPORTED),
 ])
 def test_route_parameter_validation(kw, status):
     base = dict(n_experts=16, top_k=2, warmup_k0=1, budget=8, budget_mode=0, score_mode=0,
-                per_request_budget=0)
+                per_request_budget=0, threshold=0.0)
     base.update(kw)
     p = X.RouteParams(*[base[f] for f, _ in X.RouteParams._fields_])
-    assert _route(p) == status
+    assert _route(p, ws=None) == status             # valid parameters stop at the workspace
 
 
 def test_route_size_and_pointer_validation():

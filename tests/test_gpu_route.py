@@ -120,6 +120,41 @@ def test_hier_invalid_device_offsets_yield_empty_selection():
     assert np.all(got["ids"] == -1)
 
 
+def _threshold_case(h, k, k0, tau, score="topk", offsets=None, m_r=0, label=""):
+    t = float(np.float32(tau))
+    say(f"route case {label} T={h.shape[0]} N={h.shape[1]} k={k} k0={k0} tau={t} {score}"
+        f"{'' if offsets is None else f' hier m_r={m_r}'}")
+    got = gpu_route(h, k, k0, 0, "threshold", score, offsets, m_r, tau=t)
+    ref = oracle_route(h, k, k0, 0, "threshold", score, offsets, m_r, tau=t)
+    assert_route_equal(got, ref, label)
+
+
+def test_route_threshold_rule():
+    """Algorithm 1's threshold: the stopping size depends on fp32 sums in the stated order;
+    tau = 1 makes rank-order and index-order sums meet in their last bits."""
+    for cfg in ("tiny", "qwen", "ds_t8", "ds_t32", "ds_iid_t32", "mixtral"):
+        c = W.CONFIGS[cfg]
+        for seed in range(4):
+            h, _ = W.make_logits(c, seed)
+            for k0 in (0, 1, 2):
+                for tau in (0.0, 0.3, 0.6, 0.9, 0.99, 1.0, 1.5):
+                    _threshold_case(h, c["k"], k0, tau, label=f"{cfg}/s{seed}")
+            _threshold_case(h, c["k"], 1, 0.7, "dense", label=f"{cfg}/dense/s{seed}")
+            _threshold_case(h, c["k"], 1, 1.0, "dense", label=f"{cfg}/dense/s{seed}")
+    rng = np.random.default_rng(5)
+    for it in range(10):                               # ties and tiny gates
+        T, N = int(rng.integers(1, 70)), int(rng.choice([16, 64, 256, 1024]))
+        h = (np.round(rng.standard_normal((T, N)) * 3) / 4).astype(F32)
+        h[rng.random(h.shape) < 0.1] = F32(-40.0)
+        _threshold_case(h, int(rng.integers(1, 9)), 1, float(rng.uniform(0.5, 1.0)),
+                        label=f"ties{it}")
+    c = W.CONFIGS["spec"]
+    for seed in range(3):
+        h, off = W.make_logits(c, seed)
+        for tau in (0.5, 0.9, 1.0):
+            _threshold_case(h, 8, 1, tau, offsets=off, m_r=4, label=f"spec/s{seed}")
+
+
 def test_route_is_deterministic():
     c = W.CONFIGS["spec"]
     h, off = W.make_logits(c, 9)
