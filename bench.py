@@ -61,6 +61,8 @@ def parse():
     ap.add_argument("--workload", default="ds_t32",
                     help="ds_t32 (default; the headline), ds_t8, qwen, mixtral, spec")
     ap.add_argument("--budget", type=int, default=None, help="total budget M (default: workload's)")
+    ap.add_argument("--tau", type=float, default=None,
+                    help="Algorithm 1's threshold rule instead of a budget: |S| adapts per batch")
     ap.add_argument("--replicas", type=int, default=None,
                     help="weight copies rotated over (default: enough for >= 4 GB of weights)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -131,7 +133,9 @@ def main():
     logits = [torch.from_numpy(h).to(dev) for h, _ in made]
     offs = [None if o is None else [int(v) for v in o] for _, o in made]
     xs = [W.activations(T, d, s, dev) for s in range(nb)]
-    p = X.params(N, k, k0, M, "total")
+    bmode = "total" if args.tau is None else "threshold"
+    tau = 0.0 if args.tau is None else args.tau
+    p = X.params(N, k, k0, M, bmode, threshold=tau)
     ws = torch.empty(X.moe_workspace_bytes(T, d, f, p), dtype=torch.uint8, device=dev)
     y = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
     torch.cuda.synchronize()
@@ -140,9 +144,9 @@ def main():
         b = s % nb
         wa, wb, wc = wsets[s % reps]
         if mode == "xshare":
-            return X.moe_forward(xs[b], logits[b], wa, wb, wc, k, k0, M, "total", y=y,
+            return X.moe_forward(xs[b], logits[b], wa, wb, wc, k, k0, M, bmode, y=y,
                                  workspace=ws, req_offsets=offs[b] if hier else None,
-                                 per_request_budget=m_r, **kw)
+                                 per_request_budget=m_r, tau=tau, **kw)
         return X.moe_forward(xs[b], logits[b], wa, wb, wc, k, 0, N, "extra", y=y, workspace=ws,
                              **kw)
 
@@ -199,12 +203,13 @@ def main():
     gbs = float(lay_bytes.mean()) / (ms_step * 1e-3) / 1e9
     gu_achieved = float(gu_bytes.mean()) / (float(gu_ms.mean()) * 1e-3) / 1e9
     # the committed counter record covers the headline workload only
-    traffic = counters_traffic() if (args.workload, M, T) == ("ds_t32", 48, 32) else None
+    traffic = counters_traffic() if (args.workload, M, T, args.tau) == ("ds_t32", 48, 32, None) \
+        else None
 
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(W, xs, logits, offs if hier else None, m_r, w1, w3, w2, T, N, k, k0, M,
-                           d, f)
+                           d, f, bmode, args.tau)
 
     out = {
         "metric": METRIC,
@@ -220,15 +225,19 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": WORKLOAD_NAMES[args.workload].format(T=T, N=N, k=k, d=d, f=f, M=M,
-                                                                     k0=k0, m_r=m_r),
+                                                                     k0=k0, m_r=m_r)
+                   + ("" if args.tau is None else f"_tau{args.tau:g}"),
                    "tokens": T, "n_experts": N, "top_k": k, "d_model": d, "d_ffn": f,
-                   "budget": M, "budget_mode": "total", "warmup_k0": k0,
+                   "budget": None if args.tau is not None else M, "budget_mode": bmode,
+                   "threshold": args.tau, "warmup_k0": k0,
                    "per_request_budget": m_r if hier else None,
                    "logits": LOGITS_RECIPE[cfg["logits"]].format(Q=cfg.get("Q")),
                    "batches_rotated": nb, "weight_replicas": reps},
         "us_per_batch": round(ms_step * 1e3, 2),
         "tokens_per_s": round(T / (ms_step * 1e-3), 1),
         "experts_activated": round(float(np.mean(act)), 2),
+        "experts_selected_range": [int(min(s[0]["n_selected"] for s in stats)),
+                                   int(max(s[0]["n_selected"] for s in stats))],
         "experts_vanilla": round(float(np.mean(act_v)), 2),
         "vanilla_us_per_batch": None if vanilla is None else round(vanilla * 1e3, 2),
         "speedup_vs_vanilla": None if vanilla is None else round(vanilla / ms_step, 3),
@@ -348,7 +357,8 @@ def run_ep(args, W, X, np, torch):
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(W, xs, logits, offs, m_r, w1, w3, w2, T, N, k, k0, M, d, f, budget_s=10.0):
+def cpu_baseline(W, xs, logits, offs, m_r, w1, w3, w2, T, N, k, k0, M, d, f, mode="total",
+                 tau=None, budget_s=10.0):
     """The oracle on the host cores: routing plus the float64 SwiGLU layer of whole batches,
     over as many of the rotated batches as fit in about budget_s seconds (at least one)."""
     import numpy as np
@@ -366,7 +376,8 @@ def cpu_baseline(W, xs, logits, offs, m_r, w1, w3, w2, T, N, k, k0, M, d, f, bud
         h = logits[b].cpu().numpy()
         xb = W.bf16_bits(xs[b])
         t0 = time.perf_counter()
-        r = OR.route(h, k, k0, M) if offs is None else OR.select_hier(h, offs[b], k, k0, m_r, M)
+        r = OR.route(h, k, k0, M, mode, tau=tau) if offs is None else \
+            OR.select_hier(h, offs[b], k, k0, m_r, M, mode, tau=tau)
         t_route = time.perf_counter() - t0
         used = sorted(set(int(e) for e in r.ids.reshape(-1)))
         cache = {e: tuple(W.bf16_bits(m[e]) for m in (w1, w3, w2)) for e in used}   # not timed

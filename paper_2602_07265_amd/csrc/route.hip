@@ -274,8 +274,10 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   __shared__ int s_wsum[kWaves];
   __shared__ int s_cnt[8];
   __shared__ int s_gload[kMaxExperts];   // GPU groups: warm-up experts per group, then |S| per group
-  __shared__ int s_gcand[kMaxExperts];   // candidates per group outside the warm-up set
-  __shared__ int s_hist[kMaxExperts];    // takeable candidates per rank inside their group
+  // GPU groups: candidates per group outside the warm-up set; threshold rule: scores by index
+  __shared__ __align__(16) int s_gcand[kMaxExperts];
+  // GPU groups: takeable candidates per rank inside their group; threshold rule: scores by rank
+  __shared__ __align__(16) int s_hist[kMaxExperts];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -518,11 +520,21 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
       float* const by_index = reinterpret_cast<float*>(s_gcand);
       float* const by_rank = reinterpret_cast<float*>(s_hist);
       if (j < N) by_index[j] = s;
+      if (j >= N && j < ((N + 3) & ~3)) by_index[j] = 0.0f;   // pad to whole float4s
       if (mykey != 0) by_rank[rank] = s;
       __syncthreads();
       if (tid == 0) {
+        // sequential fp32 sums; 16-byte LDS reads keep the loads ahead of the adds
+        const float4* e4 = reinterpret_cast<const float4*>(by_index);
         float f_E = 0.0f;
-        for (int jj = 0; jj < N; ++jj) f_E = f_E + by_index[jj];
+#pragma unroll 4
+        for (int q = 0; q < (N + 3) / 4; ++q) {
+          const float4 v = e4[q];
+          f_E = f_E + v.x;
+          f_E = f_E + v.y;
+          f_E = f_E + v.z;
+          f_E = f_E + v.w;
+        }
         const float target = a.tau * f_E;
         float f_S = 0.0f;
         for (int r = 0; r < n_start; ++r) f_S = f_S + by_rank[r];
