@@ -30,12 +30,20 @@ def expert_ffn(x, w1_bits, w3_bits, w2_bits) -> np.ndarray:
     return (silu(a) * b) @ W2.T
 
 
-def moe_forward(x_bits, ids, w, expert, rows=None, local=None) -> np.ndarray:
-    """y[i] = sum_r w[i,r] * E_{ids[i,r]}(x_i) for the tokens in ``rows`` (default: all).
+def router_logits(x_bits, wg_bits) -> np.ndarray:
+    """h = W_g x for every token (Section 2.2): float64 [T, N] from bf16 x [T,d] and
+    W_g [N,d]."""
+    return bf16_to_f64(x_bits) @ bf16_to_f64(wg_bits).T
 
-    ``expert(e)`` returns the bf16 bit arrays (w1 [f,d], w3 [f,d], w2 [d,f]) of expert e.
-    With ``local`` (a set of experts, those one GPU group hosts under expert parallelism,
-    Section 5) only the terms of those experts are summed: that group's share of y.
+
+def moe_forward(x_bits, ids, w, expert, rows=None, local=None, shared=()) -> np.ndarray:
+    """y[i] = sum_r w[i,r] * E_{ids[i,r]}(x_i) + sum_s E^s_s(x_i) for the tokens in ``rows``
+    (default: all); the second sum runs over the always-on shared experts of Section 2.1.
+
+    ``expert(e)`` returns the bf16 bit arrays (w1 [f,d], w3 [f,d], w2 [d,f]) of expert e;
+    ``shared`` is a sequence of such triples.  With ``local`` (a set of experts, those one
+    GPU group hosts under expert parallelism, Section 5) only the terms of those routed
+    experts are summed: that group's share of y.
     Returns float64 [len(rows), d].
     """
     X = bf16_to_f64(x_bits)
@@ -54,4 +62,6 @@ def moe_forward(x_bits, ids, w, expert, rows=None, local=None) -> np.ndarray:
         out = expert_ffn(X[[rows[p] for p, _ in pairs]], w1, w3, w2)
         for q, (p, r) in enumerate(pairs):
             y[p] += w[rows[p], r] * out[q]
+    for w1, w3, w2 in shared:
+        y += expert_ffn(X[rows], w1, w3, w2)
     return y

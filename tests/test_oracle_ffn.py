@@ -114,3 +114,65 @@ def test_group_shares_sum_to_the_layer():
         assert np.allclose(share, dense, rtol=1e-12, atol=1e-14)
         total += share
     assert np.allclose(total, y, rtol=1e-12, atol=1e-14)
+
+
+def test_router_logits_closed_forms():
+    """h = W_g x (Section 2.2): one-hot router rows read out columns of x (a transposed
+    operand fails since N != d), and a pure-Python dot product on a tiny case."""
+    import torch
+    T, d, N = 5, 12, 7
+    x = W.activations(T, d, 3)
+    eye = torch.zeros((N, d), dtype=torch.bfloat16)
+    cols = [3, 0, 11, 5, 5, 8, 1]
+    for j, c in enumerate(cols):
+        eye[j, c] = 1.0
+    h = O.router_logits(W.bf16_bits(x), W.bf16_bits(eye))
+    X = O.bf16_to_f64(W.bf16_bits(x))
+    assert np.array_equal(h, X[:, cols])
+    wg = W.router_weights(N, d, 3)
+    Wg = O.bf16_to_f64(W.bf16_bits(wg))
+    h = O.router_logits(W.bf16_bits(x), W.bf16_bits(wg))
+    for i in range(T):
+        for j in range(N):
+            ref = 0.0
+            for q in range(d):
+                ref += float(X[i, q]) * float(Wg[j, q])
+            assert abs(h[i, j] - ref) <= 1e-12 * (1 + abs(ref))
+
+
+def test_shared_expert_is_an_always_routed_expert_with_weight_one():
+    """Section 2.1: the shared term equals routing every token to that expert with gate 1."""
+    c = W.CONFIGS["tiny"]
+    h, _ = W.make_logits(c, 4)
+    r = R.route(h, c["k"], 1, c["M"])
+    x = W.bf16_bits(W.activations(c["T"], c["d"], 4))
+    ws = [tuple(W.bf16_bits(W.expert_matrix(e, m, c["d"], c["f"], 4)) for m in ("w1", "w3", "w2"))
+          for e in range(c["N"])]
+    sh = [tuple(W.bf16_bits(m[e]) for m in W.shared_weights(2, c["d"], c["f"], 4))
+          for e in range(2)]
+    base = O.moe_forward(x, r.ids, r.w, lambda e: ws[e])
+    both = O.moe_forward(x, r.ids, r.w, lambda e: ws[e], shared=sh)
+    ones = np.ones((c["T"], 1))
+    alone = sum(O.moe_forward(x, np.zeros((c["T"], 1), np.int32), ones, lambda e, t=t: t)
+                for t in sh)
+    assert np.allclose(both - base, alone, rtol=1e-12, atol=1e-14)
+    # one SwiGLU of width 2f equals two of width f holding its halves (the hidden units are
+    # independent), which is how a wider shared expert maps onto experts of width f
+    wide = tuple(np.concatenate(p, axis=1 if i == 2 else 0) for i, p in enumerate(zip(*sh)))
+    X = O.bf16_to_f64(x)
+    assert np.allclose(O.expert_ffn(X, *wide), O.expert_ffn(X, *sh[0]) + O.expert_ffn(X, *sh[1]),
+                       rtol=1e-12, atol=1e-14)
+
+
+def test_domain_activations_carry_the_routing_structure():
+    """Tokens of one domain share most of their hidden state, so the router's logits of two
+    such tokens are strongly correlated; iid activations give uncorrelated logits."""
+    T, d, N, Q = 48, 512, 128, 6
+    x = W.bf16_bits(W.activations_domains(T, d, Q, 1))
+    wg = W.bf16_bits(W.router_weights(N, d, 1))
+    h = O.router_logits(x, wg)
+    dom = W._rng(W._S_X, 2, T, d, Q, 1).integers(0, Q, T)
+    same = [np.corrcoef(h[i], h[j])[0, 1] for i in range(T) for j in range(i) if dom[i] == dom[j]]
+    diff = [np.corrcoef(h[i], h[j])[0, 1] for i in range(T) for j in range(i) if dom[i] != dom[j]]
+    assert np.mean(same) > 0.6 and abs(np.mean(diff)) < 0.2
+    assert 1.2 < h.std() < 2.0

@@ -25,6 +25,13 @@ datasets that are not available; these stand in for them):
   integer op or one IEEE fp32 multiply, so torch produces identical bits on the
   CPU and on the GPU, and any single expert matrix can be regenerated on its own.
   x ~ N(0,1), weights ~ N(0, 0.02) (standard deviation, not variance).
+* the whole layer (router GEMM h = W_g x and shared experts, Section 2.1): the
+  router sees x, so x carries the domain structure instead of the logits:
+  x_i = c_q(i) + 0.5 eps_i with Q centroids c_q ~ N(0,1) per feature and
+  eps ~ N(0,1) (both bf16 draws as above, summed in fp32, rounded to bf16 in
+  integer RNE); W_g ~ N(0, 1.5 / sqrt(d)) in bf16, so a logit has a domain part
+  of standard deviation about 1.5 and a token part of about 0.75.  Shared
+  experts have the routed experts' shape and N(0, 0.02) weights.
 """
 from __future__ import annotations
 
@@ -38,7 +45,8 @@ SEED_ROOT = 260207265
 _S_LOGITS = 0
 _S_X = 1
 _S_W = 2
-_MATRIX_ID = {"w1": 0, "w3": 1, "w2": 2}
+_MATRIX_ID = {"w1": 0, "w3": 1, "w2": 2, "s1": 3, "s3": 4, "s2": 5}
+_S_ROUTER = 3
 
 
 def _rng(*ids: int) -> np.random.Generator:
@@ -146,9 +154,49 @@ def activations(T: int, d: int, seed: int, device="cpu"):
     return bf16_normal((T, d), 1.0, (_S_X, T, d, seed), device)
 
 
+def _round_bf16(v):
+    """fp32 tensor -> bf16 with round-to-nearest-even done in integer arithmetic."""
+    import torch
+
+    b = v.contiguous().view(torch.int32).to(torch.int64) & 0xFFFFFFFF
+    b = (b + 0x7FFF + ((b >> 16) & 1)) >> 16
+    return (b - ((b & 0x8000) << 1)).to(torch.int16).view(torch.bfloat16)
+
+
+def activations_domains(T: int, d: int, n_domains: int, seed: int, device="cpu"):
+    """x [T,d] bf16 = c[domain(token)] + 0.5 eps: hidden states with domain structure."""
+    import torch
+
+    dom = _rng(_S_X, 2, T, d, n_domains, seed).integers(0, n_domains, T)
+    c = bf16_normal((n_domains, d), 1.0, (_S_X, 3, d, n_domains, seed), device).float()
+    eps = bf16_normal((T, d), 1.0, (_S_X, 4, T, d, seed), device).float()
+    v = c[torch.as_tensor(dom, device=device)] + eps * 0.5      # fp32: one multiply, one add
+    return _round_bf16(v).reshape(T, d)
+
+
+def router_weights(N: int, d: int, seed: int, device="cpu"):
+    """W_g [N,d] bf16 ~ N(0, 1.5 / sqrt(d)) (nn.Linear [out,in] layout)."""
+    return bf16_normal((N, d), 1.5 / math.sqrt(d), (_S_ROUTER, N, d, seed), device)
+
+
+def shared_weights(n_shared: int, d: int, f: int, seed: int, device="cpu", std: float = 0.02):
+    """(w1 [N_s,f,d], w3 [N_s,f,d], w2 [N_s,d,f]) bf16 of the always-on shared experts."""
+    import torch
+
+    w1 = torch.empty((n_shared, f, d), dtype=torch.bfloat16, device=device)
+    w3 = torch.empty((n_shared, f, d), dtype=torch.bfloat16, device=device)
+    w2 = torch.empty((n_shared, d, f), dtype=torch.bfloat16, device=device)
+    for e in range(n_shared):
+        w1[e] = expert_matrix(e, "s1", d, f, seed, device, std)
+        w3[e] = expert_matrix(e, "s3", d, f, seed, device, std)
+        w2[e] = expert_matrix(e, "s2", d, f, seed, device, std)
+    return w1, w3, w2
+
+
 def expert_matrix(e: int, which: str, d: int, f: int, seed: int, device="cpu", std: float = 0.02):
-    """One expert matrix in nn.Linear [out,in] layout: w1/w3 are [f,d], w2 is [d,f]."""
-    shape = (d, f) if which == "w2" else (f, d)
+    """One expert matrix in nn.Linear [out,in] layout: w1/w3 (s1/s3 for shared experts) are
+    [f,d], w2 (s2) is [d,f]."""
+    shape = (d, f) if which in ("w2", "s2") else (f, d)
     return bf16_normal(shape, std, (_S_W, _MATRIX_ID[which], e, d, f, seed), device)
 
 
