@@ -8,7 +8,9 @@
  * read.  For speculative-decoding batches the set is built per request first and then
  * completed at batch level (Section 4.1, Algorithms 3 and 4).  Under expert parallelism the
  * experts are spread over G GPU groups and the set is grown one expert per group in turn,
- * which bounds the most loaded group (Section 5, Eq. (5), Algorithms 5 and 6).
+ * which bounds the most loaded group (Section 5, Eq. (5), Algorithms 5 and 6).  The whole
+ * layer of Section 2.1 is available too: router logits h = W_g x on the device, the routed
+ * experts of the selected set, and always-on shared experts.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -129,13 +131,54 @@ typedef struct {
   const int32_t* host_expert_group;
 } xshare_ep_layout;
 
+/*
+ * Always-on shared experts (Section 2.1: y gains sum_s E^s_s(x) with weight 1).  Each has
+ * the routed experts' shape, SwiGLU with hidden width f; a wider shared expert of width
+ * m * f is m of these holding slices of its hidden units (the hidden units of a SwiGLU are
+ * independent, so the sum is the same function).
+ *
+ *   n_shared  N_s, 0 <= N_s <= 64 (more: XSHARE_EUNSUPPORTED).
+ *   w1, w3    DEVICE [N_s, f, d] bf16; w2 DEVICE [N_s, d, f] bf16; 16-byte aligned.
+ */
+typedef struct {
+  int32_t n_shared;
+  const uint16_t* w1;
+  const uint16_t* w3;
+  const uint16_t* w2;
+} xshare_shared_experts;
+
 /* Workspace for xshare_route / xshare_select_hier with T tokens (bytes, 256-aligned).    */
 size_t xshare_route_workspace_bytes(int32_t T, const xshare_route_params* params);
 
-/* Workspace for xshare_moe_forward (includes the routing workspace); `ep` as passed to   *
- * xshare_moe_forward (nullable).  Returns 0 for invalid arguments.                        */
+/* Workspace for xshare_moe_forward (includes the routing workspace); `ep` and `shared` as *
+ * passed to xshare_moe_forward (nullable).  Returns 0 for invalid arguments.              */
 size_t xshare_moe_workspace_bytes(int32_t T, int32_t d, int32_t f,
-                                  const xshare_route_params* params, const xshare_ep_layout* ep);
+                                  const xshare_route_params* params, const xshare_ep_layout* ep,
+                                  const xshare_shared_experts* shared);
+
+/* Workspace for xshare_moe_layer: that of xshare_moe_forward plus the router's partials.  */
+size_t xshare_layer_workspace_bytes(int32_t T, int32_t d, int32_t f,
+                                    const xshare_route_params* params,
+                                    const xshare_ep_layout* ep,
+                                    const xshare_shared_experts* shared);
+
+/* Workspace for xshare_router_logits (bytes, 256-aligned); 0 for invalid sizes.           */
+size_t xshare_router_workspace_bytes(int32_t T, int32_t d, int32_t n_experts);
+
+/*
+ * xshare_router_logits -- router logits h = W_g x of a batch (Section 2.2).
+ *
+ *   x        [T, d] bf16 row-major, 16-byte aligned.
+ *   w_gate   [N, d] bf16 (nn.Linear [out, in]), 16-byte aligned; N = n_experts <= 1024.
+ *   logits   out [T, N] fp32: h_ij = sum_q x_iq * W_g[j, q]; the bf16 products are exact in
+ *            fp32 and accumulated in fp32 (matrix-core blocks of 32, the parts of d summed
+ *            in a fixed order), so |h - exact| <= d * 2^-24 * sum_q |x_iq W_g[j, q]| (up to
+ *            second order) and repeated calls give identical bits.
+ *   d        multiple of 32.
+ */
+xshare_status xshare_router_logits(const uint16_t* x, const uint16_t* w_gate, int32_t T,
+                                   int32_t d, int32_t n_experts, float* logits, void* ws,
+                                   size_t ws_bytes, hipStream_t stream);
 
 /*
  * xshare_route -- batch-aware expert selection for one layer (Algorithm 2, Section 3.4).
@@ -213,6 +256,8 @@ xshare_status xshare_select_ep(const float* logits, int32_t T, const xshare_rout
  *   ep       nullable HOST pointer: the expert-parallel selection of xshare_select_ep and,
  *            with ep->local_group >= 0, one group's share of y (see xshare_ep_layout).
  *            Not combined with req_offsets (XSHARE_EUNSUPPORTED).
+ *   shared   nullable HOST pointer: always-on shared experts, added to y after the routed
+ *            terms with weight 1 (not with a local group: XSHARE_EUNSUPPORTED).
  *   y        out [T, d] bf16: y_i = sum_r w_ir * E_{e_ir}(x_i) with the refined routing
  *            (Section 2.1 without the shared-expert term), E(x) = W2 (silu(W1 x) * (W3 x)),
  *            fp32 accumulation, rounded to bf16 (nearest even) once at the end.
@@ -222,15 +267,40 @@ xshare_status xshare_select_ep(const float* logits, int32_t T, const xshare_rout
  *
  * Only the weights of experts that receive at least one token are read, each once per
  * (up to) 32 tokens routed to it.  Pointers x, w1, w3, w2 and y must be 16-byte aligned.
+ * With shared experts, y_i = sum_r w_ir * E_{e_ir}(x_i) + sum_s E^s_s(x_i), the shared
+ * terms added after the routed ones.
  */
 xshare_status xshare_moe_forward(const uint16_t* x, const float* logits, int32_t T, int32_t d,
                                  int32_t f, const uint16_t* w1, const uint16_t* w3,
                                  const uint16_t* w2, const xshare_route_params* params,
                                  const int32_t* req_offsets, const int32_t* host_offsets,
-                                 int32_t R, const xshare_ep_layout* ep, uint16_t* y,
+                                 int32_t R, const xshare_ep_layout* ep,
+                                 const xshare_shared_experts* shared, uint16_t* y,
                                  uint8_t* sel_mask, int32_t* topk_ids, float* topk_w,
                                  xshare_stats* stats, void* ws, size_t ws_bytes,
                                  void* const* stage_events, hipStream_t stream);
+
+/*
+ * xshare_moe_layer -- the whole MoE layer of Section 2.1 from the hidden states: router
+ * logits h = W_g x (as xshare_router_logits), selection, the selected routed experts and
+ * the shared experts, combine.
+ *
+ *   w_gate      [N, d] bf16 router weights (16-byte aligned).
+ *   logits_out  nullable out [T, N] fp32: the logits the selection used (bit-identical to
+ *               xshare_router_logits on the same inputs).
+ *   ws          at least xshare_layer_workspace_bytes.
+ *   Other arguments as xshare_moe_forward; stage event 1 marks the end of router plus
+ *   selection.
+ */
+xshare_status xshare_moe_layer(const uint16_t* x, const uint16_t* w_gate, int32_t T, int32_t d,
+                               int32_t f, const uint16_t* w1, const uint16_t* w3,
+                               const uint16_t* w2, const xshare_shared_experts* shared,
+                               const xshare_route_params* params, const int32_t* req_offsets,
+                               const int32_t* host_offsets, int32_t R,
+                               const xshare_ep_layout* ep, uint16_t* y, float* logits_out,
+                               uint8_t* sel_mask, int32_t* topk_ids, float* topk_w,
+                               xshare_stats* stats, void* ws, size_t ws_bytes,
+                               void* const* stage_events, hipStream_t stream);
 
 /* Static description of a status code (never NULL).                                      */
 const char* xshare_status_string(int32_t status);

@@ -4,6 +4,7 @@ The computation lives in hand-written HIP kernels behind the C ABI of include/xs
 (libxshare.so, built in-tree by ``paper_2602_07265_amd.build``); ``xshare`` is the Python
 binding with the same entry points.
 """
-from .xshare import (GroupMap, HipEvent, XShareError, lib, moe_forward,  # noqa: F401
-                     moe_workspace_bytes, params, route, route_workspace_bytes, select_ep,
-                     select_hier, stats_dict, status_string, version)
+from .xshare import (GroupMap, HipEvent, XShareError, layer_workspace_bytes,  # noqa: F401
+                     lib, moe_forward, moe_layer, moe_workspace_bytes, params, route,
+                     route_workspace_bytes, router_logits, select_ep, select_hier, stats_dict,
+                     status_string, version)

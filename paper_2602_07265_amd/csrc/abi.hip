@@ -137,6 +137,33 @@ xs::RouteArgs route_args(const float* logits, int32_t T, const xshare_route_para
   return a;
 }
 
+int n_shared_of(const xshare_shared_experts* shared) { return shared ? shared->n_shared : 0; }
+
+xs::FfnLayout layer_layout(int32_t T, int32_t d, int32_t f, const xshare_route_params* p,
+                           const xshare_ep_layout* ep, int n_shared) {
+  return xs::ffn_layout(T, p->n_experts, p->top_k, p->score_mode == XSHARE_SCORE_DENSE, d, f,
+                        layer_estimate(T, p, ep) + n_shared, n_shared);
+}
+
+// Router partial planes [splits, T, N] fp32 (none when the router does not split).
+size_t router_parts_bytes(int32_t T, int32_t d, int32_t N) {
+  const int s = xs::router_splits(T, d, N);
+  return s > 1 ? xs::align256(sizeof(float) * size_t(s) * size_t(T > 0 ? T : 1) * N) : 256;
+}
+
+// Shared experts: 0 <= N_s <= 64 experts of the routed shape, 16-byte aligned; none with a
+// local GPU group (a group's share holds routed experts only).
+xshare_status check_shared(const xshare_shared_experts* shared, const xshare_ep_layout* ep) {
+  if (!shared || shared->n_shared == 0) return XSHARE_OK;
+  if (shared->n_shared < 0) return XSHARE_EINVAL;
+  if (shared->n_shared > 64) return XSHARE_EUNSUPPORTED;
+  if (!shared->w1 || !shared->w3 || !shared->w2) return XSHARE_EINVAL;
+  if (!aligned16(shared->w1) || !aligned16(shared->w3) || !aligned16(shared->w2))
+    return XSHARE_EINVAL;
+  if (ep && ep->local_group >= 0) return XSHARE_EUNSUPPORTED;
+  return XSHARE_OK;
+}
+
 xshare_status route_common(const float* logits, int32_t T, const int32_t* req_offsets,
                            const int32_t* host_offsets, int32_t R, bool hier,
                            const xshare_route_params* p, uint8_t* sel_mask, int32_t* ids,
@@ -157,6 +184,107 @@ xshare_status route_common(const float* logits, int32_t T, const int32_t* req_of
   return xs::launch_route(a, stream) == hipSuccess ? XSHARE_OK : XSHARE_EHIP;
 }
 
+// The layer: optional router GEMM (w_gate given: its partial planes go to the workspace and
+// the selection kernel sums them), selection, expert GEMMs (routed and shared), combine.
+xshare_status layer_common(const uint16_t* x, const float* logits, const uint16_t* w_gate,
+                           int32_t T, int32_t d, int32_t f, const uint16_t* w1,
+                           const uint16_t* w3, const uint16_t* w2,
+                           const xshare_shared_experts* shared, const xshare_route_params* params,
+                           const int32_t* req_offsets, const int32_t* host_offsets, int32_t R,
+                           const xshare_ep_layout* ep, uint16_t* y, float* logits_out,
+                           uint8_t* sel_mask, int32_t* topk_ids, float* topk_w,
+                           xshare_stats* stats, void* ws, size_t ws_bytes,
+                           void* const* stage_events, hipStream_t stream) {
+  const bool hier = req_offsets != nullptr;
+  if (hier && ep) return XSHARE_EUNSUPPORTED;
+  xshare_status st = check_params(T, params, hier, ep != nullptr);
+  if (st != XSHARE_OK) return st;
+  if (hier) {
+    st = check_offsets(T, req_offsets, host_offsets, R);
+    if (st != XSHARE_OK) return st;
+  }
+  st = check_ep(params->n_experts, ep, true);
+  if (st != XSHARE_OK) return st;
+  st = check_shared(shared, ep);
+  if (st != XSHARE_OK) return st;
+  if (d <= 0 || f <= 0) return XSHARE_EINVAL;
+  if (d % xs::kDimAlign != 0 || f % xs::kDimAlign != 0) return XSHARE_EUNSUPPORTED;
+  if (T > 0 && (!x || !w1 || !w3 || !w2 || !y)) return XSHARE_EINVAL;
+  if (!aligned16(x) || !aligned16(w1) || !aligned16(w3) || !aligned16(w2) || !aligned16(y) ||
+      (w_gate && !aligned16(w_gate)))
+    return XSHARE_EINVAL;
+  const int N = params->n_experts, k = params->top_k;
+  const int n_shared = n_shared_of(shared);
+  const int bound = layer_bound(T, params, ep);
+  const xs::FfnLayout L = layer_layout(T, d, f, params, ep, n_shared);
+  const size_t need = L.total + (w_gate ? router_parts_bytes(T, d, N) : 0);
+  if (!ws || ws_bytes < need) return XSHARE_EWORKSPACE;
+
+  // The selection kernel always writes a mask; keep it in the workspace if not wanted.
+  uint8_t* mask = sel_mask ? sel_mask : at<uint8_t>(ws, L.route.mask);
+  auto record = [&](int s) -> bool {
+    if (!stage_events) return true;
+    return hipEventRecord(static_cast<hipEvent_t>(stage_events[s]), stream) == hipSuccess;
+  };
+  if (!record(0)) return XSHARE_EHIP;
+  xs::RouteArgs ra = route_args(logits, T, params, hier ? req_offsets : nullptr, R, ep, nullptr,
+                                mask, topk_ids, topk_w, stats, ws, L.route);
+  if (ep) ra.local_group = ep->local_group;
+  ra.logits_out = logits_out;
+  if (w_gate && T > 0) {
+    const int s = xs::router_splits(T, d, N);
+    float* parts = at<float>(ws, L.total);
+    xs::RouterArgs r{x, w_gate, T, d, N, s, parts};
+    if (xs::launch_router(r, stream) != hipSuccess) return XSHARE_EHIP;
+    ra.logits = nullptr;
+    ra.parts = parts;
+    ra.n_parts = s;
+  }
+  if (xs::launch_route(ra, stream) != hipSuccess || !record(1)) return XSHARE_EHIP;
+  if (T == 0) {
+    for (int s = 2; s < XSHARE_N_STAGE_EVENTS; ++s)
+      if (!record(s)) return XSHARE_EHIP;
+    return XSHARE_OK;
+  }
+
+  xs::FfnArgs fa{};
+  fa.x = x;
+  fa.w1 = w1;
+  fa.w3 = w3;
+  fa.w2 = w2;
+  fa.T = T;
+  fa.N = N;
+  fa.k = k;
+  fa.d = d;
+  fa.f = f;
+  fa.max_active = bound;
+  fa.splits = L.splits;
+  fa.gu_splits = L.gu_splits;
+  fa.gpart = at<float>(ws, L.gpart);
+  fa.G = ra.G;
+  fa.group = ra.group;
+  fa.local_group = ra.local_group;
+  fa.n_shared = n_shared;
+  fa.sw1 = n_shared ? shared->w1 : nullptr;
+  fa.sw3 = n_shared ? shared->w3 : nullptr;
+  fa.sw2 = n_shared ? shared->w2 : nullptr;
+  fa.rows = (long)xs::ffn_rows(T, k, n_shared);
+  fa.offsets = ra.offsets;
+  fa.perm = ra.perm;
+  fa.active = ra.active;
+  fa.counters = ra.counters;
+  fa.ids = ra.ids;
+  fa.w = ra.w;
+  fa.h = at<uint16_t>(ws, L.h);
+  fa.hlo = at<uint16_t>(ws, L.hlo);
+  fa.yslot = at<float>(ws, L.y);
+  fa.y = y;
+  if (xs::launch_gate_up(fa, stream) != hipSuccess || !record(2)) return XSHARE_EHIP;
+  if (xs::launch_down(fa, stream) != hipSuccess || !record(3)) return XSHARE_EHIP;
+  if (xs::launch_combine(fa, stream) != hipSuccess || !record(4)) return XSHARE_EHIP;
+  return XSHARE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -170,13 +298,19 @@ size_t xshare_route_workspace_bytes(int32_t T, const xshare_route_params* params
 }
 
 size_t xshare_moe_workspace_bytes(int32_t T, int32_t d, int32_t f,
-                                  const xshare_route_params* params, const xshare_ep_layout* ep) {
+                                  const xshare_route_params* params, const xshare_ep_layout* ep,
+                                  const xshare_shared_experts* shared) {
   if (check_params(T, params, false, ep != nullptr) != XSHARE_OK || d <= 0 || f <= 0) return 0;
   if (check_ep(params->n_experts, ep, true) != XSHARE_OK) return 0;
-  return xs::ffn_layout(T, params->n_experts, params->top_k,
-                        params->score_mode == XSHARE_SCORE_DENSE, d, f,
-                        layer_estimate(T, params, ep))
-      .total;
+  return layer_layout(T, d, f, params, ep, n_shared_of(shared)).total;
+}
+
+size_t xshare_layer_workspace_bytes(int32_t T, int32_t d, int32_t f,
+                                    const xshare_route_params* params,
+                                    const xshare_ep_layout* ep,
+                                    const xshare_shared_experts* shared) {
+  const size_t m = xshare_moe_workspace_bytes(T, d, f, params, ep, shared);
+  return m == 0 ? 0 : m + router_parts_bytes(T, d, params->n_experts);
 }
 
 xshare_status xshare_route(const float* logits, int32_t T, const xshare_route_params* params,
@@ -217,77 +351,53 @@ xshare_status xshare_moe_forward(const uint16_t* x, const float* logits, int32_t
                                  int32_t f, const uint16_t* w1, const uint16_t* w3,
                                  const uint16_t* w2, const xshare_route_params* params,
                                  const int32_t* req_offsets, const int32_t* host_offsets,
-                                 int32_t R, const xshare_ep_layout* ep, uint16_t* y,
+                                 int32_t R, const xshare_ep_layout* ep,
+                                 const xshare_shared_experts* shared, uint16_t* y,
                                  uint8_t* sel_mask, int32_t* topk_ids, float* topk_w,
                                  xshare_stats* stats, void* ws, size_t ws_bytes,
                                  void* const* stage_events, hipStream_t stream) {
-  const bool hier = req_offsets != nullptr;
-  if (hier && ep) return XSHARE_EUNSUPPORTED;
-  xshare_status st = check_params(T, params, hier, ep != nullptr);
-  if (st != XSHARE_OK) return st;
-  if (hier) {
-    st = check_offsets(T, req_offsets, host_offsets, R);
-    if (st != XSHARE_OK) return st;
-  }
-  st = check_ep(params->n_experts, ep, true);
-  if (st != XSHARE_OK) return st;
-  if (d <= 0 || f <= 0) return XSHARE_EINVAL;
-  if (d % xs::kDimAlign != 0 || f % xs::kDimAlign != 0) return XSHARE_EUNSUPPORTED;
-  if (T > 0 && (!x || !logits || !w1 || !w3 || !w2 || !y)) return XSHARE_EINVAL;
-  if (!aligned16(x) || !aligned16(w1) || !aligned16(w3) || !aligned16(w2) || !aligned16(y))
-    return XSHARE_EINVAL;
-  const int N = params->n_experts, k = params->top_k;
-  const int bound = layer_bound(T, params, ep);
-  const xs::FfnLayout L = xs::ffn_layout(T, N, k, params->score_mode == XSHARE_SCORE_DENSE, d,
-                                         f, layer_estimate(T, params, ep));
-  if (!ws || ws_bytes < L.total) return XSHARE_EWORKSPACE;
+  if (T > 0 && !logits) return XSHARE_EINVAL;
+  return layer_common(x, logits, nullptr, T, d, f, w1, w3, w2, shared, params, req_offsets,
+                      host_offsets, R, ep, y, nullptr, sel_mask, topk_ids, topk_w, stats, ws,
+                      ws_bytes, stage_events, stream);
+}
 
-  // The selection kernel always writes a mask; keep it in the workspace if not wanted.
-  uint8_t* mask = sel_mask ? sel_mask : at<uint8_t>(ws, L.route.mask);
-  auto record = [&](int s) -> bool {
-    if (!stage_events) return true;
-    return hipEventRecord(static_cast<hipEvent_t>(stage_events[s]), stream) == hipSuccess;
-  };
-  if (!record(0)) return XSHARE_EHIP;
-  xs::RouteArgs ra = route_args(logits, T, params, hier ? req_offsets : nullptr, R, ep, nullptr,
-                                mask, topk_ids, topk_w, stats, ws, L.route);
-  if (ep) ra.local_group = ep->local_group;
-  if (xs::launch_route(ra, stream) != hipSuccess || !record(1)) return XSHARE_EHIP;
-  if (T == 0) {
-    for (int s = 2; s < XSHARE_N_STAGE_EVENTS; ++s)
-      if (!record(s)) return XSHARE_EHIP;
-    return XSHARE_OK;
-  }
+xshare_status xshare_moe_layer(const uint16_t* x, const uint16_t* w_gate, int32_t T, int32_t d,
+                               int32_t f, const uint16_t* w1, const uint16_t* w3,
+                               const uint16_t* w2, const xshare_shared_experts* shared,
+                               const xshare_route_params* params, const int32_t* req_offsets,
+                               const int32_t* host_offsets, int32_t R,
+                               const xshare_ep_layout* ep, uint16_t* y, float* logits_out,
+                               uint8_t* sel_mask, int32_t* topk_ids, float* topk_w,
+                               xshare_stats* stats, void* ws, size_t ws_bytes,
+                               void* const* stage_events, hipStream_t stream) {
+  if (T > 0 && !w_gate) return XSHARE_EINVAL;
+  return layer_common(x, nullptr, w_gate, T, d, f, w1, w3, w2, shared, params, req_offsets,
+                      host_offsets, R, ep, y, logits_out, sel_mask, topk_ids, topk_w, stats, ws,
+                      ws_bytes, stage_events, stream);
+}
 
-  xs::FfnArgs fa{};
-  fa.x = x;
-  fa.w1 = w1;
-  fa.w3 = w3;
-  fa.w2 = w2;
-  fa.T = T;
-  fa.N = N;
-  fa.k = k;
-  fa.d = d;
-  fa.f = f;
-  fa.max_active = bound;
-  fa.splits = L.splits;
-  fa.gu_splits = L.gu_splits;
-  fa.gpart = at<float>(ws, L.gpart);
-  fa.G = ra.G;
-  fa.group = ra.group;
-  fa.local_group = ra.local_group;
-  fa.offsets = ra.offsets;
-  fa.perm = ra.perm;
-  fa.active = ra.active;
-  fa.counters = ra.counters;
-  fa.ids = ra.ids;
-  fa.w = ra.w;
-  fa.h = at<uint16_t>(ws, L.h);
-  fa.yslot = at<float>(ws, L.y);
-  fa.y = y;
-  if (xs::launch_gate_up(fa, stream) != hipSuccess || !record(2)) return XSHARE_EHIP;
-  if (xs::launch_down(fa, stream) != hipSuccess || !record(3)) return XSHARE_EHIP;
-  if (xs::launch_combine(fa, stream) != hipSuccess || !record(4)) return XSHARE_EHIP;
+size_t xshare_router_workspace_bytes(int32_t T, int32_t d, int32_t n_experts) {
+  if (T < 0 || T > kMaxTokens || d <= 0 || d % xs::kDimAlign != 0 || n_experts < 1 ||
+      n_experts > kMaxExperts)
+    return 0;
+  return router_parts_bytes(T, d, n_experts);
+}
+
+xshare_status xshare_router_logits(const uint16_t* x, const uint16_t* w_gate, int32_t T,
+                                   int32_t d, int32_t n_experts, float* logits, void* ws,
+                                   size_t ws_bytes, hipStream_t stream) {
+  if (T < 0 || d <= 0 || n_experts < 1) return XSHARE_EINVAL;
+  if (T > kMaxTokens || n_experts > kMaxExperts || d % xs::kDimAlign != 0)
+    return XSHARE_EUNSUPPORTED;
+  if (T == 0) return XSHARE_OK;
+  if (!x || !w_gate || !logits || !aligned16(x) || !aligned16(w_gate)) return XSHARE_EINVAL;
+  const int s = xs::router_splits(T, d, n_experts);
+  if (s > 1 && (!ws || ws_bytes < router_parts_bytes(T, d, n_experts))) return XSHARE_EWORKSPACE;
+  xs::RouterArgs r{x, w_gate, T, d, n_experts, s, s > 1 ? static_cast<float*>(ws) : logits};
+  if (xs::launch_router(r, stream) != hipSuccess) return XSHARE_EHIP;
+  if (s > 1 && xs::launch_router_reduce(r.out, s, T, n_experts, logits, stream) != hipSuccess)
+    return XSHARE_EHIP;
   return XSHARE_OK;
 }
 

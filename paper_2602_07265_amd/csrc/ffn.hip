@@ -1,7 +1,14 @@
 // Expert FFNs of the selected experts only (SwiGLU, nn.Linear [out, in] weights, bf16):
 //   gate/up:  H[p, :] = silu(x_i W1_e^T) * (x_i W3_e^T)      for every permuted row p = (i, r)
 //   down:     Y[i*k + r, :] = H[p, :] W2_e^T
+// H is kept as two bf16 arrays, hi = bf16(H) and lo = bf16(H - hi) (about 16 significant
+// bits): with H in bf16 alone its rounding moved large outputs across a bf16 rounding
+// boundary of y.  The down GEMM feeds both halves to one MFMA: 8 tokens per 16-row tile,
+// hi rows 0-7 and lo rows 8-15, summed after the reduction.
 //   combine:  y_i = sum_r w_ir Y[i*k + r, :]  (rank order, fp32) -> bf16
+// Always-on shared experts (Section 2.1) are extra slots after the routed ones, with all T
+// tokens; their output rows are added after the routed terms with weight 1.  The router
+// GEMM h = W_g x uses the same wave pass with the router rows as weights.
 //
 // Decode batches give an expert 1..T tokens, so each weight element is used a few times:
 // the GEMMs are bound by streaming the selected experts' weights from HBM.  Each wave owns
@@ -40,6 +47,15 @@ __device__ __forceinline__ uint16_t to_bf16(float v) {
   return (uint16_t)(b >> 16);
 }
 
+__device__ __forceinline__ float from_bf16(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// Stores v as hi = bf16(v) and lo = bf16(v - hi).
+__device__ __forceinline__ void store_hilo(uint16_t* hi, uint16_t* lo, size_t at, float v) {
+  const uint16_t h = to_bf16(v);
+  hi[at] = h;
+  lo[at] = to_bf16(v - from_bf16(h));
+}
+
 // One pass of a wave over the reduction dimension K for up to kTiles token tiles:
 // acc[m][rt] += A_rt (16 x K) * B_m^T (K x 16) for the NM weight matrices B_m.
 // `arow[rt]` points at the token row this lane feeds (a duplicate of a valid row for
@@ -49,26 +65,26 @@ __device__ __forceinline__ uint16_t to_bf16(float v) {
 // both already offset by this lane's group position g * 8U.  Weight loads (HBM) run one
 // step ahead; token loads (L2-resident) are issued either one step ahead too (ADBL) or
 // at the top of their own step, which halves their register footprint.
-template <int U, int NM, bool ADBL>
-__device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[kTiles], int nt,
+template <int U, int NM, bool ADBL, int TL = kTiles>
+__device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[TL], int nt,
                                           const uint16_t* const (&brow)[NM], int K,
-                                          floatx4 (&acc)[NM][kTiles]) {
+                                          floatx4 (&acc)[NM][TL]) {
   constexpr int KB = 32 * U;
-  bf16x8 b[NM][U], x[kTiles][U];
+  bf16x8 b[NM][U], x[TL][U];
 #pragma unroll
   for (int m = 0; m < NM; ++m)
 #pragma unroll
     for (int u = 0; u < U; ++u) b[m][u] = load8(brow[m] + 8 * u);
   if (ADBL) {
 #pragma unroll
-    for (int rt = 0; rt < kTiles; ++rt)
+    for (int rt = 0; rt < TL; ++rt)
       if (rt < nt)
 #pragma unroll
         for (int u = 0; u < U; ++u) x[rt][u] = load8(arow[rt] + 8 * u);
   }
 
   for (int kb = 0; kb < K; kb += KB) {
-    bf16x8 nb[NM][U], nx[ADBL ? kTiles : 1][U];
+    bf16x8 nb[NM][U], nx[ADBL ? TL : 1][U];
     const bool more = kb + KB < K;
     if (more) {
 #pragma unroll
@@ -77,7 +93,7 @@ __device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[kTiles],
         for (int u = 0; u < U; ++u) nb[m][u] = load8(brow[m] + kb + KB + 8 * u);
       if (ADBL) {
 #pragma unroll
-        for (int rt = 0; rt < kTiles; ++rt)
+        for (int rt = 0; rt < TL; ++rt)
           if (rt < nt)
 #pragma unroll
             for (int u = 0; u < U; ++u) nx[rt][u] = load8(arow[rt] + kb + KB + 8 * u);
@@ -85,7 +101,7 @@ __device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[kTiles],
     }
     if (!ADBL) {
 #pragma unroll
-      for (int rt = 0; rt < kTiles; ++rt)
+      for (int rt = 0; rt < TL; ++rt)
         if (rt < nt)
 #pragma unroll
           for (int u = 0; u < U; ++u) x[rt][u] = load8(arow[rt] + kb + 8 * u);
@@ -93,7 +109,7 @@ __device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[kTiles],
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int rt = 0; rt < kTiles; ++rt)
+      for (int rt = 0; rt < TL; ++rt)
         if (rt < nt)
 #pragma unroll
           for (int m = 0; m < NM; ++m) acc[m][rt] = mfma(x[rt][u], b[m][u], acc[m][rt]);
@@ -104,7 +120,7 @@ __device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[kTiles],
         for (int u = 0; u < U; ++u) b[m][u] = nb[m][u];
       if (ADBL) {
 #pragma unroll
-        for (int rt = 0; rt < kTiles; ++rt)
+        for (int rt = 0; rt < TL; ++rt)
 #pragma unroll
           for (int u = 0; u < U; ++u) x[rt][u] = nx[ADBL ? rt : 0][u];
       }
@@ -120,24 +136,57 @@ __device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[kTiles],
 #define XS_GATE_UP_ADBL 1
 #endif
 #ifndef XS_DOWN_U
-#define XS_DOWN_U 8
+#define XS_DOWN_U 2
 #endif
 #ifndef XS_DOWN_ADBL
 #define XS_DOWN_ADBL 0
 #endif
-#ifndef XS_DOWN_NM
-#define XS_DOWN_NM 2
+#ifndef XS_DOWN_TL
+#define XS_DOWN_TL 4                 // 8-token (hi + lo) tiles per pass of the down GEMM
 #endif
+
+// Work of grid row `slot` of the expert GEMMs: the routed active experts first (their
+// tokens' rows in permuted order), then the shared experts (all T tokens, rows
+// T*k + s*T + t).  False for rows beyond both.
+struct SlotWork {
+  const uint16_t* w1;
+  const uint16_t* w3;
+  const uint16_t* w2;
+  int p0, te;
+  bool shared;
+};
+
+__device__ __forceinline__ bool slot_work(const FfnArgs& a, int slot, SlotWork& w) {
+  const int n_active = a.counters[kCntActive];
+  const size_t fd = (size_t)a.f * a.d;
+  if (slot < n_active) {
+    const int e = a.active[slot];
+    w.p0 = a.offsets[e];
+    w.te = a.offsets[e + 1] - w.p0;
+    w.w1 = a.w1 + e * fd;
+    w.w3 = a.w3 + e * fd;
+    w.w2 = a.w2 + e * fd;
+    w.shared = false;
+    return true;
+  }
+  const int sh = slot - n_active;
+  if (sh >= a.n_shared) return false;
+  w.p0 = a.T * a.k + sh * a.T;
+  w.te = a.T;
+  w.w1 = a.sw1 + sh * fd;
+  w.w3 = a.sw3 + sh * fd;
+  w.w2 = a.sw2 + sh * fd;
+  w.shared = true;
+  return true;
+}
 
 // kSplit: the block covers one part of the reduction (blockIdx.z) and writes fp32 gate and
 // up partials; otherwise it covers all of d and writes H directly.
 template <int U, bool kSplit>
 __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
-  const int slot = blockIdx.y;
-  if (slot >= a.counters[kCntActive]) return;
-  const int e = a.active[slot];
-  const int p0 = a.offsets[e];
-  const int te = a.offsets[e + 1] - p0;
+  SlotWork sw;
+  if (!slot_work(a, blockIdx.y, sw)) return;
+  const int p0 = sw.p0, te = sw.te;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int j0 = (blockIdx.x * kWaves + wave) * kCols;
   if (j0 >= a.f) return;
@@ -145,9 +194,9 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
   const int d = a.d, f = a.f;
   const int Kg = kSplit ? d / a.gu_splits : d;   // this block's part of the reduction
   const size_t k0 = (kSplit ? (size_t)blockIdx.z * Kg : 0) + (size_t)g * 8 * U;
-  const size_t wrow = ((size_t)e * f + j0 + n) * d + k0;
-  const uint16_t* const brow[2] = {a.w1 + wrow, a.w3 + wrow};
-  const size_t plane = (size_t)a.T * a.k * f;  // one fp32 partial plane [T * k, f]
+  const size_t wrow = (size_t)(j0 + n) * d + k0;
+  const uint16_t* const brow[2] = {sw.w1 + wrow, sw.w3 + wrow};
+  const size_t plane = (size_t)a.rows * f;     // one fp32 partial plane [rows, f]
 
   for (int c0 = 0; c0 < te; c0 += 16 * kTiles) {
     const int nt = min(kTiles, (te - c0 + 15) / 16);
@@ -155,7 +204,8 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
 #pragma unroll
     for (int rt = 0; rt < kTiles; ++rt) {
       const int t = min(c0 + rt * 16 + n, te - 1);
-      arow[rt] = a.x + (size_t)(a.perm[p0 + t] / a.k) * d + k0;
+      const int tok = sw.shared ? t : a.perm[p0 + t] / a.k;
+      arow[rt] = a.x + (size_t)tok * d + k0;
     }
     floatx4 acc[2][kTiles];
 #pragma unroll
@@ -173,7 +223,7 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
           const float h1 = acc[0][rt][i], h3 = acc[1][rt][i];
           const size_t at = (size_t)(p0 + t) * f + j0 + n;
           if (!kSplit) {
-            a.h[at] = to_bf16(h1 / (1.0f + __expf(-h1)) * h3);
+            store_hilo(a.h, a.hlo, at, h1 / (1.0f + __expf(-h1)) * h3);
           } else {
             float* const part = a.gpart + 2 * blockIdx.z * plane;
             part[at] = h1;
@@ -188,11 +238,10 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
 template <int U>
 __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
   constexpr int NM = XS_DOWN_NM;  // 16-row tiles of W2 per wave, sharing the token operand
-  const int slot = blockIdx.y;
-  if (slot >= a.counters[kCntActive]) return;
-  const int e = a.active[slot];
-  const int p0 = a.offsets[e];
-  const int te = a.offsets[e + 1] - p0;
+  constexpr int TL = XS_DOWN_TL;  // token tiles per pass, 8 tokens each (hi and lo rows)
+  SlotWork sw;
+  if (!slot_work(a, blockIdx.y, sw)) return;
+  const int p0 = sw.p0, te = sw.te;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int n0 = (blockIdx.x * kWaves + wave) * kCols * NM;
   if (n0 >= a.d) return;
@@ -200,37 +249,43 @@ __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
   const int d = a.d, f = a.f;
   const int Ks = f / a.splits;                 // this block's part of the reduction
   const size_t k0 = (size_t)blockIdx.z * Ks + (size_t)g * 8 * U;
-  float* const ypart = a.yslot + (size_t)blockIdx.z * a.T * a.k * d;
+  float* const ypart = a.yslot + (size_t)blockIdx.z * a.rows * d;
+  const uint16_t* const hsrc = n < 8 ? a.h : a.hlo;   // A rows 0-7: hi, rows 8-15: lo
   const uint16_t* brow[NM];
 #pragma unroll
   for (int m = 0; m < NM; ++m)
-    brow[m] = a.w2 + ((size_t)e * d + min(n0 + 16 * m, d - 16) + n) * f + k0;
+    brow[m] = sw.w2 + ((size_t)min(n0 + 16 * m, d - 16) + n) * f + k0;
 
-  for (int c0 = 0; c0 < te; c0 += 16 * kTiles) {
-    const int nt = min(kTiles, (te - c0 + 15) / 16);
-    const uint16_t* arow[kTiles];
+  for (int c0 = 0; c0 < te; c0 += 8 * TL) {
+    const int nt = min(TL, (te - c0 + 7) / 8);
+    const uint16_t* arow[TL];
 #pragma unroll
-    for (int rt = 0; rt < kTiles; ++rt) {
-      const int t = min(c0 + rt * 16 + n, te - 1);
-      arow[rt] = a.h + (size_t)(p0 + t) * f + k0;
+    for (int rt = 0; rt < TL; ++rt) {
+      const int t = min(c0 + rt * 8 + (n & 7), te - 1);
+      arow[rt] = hsrc + (size_t)(p0 + t) * f + k0;
     }
-    floatx4 acc[NM][kTiles];
+    floatx4 acc[NM][TL];
 #pragma unroll
     for (int m = 0; m < NM; ++m)
 #pragma unroll
-      for (int rt = 0; rt < kTiles; ++rt) acc[m][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    wave_pass<U, NM, XS_DOWN_ADBL != 0>(arow, nt, brow, Ks, acc);
+      for (int rt = 0; rt < TL; ++rt) acc[m][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    wave_pass<U, NM, XS_DOWN_ADBL != 0, TL>(arow, nt, brow, Ks, acc);
 #pragma unroll
-    for (int rt = 0; rt < kTiles; ++rt) {
+    for (int rt = 0; rt < TL; ++rt) {
       if (rt >= nt) break;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int t = c0 + rt * 16 + 4 * g + i;
-        if (t < te) {
-          float* yrow = ypart + (size_t)a.perm[p0 + t] * d;
+        // lanes g = 0, 1 hold the hi rows of tokens 4g + i, lanes 32 above them the lo rows
+        float v[NM];
+#pragma unroll
+        for (int m = 0; m < NM; ++m) v[m] = acc[m][rt][i] + __shfl_xor(acc[m][rt][i], 32, 64);
+        const int t = c0 + rt * 8 + 4 * g + i;
+        if (g < 2 && t < te) {
+          // routed rows go to their (token, slot) row, shared rows keep their own
+          float* yrow = ypart + (size_t)(sw.shared ? p0 + t : a.perm[p0 + t]) * d;
 #pragma unroll
           for (int m = 0; m < NM; ++m)
-            if (n0 + 16 * m < d) yrow[n0 + 16 * m + n] = acc[m][rt][i];
+            if (n0 + 16 * m < d) yrow[n0 + 16 * m + n] = v[m];
         }
       }
     }
@@ -238,18 +293,19 @@ __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
 }
 
 // Split gate/up reduction: sums the gate and up partials in split order, then
-// H = silu(gate) * up in bf16.  One block row per hidden row (permuted order); rows whose
-// expert the GEMMs did not cover (another GPU group's) are skipped.
+// H = silu(gate) * up in bf16.  One block row per hidden row; routed rows beyond the routed
+// count, and rows whose expert the GEMMs did not cover (another GPU group's), are skipped.
 __global__ __launch_bounds__(kBlock) void gate_up_finish_kernel(FfnArgs a) {
   const int p = blockIdx.y;
-  if (p >= a.offsets[a.N]) return;
-  if (a.local_group >= 0) {
+  const bool shared_row = p >= a.T * a.k;
+  if (!shared_row && p >= a.offsets[a.N]) return;
+  if (!shared_row && a.local_group >= 0) {
     const int e = a.ids[a.perm[p]];
     if ((a.group ? a.group[e] : e / (a.N / a.G)) != a.local_group) return;
   }
   const int c = (blockIdx.x * kBlock + threadIdx.x) * 4;
   if (c >= a.f) return;
-  const size_t plane = (size_t)a.T * a.k * a.f;
+  const size_t plane = (size_t)a.rows * a.f;
   const size_t at = (size_t)p * a.f + c;
   float4 gs = *reinterpret_cast<const float4*>(a.gpart + at);
   float4 us = *reinterpret_cast<const float4*>(a.gpart + plane + at);
@@ -259,11 +315,10 @@ __global__ __launch_bounds__(kBlock) void gate_up_finish_kernel(FfnArgs a) {
     gs.x += gz.x; gs.y += gz.y; gs.z += gz.z; gs.w += gz.w;
     us.x += uz.x; us.y += uz.y; us.z += uz.z; us.w += uz.w;
   }
-  const uint32_t lo = (uint32_t)to_bf16(gs.x / (1.0f + __expf(-gs.x)) * us.x) |
-                      ((uint32_t)to_bf16(gs.y / (1.0f + __expf(-gs.y)) * us.y) << 16);
-  const uint32_t hi = (uint32_t)to_bf16(gs.z / (1.0f + __expf(-gs.z)) * us.z) |
-                      ((uint32_t)to_bf16(gs.w / (1.0f + __expf(-gs.w)) * us.w) << 16);
-  *reinterpret_cast<uint2*>(a.h + at) = make_uint2(lo, hi);
+  store_hilo(a.h, a.hlo, at + 0, gs.x / (1.0f + __expf(-gs.x)) * us.x);
+  store_hilo(a.h, a.hlo, at + 1, gs.y / (1.0f + __expf(-gs.y)) * us.y);
+  store_hilo(a.h, a.hlo, at + 2, gs.z / (1.0f + __expf(-gs.z)) * us.z);
+  store_hilo(a.h, a.hlo, at + 3, gs.w / (1.0f + __expf(-gs.w)) * us.w);
 }
 
 __global__ __launch_bounds__(kBlock) void combine_kernel(FfnArgs a) {
@@ -281,7 +336,7 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(FfnArgs a) {
     float4 v = *reinterpret_cast<const float4*>(a.yslot + (size_t)slot * a.d + c);
     for (int s = 1; s < a.splits; ++s) {   // partial sums of a split reduction, in order
       const float4 u = *reinterpret_cast<const float4*>(
-          a.yslot + ((size_t)s * a.T * a.k + slot) * a.d + c);
+          a.yslot + ((size_t)s * a.rows + slot) * a.d + c);
       v.x += u.x;
       v.y += u.y;
       v.z += u.z;
@@ -292,9 +347,69 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(FfnArgs a) {
     acc[2] += wr * v.z;
     acc[3] += wr * v.w;
   }
+  for (int sh = 0; sh < a.n_shared; ++sh) {  // shared experts, weight 1, after the routed terms
+    const size_t row = (size_t)a.T * a.k + (size_t)sh * a.T + i;
+    float4 v = *reinterpret_cast<const float4*>(a.yslot + row * a.d + c);
+    for (int s = 1; s < a.splits; ++s) {
+      const float4 u = *reinterpret_cast<const float4*>(
+          a.yslot + ((size_t)s * a.rows + row) * a.d + c);
+      v.x += u.x;
+      v.y += u.y;
+      v.z += u.z;
+      v.w += u.w;
+    }
+    acc[0] += v.x;
+    acc[1] += v.y;
+    acc[2] += v.z;
+    acc[3] += v.w;
+  }
   const uint32_t lo = (uint32_t)to_bf16(acc[0]) | ((uint32_t)to_bf16(acc[1]) << 16);
   const uint32_t hi = (uint32_t)to_bf16(acc[2]) | ((uint32_t)to_bf16(acc[3]) << 16);
   *reinterpret_cast<uint2*>(a.y + (size_t)i * a.d + c) = make_uint2(lo, hi);
+}
+
+// Router GEMM h = W_g x: each wave owns 16 router rows (experts) and one part of d
+// (blockIdx.z), the token tiles of blockIdx.y; fp32 results go to that part's plane.
+template <int U>
+__global__ __launch_bounds__(kBlock) void router_kernel(RouterArgs r) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int j0 = (blockIdx.x * kWaves + wave) * kCols;
+  if (j0 >= r.N) return;
+  const int n = lane & 15, g = lane >> 4;
+  const int Kr = r.d / r.splits;
+  const size_t k0 = (size_t)blockIdx.z * Kr + (size_t)g * 8 * U;
+  const uint16_t* const brow[1] = {r.wg + (size_t)min(j0 + n, r.N - 1) * r.d + k0};
+  float* const out = r.out + (size_t)blockIdx.z * r.T * r.N;
+  for (int c0 = blockIdx.y * 16 * kTiles; c0 < r.T; c0 += gridDim.y * 16 * kTiles) {
+    const int nt = min(kTiles, (r.T - c0 + 15) / 16);
+    const uint16_t* arow[kTiles];
+#pragma unroll
+    for (int rt = 0; rt < kTiles; ++rt)
+      arow[rt] = r.x + (size_t)min(c0 + rt * 16 + n, r.T - 1) * r.d + k0;
+    floatx4 acc[1][kTiles];
+#pragma unroll
+    for (int rt = 0; rt < kTiles; ++rt) acc[0][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    wave_pass<U, 1, false>(arow, nt, brow, Kr, acc);
+#pragma unroll
+    for (int rt = 0; rt < kTiles; ++rt) {
+      if (rt >= nt) break;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t = c0 + rt * 16 + 4 * g + i;
+        if (t < r.T && j0 + n < r.N) out[(size_t)t * r.N + j0 + n] = acc[0][rt][i];
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void router_reduce_kernel(const float* parts, int n_parts,
+                                                               int T, int N, float* logits) {
+  const size_t idx = (size_t)blockIdx.x * kBlock + threadIdx.x;
+  const size_t plane = (size_t)T * N;
+  if (idx >= plane) return;
+  float v = parts[idx];
+  for (int z = 1; z < n_parts; ++z) v = v + parts[z * plane + idx];
+  logits[idx] = v;
 }
 
 template <int U>
@@ -314,7 +429,8 @@ int unroll_for(int K, int want) {
 }  // namespace
 
 hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
-  const dim3 grid((a.f + kWaves * kCols - 1) / (kWaves * kCols), a.max_active, a.gu_splits),
+  const dim3 grid((a.f + kWaves * kCols - 1) / (kWaves * kCols), a.max_active + a.n_shared,
+                  a.gu_splits),
       block(kBlock);
   const bool split = a.gu_splits > 1;
   switch (unroll_for(a.d / a.gu_splits, XS_GATE_UP_U)) {
@@ -324,7 +440,7 @@ hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
     default: launch_gu<1>(a, split, grid, block, stream); break;
   }
   if (split) {
-    const dim3 fgrid((a.f + kBlock * 4 - 1) / (kBlock * 4), a.T * a.k);
+    const dim3 fgrid((a.f + kBlock * 4 - 1) / (kBlock * 4), (unsigned)a.rows);
     hipLaunchKernelGGL(gate_up_finish_kernel, fgrid, block, 0, stream, a);
   }
   return hipGetLastError();
@@ -332,13 +448,33 @@ hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
 
 hipError_t launch_down(const FfnArgs& a, hipStream_t stream) {
   constexpr int cols = kWaves * kCols * XS_DOWN_NM;
-  const dim3 grid((a.d + cols - 1) / cols, a.max_active, a.splits), block(kBlock);
+  const dim3 grid((a.d + cols - 1) / cols, a.max_active + a.n_shared, a.splits), block(kBlock);
   switch (unroll_for(a.f / a.splits, XS_DOWN_U)) {
     case 8: hipLaunchKernelGGL(down_kernel<8>, grid, block, 0, stream, a); break;
     case 4: hipLaunchKernelGGL(down_kernel<4>, grid, block, 0, stream, a); break;
     case 2: hipLaunchKernelGGL(down_kernel<2>, grid, block, 0, stream, a); break;
     default: hipLaunchKernelGGL(down_kernel<1>, grid, block, 0, stream, a); break;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_router(const RouterArgs& r, hipStream_t stream) {
+  const dim3 grid((r.N + kWaves * kCols - 1) / (kWaves * kCols), router_token_tiles(r.T),
+                  r.splits),
+      block(kBlock);
+  switch (unroll_for(r.d / r.splits, 4)) {
+    case 4: hipLaunchKernelGGL(router_kernel<4>, grid, block, 0, stream, r); break;
+    case 2: hipLaunchKernelGGL(router_kernel<2>, grid, block, 0, stream, r); break;
+    default: hipLaunchKernelGGL(router_kernel<1>, grid, block, 0, stream, r); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_router_reduce(const float* parts, int n_parts, int T, int N, float* logits,
+                                hipStream_t stream) {
+  const size_t n = (size_t)T * N;
+  const dim3 grid((unsigned)((n + kBlock - 1) / kBlock)), block(kBlock);
+  hipLaunchKernelGGL(router_reduce_kernel, grid, block, 0, stream, parts, n_parts, T, N, logits);
   return hipGetLastError();
 }
 

@@ -96,37 +96,81 @@ inline int gate_up_splits(int est_active, int d, int f) {
   return split_for((long)est_active * (f / 16), d, 128, XS_GU_SPLIT_BELOW, XS_GU_SPLIT_TARGET,
                    XS_GATE_UP_MAX_SPLITS);
 }
+// 16-row tiles of W2 per wave of the down GEMM (output rows per wave = 16 * XS_DOWN_NM).
+#ifndef XS_DOWN_NM
+#define XS_DOWN_NM 2
+#endif
 inline int down_splits(int est_active, int d, int f) {
-  return split_for((long)est_active * (d / 32), f, 128, XS_DN_SPLIT_BELOW, XS_DN_SPLIT_TARGET);
+  return split_for((long)est_active * (d / (16 * XS_DOWN_NM)), f, 128, XS_DN_SPLIT_BELOW,
+                   XS_DN_SPLIT_TARGET);
+}
+
+// Hidden and output rows of the expert GEMMs: the T * k routed (token, slot) rows in
+// permuted order, then T rows per always-on shared expert (token order).
+inline size_t ffn_rows(int T, int k, int n_shared) {
+  const size_t t = size_t(T > 0 ? T : 1);
+  return t * size_t(k) + size_t(n_shared) * t;
 }
 
 struct FfnLayout {
   RouteLayout route;
   int gu_splits;  // K-splits of the gate/up GEMM
   int splits;     // K-splits of the down GEMM
-  size_t gpart;   // fp32 [gu_splits, 2, T * k, f] gate and up partial sums (gu_splits > 1)
-  size_t h;       // bf16 [T * k, f]            SwiGLU hidden rows in permuted order
-  size_t y;       // fp32 [splits, T * k, d]    per-(token, slot) partial expert outputs
+  size_t gpart;   // fp32 [gu_splits, 2, rows, f] gate and up partial sums (gu_splits > 1)
+  size_t h;       // bf16 [rows, f]             SwiGLU hidden rows, rounded to bf16 (hi)
+  size_t hlo;     // bf16 [rows, f]             their rounding remainders (lo), H ~ hi + lo
+  size_t y;       // fp32 [splits, rows, d]     per-row partial expert outputs
   size_t total;
 };
 
-inline FfnLayout ffn_layout(int T, int N, int k, bool dense, int d, int f, int est_active) {
+// est_active: experts expected to be active (routed plus shared), for the split counts.
+inline FfnLayout ffn_layout(int T, int N, int k, bool dense, int d, int f, int est_active,
+                            int n_shared) {
   FfnLayout L{};
   L.route = route_layout(T, N, k, dense);
   L.gu_splits = gate_up_splits(est_active, d, f);
   L.splits = down_splits(est_active, d, f);
-  size_t tk = size_t(T > 0 ? T : 1) * size_t(k);
+  const size_t rows = ffn_rows(T, k, n_shared);
   size_t o = L.route.total;
   L.gpart = o;
-  if (L.gu_splits > 1) o += align256(sizeof(float) * 2 * size_t(L.gu_splits) * tk * size_t(f));
-  L.h = o; o += align256(sizeof(uint16_t) * tk * size_t(f));
-  L.y = o; o += align256(sizeof(float) * size_t(L.splits) * tk * size_t(d));
+  if (L.gu_splits > 1) o += align256(sizeof(float) * 2 * size_t(L.gu_splits) * rows * size_t(f));
+  L.h = o; o += align256(sizeof(uint16_t) * rows * size_t(f));
+  L.hlo = o; o += align256(sizeof(uint16_t) * rows * size_t(f));
+  L.y = o; o += align256(sizeof(float) * size_t(L.splits) * rows * size_t(d));
   L.total = o;
   return L;
 }
 
+// The router GEMM h = W_g x splits d into this many parts (fp32 partial planes summed in
+// order by whoever reads the logits) so that N/16 x token-tile waves become >= 512.
+inline int router_token_tiles(int T) {
+  const int tiles = (T + 31) / 32;
+  return tiles < 64 ? (tiles > 0 ? tiles : 1) : 64;
+}
+inline int router_splits(int T, int d, int N) {
+  const long waves = (long)((N + 15) / 16) * router_token_tiles(T);
+  int s = 1;
+  while (s < 16 && waves * s < 512 && d % (2 * s * 32) == 0) s *= 2;
+  return s;
+}
+
+struct RouterArgs {
+  const uint16_t* x;           // bf16 [T, d]
+  const uint16_t* wg;          // bf16 [N, d]
+  int T, d, N, splits;
+  float* out;                  // fp32 [splits, T, N] partial planes (the logits if splits == 1)
+};
+
+hipError_t launch_router(const RouterArgs& r, hipStream_t stream);
+// logits[t, j] = sum over z of parts[z, t, j], z ascending
+hipError_t launch_router_reduce(const float* parts, int n_parts, int T, int N, float* logits,
+                                hipStream_t stream);
+
 struct RouteArgs {
-  const float* logits;
+  const float* logits;         // [T, N], or nullptr when `parts` holds the router's partials
+  const float* parts;          // [n_parts, T, N] router partial planes, summed in order
+  int n_parts;
+  float* logits_out;           // nullable: the logits used, [T, N]
   int T, N, k, k0, budget, budget_mode, score_mode, m_r;
   float tau;                   // threshold mode (budget_mode 3)
   const int32_t* req_offsets;  // nullptr: flat Algorithm 2
@@ -161,13 +205,19 @@ struct FfnArgs {
   int G;                       // GPU groups, with `group` and `local_group` as in RouteArgs
   const int32_t* group;
   int local_group;
+  int n_shared;                // always-on shared experts (slots after the routed ones)
+  const uint16_t* sw1;         // [n_shared, f, d]
+  const uint16_t* sw3;
+  const uint16_t* sw2;         // [n_shared, d, f]
+  long rows;                   // T * k + n_shared * T hidden / output rows
   const int32_t* offsets;
   const int32_t* perm;
   const int32_t* active;
   const int32_t* counters;
   const int32_t* ids;
   const float* w;
-  uint16_t* h;
+  uint16_t* h;                 // hidden rows, bf16 hi part
+  uint16_t* hlo;               // hidden rows, bf16 lo part (H - hi rounded to bf16)
   float* yslot;
   uint16_t* y;
 };

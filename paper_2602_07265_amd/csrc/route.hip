@@ -152,13 +152,30 @@ __device__ __forceinline__ float ranked_gate(float my_h, int lane, int k) {
   return lane < k ? e / z : 0.0f;
 }
 
-// Raw logits of one token, lane l holding experts l, l + 64, ...
+// Raw logits of token i, lane l holding experts l, l + 64, ...: read from the logits, or
+// summed over the router's partial planes in plane order.
 template <int Q>
-__device__ __forceinline__ void load_row(const float* row, int N, int lane, float (&raw)[Q]) {
+__device__ __forceinline__ void load_row(const RouteArgs& a, int i, int lane, float (&raw)[Q]) {
+  const int N = a.N;
+  const size_t row = (size_t)i * N;
+  if (!a.parts) {
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int j = lane + 64 * q;
+      raw[q] = j < N ? a.logits[row + j] : 0.0f;
+    }
+    return;
+  }
+  const size_t plane = (size_t)a.T * N;
 #pragma unroll
   for (int q = 0; q < Q; ++q) {
     const int j = lane + 64 * q;
-    raw[q] = j < N ? row[j] : 0.0f;
+    float v = 0.0f;
+    if (j < N) {
+      v = a.parts[row + j];
+      for (int z = 1; z < a.n_parts; ++z) v = v + a.parts[z * plane + row + j];
+    }
+    raw[q] = v;
   }
 }
 
@@ -346,13 +363,17 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   const bool cached = T <= kCache * kWaves;
   uint32_t kc[kCache][Q];
   float raw_next[Q];
-  if (wave < T) load_row<Q>(a.logits + (size_t)wave * N, N, lane, raw_next);
+  if (wave < T) load_row<Q>(a, wave, lane, raw_next);
   for (int i = wave, it = 0; i < T; i += kWaves, ++it) {
     float raw[Q], v[Q];
     uint32_t key[Q];
 #pragma unroll
     for (int q = 0; q < Q; ++q) raw[q] = raw_next[q];
-    if (i + kWaves < T) load_row<Q>(a.logits + (size_t)(i + kWaves) * N, N, lane, raw_next);
+    if (i + kWaves < T) load_row<Q>(a, i + kWaves, lane, raw_next);
+    if (a.logits_out)
+#pragma unroll
+      for (int q = 0; q < Q; ++q)
+        if (lane + 64 * q < N) a.logits_out[(size_t)i * N + lane + 64 * q] = raw[q];
     row_keys<Q>(raw, N, lane, v, key);
     float my_h;
     int my_j;
@@ -649,7 +670,7 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   // ---- (e) refinement: every token to its top-k inside S, gates renormalised (Section 3.4).
   //      The token's plain top-k experts that are in S are its first refined ranks (in
   //      their order); only the remaining ranks are searched, among the other experts.
-  if (!cached && wave < T) load_row<Q>(a.logits + (size_t)wave * N, N, lane, raw_next);
+  if (!cached && wave < T) load_row<Q>(a, wave, lane, raw_next);
   for (int i = wave, it = 0; i < T; i += kWaves, ++it) {
     uint32_t key[Q];
     const uint32_t vent = lane < k ? (uint32_t)s_ent[i * k + lane] : kNoEntry;
@@ -660,7 +681,7 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
       float raw[Q], v[Q];
 #pragma unroll
       for (int q = 0; q < Q; ++q) raw[q] = raw_next[q];
-      if (i + kWaves < T) load_row<Q>(a.logits + (size_t)(i + kWaves) * N, N, lane, raw_next);
+      if (i + kWaves < T) load_row<Q>(a, i + kWaves, lane, raw_next);
       row_keys<Q>(raw, N, lane, v, key);
       for (int r = 0; r < k; ++r) {     // the plain top-k is not searched again
         const int vr = __builtin_amdgcn_readlane(vid, r);

@@ -44,6 +44,15 @@ class EpLayout(ctypes.Structure):
     ]
 
 
+class SharedExperts(ctypes.Structure):
+    _fields_ = [
+        ("n_shared", ctypes.c_int32),
+        ("w1", ctypes.c_void_p),
+        ("w3", ctypes.c_void_p),
+        ("w2", ctypes.c_void_p),
+    ]
+
+
 STATS_FIELDS = ("n_selected", "n_active", "n_vanilla_union", "n_warmup", "n_start",
                 "budget_eff", "max_group_load")
 
@@ -71,8 +80,22 @@ def lib() -> ctypes.CDLL:
         L.xshare_route_workspace_bytes.argtypes = [_I32, ctypes.POINTER(RouteParams)]
         L.xshare_route_workspace_bytes.restype = _SZ
         L.xshare_moe_workspace_bytes.argtypes = [_I32, _I32, _I32, ctypes.POINTER(RouteParams),
-                                                 ctypes.POINTER(EpLayout)]
+                                                 ctypes.POINTER(EpLayout),
+                                                 ctypes.POINTER(SharedExperts)]
         L.xshare_moe_workspace_bytes.restype = _SZ
+        L.xshare_layer_workspace_bytes.argtypes = [_I32, _I32, _I32, ctypes.POINTER(RouteParams),
+                                                   ctypes.POINTER(EpLayout),
+                                                   ctypes.POINTER(SharedExperts)]
+        L.xshare_layer_workspace_bytes.restype = _SZ
+        L.xshare_router_workspace_bytes.argtypes = [_I32, _I32, _I32]
+        L.xshare_router_workspace_bytes.restype = _SZ
+        L.xshare_router_logits.argtypes = [_P, _P, _I32, _I32, _I32, _P, _P, _SZ, _P]
+        L.xshare_router_logits.restype = ctypes.c_int
+        L.xshare_moe_layer.argtypes = [_P, _P, _I32, _I32, _I32, _P, _P, _P,
+                                       ctypes.POINTER(SharedExperts), ctypes.POINTER(RouteParams),
+                                       _P, _P, _I32, ctypes.POINTER(EpLayout), _P, _P, _P, _P, _P,
+                                       _P, _P, _SZ, _P, _P]
+        L.xshare_moe_layer.restype = ctypes.c_int
         L.xshare_route.argtypes = [_P, _I32, ctypes.POINTER(RouteParams), _P, _P, _P, _P, _P, _SZ,
                                    _P]
         L.xshare_route.restype = ctypes.c_int
@@ -84,8 +107,8 @@ def lib() -> ctypes.CDLL:
         L.xshare_select_ep.restype = ctypes.c_int
         L.xshare_moe_forward.argtypes = [_P, _P, _I32, _I32, _I32, _P, _P, _P,
                                          ctypes.POINTER(RouteParams), _P, _P, _I32,
-                                         ctypes.POINTER(EpLayout), _P, _P, _P, _P, _P, _P, _SZ, _P,
-                                         _P]
+                                         ctypes.POINTER(EpLayout), ctypes.POINTER(SharedExperts),
+                                         _P, _P, _P, _P, _P, _P, _SZ, _P, _P]
         L.xshare_moe_forward.restype = ctypes.c_int
         L.xshare_status_string.argtypes = [_I32]
         L.xshare_status_string.restype = ctypes.c_char_p
@@ -116,10 +139,47 @@ def route_workspace_bytes(T: int, p: RouteParams) -> int:
     return int(lib().xshare_route_workspace_bytes(int(T), ctypes.byref(p)))
 
 
-def moe_workspace_bytes(T: int, d: int, f: int, p: RouteParams, ep=None) -> int:
-    """``ep``: an EpLayout (see ep_layout) or None."""
+def moe_workspace_bytes(T: int, d: int, f: int, p: RouteParams, ep=None, shared=None) -> int:
+    """``ep``: an EpLayout or None; ``shared``: a SharedExperts or None."""
     return int(lib().xshare_moe_workspace_bytes(int(T), int(d), int(f), ctypes.byref(p),
-                                                None if ep is None else ctypes.byref(ep)))
+                                                None if ep is None else ctypes.byref(ep),
+                                                None if shared is None else ctypes.byref(shared)))
+
+
+def layer_workspace_bytes(T: int, d: int, f: int, p: RouteParams, ep=None, shared=None) -> int:
+    return int(lib().xshare_layer_workspace_bytes(int(T), int(d), int(f), ctypes.byref(p),
+                                                  None if ep is None else ctypes.byref(ep),
+                                                  None if shared is None else ctypes.byref(shared)))
+
+
+def _shared(shared, d, f, dev):
+    """SharedExperts from a (w1 [N_s,f,d], w3 [N_s,f,d], w2 [N_s,d,f]) tuple of bf16 tensors."""
+    if shared is None:
+        return None
+    w1, w3, w2 = shared
+    ns = w1.shape[0]
+    _dev(w1, torch.bfloat16, (ns, f, d), "shared w1")
+    _dev(w3, torch.bfloat16, (ns, f, d), "shared w3")
+    _dev(w2, torch.bfloat16, (ns, d, f), "shared w2")
+    return SharedExperts(int(ns), w1.data_ptr(), w3.data_ptr(), w2.data_ptr())
+
+
+def router_logits(x: torch.Tensor, w_gate: torch.Tensor, *, out=None, workspace=None,
+                  stream=None) -> torch.Tensor:
+    """h = W_g x on the GPU (fp32 [T, N])."""
+    T, d = x.shape
+    N = w_gate.shape[0]
+    _dev(x, torch.bfloat16, (T, d), "x")
+    _dev(w_gate, torch.bfloat16, (N, d), "w_gate")
+    out = torch.empty((T, N), dtype=torch.float32, device=x.device) if out is None else out
+    _dev(out, torch.float32, (T, N), "logits")
+    need = int(lib().xshare_router_workspace_bytes(T, d, N))
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=x.device)
+    st = lib().xshare_router_logits(_ptr(x), _ptr(w_gate), T, d, N, _ptr(out), _ptr(workspace),
+                                    workspace.numel(), _stream(stream))
+    _check(st, "xshare_router_logits")
+    return out
 
 
 class GroupMap:
@@ -273,8 +333,8 @@ def select_hier(logits: torch.Tensor, req_offsets, top_k: int, warmup_k0: int,
 def moe_forward(x: torch.Tensor, logits: torch.Tensor, w1: torch.Tensor, w3: torch.Tensor,
                 w2: torch.Tensor, top_k: int, warmup_k0: int, budget: int, budget_mode="total",
                 score_mode="topk", *, req_offsets=None, per_request_budget: int = 0,
-                groups: GroupMap | None = None, tau: float = 0.0, y=None, routing_out=True,
-                workspace=None, stage_events=None, stream=None) -> dict:
+                groups: GroupMap | None = None, tau: float = 0.0, shared=None, y=None,
+                routing_out=True, workspace=None, stage_events=None, stream=None) -> dict:
     """The MoE layer: returns dict(y [T,d] bf16, and sel_mask/ids/w/stats if routing_out).
 
     With ``groups`` the selection is Algorithms 5-6 (``budget`` is m_g, budget_mode is
@@ -292,6 +352,7 @@ def moe_forward(x: torch.Tensor, logits: torch.Tensor, w1: torch.Tensor, w3: tor
         budget_mode = "per_group"
     p = params(N, top_k, warmup_k0, budget, budget_mode, score_mode, per_request_budget, tau)
     ep = None if groups is None else groups.layout
+    sh = _shared(shared, d, f, dev)
     if y is None:
         y = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
     _dev(y, torch.bfloat16, (T, d), "y")
@@ -301,7 +362,7 @@ def moe_forward(x: torch.Tensor, logits: torch.Tensor, w1: torch.Tensor, w3: tor
                    ids=torch.empty((T, top_k), dtype=torch.int32, device=dev),
                    w=torch.empty((T, top_k), dtype=torch.float32, device=dev),
                    stats=torch.empty(8, dtype=torch.int32, device=dev))
-    need = moe_workspace_bytes(T, d, f, p, ep)
+    need = moe_workspace_bytes(T, d, f, p, ep, sh)
     if workspace is None:
         workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
     d_off = h_off = None
@@ -317,10 +378,67 @@ def moe_forward(x: torch.Tensor, logits: torch.Tensor, w1: torch.Tensor, w3: tor
     st = lib().xshare_moe_forward(
         _ptr(x), _ptr(logits), T, d, f, _ptr(w1), _ptr(w3), _ptr(w2), ctypes.byref(p),
         _ptr(d_off), None if h_off is None else ctypes.c_void_p(h_off.data_ptr()), R,
-        None if ep is None else ctypes.byref(ep), _ptr(y),
+        None if ep is None else ctypes.byref(ep), None if sh is None else ctypes.byref(sh),
+        _ptr(y),
         _ptr(res.get("sel_mask")), _ptr(res.get("ids")), _ptr(res.get("w")),
         _ptr(res.get("stats")), _ptr(workspace), workspace.numel(), ev, _stream(stream))
     _check(st, "xshare_moe_forward")
+    return res
+
+
+def moe_layer(x: torch.Tensor, w_gate: torch.Tensor, w1: torch.Tensor, w3: torch.Tensor,
+              w2: torch.Tensor, top_k: int, warmup_k0: int, budget: int, budget_mode="total",
+              score_mode="topk", *, shared=None, req_offsets=None, per_request_budget: int = 0,
+              groups: GroupMap | None = None, tau: float = 0.0, y=None, routing_out=True,
+              logits_out=True, workspace=None, stage_events=None, stream=None) -> dict:
+    """The whole layer from hidden states: router GEMM, selection, routed and shared experts.
+    Returns dict(y, and logits/sel_mask/ids/w/stats as requested)."""
+    T, d = x.shape
+    N = w_gate.shape[0]
+    f = w1.shape[1]
+    dev = x.device
+    _dev(x, torch.bfloat16, (T, d), "x")
+    _dev(w_gate, torch.bfloat16, (N, d), "w_gate")
+    _dev(w1, torch.bfloat16, (N, f, d), "w1")
+    _dev(w3, torch.bfloat16, (N, f, d), "w3")
+    _dev(w2, torch.bfloat16, (N, d, f), "w2")
+    if groups is not None:
+        budget_mode = "per_group"
+    p = params(N, top_k, warmup_k0, budget, budget_mode, score_mode, per_request_budget, tau)
+    ep = None if groups is None else groups.layout
+    sh = _shared(shared, d, f, dev)
+    if y is None:
+        y = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
+    _dev(y, torch.bfloat16, (T, d), "y")
+    res = {"y": y}
+    if logits_out:
+        res["logits"] = torch.empty((T, N), dtype=torch.float32, device=dev)
+    if routing_out:
+        res.update(sel_mask=torch.empty(N, dtype=torch.uint8, device=dev),
+                   ids=torch.empty((T, top_k), dtype=torch.int32, device=dev),
+                   w=torch.empty((T, top_k), dtype=torch.float32, device=dev),
+                   stats=torch.empty(8, dtype=torch.int32, device=dev))
+    need = layer_workspace_bytes(T, d, f, p, ep, sh)
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    d_off = h_off = None
+    R = 0
+    if req_offsets is not None:
+        d_off, h_off = _offsets(req_offsets, dev)
+        R = d_off.numel() - 1
+    ev = None
+    if stage_events is not None:
+        if len(stage_events) != N_STAGE_EVENTS:
+            raise ValueError(f"stage_events needs {N_STAGE_EVENTS} events")
+        ev = (ctypes.c_void_p * N_STAGE_EVENTS)(*[e.handle for e in stage_events])
+    st = lib().xshare_moe_layer(
+        _ptr(x), _ptr(w_gate), T, d, f, _ptr(w1), _ptr(w3), _ptr(w2),
+        None if sh is None else ctypes.byref(sh), ctypes.byref(p), _ptr(d_off),
+        None if h_off is None else ctypes.c_void_p(h_off.data_ptr()), R,
+        None if ep is None else ctypes.byref(ep), _ptr(y), _ptr(res.get("logits")),
+        _ptr(res.get("sel_mask")), _ptr(res.get("ids")), _ptr(res.get("w")),
+        _ptr(res.get("stats")), _ptr(workspace), workspace.numel(), ev, _stream(stream))
+    _check(st, "xshare_moe_layer")
     return res
 
 

@@ -131,8 +131,8 @@ def test_moe_forward_validation():
 
     def call(d=64, f=128, x=FAKE, y=FAKE, ws=None, T=8):
         return L.xshare_moe_forward(x, FAKE, T, d, f, FAKE, FAKE, FAKE, ctypes.byref(p), None,
-                                    None, 0, None, y, None, None, None, None, ws, 1 << 30, None,
-                                    None)
+                                    None, 0, None, None, y, None, None, None, None, ws, 1 << 30,
+                                    None, None)
 
     assert call(d=48) == X.EUNSUPPORTED
     assert call(f=100) == X.EUNSUPPORTED
@@ -186,7 +186,7 @@ def test_moe_forward_ep_validation():
     def call(ep, pp=pg, offsets=None, R=0):
         return L.xshare_moe_forward(FAKE, FAKE, 8, 64, 128, FAKE, FAKE, FAKE, ctypes.byref(pp),
                                     offsets, None, R, None if ep is None else ctypes.byref(ep),
-                                    FAKE, None, None, None, None, None, 1 << 30, None, None)
+                                    None, FAKE, None, None, None, None, None, 1 << 30, None, None)
 
     assert call(_ep(4, local=4)) == X.EINVAL                    # local group out of range
     assert call(_ep(4, local=-2)) == X.EINVAL
@@ -194,6 +194,50 @@ def test_moe_forward_ep_validation():
     assert call(_ep(4), offsets=FAKE, R=2) == X.EUNSUPPORTED    # not with request offsets
     assert call(None, pp=pg) == X.EINVAL                        # per-group mode needs groups
     full = X.moe_workspace_bytes(32, 7168, 2048, X.params(256, 8, 1, 5, "per_group"), _ep(8))
-    share = X.moe_workspace_bytes(32, 7168, 2048, X.params(256, 8, 1, 5, "per_group"), _ep(8, 0))
+    share = X.moe_workspace_bytes(32, 7168, 2048, X.params(256, 8, 1, 5, "per_group"),
+                                  _ep(8, 0))
     assert full > 0 and share > 0
     assert X.moe_workspace_bytes(32, 7168, 2048, X.params(256, 8, 1, 5, "per_group"), None) == 0
+
+
+def test_router_and_layer_validation():
+    L = X.lib()
+    assert X.lib().xshare_router_workspace_bytes(32, 7168, 256) > 0
+    assert X.lib().xshare_router_workspace_bytes(32, 100, 256) == 0     # d % 32
+    assert X.lib().xshare_router_workspace_bytes(32, 7168, 2000) == 0   # N > 1024
+
+    def router(T=8, d=64, N=16, x=FAKE, wg=FAKE, out=FAKE):
+        return L.xshare_router_logits(x, wg, T, d, N, out, None, 0, None)
+
+    assert router(d=48) == X.EUNSUPPORTED
+    assert router(N=0) == X.EINVAL
+    assert router(N=2048) == X.EUNSUPPORTED
+    assert router(x=None) == X.EINVAL
+    assert router(x=FAKE_ODD) == X.EINVAL
+    assert router(T=0) == X.OK                       # empty batch: nothing to do
+    assert router(T=64, d=7168, N=256) == X.EWORKSPACE   # splits d; needs the partials
+
+    p = X.params(16, 2, 1, 8)
+
+    def layer(shared=None, ep=None, wg=FAKE, ws=None):
+        return L.xshare_moe_layer(FAKE, wg, 8, 64, 128, FAKE, FAKE, FAKE,
+                                  None if shared is None else ctypes.byref(shared),
+                                  ctypes.byref(p if ep is None else pg), None, None, 0,
+                                  None if ep is None else ctypes.byref(ep), FAKE, None, None,
+                                  None, None, None, ws, 1 << 30, None, None)
+
+    pg = X.params(16, 2, 1, 3, "per_group")
+    assert layer() == X.EWORKSPACE
+    assert layer(wg=None) == X.EINVAL
+    assert layer(wg=FAKE_ODD) == X.EINVAL
+    assert layer(X.SharedExperts(-1, None, None, None)) == X.EINVAL
+    assert layer(X.SharedExperts(65, 1 << 20, 1 << 20, 1 << 20)) == X.EUNSUPPORTED
+    assert layer(X.SharedExperts(1, None, 1 << 20, 1 << 20)) == X.EINVAL
+    assert layer(X.SharedExperts(1, (1 << 20) + 2, 1 << 20, 1 << 20)) == X.EINVAL
+    assert layer(X.SharedExperts(1, 1 << 20, 1 << 20, 1 << 20)) == X.EWORKSPACE
+    assert layer(X.SharedExperts(1, 1 << 20, 1 << 20, 1 << 20), _ep(4, 1)) == X.EUNSUPPORTED
+    q = X.params(256, 8, 1, 48)
+    no = X.moe_workspace_bytes(32, 7168, 2048, q)
+    one = X.moe_workspace_bytes(32, 7168, 2048, q, None, X.SharedExperts(1, 0, 0, 0))
+    assert one >= no + 32 * (2048 * 2 + 7168 * 4)     # H and Y rows of the shared expert
+    assert X.layer_workspace_bytes(32, 7168, 2048, q) > no
