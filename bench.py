@@ -70,6 +70,11 @@ def parse():
     ap.add_argument("--ep-groups", type=int, default=0,
                     help="G > 0: expert-parallel selection and per-group shares")
     ap.add_argument("--per-group-budget", type=int, default=5, help="m_g (with --ep-groups)")
+    ap.add_argument("--full-layer", action="store_true",
+                    help="the whole layer from hidden states: router GEMM, selection, routed "
+                         "and shared experts (xshare_moe_layer)")
+    ap.add_argument("--shared", type=int, default=None,
+                    help="shared experts with --full-layer (default: 1 for DeepSeek shapes, else 0)")
     return ap.parse_args()
 
 
@@ -114,6 +119,8 @@ def main():
     X.lib()
     if args.ep_groups > 0:
         return run_ep(args, W, X, np, torch)
+    if args.full_layer:
+        return run_full(args, W, X, np, torch)
     dev = "cuda:0"
     cfg = dict(W.CONFIGS[args.workload])
     T, N, k, d, f = cfg["T"], cfg["N"], cfg["k"], cfg["d"], cfg["f"]
@@ -250,6 +257,126 @@ def main():
                      "avg_launch_us": round(float(gu_ms.mean()) * 1e3, 2)},
         "cpu_baseline": cpu,
         "wall_s_timed": round(wall, 3),
+    }
+    print(json.dumps(out), flush=True)
+
+
+def run_full(args, W, X, np, torch):
+    """The whole layer from hidden states (xshare_moe_layer), against plain top-k routing on
+    the same path; the oracle's layer (router, selection, routed and shared experts) as the
+    CPU baseline."""
+    dev = "cuda:0"
+    cfg = dict(W.CONFIGS[args.workload])
+    if cfg["logits"] == "spec":
+        raise SystemExit("--full-layer takes a flat workload")
+    T, N, k, d, f, k0 = cfg["T"], cfg["N"], cfg["k"], cfg["d"], cfg["f"], cfg["k0"]
+    M = cfg["M"] if args.budget is None else args.budget
+    ns = args.shared if args.shared is not None else (1 if N == 256 else 0)
+    Q, nb = cfg.get("Q", 8), args.batches
+    print(f"[bench] {args.workload}: whole layer, {ns} shared expert(s)", file=sys.stderr,
+          flush=True)
+    w1, w3, w2 = W.expert_weights(N, d, f, 0, dev)
+    wg = W.router_weights(N, d, 0, dev)
+    sh = W.shared_weights(ns, d, f, 0, dev) if ns else None
+    xs = [W.activations_domains(T, d, Q, s, dev) for s in range(nb)]
+    y = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
+    p = X.params(N, k, k0, M, "total")
+    ws = torch.empty(max(X.layer_workspace_bytes(T, d, f, p, None, X._shared(sh, d, f, dev)),
+                         X.layer_workspace_bytes(T, d, f, X.params(N, k, 0, N, "extra"), None,
+                                                 X._shared(sh, d, f, dev))),
+                     dtype=torch.uint8, device=dev)
+
+    def call(s, vanilla=False, **kw):
+        b = s % nb
+        if vanilla:
+            return X.moe_layer(xs[b], wg, w1, w3, w2, k, 0, N, "extra", shared=sh, y=y,
+                               workspace=ws, **kw)
+        return X.moe_layer(xs[b], wg, w1, w3, w2, k, k0, M, "total", shared=sh, y=y,
+                           workspace=ws, **kw)
+
+    act = [X.stats_dict(call(b)["stats"])["n_active"] for b in range(nb)]
+    act_v = [X.stats_dict(call(b, True)["stats"])["n_active"] for b in range(nb)]
+    stream = torch.cuda.current_stream()
+
+    def timed(vanilla):
+        for s in range(args.warmup):
+            call(s, vanilla, routing_out=False, logits_out=False)
+        torch.cuda.synchronize()
+        e0, e1 = X.HipEvent(), X.HipEvent()
+        e0.record(stream)
+        for s in range(args.steps):
+            call(s, vanilla, routing_out=False, logits_out=False)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_ms(e1) / args.steps
+
+    ms = timed(False)
+    evs = [[X.HipEvent() for _ in range(X.N_STAGE_EVENTS)] for _ in range(args.steps)]
+    for s in range(args.steps):
+        call(s, routing_out=False, logits_out=False, stage_events=evs[s])
+    torch.cuda.synchronize()
+    stage_ms = {name: float(np.mean([e[i].elapsed_ms(e[i + 1]) for e in evs]))
+                for i, name in enumerate(("router+route", "gate_up", "down", "combine"))}
+    ms_v = None if args.no_vanilla else timed(True)
+
+    def layer_b(n_active):
+        return ((n_active + ns) * 3 * f * d * 2 + N * d * 2 + T * d * 2 * 2)
+    gbs = float(np.mean([layer_b(a) for a in act])) / (ms * 1e-3) / 1e9
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import ffn as OF
+        from oracle import route as OR
+        wgb = W.bf16_bits(wg)
+        shb = [] if sh is None else [tuple(W.bf16_bits(m[s]) for m in sh) for s in range(ns)]
+        spent, done = 0.0, 0
+        for b in range(nb):
+            xb = W.bf16_bits(xs[b])
+            t0 = time.perf_counter()
+            h = OF.router_logits(xb, wgb).astype(np.float32)
+            r = OR.route(h, k, k0, M)
+            t1 = time.perf_counter()
+            used = sorted(set(int(e) for e in r.ids.reshape(-1)))
+            cache = {e: tuple(W.bf16_bits(m[e]) for m in (w1, w3, w2)) for e in used}
+            t2 = time.perf_counter()
+            OF.moe_forward(xb, r.ids, r.w, lambda e: cache[e], shared=shb)
+            spent += (t1 - t0) + (time.perf_counter() - t2)
+            done += 1
+            if spent >= 10.0:
+                break
+        cpu = {"value": round(float(np.mean([layer_b(a) for a in act])) / (spent / done) / 1e9, 3),
+               "unit": "GB/s", "us_per_batch": round(spent / done * 1e6, 1),
+               "cores": len(os.sched_getaffinity(0)), "kind": "oracle",
+               "sample": f"full oracle layer (float64 router, numpy selection, float64 SwiGLU "
+                         f"of routed and shared experts) on {done} batches, {spent:.1f} s"}
+    out = {
+        "metric": "whole MoE layer (router + selection + routed + shared experts): us/batch "
+                  "+ HBM GB/s; experts activated/batch",
+        "value": round(gbs, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}_full_layer_shared{ns}_M{M}_k0{k0}", "tokens": T,
+                   "n_experts": N, "top_k": k, "d_model": d, "d_ffn": f, "shared_experts": ns,
+                   "budget": M, "budget_mode": "total", "warmup_k0": k0,
+                   "activations": f"{Q} domain centroids N(0,1) + 0.5 N(0,1), bf16",
+                   "router": "W_g ~ N(0, 1.5/sqrt(d)) bf16", "batches_rotated": nb},
+        "us_per_batch": round(ms * 1e3, 2),
+        "tokens_per_s": round(T / (ms * 1e-3), 1),
+        "experts_activated": round(float(np.mean(act)), 2),
+        "experts_vanilla": round(float(np.mean(act_v)), 2),
+        "vanilla_us_per_batch": None if ms_v is None else round(ms_v * 1e3, 2),
+        "speedup_vs_vanilla": None if ms_v is None else round(ms_v / ms, 3),
+        "layer_frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+        "stages_us": {kk: round(v * 1e3, 2) for kk, v in stage_ms.items()},
+        "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
 

@@ -156,13 +156,15 @@ size_t xshare_moe_workspace_bytes(int32_t T, int32_t d, int32_t f,
                                   const xshare_route_params* params, const xshare_ep_layout* ep,
                                   const xshare_shared_experts* shared);
 
-/* Workspace for xshare_moe_layer: that of xshare_moe_forward plus the router's partials.  */
+/* Workspace for xshare_moe_layer: that of xshare_moe_forward plus the router's scratch    *
+ * and a [T, N] fp32 logits buffer.                                                        */
 size_t xshare_layer_workspace_bytes(int32_t T, int32_t d, int32_t f,
                                     const xshare_route_params* params,
                                     const xshare_ep_layout* ep,
                                     const xshare_shared_experts* shared);
 
-/* Workspace for xshare_router_logits (bytes, 256-aligned); 0 for invalid sizes.           */
+/* Workspace for xshare_router_logits (bytes, 256-aligned: fp32 partial sums over parts of *
+ * d); 0 for invalid sizes.                                                                */
 size_t xshare_router_workspace_bytes(int32_t T, int32_t d, int32_t n_experts);
 
 /*
@@ -171,9 +173,10 @@ size_t xshare_router_workspace_bytes(int32_t T, int32_t d, int32_t n_experts);
  *   x        [T, d] bf16 row-major, 16-byte aligned.
  *   w_gate   [N, d] bf16 (nn.Linear [out, in]), 16-byte aligned; N = n_experts <= 1024.
  *   logits   out [T, N] fp32: h_ij = sum_q x_iq * W_g[j, q]; the bf16 products are exact in
- *            fp32 and accumulated in fp32 (matrix-core blocks of 32, the parts of d summed
- *            in a fixed order), so |h - exact| <= d * 2^-24 * sum_q |x_iq W_g[j, q]| (up to
- *            second order) and repeated calls give identical bits.
+ *            fp32 and accumulated in fp32 (matrix-core blocks of 32 within parts of d; the
+ *            parts' sums added in part order), so
+ *            |h - exact| <= d * 2^-24 * sum_q |x_iq W_g[j, q]| (up to second order) and
+ *            repeated calls give identical bits.
  *   d        multiple of 32.
  */
 xshare_status xshare_router_logits(const uint16_t* x, const uint16_t* w_gate, int32_t T,
@@ -286,8 +289,8 @@ xshare_status xshare_moe_forward(const uint16_t* x, const float* logits, int32_t
  * the shared experts, combine.
  *
  *   w_gate      [N, d] bf16 router weights (16-byte aligned).
- *   logits_out  nullable out [T, N] fp32: the logits the selection used (bit-identical to
- *               xshare_router_logits on the same inputs).
+ *   logits_out  nullable out [T, N] fp32: the logits the selection used (written by the
+ *               router GEMM; bit-identical to xshare_router_logits on the same inputs).
  *   ws          at least xshare_layer_workspace_bytes.
  *   Other arguments as xshare_moe_forward; stage event 1 marks the end of router plus
  *   selection.

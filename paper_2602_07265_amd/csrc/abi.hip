@@ -145,10 +145,17 @@ xs::FfnLayout layer_layout(int32_t T, int32_t d, int32_t f, const xshare_route_p
                         layer_estimate(T, p, ep) + n_shared, n_shared);
 }
 
-// Router partial planes [splits, T, N] fp32 (none when the router does not split).
-size_t router_parts_bytes(int32_t T, int32_t d, int32_t N) {
-  const int s = xs::router_splits(T, d, N);
-  return s > 1 ? xs::align256(sizeof(float) * size_t(s) * size_t(T > 0 ? T : 1) * N) : 256;
+// Router scratch: its fp32 part planes [parts, T, N].
+size_t router_planes_bytes(int32_t T, int32_t d, int32_t N) {
+  return xs::align256(sizeof(float) * size_t(xs::router_parts(T, d, N)) *
+                      size_t(T > 0 ? T : 1) * size_t(N));
+}
+
+// xshare_moe_layer's extra scratch: the router planes, then a logits buffer [T, N] used when
+// the caller does not take the logits.
+size_t layer_router_bytes(int32_t T, int32_t d, int32_t N) {
+  return router_planes_bytes(T, d, N) +
+         xs::align256(sizeof(float) * size_t(T > 0 ? T : 1) * size_t(N));
 }
 
 // Shared experts: 0 <= N_s <= 64 experts of the routed shape, 16-byte aligned; none with a
@@ -217,7 +224,7 @@ xshare_status layer_common(const uint16_t* x, const float* logits, const uint16_
   const int n_shared = n_shared_of(shared);
   const int bound = layer_bound(T, params, ep);
   const xs::FfnLayout L = layer_layout(T, d, f, params, ep, n_shared);
-  const size_t need = L.total + (w_gate ? router_parts_bytes(T, d, N) : 0);
+  const size_t need = L.total + (w_gate ? layer_router_bytes(T, d, N) : 0);
   if (!ws || ws_bytes < need) return XSHARE_EWORKSPACE;
 
   // The selection kernel always writes a mask; keep it in the workspace if not wanted.
@@ -230,15 +237,12 @@ xshare_status layer_common(const uint16_t* x, const float* logits, const uint16_
   xs::RouteArgs ra = route_args(logits, T, params, hier ? req_offsets : nullptr, R, ep, nullptr,
                                 mask, topk_ids, topk_w, stats, ws, L.route);
   if (ep) ra.local_group = ep->local_group;
-  ra.logits_out = logits_out;
   if (w_gate && T > 0) {
-    const int s = xs::router_splits(T, d, N);
-    float* parts = at<float>(ws, L.total);
-    xs::RouterArgs r{x, w_gate, T, d, N, s, parts};
+    float* planes = at<float>(ws, L.total);
+    float* h = logits_out ? logits_out : at<float>(ws, L.total + router_planes_bytes(T, d, N));
+    const xs::RouterArgs r{x, w_gate, T, d, N, xs::router_parts(T, d, N), planes, h};
     if (xs::launch_router(r, stream) != hipSuccess) return XSHARE_EHIP;
-    ra.logits = nullptr;
-    ra.parts = parts;
-    ra.n_parts = s;
+    ra.logits = h;
   }
   if (xs::launch_route(ra, stream) != hipSuccess || !record(1)) return XSHARE_EHIP;
   if (T == 0) {
@@ -310,7 +314,7 @@ size_t xshare_layer_workspace_bytes(int32_t T, int32_t d, int32_t f,
                                     const xshare_ep_layout* ep,
                                     const xshare_shared_experts* shared) {
   const size_t m = xshare_moe_workspace_bytes(T, d, f, params, ep, shared);
-  return m == 0 ? 0 : m + router_parts_bytes(T, d, params->n_experts);
+  return m == 0 || d % xs::kDimAlign != 0 ? 0 : m + layer_router_bytes(T, d, params->n_experts);
 }
 
 xshare_status xshare_route(const float* logits, int32_t T, const xshare_route_params* params,
@@ -381,7 +385,7 @@ size_t xshare_router_workspace_bytes(int32_t T, int32_t d, int32_t n_experts) {
   if (T < 0 || T > kMaxTokens || d <= 0 || d % xs::kDimAlign != 0 || n_experts < 1 ||
       n_experts > kMaxExperts)
     return 0;
-  return router_parts_bytes(T, d, n_experts);
+  return router_planes_bytes(T, d, n_experts);
 }
 
 xshare_status xshare_router_logits(const uint16_t* x, const uint16_t* w_gate, int32_t T,
@@ -392,13 +396,10 @@ xshare_status xshare_router_logits(const uint16_t* x, const uint16_t* w_gate, in
     return XSHARE_EUNSUPPORTED;
   if (T == 0) return XSHARE_OK;
   if (!x || !w_gate || !logits || !aligned16(x) || !aligned16(w_gate)) return XSHARE_EINVAL;
-  const int s = xs::router_splits(T, d, n_experts);
-  if (s > 1 && (!ws || ws_bytes < router_parts_bytes(T, d, n_experts))) return XSHARE_EWORKSPACE;
-  xs::RouterArgs r{x, w_gate, T, d, n_experts, s, s > 1 ? static_cast<float*>(ws) : logits};
-  if (xs::launch_router(r, stream) != hipSuccess) return XSHARE_EHIP;
-  if (s > 1 && xs::launch_router_reduce(r.out, s, T, n_experts, logits, stream) != hipSuccess)
-    return XSHARE_EHIP;
-  return XSHARE_OK;
+  if (!ws || ws_bytes < router_planes_bytes(T, d, n_experts)) return XSHARE_EWORKSPACE;
+  const xs::RouterArgs r{x, w_gate, T, d, n_experts, xs::router_parts(T, d, n_experts),
+                         static_cast<float*>(ws), logits};
+  return xs::launch_router(r, stream) == hipSuccess ? XSHARE_OK : XSHARE_EHIP;
 }
 
 const char* xshare_status_string(int32_t status) {

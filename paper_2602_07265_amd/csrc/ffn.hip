@@ -368,18 +368,18 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(FfnArgs a) {
   *reinterpret_cast<uint2*>(a.y + (size_t)i * a.d + c) = make_uint2(lo, hi);
 }
 
-// Router GEMM h = W_g x: each wave owns 16 router rows (experts) and one part of d
-// (blockIdx.z), the token tiles of blockIdx.y; fp32 results go to that part's plane.
+// Router GEMM h = W_g x: each wave owns 16 router rows (experts) and part blockIdx.z of d,
+// for the token tiles of blockIdx.y; fp32 results go to that part's plane.
 template <int U>
 __global__ __launch_bounds__(kBlock) void router_kernel(RouterArgs r) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int j0 = (blockIdx.x * kWaves + wave) * kCols;
   if (j0 >= r.N) return;
   const int n = lane & 15, g = lane >> 4;
-  const int Kr = r.d / r.splits;
-  const size_t k0 = (size_t)blockIdx.z * Kr + (size_t)g * 8 * U;
+  const int Kp = r.d / r.parts;
+  const size_t k0 = (size_t)blockIdx.z * Kp + (size_t)g * 8 * U;
   const uint16_t* const brow[1] = {r.wg + (size_t)min(j0 + n, r.N - 1) * r.d + k0};
-  float* const out = r.out + (size_t)blockIdx.z * r.T * r.N;
+  float* const out = r.planes + (size_t)blockIdx.z * r.T * r.N;
   for (int c0 = blockIdx.y * 16 * kTiles; c0 < r.T; c0 += gridDim.y * 16 * kTiles) {
     const int nt = min(kTiles, (r.T - c0 + 15) / 16);
     const uint16_t* arow[kTiles];
@@ -389,7 +389,7 @@ __global__ __launch_bounds__(kBlock) void router_kernel(RouterArgs r) {
     floatx4 acc[1][kTiles];
 #pragma unroll
     for (int rt = 0; rt < kTiles; ++rt) acc[0][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    wave_pass<U, 1, false>(arow, nt, brow, Kr, acc);
+    wave_pass<U, 1, true>(arow, nt, brow, Kp, acc);
 #pragma unroll
     for (int rt = 0; rt < kTiles; ++rt) {
       if (rt >= nt) break;
@@ -402,14 +402,22 @@ __global__ __launch_bounds__(kBlock) void router_kernel(RouterArgs r) {
   }
 }
 
-__global__ __launch_bounds__(kBlock) void router_reduce_kernel(const float* parts, int n_parts,
-                                                               int T, int N, float* logits) {
+// logits = sum of the router's part planes, in part order.
+__global__ __launch_bounds__(kBlock) void router_sum_kernel(RouterArgs r) {
   const size_t idx = (size_t)blockIdx.x * kBlock + threadIdx.x;
-  const size_t plane = (size_t)T * N;
+  const size_t plane = (size_t)r.T * r.N;
   if (idx >= plane) return;
-  float v = parts[idx];
-  for (int z = 1; z < n_parts; ++z) v = v + parts[z * plane + idx];
-  logits[idx] = v;
+  float v = r.planes[idx];
+  int z = 1;
+  for (; z + 8 <= r.parts; z += 8) {   // eight loads in flight, then the adds in order
+    float t[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) t[u] = r.planes[(z + u) * plane + idx];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v = v + t[u];
+  }
+  for (; z < r.parts; ++z) v = v + r.planes[z * plane + idx];
+  r.logits[idx] = v;
 }
 
 template <int U>
@@ -459,22 +467,17 @@ hipError_t launch_down(const FfnArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_router(const RouterArgs& r, hipStream_t stream) {
-  const dim3 grid((r.N + kWaves * kCols - 1) / (kWaves * kCols), router_token_tiles(r.T),
-                  r.splits),
+  const dim3 grid((r.N + kWaves * kCols - 1) / (kWaves * kCols), router_token_groups(r.T),
+                  r.parts),
       block(kBlock);
-  switch (unroll_for(r.d / r.splits, 4)) {
+  switch (unroll_for(r.d / r.parts, 4)) {
     case 4: hipLaunchKernelGGL(router_kernel<4>, grid, block, 0, stream, r); break;
     case 2: hipLaunchKernelGGL(router_kernel<2>, grid, block, 0, stream, r); break;
     default: hipLaunchKernelGGL(router_kernel<1>, grid, block, 0, stream, r); break;
   }
-  return hipGetLastError();
-}
-
-hipError_t launch_router_reduce(const float* parts, int n_parts, int T, int N, float* logits,
-                                hipStream_t stream) {
-  const size_t n = (size_t)T * N;
-  const dim3 grid((unsigned)((n + kBlock - 1) / kBlock)), block(kBlock);
-  hipLaunchKernelGGL(router_reduce_kernel, grid, block, 0, stream, parts, n_parts, T, N, logits);
+  const size_t n = (size_t)r.T * r.N;
+  hipLaunchKernelGGL(router_sum_kernel, dim3((unsigned)((n + kBlock - 1) / kBlock)), block, 0,
+                     stream, r);
   return hipGetLastError();
 }
 

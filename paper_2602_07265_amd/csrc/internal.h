@@ -141,36 +141,36 @@ inline FfnLayout ffn_layout(int T, int N, int k, bool dense, int d, int f, int e
   return L;
 }
 
-// The router GEMM h = W_g x splits d into this many parts (fp32 partial planes summed in
-// order by whoever reads the logits) so that N/16 x token-tile waves become >= 512.
-inline int router_token_tiles(int T) {
+// The router GEMM h = W_g x: waves of 16 router rows (experts) x one part of d, parts of 128
+// elements where d allows (one load step per wave, so the whole weight read is in flight at
+// once), at most 64 parts and 16 MB of fp32 partial planes [parts, T, N]; a second kernel
+// sums the planes in part order.
+inline int router_parts(int T, int d, int N) {
+  const int q = d / 32;                                   // 32-element chunks of d
+  int s = (q % 4 == 0) ? q / 4 : (q % 2 == 0 ? q / 2 : q);
+  const long per_plane = 4L * (T > 0 ? T : 1) * N;
+  long cap = (16L << 20) / per_plane;
+  cap = cap < 1 ? 1 : (cap > 64 ? 64 : cap);
+  while (s > cap || q % s != 0) --s;                      // largest divisor of q within the cap
+  return s;
+}
+inline int router_token_groups(int T) {
   const int tiles = (T + 31) / 32;
   return tiles < 64 ? (tiles > 0 ? tiles : 1) : 64;
-}
-inline int router_splits(int T, int d, int N) {
-  const long waves = (long)((N + 15) / 16) * router_token_tiles(T);
-  int s = 1;
-  while (s < 16 && waves * s < 512 && d % (2 * s * 32) == 0) s *= 2;
-  return s;
 }
 
 struct RouterArgs {
   const uint16_t* x;           // bf16 [T, d]
   const uint16_t* wg;          // bf16 [N, d]
-  int T, d, N, splits;
-  float* out;                  // fp32 [splits, T, N] partial planes (the logits if splits == 1)
+  int T, d, N, parts;
+  float* planes;               // fp32 [parts, T, N]
+  float* logits;               // fp32 [T, N]
 };
 
-hipError_t launch_router(const RouterArgs& r, hipStream_t stream);
-// logits[t, j] = sum over z of parts[z, t, j], z ascending
-hipError_t launch_router_reduce(const float* parts, int n_parts, int T, int N, float* logits,
-                                hipStream_t stream);
+hipError_t launch_router(const RouterArgs& r, hipStream_t stream);   // GEMM, then the sum
 
 struct RouteArgs {
-  const float* logits;         // [T, N], or nullptr when `parts` holds the router's partials
-  const float* parts;          // [n_parts, T, N] router partial planes, summed in order
-  int n_parts;
-  float* logits_out;           // nullable: the logits used, [T, N]
+  const float* logits;         // [T, N]
   int T, N, k, k0, budget, budget_mode, score_mode, m_r;
   float tau;                   // threshold mode (budget_mode 3)
   const int32_t* req_offsets;  // nullptr: flat Algorithm 2

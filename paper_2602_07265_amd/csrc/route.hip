@@ -152,30 +152,14 @@ __device__ __forceinline__ float ranked_gate(float my_h, int lane, int k) {
   return lane < k ? e / z : 0.0f;
 }
 
-// Raw logits of token i, lane l holding experts l, l + 64, ...: read from the logits, or
-// summed over the router's partial planes in plane order.
+// Raw logits of token i, lane l holding experts l, l + 64, ...
 template <int Q>
 __device__ __forceinline__ void load_row(const RouteArgs& a, int i, int lane, float (&raw)[Q]) {
-  const int N = a.N;
-  const size_t row = (size_t)i * N;
-  if (!a.parts) {
-#pragma unroll
-    for (int q = 0; q < Q; ++q) {
-      const int j = lane + 64 * q;
-      raw[q] = j < N ? a.logits[row + j] : 0.0f;
-    }
-    return;
-  }
-  const size_t plane = (size_t)a.T * N;
+  const size_t row = (size_t)i * a.N;
 #pragma unroll
   for (int q = 0; q < Q; ++q) {
     const int j = lane + 64 * q;
-    float v = 0.0f;
-    if (j < N) {
-      v = a.parts[row + j];
-      for (int z = 1; z < a.n_parts; ++z) v = v + a.parts[z * plane + row + j];
-    }
-    raw[q] = v;
+    raw[q] = j < a.N ? a.logits[row + j] : 0.0f;
   }
 }
 
@@ -370,10 +354,6 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
 #pragma unroll
     for (int q = 0; q < Q; ++q) raw[q] = raw_next[q];
     if (i + kWaves < T) load_row<Q>(a, i + kWaves, lane, raw_next);
-    if (a.logits_out)
-#pragma unroll
-      for (int q = 0; q < Q; ++q)
-        if (lane + 64 * q < N) a.logits_out[(size_t)i * N + lane + 64 * q] = raw[q];
     row_keys<Q>(raw, N, lane, v, key);
     float my_h;
     int my_j;

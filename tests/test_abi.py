@@ -215,7 +215,7 @@ def test_router_and_layer_validation():
     assert router(x=None) == X.EINVAL
     assert router(x=FAKE_ODD) == X.EINVAL
     assert router(T=0) == X.OK                       # empty batch: nothing to do
-    assert router(T=64, d=7168, N=256) == X.EWORKSPACE   # splits d; needs the partials
+    assert router(T=64, d=7168, N=256) == X.EWORKSPACE   # needs the partial sums
 
     p = X.params(16, 2, 1, 8)
 
