@@ -79,8 +79,9 @@ def parse():
 
 
 def gate_up_bytes(n_active, T, k, d, f):
-    """Algorithmic HBM bytes of one gate/up launch: W1, W3 of every active expert, x, H."""
-    return n_active * 2 * f * d * 2 + T * d * 2 + T * k * f * 2
+    """Algorithmic HBM bytes of one gate/up launch: W1, W3 of every active expert, x, and H
+    written as two bf16 arrays (hi and lo)."""
+    return n_active * 2 * f * d * 2 + T * d * 2 + T * k * f * 2 * 2
 
 
 def layer_bytes(n_active, T, N, d, f):

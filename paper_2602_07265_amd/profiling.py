@@ -10,7 +10,8 @@ Runs the DeepSeek-R1-shaped layer (N=256, k=8, d=7168, f=2048, T=32 tokens, tota
 a plain device-to-device copy of --copy-mib MiB (torch's copy kernel) --copies times.  The
 copy reads and writes a known number of bytes, so it calibrates what the counters report
 per byte.  Prints, per batch, the active experts and the algorithmic bytes of one gate/up
-launch (weights of the active experts, x, H) to compare with the counters.
+launch (weights of the active experts, x, H as bf16 hi and lo) to compare with the
+counters.
 """
 from __future__ import annotations
 
@@ -54,8 +55,8 @@ def main():
         r = X.moe_forward(xs[b], logits[b], w1, w3, w2, k, k0, M, y=y, workspace=ws)
         st = X.stats_dict(r["stats"])
         per_call.append({"call": s, "n_active": st["n_active"],
-                         "gate_up_bytes": st["n_active"] * 2 * f * d * 2 + T * d * 2 + T * k * f * 2,
-                         "down_bytes": st["n_active"] * f * d * 2 + T * k * f * 2 + T * k * d * 4})
+                         "gate_up_bytes": st["n_active"] * 2 * f * d * 2 + T * d * 2 + T * k * f * 4,
+                         "down_bytes": st["n_active"] * f * d * 2 + T * k * f * 4 + T * k * d * 4})
     nbytes = args.copy_mib << 20
     src = torch.empty(nbytes, dtype=torch.uint8, device=dev)
     dst = torch.empty_like(src)
