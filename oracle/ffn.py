@@ -1,10 +1,16 @@
 """MoE layer output with SwiGLU experts (oracle side), in float64.
 
-Section 2.1: y = sum_i g_i(x) E_i(x) over the routed experts (the shared-expert
-term is not part of this layer).  Each expert is a SwiGLU FFN in nn.Linear
-[out, in] layout:  E(x) = W2 (silu(W1 x) * (W3 x)),  silu(z) = z / (1 + e^-z),
+Section 2.1: y = sum_i g_i(x) E_i(x) over the routed experts, plus the always-on
+shared experts when given.  Each expert is a SwiGLU FFN in nn.Linear [out, in]
+layout:  E(x) = W2 (silu(W1 x) * (W3 x)),  silu(z) = z / (1 + e^-z),
 W1, W3 in R^{f x d}, W2 in R^{d x f}.  Inputs are bf16 bit patterns (exact in
-float64); nothing is rounded until the caller compares.
+float64), or expert weights already in float64 (the FP8 weights below, decoded
+and scaled exactly); nothing is rounded until the caller compares.
+
+FP8 expert weights (the paper is silent on precision): OCP FP8 E4M3FN codes
+(1 sign bit, 4 exponent bits with bias 7, 3 mantissa bits; exponent field 0 is
+subnormal, code 0x7F / 0xFF is NaN, no infinities, largest finite 448) with one
+fp32 scale per output row: w[r, c] = decode(q[r, c]) * scale[r].
 """
 from __future__ import annotations
 
@@ -20,11 +26,33 @@ def silu(z):
     return z / (1.0 + np.exp(-z))
 
 
-def expert_ffn(x, w1_bits, w3_bits, w2_bits) -> np.ndarray:
-    """SwiGLU expert applied to the rows of x (float64 [t,d]) -> float64 [t,d]."""
-    W1 = bf16_to_f64(w1_bits)
-    W3 = bf16_to_f64(w3_bits)
-    W2 = bf16_to_f64(w2_bits)
+def decode_e4m3(codes) -> np.ndarray:
+    """OCP FP8 E4M3FN codes -> float64 values (NaN for 0x7F and 0xFF)."""
+    c = np.asarray(codes, dtype=np.uint8).astype(np.int64)
+    sign = np.where(c >> 7, -1.0, 1.0)
+    e = (c >> 3) & 15
+    m = (c & 7).astype(np.float64)
+    v = np.where(e == 0, m / 8.0 * 2.0 ** -6, (1.0 + m / 8.0) * np.exp2(e - 7.0))
+    v = sign * v
+    return np.where((e == 15) & ((c & 7) == 7), np.nan, v)
+
+
+def dequant_rows(codes, scale) -> np.ndarray:
+    """Weights of one FP8 matrix: decode(q[r, c]) * scale[r] in float64 (exact)."""
+    return decode_e4m3(codes) * np.asarray(scale, dtype=np.float32).astype(np.float64)[:, None]
+
+
+def _as_f64(w) -> np.ndarray:
+    w = np.asarray(w)
+    return bf16_to_f64(w) if w.dtype == np.uint16 else w.astype(np.float64)
+
+
+def expert_ffn(x, w1, w3, w2) -> np.ndarray:
+    """SwiGLU expert applied to the rows of x (float64 [t,d]) -> float64 [t,d]; the weights
+    are bf16 bit patterns (uint16) or float64 values."""
+    W1 = _as_f64(w1)
+    W3 = _as_f64(w3)
+    W2 = _as_f64(w2)
     a = x @ W1.T
     b = x @ W3.T
     return (silu(a) * b) @ W2.T

@@ -193,6 +193,36 @@ def shared_weights(n_shared: int, d: int, f: int, seed: int, device="cpu", std: 
     return w1, w3, w2
 
 
+def quantize_rows_e4m3(w):
+    """bf16 matrix [rows, cols] -> (OCP FP8 E4M3FN codes uint8 [rows, cols], fp32 scale
+    [rows]) with scale = max|row| / 448 (1 for an all-zero row) and codes = w / scale
+    rounded to nearest even by torch's float8_e4m3fn conversion."""
+    import torch
+
+    v = w.float()
+    amax = v.abs().amax(dim=1)
+    scale = torch.where(amax > 0, amax / 448.0, torch.ones_like(amax))
+    q = (v / scale[:, None]).clamp(-448.0, 448.0).to(torch.float8_e4m3fn)
+    return q.view(torch.uint8), scale
+
+
+def expert_weights_fp8(N: int, d: int, f: int, seed: int, device="cpu", std: float = 0.02):
+    """FP8 versions of expert_weights, quantized per output row:
+    (q1 [N,f,d], q3 [N,f,d], q2 [N,d,f] uint8 codes; s1 [N,f], s3 [N,f], s2 [N,d] fp32)."""
+    import torch
+
+    q = [torch.empty((N, f, d), dtype=torch.uint8, device=device),
+         torch.empty((N, f, d), dtype=torch.uint8, device=device),
+         torch.empty((N, d, f), dtype=torch.uint8, device=device)]
+    sc = [torch.empty((N, f), dtype=torch.float32, device=device),
+          torch.empty((N, f), dtype=torch.float32, device=device),
+          torch.empty((N, d), dtype=torch.float32, device=device)]
+    for e in range(N):
+        for i, which in enumerate(("w1", "w3", "w2")):
+            q[i][e], sc[i][e] = quantize_rows_e4m3(expert_matrix(e, which, d, f, seed, device, std))
+    return (*q, *sc)
+
+
 def expert_matrix(e: int, which: str, d: int, f: int, seed: int, device="cpu", std: float = 0.02):
     """One expert matrix in nn.Linear [out,in] layout: w1/w3 (s1/s3 for shared experts) are
     [f,d], w2 (s2) is [d,f]."""
