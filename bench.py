@@ -70,6 +70,9 @@ def parse():
     ap.add_argument("--ep-groups", type=int, default=0,
                     help="G > 0: expert-parallel selection and per-group shares")
     ap.add_argument("--per-group-budget", type=int, default=5, help="m_g (with --ep-groups)")
+    ap.add_argument("--weights", choices=("bf16", "fp8"), default="bf16",
+                    help="routed-expert weight format (fp8: OCP E4M3FN codes, one fp32 scale "
+                         "per output row)")
     ap.add_argument("--full-layer", action="store_true",
                     help="the whole layer from hidden states: router GEMM, selection, routed "
                          "and shared experts (xshare_moe_layer)")
@@ -78,15 +81,18 @@ def parse():
     return ap.parse_args()
 
 
-def gate_up_bytes(n_active, T, k, d, f):
-    """Algorithmic HBM bytes of one gate/up launch: W1, W3 of every active expert, x, and H
-    written as two bf16 arrays (hi and lo)."""
-    return n_active * 2 * f * d * 2 + T * d * 2 + T * k * f * 2 * 2
+def gate_up_bytes(n_active, T, k, d, f, wb=2):
+    """Algorithmic HBM bytes of one gate/up launch: W1, W3 of every active expert (wb bytes
+    per weight; FP8 adds its row scales), x, and H written as two bf16 arrays (hi and lo)."""
+    scales = 0 if wb == 2 else n_active * 2 * f * 4
+    return n_active * 2 * f * d * wb + scales + T * d * 2 + T * k * f * 2 * 2
 
 
-def layer_bytes(n_active, T, N, d, f):
-    """Algorithmic HBM bytes of one layer call: active experts' weights, x, logits, y."""
-    return n_active * 3 * f * d * 2 + T * d * 2 + T * N * 4 + T * d * 2
+def layer_bytes(n_active, T, N, d, f, wb=2):
+    """Algorithmic HBM bytes of one layer call: active experts' weights (and FP8 row scales),
+    x, logits, y."""
+    scales = 0 if wb == 2 else n_active * (2 * f + d) * 4
+    return n_active * 3 * f * d * wb + scales + T * d * 2 + T * N * 4 + T * d * 2
 
 
 def counters_traffic():
@@ -129,14 +135,20 @@ def main():
     k0, m_r = cfg["k0"], cfg.get("m_r", 0)
     hier = cfg["logits"] == "spec"
     nb = args.batches
-    layer_gb = N * 3 * d * f * 2 / 1e9
     # small layers would sit in the 256 MB Infinity Cache between steps: rotate weight copies
-    reps = args.replicas or max(1, min(8, int(np.ceil(4.0 / layer_gb))))
 
+    fp8 = args.weights == "fp8"
+    wb = 1 if fp8 else 2
+    layer_gb = N * 3 * d * f * wb / 1e9
+    reps = args.replicas or max(1, min(8, int(np.ceil(4.0 / layer_gb))))
     print(f"[bench] {args.workload}: generating layer weights ({layer_gb:.2f} GB x {reps})",
           file=sys.stderr, flush=True)
-    w1, w3, w2 = W.expert_weights(N, d, f, 0, dev)
-    wsets = [(w1, w3, w2)] + [(w1.clone(), w3.clone(), w2.clone()) for _ in range(reps - 1)]
+    if fp8:
+        base = W.expert_weights_fp8(N, d, f, 0, dev)
+    else:
+        base = W.expert_weights(N, d, f, 0, dev)
+    wsets = [base] + [tuple(t.clone() for t in base) for _ in range(reps - 1)]
+    forward = X.moe_forward_fp8 if fp8 else X.moe_forward
     made = [W.make_logits(cfg, s) for s in range(nb)]
     logits = [torch.from_numpy(h).to(dev) for h, _ in made]
     offs = [None if o is None else [int(v) for v in o] for _, o in made]
@@ -150,13 +162,12 @@ def main():
 
     def call(s, mode, **kw):
         b = s % nb
-        wa, wb, wc = wsets[s % reps]
+        wset = wsets[s % reps]
         if mode == "xshare":
-            return X.moe_forward(xs[b], logits[b], wa, wb, wc, k, k0, M, bmode, y=y,
-                                 workspace=ws, req_offsets=offs[b] if hier else None,
-                                 per_request_budget=m_r, tau=tau, **kw)
-        return X.moe_forward(xs[b], logits[b], wa, wb, wc, k, 0, N, "extra", y=y, workspace=ws,
-                             **kw)
+            return forward(xs[b], logits[b], *wset, k, k0, M, bmode, y=y, workspace=ws,
+                           req_offsets=offs[b] if hier else None, per_request_budget=m_r,
+                           tau=tau, **kw)
+        return forward(xs[b], logits[b], *wset, k, 0, N, "extra", y=y, workspace=ws, **kw)
 
     # per-batch routing statistics (deterministic per batch)
     stats = []
@@ -194,8 +205,8 @@ def main():
     stage_ms = {name: float(np.mean([e[i].elapsed_ms(e[i + 1]) for e in evs]))
                 for i, name in enumerate(X.STAGES)}
     gu_ms = np.array([e[1].elapsed_ms(e[2]) for e in evs])
-    gu_bytes = np.array([gate_up_bytes(act[s % nb], T, k, d, f) for s in range(args.steps)])
-    lay_bytes = np.array([layer_bytes(act[s % nb], T, N, d, f) for s in range(args.steps)])
+    gu_bytes = np.array([gate_up_bytes(act[s % nb], T, k, d, f, wb) for s in range(args.steps)])
+    lay_bytes = np.array([layer_bytes(act[s % nb], T, N, d, f, wb) for s in range(args.steps)])
 
     vanilla = None
     if not args.no_vanilla:
@@ -211,13 +222,13 @@ def main():
     gbs = float(lay_bytes.mean()) / (ms_step * 1e-3) / 1e9
     gu_achieved = float(gu_bytes.mean()) / (float(gu_ms.mean()) * 1e-3) / 1e9
     # the committed counter record covers the headline workload only
-    traffic = counters_traffic() if (args.workload, M, T, args.tau) == ("ds_t32", 48, 32, None) \
-        else None
+    traffic = counters_traffic() if (args.workload, M, T, args.tau, fp8) == \
+        ("ds_t32", 48, 32, None, False) else None
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(W, xs, logits, offs if hier else None, m_r, w1, w3, w2, T, N, k, k0, M,
-                           d, f, bmode, args.tau)
+        cpu = cpu_baseline(W, xs, logits, offs if hier else None, m_r, base, fp8, T, N, k, k0,
+                           M, d, f, bmode, args.tau)
 
     out = {
         "metric": METRIC,
@@ -230,11 +241,12 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "fp8-e4m3 weights, bf16 activations" if fp8 else "bf16",
         "data": "synthetic",
         "config": {"workload": WORKLOAD_NAMES[args.workload].format(T=T, N=N, k=k, d=d, f=f, M=M,
                                                                      k0=k0, m_r=m_r)
-                   + ("" if args.tau is None else f"_tau{args.tau:g}"),
+                   + ("" if args.tau is None else f"_tau{args.tau:g}")
+                   + ("_fp8" if fp8 else ""), "weights": args.weights,
                    "tokens": T, "n_experts": N, "top_k": k, "d_model": d, "d_ffn": f,
                    "budget": None if args.tau is not None else M, "budget_mode": bmode,
                    "threshold": args.tau, "warmup_k0": k0,
@@ -485,7 +497,7 @@ def run_ep(args, W, X, np, torch):
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(W, xs, logits, offs, m_r, w1, w3, w2, T, N, k, k0, M, d, f, mode="total",
+def cpu_baseline(W, xs, logits, offs, m_r, weights, fp8, T, N, k, k0, M, d, f, mode="total",
                  tau=None, budget_s=10.0):
     """The oracle on the host cores: routing plus the float64 SwiGLU layer of whole batches,
     over as many of the rotated batches as fit in about budget_s seconds (at least one)."""
@@ -500,7 +512,10 @@ def cpu_baseline(W, xs, logits, offs, m_r, w1, w3, w2, T, N, k, k0, M, d, f, mod
         cores = len(os.sched_getaffinity(0))
     print("[bench] cpu baseline: full oracle on rotated batches", file=sys.stderr, flush=True)
     spent, done, active = 0.0, 0, []
+    wall0 = time.perf_counter()
     for b in range(len(xs)):
+        if done and time.perf_counter() - wall0 > 100.0:     # FP8 weight preparation is slow
+            break
         h = logits[b].cpu().numpy()
         xb = W.bf16_bits(xs[b])
         t0 = time.perf_counter()
@@ -508,22 +523,35 @@ def cpu_baseline(W, xs, logits, offs, m_r, w1, w3, w2, T, N, k, k0, M, d, f, mod
             OR.select_hier(h, offs[b], k, k0, m_r, M, mode, tau=tau)
         t_route = time.perf_counter() - t0
         used = sorted(set(int(e) for e in r.ids.reshape(-1)))
-        cache = {e: tuple(W.bf16_bits(m[e]) for m in (w1, w3, w2)) for e in used}   # not timed
+        if fp8:                                                             # not timed
+            q1, q3, q2, s1, s3, s2 = weights
+            cache = {}
+            for n_done, e in enumerate(used):
+                cache[e] = tuple(OF.dequant_rows(q[e].cpu().numpy(), sc[e].cpu().numpy())
+                                 for q, sc in ((q1, s1), (q3, s3), (q2, s2)))
+                if n_done % 8 == 7:
+                    print(f"[bench] cpu baseline: batch {b}, {n_done + 1}/{len(used)} experts "
+                          "decoded", file=sys.stderr, flush=True)
+        else:
+            cache = {e: tuple(W.bf16_bits(m[e]) for m in weights) for e in used}
         t0 = time.perf_counter()
         OF.moe_forward(xb, r.ids, r.w, lambda e: cache[e])
         spent += t_route + time.perf_counter() - t0
         done += 1
+        print(f"[bench] cpu baseline: batch {b} done, {spent:.1f} s timed so far", file=sys.stderr,
+              flush=True)
         active.append(r.n_active)
         del cache
         if spent >= budget_s:
             break
     t_batch = spent / done
-    bytes_batch = float(np.mean([layer_bytes(a, T, N, d, f) for a in active]))
+    bytes_batch = float(np.mean([layer_bytes(a, T, N, d, f, 1 if fp8 else 2) for a in active]))
     return {"value": round(bytes_batch / t_batch / 1e9, 3), "unit": "GB/s",
             "us_per_batch": round(t_batch * 1e6, 1), "cores": int(cores), "kind": "oracle",
             "sample": f"full oracle (numpy routing, float64 SwiGLU of all {T} tokens over their "
                       f"{np.mean(active):.0f} active experts) on {done} of the rotated batches, "
-                      f"{spent:.1f} s total; BLAS threads = cores, weight conversion single-threaded"}
+                      f"{spent:.1f} s total; BLAS threads = cores, weight conversion "
+                      f"{'(FP8 decode) ' if fp8 else ''}single-threaded and not timed"}
 
 
 if __name__ == "__main__":

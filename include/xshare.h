@@ -284,6 +284,30 @@ xshare_status xshare_moe_forward(const uint16_t* x, const float* logits, int32_t
                                  void* const* stage_events, hipStream_t stream);
 
 /*
+ * xshare_moe_forward_fp8 -- xshare_moe_forward with FP8 routed-expert weights (half the
+ * bytes of bf16 on the stream that bounds the layer; the paper is silent on precision).
+ *
+ *   w1, w3    [N, f, d] uint8: OCP FP8 E4M3FN codes (1 sign, 4 exponent bits with bias 7,
+ *             3 mantissa bits; 0x7F and 0xFF are NaN and must not occur), 16-byte aligned.
+ *   w2        [N, d, f] uint8, same format.
+ *   w1_scale, w3_scale  [N, f] fp32; w2_scale [N, d] fp32: one scale per output row, the
+ *             weight being decode(code) * scale.  Codes are decoded exactly to bf16 and the
+ *             row scale multiplies the fp32 result of the row's dot product.
+ *   Everything else as xshare_moe_forward (workspace from xshare_moe_workspace_bytes); shared
+ *   experts are not taken here.
+ */
+xshare_status xshare_moe_forward_fp8(const uint16_t* x, const float* logits, int32_t T,
+                                     int32_t d, int32_t f, const uint8_t* w1, const uint8_t* w3,
+                                     const uint8_t* w2, const float* w1_scale,
+                                     const float* w3_scale, const float* w2_scale,
+                                     const xshare_route_params* params,
+                                     const int32_t* req_offsets, const int32_t* host_offsets,
+                                     int32_t R, const xshare_ep_layout* ep, uint16_t* y,
+                                     uint8_t* sel_mask, int32_t* topk_ids, float* topk_w,
+                                     xshare_stats* stats, void* ws, size_t ws_bytes,
+                                     void* const* stage_events, hipStream_t stream);
+
+/*
  * xshare_moe_layer -- the whole MoE layer of Section 2.1 from the hidden states: router
  * logits h = W_g x (as xshare_router_logits), selection, the selected routed experts and
  * the shared experts, combine.

@@ -37,9 +37,17 @@ def decode_e4m3(codes) -> np.ndarray:
     return np.where((e == 15) & ((c & 7) == 7), np.nan, v)
 
 
+_E4M3_VALUES = None
+
+
 def dequant_rows(codes, scale) -> np.ndarray:
-    """Weights of one FP8 matrix: decode(q[r, c]) * scale[r] in float64 (exact)."""
-    return decode_e4m3(codes) * np.asarray(scale, dtype=np.float32).astype(np.float64)[:, None]
+    """Weights of one FP8 matrix: decode(q[r, c]) * scale[r] in float64 (exact); the codes are
+    looked up in the table of all 256 decoded values."""
+    global _E4M3_VALUES
+    if _E4M3_VALUES is None:
+        _E4M3_VALUES = decode_e4m3(np.arange(256, dtype=np.uint8))
+    return _E4M3_VALUES[np.asarray(codes, dtype=np.uint8)] * \
+        np.asarray(scale, dtype=np.float32).astype(np.float64)[:, None]
 
 
 def _as_f64(w) -> np.ndarray:

@@ -5,6 +5,6 @@ The computation lives in hand-written HIP kernels behind the C ABI of include/xs
 binding with the same entry points.
 """
 from .xshare import (GroupMap, HipEvent, XShareError, layer_workspace_bytes,  # noqa: F401
-                     lib, moe_forward, moe_layer, moe_workspace_bytes, params, route,
+                     lib, moe_forward, moe_forward_fp8, moe_layer, moe_workspace_bytes, params, route,
                      route_workspace_bytes, router_logits, select_ep, select_hier, stats_dict,
                      status_string, version)

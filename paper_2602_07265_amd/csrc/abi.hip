@@ -191,11 +191,31 @@ xshare_status route_common(const float* logits, int32_t T, const int32_t* req_of
   return xs::launch_route(a, stream) == hipSuccess ? XSHARE_OK : XSHARE_EHIP;
 }
 
-// The layer: optional router GEMM (w_gate given: its partial planes go to the workspace and
-// the selection kernel sums them), selection, expert GEMMs (routed and shared), combine.
+// Routed expert weights: bf16 matrices, or FP8 E4M3FN codes with one fp32 scale per row.
+struct Weights {
+  const uint16_t* w1 = nullptr;
+  const uint16_t* w3 = nullptr;
+  const uint16_t* w2 = nullptr;
+  const uint8_t* q1 = nullptr;
+  const uint8_t* q3 = nullptr;
+  const uint8_t* q2 = nullptr;
+  const float* s1 = nullptr;
+  const float* s3 = nullptr;
+  const float* s2 = nullptr;
+  bool fp8() const { return q1 != nullptr; }
+  bool present() const {
+    return fp8() ? (q3 && q2 && s1 && s3 && s2) : (w1 && w3 && w2);
+  }
+  bool aligned() const {
+    return fp8() ? (aligned16(q1) && aligned16(q3) && aligned16(q2))
+                 : (aligned16(w1) && aligned16(w3) && aligned16(w2));
+  }
+};
+
+// The layer: optional router GEMM (w_gate given: logits computed on the device), selection,
+// expert GEMMs (routed and shared), combine.
 xshare_status layer_common(const uint16_t* x, const float* logits, const uint16_t* w_gate,
-                           int32_t T, int32_t d, int32_t f, const uint16_t* w1,
-                           const uint16_t* w3, const uint16_t* w2,
+                           int32_t T, int32_t d, int32_t f, const Weights& wt,
                            const xshare_shared_experts* shared, const xshare_route_params* params,
                            const int32_t* req_offsets, const int32_t* host_offsets, int32_t R,
                            const xshare_ep_layout* ep, uint16_t* y, float* logits_out,
@@ -214,11 +234,11 @@ xshare_status layer_common(const uint16_t* x, const float* logits, const uint16_
   if (st != XSHARE_OK) return st;
   st = check_shared(shared, ep);
   if (st != XSHARE_OK) return st;
+  if (wt.fp8() && shared && shared->n_shared > 0) return XSHARE_EUNSUPPORTED;
   if (d <= 0 || f <= 0) return XSHARE_EINVAL;
   if (d % xs::kDimAlign != 0 || f % xs::kDimAlign != 0) return XSHARE_EUNSUPPORTED;
-  if (T > 0 && (!x || !w1 || !w3 || !w2 || !y)) return XSHARE_EINVAL;
-  if (!aligned16(x) || !aligned16(w1) || !aligned16(w3) || !aligned16(w2) || !aligned16(y) ||
-      (w_gate && !aligned16(w_gate)))
+  if (T > 0 && (!x || !wt.present() || !y)) return XSHARE_EINVAL;
+  if (!aligned16(x) || !wt.aligned() || !aligned16(y) || (w_gate && !aligned16(w_gate)))
     return XSHARE_EINVAL;
   const int N = params->n_experts, k = params->top_k;
   const int n_shared = n_shared_of(shared);
@@ -253,9 +273,15 @@ xshare_status layer_common(const uint16_t* x, const float* logits, const uint16_
 
   xs::FfnArgs fa{};
   fa.x = x;
-  fa.w1 = w1;
-  fa.w3 = w3;
-  fa.w2 = w2;
+  fa.w1 = wt.w1;
+  fa.w3 = wt.w3;
+  fa.w2 = wt.w2;
+  fa.q1 = wt.q1;
+  fa.q3 = wt.q3;
+  fa.q2 = wt.q2;
+  fa.s1 = wt.s1;
+  fa.s3 = wt.s3;
+  fa.s2 = wt.s2;
   fa.T = T;
   fa.N = N;
   fa.k = k;
@@ -361,7 +387,34 @@ xshare_status xshare_moe_forward(const uint16_t* x, const float* logits, int32_t
                                  xshare_stats* stats, void* ws, size_t ws_bytes,
                                  void* const* stage_events, hipStream_t stream) {
   if (T > 0 && !logits) return XSHARE_EINVAL;
-  return layer_common(x, logits, nullptr, T, d, f, w1, w3, w2, shared, params, req_offsets,
+  Weights wt;
+  wt.w1 = w1;
+  wt.w3 = w3;
+  wt.w2 = w2;
+  return layer_common(x, logits, nullptr, T, d, f, wt, shared, params, req_offsets,
+                      host_offsets, R, ep, y, nullptr, sel_mask, topk_ids, topk_w, stats, ws,
+                      ws_bytes, stage_events, stream);
+}
+
+xshare_status xshare_moe_forward_fp8(const uint16_t* x, const float* logits, int32_t T,
+                                     int32_t d, int32_t f, const uint8_t* w1, const uint8_t* w3,
+                                     const uint8_t* w2, const float* w1_scale,
+                                     const float* w3_scale, const float* w2_scale,
+                                     const xshare_route_params* params,
+                                     const int32_t* req_offsets, const int32_t* host_offsets,
+                                     int32_t R, const xshare_ep_layout* ep, uint16_t* y,
+                                     uint8_t* sel_mask, int32_t* topk_ids, float* topk_w,
+                                     xshare_stats* stats, void* ws, size_t ws_bytes,
+                                     void* const* stage_events, hipStream_t stream) {
+  if (T > 0 && (!logits || !w1)) return XSHARE_EINVAL;
+  Weights wt;              // with T == 0 nothing is read and the pointers may be null
+  wt.q1 = w1;
+  wt.q3 = w3;
+  wt.q2 = w2;
+  wt.s1 = w1_scale;
+  wt.s3 = w3_scale;
+  wt.s2 = w2_scale;
+  return layer_common(x, logits, nullptr, T, d, f, wt, nullptr, params, req_offsets,
                       host_offsets, R, ep, y, nullptr, sel_mask, topk_ids, topk_w, stats, ws,
                       ws_bytes, stage_events, stream);
 }
@@ -376,7 +429,11 @@ xshare_status xshare_moe_layer(const uint16_t* x, const uint16_t* w_gate, int32_
                                xshare_stats* stats, void* ws, size_t ws_bytes,
                                void* const* stage_events, hipStream_t stream) {
   if (T > 0 && !w_gate) return XSHARE_EINVAL;
-  return layer_common(x, nullptr, w_gate, T, d, f, w1, w3, w2, shared, params, req_offsets,
+  Weights wt;
+  wt.w1 = w1;
+  wt.w3 = w3;
+  wt.w2 = w2;
+  return layer_common(x, nullptr, w_gate, T, d, f, wt, shared, params, req_offsets,
                       host_offsets, R, ep, y, logits_out, sel_mask, topk_ids, topk_w, stats, ws,
                       ws_bytes, stage_events, stream);
 }

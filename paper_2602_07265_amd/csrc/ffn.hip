@@ -49,6 +49,28 @@ __device__ __forceinline__ uint16_t to_bf16(float v) {
 
 __device__ __forceinline__ float from_bf16(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
+// 8 FP8 E4M3FN codes (two words, element order = byte order) -> 8 bf16.  The hardware
+// conversion gives fp32; an E4M3 value has at most 4 significant bits, so its upper 16 bits
+// are the exact bf16 (v_perm_b32 gathers the upper halves of two floats).
+__device__ __forceinline__ bf16x8 fp8x8_to_bf16(uint2 v) {
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const f32x2 a = __builtin_amdgcn_cvt_pk_f32_fp8((int)v.x, false);
+  const f32x2 b = __builtin_amdgcn_cvt_pk_f32_fp8((int)v.x, true);
+  const f32x2 c = __builtin_amdgcn_cvt_pk_f32_fp8((int)v.y, false);
+  const f32x2 d = __builtin_amdgcn_cvt_pk_f32_fp8((int)v.y, true);
+  u32x4 r;
+  r.x = __builtin_amdgcn_perm(__float_as_uint(a.y), __float_as_uint(a.x), 0x07060302u);
+  r.y = __builtin_amdgcn_perm(__float_as_uint(b.y), __float_as_uint(b.x), 0x07060302u);
+  r.z = __builtin_amdgcn_perm(__float_as_uint(c.y), __float_as_uint(c.x), 0x07060302u);
+  r.w = __builtin_amdgcn_perm(__float_as_uint(d.y), __float_as_uint(d.x), 0x07060302u);
+  return __builtin_bit_cast(bf16x8, r);
+}
+
+__device__ __forceinline__ uint2 load_q8(const uint8_t* p) {
+  return *reinterpret_cast<const uint2*>(p);
+}
+
 // Stores v as hi = bf16(v) and lo = bf16(v - hi).
 __device__ __forceinline__ void store_hilo(uint16_t* hi, uint16_t* lo, size_t at, float v) {
   const uint16_t h = to_bf16(v);
@@ -128,6 +150,51 @@ __device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[TL], int
   }
 }
 
+// wave_pass with FP8 weights: the B operand comes from E4M3 codes (8 bytes per lane and
+// MFMA), prefetched one step ahead as raw bytes and converted to bf16 just before use.
+template <int U, int NM, int TL = kTiles>
+__device__ __forceinline__ void wave_pass_q8(const uint16_t* const (&arow)[TL], int nt,
+                                             const uint8_t* const (&brow)[NM], int K,
+                                             floatx4 (&acc)[NM][TL]) {
+  constexpr int KB = 32 * U;
+  uint2 b[NM][U];
+  bf16x8 x[TL][U];
+#pragma unroll
+  for (int m = 0; m < NM; ++m)
+#pragma unroll
+    for (int u = 0; u < U; ++u) b[m][u] = load_q8(brow[m] + 8 * u);
+  for (int kb = 0; kb < K; kb += KB) {
+    uint2 nb[NM][U];
+    const bool more = kb + KB < K;
+    if (more) {
+#pragma unroll
+      for (int m = 0; m < NM; ++m)
+#pragma unroll
+        for (int u = 0; u < U; ++u) nb[m][u] = load_q8(brow[m] + kb + KB + 8 * u);
+    }
+#pragma unroll
+    for (int rt = 0; rt < TL; ++rt)
+      if (rt < nt)
+#pragma unroll
+        for (int u = 0; u < U; ++u) x[rt][u] = load8(arow[rt] + kb + 8 * u);
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int m = 0; m < NM; ++m) {
+        const bf16x8 bv = fp8x8_to_bf16(b[m][u]);
+#pragma unroll
+        for (int rt = 0; rt < TL; ++rt)
+          if (rt < nt) acc[m][rt] = mfma(x[rt][u], bv, acc[m][rt]);
+      }
+    if (more) {
+#pragma unroll
+      for (int m = 0; m < NM; ++m)
+#pragma unroll
+        for (int u = 0; u < U; ++u) b[m][u] = nb[m][u];
+    }
+  }
+}
+
 // Unroll (32-element k-groups per step) and token-operand buffering of the two GEMMs.
 #ifndef XS_GATE_UP_U
 #define XS_GATE_UP_U 4
@@ -141,48 +208,56 @@ __device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[TL], int
 #ifndef XS_DOWN_ADBL
 #define XS_DOWN_ADBL 0
 #endif
+#ifndef XS_Q8_GATE_UP_U
+#define XS_Q8_GATE_UP_U 8            // FP8 weights: half the bytes per step, so twice the unroll
+#endif
+#ifndef XS_Q8_DOWN_U
+#define XS_Q8_DOWN_U 4
+#endif
 #ifndef XS_DOWN_TL
 #define XS_DOWN_TL 4                 // 8-token (hi + lo) tiles per pass of the down GEMM
 #endif
 
 // Work of grid row `slot` of the expert GEMMs: the routed active experts first (their
 // tokens' rows in permuted order), then the shared experts (all T tokens, rows
-// T*k + s*T + t).  False for rows beyond both.
+// T*k + s*T + t).  False for rows beyond both.  `e` is the routed expert or the shared one.
 struct SlotWork {
-  const uint16_t* w1;
-  const uint16_t* w3;
-  const uint16_t* w2;
-  int p0, te;
+  int e, p0, te;
   bool shared;
 };
 
 __device__ __forceinline__ bool slot_work(const FfnArgs& a, int slot, SlotWork& w) {
   const int n_active = a.counters[kCntActive];
-  const size_t fd = (size_t)a.f * a.d;
   if (slot < n_active) {
-    const int e = a.active[slot];
-    w.p0 = a.offsets[e];
-    w.te = a.offsets[e + 1] - w.p0;
-    w.w1 = a.w1 + e * fd;
-    w.w3 = a.w3 + e * fd;
-    w.w2 = a.w2 + e * fd;
+    w.e = a.active[slot];
+    w.p0 = a.offsets[w.e];
+    w.te = a.offsets[w.e + 1] - w.p0;
     w.shared = false;
     return true;
   }
   const int sh = slot - n_active;
   if (sh >= a.n_shared) return false;
+  w.e = sh;
   w.p0 = a.T * a.k + sh * a.T;
   w.te = a.T;
-  w.w1 = a.sw1 + sh * fd;
-  w.w3 = a.sw3 + sh * fd;
-  w.w2 = a.sw2 + sh * fd;
   w.shared = true;
   return true;
 }
 
+// The slot's bf16 weight matrix (routed or shared), or its FP8 codes (routed only).
+__device__ __forceinline__ const uint16_t* slot_w(const FfnArgs& a, const SlotWork& w,
+                                                  const uint16_t* routed,
+                                                  const uint16_t* shared) {
+  return (w.shared ? shared : routed) + (size_t)w.e * a.f * a.d;
+}
+__device__ __forceinline__ const uint8_t* slot_q(const FfnArgs& a, const SlotWork& w,
+                                                 const uint8_t* codes) {
+  return codes + (size_t)w.e * a.f * a.d;
+}
+
 // kSplit: the block covers one part of the reduction (blockIdx.z) and writes fp32 gate and
 // up partials; otherwise it covers all of d and writes H directly.
-template <int U, bool kSplit>
+template <int U, bool kSplit, bool kQ8>
 __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
   SlotWork sw;
   if (!slot_work(a, blockIdx.y, sw)) return;
@@ -195,8 +270,12 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
   const int Kg = kSplit ? d / a.gu_splits : d;   // this block's part of the reduction
   const size_t k0 = (kSplit ? (size_t)blockIdx.z * Kg : 0) + (size_t)g * 8 * U;
   const size_t wrow = (size_t)(j0 + n) * d + k0;
-  const uint16_t* const brow[2] = {sw.w1 + wrow, sw.w3 + wrow};
   const size_t plane = (size_t)a.rows * f;     // one fp32 partial plane [rows, f]
+  float sc1 = 1.0f, sc3 = 1.0f;                // FP8 per-row scales of this lane's column
+  if (kQ8) {
+    sc1 = a.s1[(size_t)sw.e * f + j0 + n];
+    sc3 = a.s3[(size_t)sw.e * f + j0 + n];
+  }
 
   for (int c0 = 0; c0 < te; c0 += 16 * kTiles) {
     const int nt = min(kTiles, (te - c0 + 15) / 16);
@@ -212,7 +291,14 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
     for (int m = 0; m < 2; ++m)
 #pragma unroll
       for (int rt = 0; rt < kTiles; ++rt) acc[m][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    wave_pass<U, 2, XS_GATE_UP_ADBL != 0>(arow, nt, brow, Kg, acc);
+    if (kQ8) {
+      const uint8_t* const brow[2] = {slot_q(a, sw, a.q1) + wrow, slot_q(a, sw, a.q3) + wrow};
+      wave_pass_q8<U, 2>(arow, nt, brow, Kg, acc);
+    } else {
+      const uint16_t* const brow[2] = {slot_w(a, sw, a.w1, a.sw1) + wrow,
+                                       slot_w(a, sw, a.w3, a.sw3) + wrow};
+      wave_pass<U, 2, XS_GATE_UP_ADBL != 0>(arow, nt, brow, Kg, acc);
+    }
 #pragma unroll
     for (int rt = 0; rt < kTiles; ++rt) {
       if (rt >= nt) break;
@@ -220,7 +306,7 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
       for (int i = 0; i < 4; ++i) {
         const int t = c0 + rt * 16 + 4 * g + i;
         if (t < te) {
-          const float h1 = acc[0][rt][i], h3 = acc[1][rt][i];
+          const float h1 = acc[0][rt][i] * sc1, h3 = acc[1][rt][i] * sc3;
           const size_t at = (size_t)(p0 + t) * f + j0 + n;
           if (!kSplit) {
             store_hilo(a.h, a.hlo, at, h1 / (1.0f + __expf(-h1)) * h3);
@@ -235,7 +321,7 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
   }
 }
 
-template <int U>
+template <int U, bool kQ8>
 __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
   constexpr int NM = XS_DOWN_NM;  // 16-row tiles of W2 per wave, sharing the token operand
   constexpr int TL = XS_DOWN_TL;  // token tiles per pass, 8 tokens each (hi and lo rows)
@@ -251,10 +337,14 @@ __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
   const size_t k0 = (size_t)blockIdx.z * Ks + (size_t)g * 8 * U;
   float* const ypart = a.yslot + (size_t)blockIdx.z * a.rows * d;
   const uint16_t* const hsrc = n < 8 ? a.h : a.hlo;   // A rows 0-7: hi, rows 8-15: lo
-  const uint16_t* brow[NM];
+  size_t wrow[NM];
+  float sc[NM];                                        // FP8 per-row scales (1 for bf16)
 #pragma unroll
-  for (int m = 0; m < NM; ++m)
-    brow[m] = sw.w2 + ((size_t)min(n0 + 16 * m, d - 16) + n) * f + k0;
+  for (int m = 0; m < NM; ++m) {
+    const int row = min(n0 + 16 * m, d - 16) + n;
+    wrow[m] = (size_t)row * f + k0;
+    sc[m] = kQ8 ? a.s2[(size_t)sw.e * d + row] : 1.0f;
+  }
 
   for (int c0 = 0; c0 < te; c0 += 8 * TL) {
     const int nt = min(TL, (te - c0 + 7) / 8);
@@ -269,7 +359,17 @@ __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
     for (int m = 0; m < NM; ++m)
 #pragma unroll
       for (int rt = 0; rt < TL; ++rt) acc[m][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    wave_pass<U, NM, XS_DOWN_ADBL != 0, TL>(arow, nt, brow, Ks, acc);
+    if (kQ8) {
+      const uint8_t* brow[NM];
+#pragma unroll
+      for (int m = 0; m < NM; ++m) brow[m] = slot_q(a, sw, a.q2) + wrow[m];
+      wave_pass_q8<U, NM, TL>(arow, nt, brow, Ks, acc);
+    } else {
+      const uint16_t* brow[NM];
+#pragma unroll
+      for (int m = 0; m < NM; ++m) brow[m] = slot_w(a, sw, a.w2, a.sw2) + wrow[m];
+      wave_pass<U, NM, XS_DOWN_ADBL != 0, TL>(arow, nt, brow, Ks, acc);
+    }
 #pragma unroll
     for (int rt = 0; rt < TL; ++rt) {
       if (rt >= nt) break;
@@ -278,7 +378,8 @@ __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
         // lanes g = 0, 1 hold the hi rows of tokens 4g + i, lanes 32 above them the lo rows
         float v[NM];
 #pragma unroll
-        for (int m = 0; m < NM; ++m) v[m] = acc[m][rt][i] + __shfl_xor(acc[m][rt][i], 32, 64);
+        for (int m = 0; m < NM; ++m)
+          v[m] = (acc[m][rt][i] + __shfl_xor(acc[m][rt][i], 32, 64)) * sc[m];
         const int t = c0 + rt * 8 + 4 * g + i;
         if (g < 2 && t < te) {
           // routed rows go to their (token, slot) row, shared rows keep their own
@@ -420,12 +521,12 @@ __global__ __launch_bounds__(kBlock) void router_sum_kernel(RouterArgs r) {
   r.logits[idx] = v;
 }
 
-template <int U>
+template <int U, bool kQ8>
 void launch_gu(const FfnArgs& a, bool split, dim3 grid, dim3 block, hipStream_t stream) {
   if (split)
-    hipLaunchKernelGGL((gate_up_kernel<U, true>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((gate_up_kernel<U, true, kQ8>), grid, block, 0, stream, a);
   else
-    hipLaunchKernelGGL((gate_up_kernel<U, false>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((gate_up_kernel<U, false, kQ8>), grid, block, 0, stream, a);
 }
 
 int unroll_for(int K, int want) {
@@ -441,11 +542,20 @@ hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
                   a.gu_splits),
       block(kBlock);
   const bool split = a.gu_splits > 1;
-  switch (unroll_for(a.d / a.gu_splits, XS_GATE_UP_U)) {
-    case 8: launch_gu<8>(a, split, grid, block, stream); break;
-    case 4: launch_gu<4>(a, split, grid, block, stream); break;
-    case 2: launch_gu<2>(a, split, grid, block, stream); break;
-    default: launch_gu<1>(a, split, grid, block, stream); break;
+  if (a.q1) {
+    switch (unroll_for(a.d / a.gu_splits, XS_Q8_GATE_UP_U)) {
+      case 8: launch_gu<8, true>(a, split, grid, block, stream); break;
+      case 4: launch_gu<4, true>(a, split, grid, block, stream); break;
+      case 2: launch_gu<2, true>(a, split, grid, block, stream); break;
+      default: launch_gu<1, true>(a, split, grid, block, stream); break;
+    }
+  } else {
+    switch (unroll_for(a.d / a.gu_splits, XS_GATE_UP_U)) {
+      case 8: launch_gu<8, false>(a, split, grid, block, stream); break;
+      case 4: launch_gu<4, false>(a, split, grid, block, stream); break;
+      case 2: launch_gu<2, false>(a, split, grid, block, stream); break;
+      default: launch_gu<1, false>(a, split, grid, block, stream); break;
+    }
   }
   if (split) {
     const dim3 fgrid((a.f + kBlock * 4 - 1) / (kBlock * 4), (unsigned)a.rows);
@@ -457,11 +567,20 @@ hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
 hipError_t launch_down(const FfnArgs& a, hipStream_t stream) {
   constexpr int cols = kWaves * kCols * XS_DOWN_NM;
   const dim3 grid((a.d + cols - 1) / cols, a.max_active + a.n_shared, a.splits), block(kBlock);
-  switch (unroll_for(a.f / a.splits, XS_DOWN_U)) {
-    case 8: hipLaunchKernelGGL(down_kernel<8>, grid, block, 0, stream, a); break;
-    case 4: hipLaunchKernelGGL(down_kernel<4>, grid, block, 0, stream, a); break;
-    case 2: hipLaunchKernelGGL(down_kernel<2>, grid, block, 0, stream, a); break;
-    default: hipLaunchKernelGGL(down_kernel<1>, grid, block, 0, stream, a); break;
+  if (a.q1) {
+    switch (unroll_for(a.f / a.splits, XS_Q8_DOWN_U)) {
+      case 8: hipLaunchKernelGGL((down_kernel<8, true>), grid, block, 0, stream, a); break;
+      case 4: hipLaunchKernelGGL((down_kernel<4, true>), grid, block, 0, stream, a); break;
+      case 2: hipLaunchKernelGGL((down_kernel<2, true>), grid, block, 0, stream, a); break;
+      default: hipLaunchKernelGGL((down_kernel<1, true>), grid, block, 0, stream, a); break;
+    }
+  } else {
+    switch (unroll_for(a.f / a.splits, XS_DOWN_U)) {
+      case 8: hipLaunchKernelGGL((down_kernel<8, false>), grid, block, 0, stream, a); break;
+      case 4: hipLaunchKernelGGL((down_kernel<4, false>), grid, block, 0, stream, a); break;
+      case 2: hipLaunchKernelGGL((down_kernel<2, false>), grid, block, 0, stream, a); break;
+      default: hipLaunchKernelGGL((down_kernel<1, false>), grid, block, 0, stream, a); break;
+    }
   }
   return hipGetLastError();
 }

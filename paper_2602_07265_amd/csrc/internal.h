@@ -194,9 +194,15 @@ hipError_t launch_route(const RouteArgs& a, hipStream_t stream);
 
 struct FfnArgs {
   const uint16_t* x;
-  const uint16_t* w1;
+  const uint16_t* w1;          // bf16 weights (nullptr with FP8 weights)
   const uint16_t* w3;
   const uint16_t* w2;
+  const uint8_t* q1;           // FP8 E4M3FN weights, same layout (nullptr with bf16 weights)
+  const uint8_t* q3;
+  const uint8_t* q2;
+  const float* s1;             // FP8 scales, one per output row: [N, f], [N, f], [N, d]
+  const float* s3;
+  const float* s2;
   int T, N, k, d, f;
   int max_active;              // host bound on the number of active experts (grid size)
   int splits;                  // K-splits of the down GEMM (partials summed in the combine)

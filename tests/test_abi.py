@@ -21,13 +21,13 @@ FAKE_ODD = ctypes.c_void_p((1 << 20) + 2)
 def declared_functions():
     src = open(HEADER).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(xshare_[a-z_]+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(xshare_[a-z0-9_]+)\s*\(", src)))
 
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert {"xshare_route", "xshare_select_hier", "xshare_select_ep",
-            "xshare_moe_forward"} <= set(names)
+    assert {"xshare_route", "xshare_select_hier", "xshare_select_ep", "xshare_moe_forward",
+            "xshare_moe_forward_fp8", "xshare_moe_layer", "xshare_router_logits"} <= set(names)
     lib = X.lib()
     for n in names:
         assert hasattr(lib, n), n
@@ -241,3 +241,20 @@ def test_router_and_layer_validation():
     one = X.moe_workspace_bytes(32, 7168, 2048, q, None, X.SharedExperts(1, 0, 0, 0))
     assert one >= no + 32 * (2048 * 2 + 7168 * 4)     # H and Y rows of the shared expert
     assert X.layer_workspace_bytes(32, 7168, 2048, q) > no
+
+
+def test_moe_forward_fp8_validation():
+    L = X.lib()
+    p = X.params(16, 2, 1, 8)
+
+    def call(q1=FAKE, q3=FAKE, q2=FAKE, s1=FAKE, s3=FAKE, s2=FAKE, d=64, f=128, T=8):
+        return L.xshare_moe_forward_fp8(FAKE, FAKE, T, d, f, q1, q3, q2, s1, s3, s2,
+                                        ctypes.byref(p), None, None, 0, None, FAKE, None, None,
+                                        None, None, None, 1 << 30, None, None)
+
+    assert call() == X.EWORKSPACE
+    assert call(q1=None) == X.EINVAL
+    assert call(q2=None) == X.EINVAL
+    assert call(s3=None) == X.EINVAL                 # scales are required
+    assert call(q3=FAKE_ODD) == X.EINVAL             # 16-byte alignment
+    assert call(d=40) == X.EUNSUPPORTED
