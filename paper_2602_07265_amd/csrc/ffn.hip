@@ -209,7 +209,7 @@ __device__ __forceinline__ void wave_pass_q8(const uint16_t* const (&arow)[TL], 
 #define XS_DOWN_ADBL 0
 #endif
 #ifndef XS_Q8_GATE_UP_U
-#define XS_Q8_GATE_UP_U 8            // FP8 weights: half the bytes per step, so twice the unroll
+#define XS_Q8_GATE_UP_U 4
 #endif
 #ifndef XS_Q8_DOWN_U
 #define XS_Q8_DOWN_U 4
@@ -323,7 +323,7 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
 
 template <int U, bool kQ8>
 __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
-  constexpr int NM = XS_DOWN_NM;  // 16-row tiles of W2 per wave, sharing the token operand
+  constexpr int NM = kQ8 ? XS_Q8_DOWN_NM : XS_DOWN_NM;   // 16-row W2 tiles per wave
   constexpr int TL = XS_DOWN_TL;  // token tiles per pass, 8 tokens each (hi and lo rows)
   SlotWork sw;
   if (!slot_work(a, blockIdx.y, sw)) return;
@@ -565,7 +565,7 @@ hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_down(const FfnArgs& a, hipStream_t stream) {
-  constexpr int cols = kWaves * kCols * XS_DOWN_NM;
+  const int cols = kWaves * kCols * (a.q1 ? XS_Q8_DOWN_NM : XS_DOWN_NM);
   const dim3 grid((a.d + cols - 1) / cols, a.max_active + a.n_shared, a.splits), block(kBlock);
   if (a.q1) {
     switch (unroll_for(a.f / a.splits, XS_Q8_DOWN_U)) {

@@ -96,9 +96,15 @@ inline int gate_up_splits(int est_active, int d, int f) {
   return split_for((long)est_active * (f / 16), d, 128, XS_GU_SPLIT_BELOW, XS_GU_SPLIT_TARGET,
                    XS_GATE_UP_MAX_SPLITS);
 }
-// 16-row tiles of W2 per wave of the down GEMM (output rows per wave = 16 * XS_DOWN_NM).
+// 16-row tiles of W2 per wave of the down GEMM (output rows per wave = 16 * NM): 2 with
+// bf16 weights, 4 with FP8 weights (whose one-byte rows make the shared token operand
+// relatively more expensive).  The split counts below use the bf16 figure for both, so the
+// workspace does not depend on the weight format.
 #ifndef XS_DOWN_NM
 #define XS_DOWN_NM 2
+#endif
+#ifndef XS_Q8_DOWN_NM
+#define XS_Q8_DOWN_NM 4
 #endif
 inline int down_splits(int est_active, int d, int f) {
   return split_for((long)est_active * (d / (16 * XS_DOWN_NM)), f, 128, XS_DN_SPLIT_BELOW,
