@@ -306,7 +306,6 @@ xshare_status layer_common(const uint16_t* x, const float* logits, const uint16_
   fa.ids = ra.ids;
   fa.w = ra.w;
   fa.h = at<uint16_t>(ws, L.h);
-  fa.hlo = at<uint16_t>(ws, L.hlo);
   fa.yslot = at<float>(ws, L.y);
   fa.y = y;
   if (xs::launch_gate_up(fa, stream) != hipSuccess || !record(2)) return XSHARE_EHIP;

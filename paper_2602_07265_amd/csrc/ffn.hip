@@ -1,10 +1,11 @@
 // Expert FFNs of the selected experts only (SwiGLU, nn.Linear [out, in] weights, bf16):
 //   gate/up:  H[p, :] = silu(x_i W1_e^T) * (x_i W3_e^T)      for every permuted row p = (i, r)
 //   down:     Y[i*k + r, :] = H[p, :] W2_e^T
-// H is kept as two bf16 arrays, hi = bf16(H) and lo = bf16(H - hi) (about 16 significant
-// bits): with H in bf16 alone its rounding moved large outputs across a bf16 rounding
-// boundary of y.  The down GEMM feeds both halves to one MFMA: 8 tokens per 16-row tile,
-// hi rows 0-7 and lo rows 8-15, summed after the reduction.
+// H is kept as hi = bf16(H) and lo = bf16(H - hi) (about 16 significant bits): with H in
+// bf16 alone its rounding moved large outputs across a bf16 rounding boundary of y.  The two
+// are interleaved in 8-element chunks, so a token's hi and lo for one k-range share a cache
+// line.  The down GEMM feeds both to one MFMA: 8 tokens per 16-row tile, hi rows 0-7 and lo
+// rows 8-15, summed after the reduction.
 //   combine:  y_i = sum_r w_ir Y[i*k + r, :]  (rank order, fp32) -> bf16
 // Always-on shared experts (Section 2.1) are extra slots after the routed ones, with all T
 // tokens; their output rows are added after the routed terms with weight 1.  The router
@@ -71,11 +72,13 @@ __device__ __forceinline__ uint2 load_q8(const uint8_t* p) {
   return *reinterpret_cast<const uint2*>(p);
 }
 
-// Stores v as hi = bf16(v) and lo = bf16(v - hi).
-__device__ __forceinline__ void store_hilo(uint16_t* hi, uint16_t* lo, size_t at, float v) {
+// Stores v = H[p, c] as hi = bf16(v) and lo = bf16(v - hi) in the interleaved rows of 2f
+// elements: hi at 16 (c / 8) + c % 8, lo 8 elements further.
+__device__ __forceinline__ void store_hilo(uint16_t* h2, size_t p, int c, int f, float v) {
   const uint16_t h = to_bf16(v);
-  hi[at] = h;
-  lo[at] = to_bf16(v - from_bf16(h));
+  uint16_t* const at = h2 + p * 2 * (size_t)f + 2 * (c & ~7) + (c & 7);
+  at[0] = h;
+  at[8] = to_bf16(v - from_bf16(h));
 }
 
 // One pass of a wave over the reduction dimension K for up to kTiles token tiles:
@@ -87,7 +90,9 @@ __device__ __forceinline__ void store_hilo(uint16_t* hi, uint16_t* lo, size_t at
 // both already offset by this lane's group position g * 8U.  Weight loads (HBM) run one
 // step ahead; token loads (L2-resident) are issued either one step ahead too (ADBL) or
 // at the top of their own step, which halves their register footprint.
-template <int U, int NM, bool ADBL, int TL = kTiles>
+// AS: element stride of the token rows per k (2 for the interleaved hi / lo rows, whose
+// 8-element chunks alternate).
+template <int U, int NM, bool ADBL, int TL = kTiles, int AS = 1>
 __device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[TL], int nt,
                                           const uint16_t* const (&brow)[NM], int K,
                                           floatx4 (&acc)[NM][TL]) {
@@ -102,7 +107,7 @@ __device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[TL], int
     for (int rt = 0; rt < TL; ++rt)
       if (rt < nt)
 #pragma unroll
-        for (int u = 0; u < U; ++u) x[rt][u] = load8(arow[rt] + 8 * u);
+        for (int u = 0; u < U; ++u) x[rt][u] = load8(arow[rt] + AS * 8 * u);
   }
 
   for (int kb = 0; kb < K; kb += KB) {
@@ -118,7 +123,7 @@ __device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[TL], int
         for (int rt = 0; rt < TL; ++rt)
           if (rt < nt)
 #pragma unroll
-            for (int u = 0; u < U; ++u) nx[rt][u] = load8(arow[rt] + kb + KB + 8 * u);
+            for (int u = 0; u < U; ++u) nx[rt][u] = load8(arow[rt] + AS * (kb + KB + 8 * u));
       }
     }
     if (!ADBL) {
@@ -126,7 +131,7 @@ __device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[TL], int
       for (int rt = 0; rt < TL; ++rt)
         if (rt < nt)
 #pragma unroll
-          for (int u = 0; u < U; ++u) x[rt][u] = load8(arow[rt] + kb + 8 * u);
+          for (int u = 0; u < U; ++u) x[rt][u] = load8(arow[rt] + AS * (kb + 8 * u));
     }
 #pragma unroll
     for (int u = 0; u < U; ++u)
@@ -152,7 +157,7 @@ __device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[TL], int
 
 // wave_pass with FP8 weights: the B operand comes from E4M3 codes (8 bytes per lane and
 // MFMA), prefetched one step ahead as raw bytes and converted to bf16 just before use.
-template <int U, int NM, int TL = kTiles>
+template <int U, int NM, int TL = kTiles, int AS = 1>
 __device__ __forceinline__ void wave_pass_q8(const uint16_t* const (&arow)[TL], int nt,
                                              const uint8_t* const (&brow)[NM], int K,
                                              floatx4 (&acc)[NM][TL]) {
@@ -176,7 +181,7 @@ __device__ __forceinline__ void wave_pass_q8(const uint16_t* const (&arow)[TL], 
     for (int rt = 0; rt < TL; ++rt)
       if (rt < nt)
 #pragma unroll
-        for (int u = 0; u < U; ++u) x[rt][u] = load8(arow[rt] + kb + 8 * u);
+        for (int u = 0; u < U; ++u) x[rt][u] = load8(arow[rt] + AS * (kb + 8 * u));
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
@@ -309,7 +314,7 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
           const float h1 = acc[0][rt][i] * sc1, h3 = acc[1][rt][i] * sc3;
           const size_t at = (size_t)(p0 + t) * f + j0 + n;
           if (!kSplit) {
-            store_hilo(a.h, a.hlo, at, h1 / (1.0f + __expf(-h1)) * h3);
+            store_hilo(a.h, p0 + t, j0 + n, f, h1 / (1.0f + __expf(-h1)) * h3);
           } else {
             float* const part = a.gpart + 2 * blockIdx.z * plane;
             part[at] = h1;
@@ -336,7 +341,7 @@ __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
   const int Ks = f / a.splits;                 // this block's part of the reduction
   const size_t k0 = (size_t)blockIdx.z * Ks + (size_t)g * 8 * U;
   float* const ypart = a.yslot + (size_t)blockIdx.z * a.rows * d;
-  const uint16_t* const hsrc = n < 8 ? a.h : a.hlo;   // A rows 0-7: hi, rows 8-15: lo
+  const int lo_off = n < 8 ? 0 : 8;                    // A rows 0-7: hi, rows 8-15: lo
   size_t wrow[NM];
   float sc[NM];                                        // FP8 per-row scales (1 for bf16)
 #pragma unroll
@@ -352,7 +357,7 @@ __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
 #pragma unroll
     for (int rt = 0; rt < TL; ++rt) {
       const int t = min(c0 + rt * 8 + (n & 7), te - 1);
-      arow[rt] = hsrc + (size_t)(p0 + t) * f + k0;
+      arow[rt] = a.h + (size_t)(p0 + t) * 2 * f + 2 * k0 + lo_off;
     }
     floatx4 acc[NM][TL];
 #pragma unroll
@@ -363,12 +368,12 @@ __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
       const uint8_t* brow[NM];
 #pragma unroll
       for (int m = 0; m < NM; ++m) brow[m] = slot_q(a, sw, a.q2) + wrow[m];
-      wave_pass_q8<U, NM, TL>(arow, nt, brow, Ks, acc);
+      wave_pass_q8<U, NM, TL, 2>(arow, nt, brow, Ks, acc);
     } else {
       const uint16_t* brow[NM];
 #pragma unroll
       for (int m = 0; m < NM; ++m) brow[m] = slot_w(a, sw, a.w2, a.sw2) + wrow[m];
-      wave_pass<U, NM, XS_DOWN_ADBL != 0, TL>(arow, nt, brow, Ks, acc);
+      wave_pass<U, NM, XS_DOWN_ADBL != 0, TL, 2>(arow, nt, brow, Ks, acc);
     }
 #pragma unroll
     for (int rt = 0; rt < TL; ++rt) {
@@ -416,10 +421,10 @@ __global__ __launch_bounds__(kBlock) void gate_up_finish_kernel(FfnArgs a) {
     gs.x += gz.x; gs.y += gz.y; gs.z += gz.z; gs.w += gz.w;
     us.x += uz.x; us.y += uz.y; us.z += uz.z; us.w += uz.w;
   }
-  store_hilo(a.h, a.hlo, at + 0, gs.x / (1.0f + __expf(-gs.x)) * us.x);
-  store_hilo(a.h, a.hlo, at + 1, gs.y / (1.0f + __expf(-gs.y)) * us.y);
-  store_hilo(a.h, a.hlo, at + 2, gs.z / (1.0f + __expf(-gs.z)) * us.z);
-  store_hilo(a.h, a.hlo, at + 3, gs.w / (1.0f + __expf(-gs.w)) * us.w);
+  store_hilo(a.h, p, c + 0, a.f, gs.x / (1.0f + __expf(-gs.x)) * us.x);
+  store_hilo(a.h, p, c + 1, a.f, gs.y / (1.0f + __expf(-gs.y)) * us.y);
+  store_hilo(a.h, p, c + 2, a.f, gs.z / (1.0f + __expf(-gs.z)) * us.z);
+  store_hilo(a.h, p, c + 3, a.f, gs.w / (1.0f + __expf(-gs.w)) * us.w);
 }
 
 __global__ __launch_bounds__(kBlock) void combine_kernel(FfnArgs a) {

@@ -123,8 +123,9 @@ struct FfnLayout {
   int gu_splits;  // K-splits of the gate/up GEMM
   int splits;     // K-splits of the down GEMM
   size_t gpart;   // fp32 [gu_splits, 2, rows, f] gate and up partial sums (gu_splits > 1)
-  size_t h;       // bf16 [rows, f]             SwiGLU hidden rows, rounded to bf16 (hi)
-  size_t hlo;     // bf16 [rows, f]             their rounding remainders (lo), H ~ hi + lo
+  size_t h;       // bf16 [rows, 2f]            SwiGLU hidden rows as hi = bf16(H) and
+                  //                            lo = bf16(H - hi), interleaved in 8-element
+                  //                            chunks: row p holds hi(c..c+7), lo(c..c+7), ...
   size_t y;       // fp32 [splits, rows, d]     per-row partial expert outputs
   size_t total;
 };
@@ -140,8 +141,7 @@ inline FfnLayout ffn_layout(int T, int N, int k, bool dense, int d, int f, int e
   size_t o = L.route.total;
   L.gpart = o;
   if (L.gu_splits > 1) o += align256(sizeof(float) * 2 * size_t(L.gu_splits) * rows * size_t(f));
-  L.h = o; o += align256(sizeof(uint16_t) * rows * size_t(f));
-  L.hlo = o; o += align256(sizeof(uint16_t) * rows * size_t(f));
+  L.h = o; o += align256(sizeof(uint16_t) * rows * 2 * size_t(f));
   L.y = o; o += align256(sizeof(float) * size_t(L.splits) * rows * size_t(d));
   L.total = o;
   return L;
@@ -228,8 +228,7 @@ struct FfnArgs {
   const int32_t* counters;
   const int32_t* ids;
   const float* w;
-  uint16_t* h;                 // hidden rows, bf16 hi part
-  uint16_t* hlo;               // hidden rows, bf16 lo part (H - hi rounded to bf16)
+  uint16_t* h;                 // hidden rows, bf16 hi and lo interleaved per 8 elements
   float* yslot;
   uint16_t* y;
 };
