@@ -61,29 +61,34 @@ __device__ __forceinline__ float unord(uint32_t k) {
   return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
 }
 
-template <int Ctrl, int RowMask>
+// One DPP step of a reduction: the value of the lane that Ctrl names, or the reduction's
+// identity in rows outside RowMask.  With the identity as the "old" operand the compiler
+// folds the move into the reducing instruction (one v_max_u32_dpp / v_min_u32_dpp per step
+// instead of two moves and the max).
+template <int Ctrl, int RowMask, uint32_t Identity>
 __device__ __forceinline__ uint32_t dpp(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, Ctrl, RowMask, 0xF, false);
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)Identity, (int)v, Ctrl, RowMask, 0xF, false);
 }
 
 // Wave-wide max / min of a uint32 with DPP (quad swaps, row mirrors, row broadcasts);
 // lane 63 ends with the result, which is returned to every lane.
 __device__ __forceinline__ uint32_t wave_max(uint32_t v) {
-  v = max(v, dpp<0xB1, 0xF>(v));   // quad_perm [1,0,3,2]
-  v = max(v, dpp<0x4E, 0xF>(v));   // quad_perm [2,3,0,1]
-  v = max(v, dpp<0x141, 0xF>(v));  // row_half_mirror
-  v = max(v, dpp<0x140, 0xF>(v));  // row_mirror
-  v = max(v, dpp<0x142, 0xA>(v));  // row_bcast:15
-  v = max(v, dpp<0x143, 0xC>(v));  // row_bcast:31
+  v = max(v, dpp<0xB1, 0xF, 0u>(v));   // quad_perm [1,0,3,2]
+  v = max(v, dpp<0x4E, 0xF, 0u>(v));   // quad_perm [2,3,0,1]
+  v = max(v, dpp<0x141, 0xF, 0u>(v));  // row_half_mirror
+  v = max(v, dpp<0x140, 0xF, 0u>(v));  // row_mirror
+  v = max(v, dpp<0x142, 0xA, 0u>(v));  // row_bcast:15
+  v = max(v, dpp<0x143, 0xC, 0u>(v));  // row_bcast:31
   return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 __device__ __forceinline__ uint32_t wave_min(uint32_t v) {
-  v = min(v, dpp<0xB1, 0xF>(v));
-  v = min(v, dpp<0x4E, 0xF>(v));
-  v = min(v, dpp<0x141, 0xF>(v));
-  v = min(v, dpp<0x140, 0xF>(v));
-  v = min(v, dpp<0x142, 0xA>(v));
-  v = min(v, dpp<0x143, 0xC>(v));
+  constexpr uint32_t kId = 0xFFFFFFFFu;
+  v = min(v, dpp<0xB1, 0xF, kId>(v));
+  v = min(v, dpp<0x4E, 0xF, kId>(v));
+  v = min(v, dpp<0x141, 0xF, kId>(v));
+  v = min(v, dpp<0x140, 0xF, kId>(v));
+  v = min(v, dpp<0x142, 0xA, kId>(v));
+  v = min(v, dpp<0x143, 0xC, kId>(v));
   return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
@@ -179,20 +184,6 @@ template <int Q>
 __device__ __forceinline__ void copy_keys(uint32_t (&dst)[Q], const uint32_t (&src)[Q]) {
 #pragma unroll
   for (int q = 0; q < Q; ++q) dst[q] = src[q];
-}
-
-// Register cache of up to C tokens' keys per wave, addressed by a run-time slot.
-template <int C, int Q>
-__device__ __forceinline__ void cache_put(uint32_t (&kc)[C][Q], int slot, const uint32_t (&key)[Q]) {
-#pragma unroll
-  for (int c = 0; c < C; ++c)
-    if (c == slot) copy_keys<Q>(kc[c], key);
-}
-template <int C, int Q>
-__device__ __forceinline__ void cache_get(const uint32_t (&kc)[C][Q], int slot, uint32_t (&key)[Q]) {
-#pragma unroll
-  for (int c = 0; c < C; ++c)
-    if (c == slot) copy_keys<Q>(key, kc[c]);
 }
 
 // Block-wide exclusive prefix sum of one int per thread; every thread must call it.
@@ -343,22 +334,23 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   //      The next token's row is loaded while the current one is ranked; for batches of
   //      up to four tokens per wave the keys left after the top-k (all experts but the
   //      token's top-k) stay in registers for the refinement.
-  constexpr int kCache = 4;
+  // tokens per wave whose keys stay in registers (1024 threads allow 128 VGPRs each)
+  constexpr int kCache = Q <= 4 ? 4 : (Q <= 8 ? 2 : 1);
   const bool cached = T <= kCache * kWaves;
   uint32_t kc[kCache][Q];
   float raw_next[Q];
   if (wave < T) load_row<Q>(a, wave, lane, raw_next);
-  for (int i = wave, it = 0; i < T; i += kWaves, ++it) {
+  // Token i: its plain top-k, gates and entries; `left` receives the keys that remain
+  // after the top-k.  The wave's next row is loaded meanwhile.
+  auto plain_topk = [&](int i, uint32_t (&left)[Q]) {
     float raw[Q], v[Q];
-    uint32_t key[Q];
 #pragma unroll
     for (int q = 0; q < Q; ++q) raw[q] = raw_next[q];
     if (i + kWaves < T) load_row<Q>(a, i + kWaves, lane, raw_next);
-    row_keys<Q>(raw, N, lane, v, key);
+    row_keys<Q>(raw, N, lane, v, left);
     float my_h;
     int my_j;
-    wave_topk<Q>(key, 0, k, lane, my_h, my_j);
-    if (cached) cache_put<kCache, Q>(kc, it, key);
+    wave_topk<Q>(left, 0, k, lane, my_h, my_j);
     const float g = ranked_gate(my_h, lane, k);
     if (lane < k) {
       s_ent[i * k + lane] = (uint16_t)(my_j < 0 ? kNoEntry : (uint32_t)((lane << 10) | my_j));
@@ -379,6 +371,17 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
 #pragma unroll
       for (int q = 0; q < Q; ++q)
         if (lane + 64 * q < N) a.dense[(size_t)i * N + lane + 64 * q] = e[q] / z;
+    }
+  };
+  if (cached) {
+    // compile-time slots keep the cache in registers
+#pragma unroll
+    for (int it = 0; it < kCache; ++it)
+      if (wave + it * kWaves < T) plain_topk(wave + it * kWaves, kc[it]);
+  } else {
+    for (int i = wave; i < T; i += kWaves) {
+      uint32_t left[Q];
+      plain_topk(i, left);
     }
   }
   __syncthreads();
@@ -650,28 +653,10 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   // ---- (e) refinement: every token to its top-k inside S, gates renormalised (Section 3.4).
   //      The token's plain top-k experts that are in S are its first refined ranks (in
   //      their order); only the remaining ranks are searched, among the other experts.
-  if (!cached && wave < T) load_row<Q>(a, wave, lane, raw_next);
-  for (int i = wave, it = 0; i < T; i += kWaves, ++it) {
-    uint32_t key[Q];
+  // Token i: `key` holds its keys without its plain top-k.
+  auto refine = [&](int i, uint32_t (&key)[Q]) {
     const uint32_t vent = lane < k ? (uint32_t)s_ent[i * k + lane] : kNoEntry;
     const int vid = vent == kNoEntry ? -1 : (int)(vent & 1023u);
-    if (cached) {
-      cache_get<kCache, Q>(kc, it, key);
-    } else {
-      float raw[Q], v[Q];
-#pragma unroll
-      for (int q = 0; q < Q; ++q) raw[q] = raw_next[q];
-      if (i + kWaves < T) load_row<Q>(a, i + kWaves, lane, raw_next);
-      row_keys<Q>(raw, N, lane, v, key);
-      for (int r = 0; r < k; ++r) {     // the plain top-k is not searched again
-        const int vr = __builtin_amdgcn_readlane(vid, r);
-        if (vr >= 0 && (vr & 63) == lane) {
-#pragma unroll
-          for (int q = 0; q < Q; ++q)
-            if (q == (vr >> 6)) key[q] = 0;
-        }
-      }
-    }
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
       const int jq = lane + 64 * q;
@@ -697,6 +682,32 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
       a.ids[i * k + lane] = my_j;
       a.w[i * k + lane] = g;
       s_ent[i * k + lane] = (uint16_t)(my_j < 0 ? kNoEntry : (uint32_t)((lane << 10) | my_j));
+    }
+  };
+  if (cached) {
+#pragma unroll
+    for (int it = 0; it < kCache; ++it)
+      if (wave + it * kWaves < T) refine(wave + it * kWaves, kc[it]);
+  } else {
+    if (wave < T) load_row<Q>(a, wave, lane, raw_next);
+    for (int i = wave; i < T; i += kWaves) {
+      float raw[Q], v[Q];
+      uint32_t key[Q];
+#pragma unroll
+      for (int q = 0; q < Q; ++q) raw[q] = raw_next[q];
+      if (i + kWaves < T) load_row<Q>(a, i + kWaves, lane, raw_next);
+      row_keys<Q>(raw, N, lane, v, key);
+      const uint32_t vent = lane < k ? (uint32_t)s_ent[i * k + lane] : kNoEntry;
+      const int vid = vent == kNoEntry ? -1 : (int)(vent & 1023u);
+      for (int r = 0; r < k; ++r) {     // the plain top-k is not searched again
+        const int vr = __builtin_amdgcn_readlane(vid, r);
+        if (vr >= 0 && (vr & 63) == lane) {
+#pragma unroll
+          for (int q = 0; q < Q; ++q)
+            if (q == (vr >> 6)) key[q] = 0;
+        }
+      }
+      refine(i, key);
     }
   }
   __syncthreads();
