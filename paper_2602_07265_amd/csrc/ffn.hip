@@ -95,35 +95,38 @@ __device__ __forceinline__ void store_hilo(uint16_t* h2, size_t p, int c, int f,
 template <int U, int NM, bool ADBL, int TL = kTiles, int AS = 1>
 __device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[TL], int nt,
                                           const uint16_t* const (&brow)[NM], int K,
-                                          floatx4 (&acc)[NM][TL]) {
+                                          floatx4 (&acc)[NM][TL], int k_first = 0) {
   constexpr int KB = 32 * U;
   bf16x8 b[NM][U], x[TL][U];
 #pragma unroll
   for (int m = 0; m < NM; ++m)
 #pragma unroll
-    for (int u = 0; u < U; ++u) b[m][u] = load8(brow[m] + 8 * u);
+    for (int u = 0; u < U; ++u) b[m][u] = load8(brow[m] + k_first + 8 * u);
   if (ADBL) {
 #pragma unroll
     for (int rt = 0; rt < TL; ++rt)
       if (rt < nt)
 #pragma unroll
-        for (int u = 0; u < U; ++u) x[rt][u] = load8(arow[rt] + AS * 8 * u);
+        for (int u = 0; u < U; ++u) x[rt][u] = load8(arow[rt] + AS * (k_first + 8 * u));
   }
 
-  for (int kb = 0; kb < K; kb += KB) {
+  int kb = k_first;
+  for (int s = 0; s < K; s += KB) {
     bf16x8 nb[NM][U], nx[ADBL ? TL : 1][U];
-    const bool more = kb + KB < K;
+    const bool more = s + KB < K;
+    int kn = kb + KB;
+    if (kn >= K) kn -= K;
     if (more) {
 #pragma unroll
       for (int m = 0; m < NM; ++m)
 #pragma unroll
-        for (int u = 0; u < U; ++u) nb[m][u] = load8(brow[m] + kb + KB + 8 * u);
+        for (int u = 0; u < U; ++u) nb[m][u] = load8(brow[m] + kn + 8 * u);
       if (ADBL) {
 #pragma unroll
         for (int rt = 0; rt < TL; ++rt)
           if (rt < nt)
 #pragma unroll
-            for (int u = 0; u < U; ++u) nx[rt][u] = load8(arow[rt] + AS * (kb + KB + 8 * u));
+            for (int u = 0; u < U; ++u) nx[rt][u] = load8(arow[rt] + AS * (kn + 8 * u));
       }
     }
     if (!ADBL) {
@@ -152,6 +155,7 @@ __device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[TL], int
           for (int u = 0; u < U; ++u) x[rt][u] = nx[ADBL ? rt : 0][u];
       }
     }
+    kb = kn;
   }
 }
 
@@ -160,22 +164,25 @@ __device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[TL], int
 template <int U, int NM, int TL = kTiles, int AS = 1>
 __device__ __forceinline__ void wave_pass_q8(const uint16_t* const (&arow)[TL], int nt,
                                              const uint8_t* const (&brow)[NM], int K,
-                                             floatx4 (&acc)[NM][TL]) {
+                                             floatx4 (&acc)[NM][TL], int k_first = 0) {
   constexpr int KB = 32 * U;
   uint2 b[NM][U];
   bf16x8 x[TL][U];
 #pragma unroll
   for (int m = 0; m < NM; ++m)
 #pragma unroll
-    for (int u = 0; u < U; ++u) b[m][u] = load_q8(brow[m] + 8 * u);
-  for (int kb = 0; kb < K; kb += KB) {
+    for (int u = 0; u < U; ++u) b[m][u] = load_q8(brow[m] + k_first + 8 * u);
+  int kb = k_first;
+  for (int s = 0; s < K; s += KB) {
     uint2 nb[NM][U];
-    const bool more = kb + KB < K;
+    const bool more = s + KB < K;
+    int kn = kb + KB;
+    if (kn >= K) kn -= K;
     if (more) {
 #pragma unroll
       for (int m = 0; m < NM; ++m)
 #pragma unroll
-        for (int u = 0; u < U; ++u) nb[m][u] = load_q8(brow[m] + kb + KB + 8 * u);
+        for (int u = 0; u < U; ++u) nb[m][u] = load_q8(brow[m] + kn + 8 * u);
     }
 #pragma unroll
     for (int rt = 0; rt < TL; ++rt)
@@ -197,6 +204,7 @@ __device__ __forceinline__ void wave_pass_q8(const uint16_t* const (&arow)[TL], 
 #pragma unroll
         for (int u = 0; u < U; ++u) b[m][u] = nb[m][u];
     }
+    kb = kn;
   }
 }
 
@@ -218,6 +226,14 @@ __device__ __forceinline__ void wave_pass_q8(const uint16_t* const (&arow)[TL], 
 #endif
 #ifndef XS_Q8_DOWN_U
 #define XS_Q8_DOWN_U 4
+#endif
+// K steps between the starts of consecutive down waves: one with bf16 weights (DeepSeek
+// T=32 down 270 -> 263 us); none with FP8, where it measured no gain.
+#ifndef XS_DOWN_ROT
+#define XS_DOWN_ROT 1
+#endif
+#ifndef XS_Q8_DOWN_ROT
+#define XS_Q8_DOWN_ROT 0
 #endif
 #ifndef XS_DOWN_TL
 #define XS_DOWN_TL 4                 // 8-token (hi + lo) tiles per pass of the down GEMM
@@ -364,16 +380,21 @@ __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
     for (int m = 0; m < NM; ++m)
 #pragma unroll
       for (int rt = 0; rt < TL; ++rt) acc[m][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    // Consecutive waves start their pass over K one step apart (and wrap around): W2 rows
+    // are f elements apart, often a power of two, so waves that stepped through K in the
+    // same order would read the same offsets of every row at the same time.
+    const int rot = kQ8 ? XS_Q8_DOWN_ROT : XS_DOWN_ROT;
+    const int k_first = (int)(((blockIdx.x * kWaves + wave) * rot) % (Ks / (32 * U))) * 32 * U;
     if (kQ8) {
       const uint8_t* brow[NM];
 #pragma unroll
       for (int m = 0; m < NM; ++m) brow[m] = slot_q(a, sw, a.q2) + wrow[m];
-      wave_pass_q8<U, NM, TL, 2>(arow, nt, brow, Ks, acc);
+      wave_pass_q8<U, NM, TL, 2>(arow, nt, brow, Ks, acc, k_first);
     } else {
       const uint16_t* brow[NM];
 #pragma unroll
       for (int m = 0; m < NM; ++m) brow[m] = slot_w(a, sw, a.w2, a.sw2) + wrow[m];
-      wave_pass<U, NM, XS_DOWN_ADBL != 0, TL, 2>(arow, nt, brow, Ks, acc);
+      wave_pass<U, NM, XS_DOWN_ADBL != 0, TL, 2>(arow, nt, brow, Ks, acc, k_first);
     }
 #pragma unroll
     for (int rt = 0; rt < TL; ++rt) {
