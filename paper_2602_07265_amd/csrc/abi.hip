@@ -131,7 +131,7 @@ xs::RouteArgs route_args(const float* logits, int32_t T, const xshare_route_para
   a.stats = reinterpret_cast<int32_t*>(stats);
   a.offsets = at<int32_t>(ws, L.offsets);
   a.perm = at<int32_t>(ws, L.perm);
-  a.active = at<int32_t>(ws, L.active);
+  a.active = at<int4>(ws, L.active);
   a.counters = at<int32_t>(ws, L.counters);
   a.dense = p->score_mode == XSHARE_SCORE_DENSE ? at<float>(ws, L.dense) : nullptr;
   return a;

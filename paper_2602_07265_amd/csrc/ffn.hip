@@ -248,11 +248,13 @@ struct SlotWork {
 };
 
 __device__ __forceinline__ bool slot_work(const FfnArgs& a, int slot, SlotWork& w) {
+  // both loads are issued together; the record is used only below the count
   const int n_active = a.counters[kCntActive];
+  const int4 rec = a.active[slot < a.N ? slot : 0];
   if (slot < n_active) {
-    w.e = a.active[slot];
-    w.p0 = a.offsets[w.e];
-    w.te = a.offsets[w.e + 1] - w.p0;
+    w.e = rec.x;
+    w.p0 = rec.y;
+    w.te = rec.z;
     w.shared = false;
     return true;
   }

@@ -28,7 +28,8 @@ enum Counter : int {
 struct RouteLayout {
   size_t offsets;   // int32 [N + 1]   exclusive prefix of tokens per expert (permuted order)
   size_t perm;      // int32 [T * k]   slot (i * k + r) of each permuted row
-  size_t active;    // int32 [N]       active experts, ascending
+  size_t active;    // int4 [N]        active experts, ascending: {expert, first permuted row,
+                    //                 rows, 0}, so a GEMM block finds its work in one load
   size_t counters;  // int32 [kCntCount]
   size_t dense;     // fp32 [T * N]    dense gates (score_mode DENSE only)
   size_t ids;       // int32 [T * k]   refined ids when the caller passes none
@@ -43,7 +44,7 @@ inline RouteLayout route_layout(int T, int N, int k, bool dense) {
   size_t o = 0;
   L.offsets = o;  o += align256(sizeof(int32_t) * (N + 1));
   L.perm = o;     o += align256(sizeof(int32_t) * tk);
-  L.active = o;   o += align256(sizeof(int32_t) * N);
+  L.active = o;   o += align256(4 * sizeof(int32_t) * N);
   L.counters = o; o += align256(sizeof(int32_t) * kCntCount);
   L.dense = o;    o += dense ? align256(sizeof(float) * size_t(T) * N) : 0;
   L.ids = o;      o += align256(sizeof(int32_t) * tk);
@@ -191,7 +192,7 @@ struct RouteArgs {
   int32_t* stats;              // nullable, xshare_stats layout (8 int32)
   int32_t* offsets;
   int32_t* perm;
-  int32_t* active;
+  int4* active;
   int32_t* counters;
   float* dense;
 };
@@ -224,7 +225,7 @@ struct FfnArgs {
   long rows;                   // T * k + n_shared * T hidden / output rows
   const int32_t* offsets;
   const int32_t* perm;
-  const int32_t* active;
+  const int4* active;
   const int32_t* counters;
   const int32_t* ids;
   const float* w;

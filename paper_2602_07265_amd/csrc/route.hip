@@ -752,7 +752,7 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   if (j < N) {
     a.offsets[j] = off;
     if (j == N - 1) a.offsets[N] = off + cnt;
-    if (listed) a.active[arank] = j;
+    if (listed) a.active[arank] = make_int4(j, off, cnt, 0);
   }
   if (tid == 0) {
     a.counters[kCntActive] = n_active;
