@@ -78,6 +78,10 @@ def parse():
                          "and shared experts (xshare_moe_layer)")
     ap.add_argument("--shared", type=int, default=None,
                     help="shared experts with --full-layer (default: 1 for DeepSeek shapes, else 0)")
+    ap.add_argument("--layers", type=int, default=0,
+                    help="L > 0: a pass over L MoE layers sharing the global budget K")
+    ap.add_argument("--global-budget", type=int, default=None,
+                    help="K (with --layers; default: the workload's M times L)")
     return ap.parse_args()
 
 
@@ -128,6 +132,8 @@ def main():
         return run_ep(args, W, X, np, torch)
     if args.full_layer:
         return run_full(args, W, X, np, torch)
+    if args.layers > 0:
+        return run_pass(args, W, X, np, torch)
     dev = "cuda:0"
     cfg = dict(W.CONFIGS[args.workload])
     T, N, k, d, f = cfg["T"], cfg["N"], cfg["k"], cfg["d"], cfg["f"]
@@ -390,6 +396,102 @@ def run_full(args, W, X, np, torch):
         "layer_frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
         "stages_us": {kk: round(v * 1e3, 2) for kk, v in stage_ms.items()},
         "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def run_pass(args, W, X, np, torch):
+    """The MoE layers of one forward pass sharing a global budget K (Section 3.2): L layers,
+    each with its own seeded logits and the uniform budget m_l = K / L, and a device ledger
+    that totals sum_l |S_l|.  One step is the whole pass; two weight sets alternate between
+    layers (a layer's 48 experts already far exceed the Infinity Cache)."""
+    dev = "cuda:0"
+    cfg = dict(W.CONFIGS[args.workload])
+    if cfg["logits"] == "spec":
+        raise SystemExit("--layers takes a flat workload")
+    T, N, k, d, f, k0 = cfg["T"], cfg["N"], cfg["k"], cfg["d"], cfg["f"], cfg["k0"]
+    L, nb = args.layers, args.batches
+    K = args.global_budget if args.global_budget is not None else cfg["M"] * L
+    m = X.layer_budgets(K, L)
+    print(f"[bench] {args.workload}: pass of {L} layers, K={K} (m_l {min(m)}..{max(m)})",
+          file=sys.stderr, flush=True)
+    wsets = [W.expert_weights(N, d, f, 0, dev)]
+    wsets.append(tuple(t.clone() for t in wsets[0]))
+    logits = [[torch.from_numpy(W.make_logits(cfg, 1000 * l + b)[0]).to(dev) for b in range(nb)]
+              for l in range(L)]
+    xs = [W.activations(T, d, b, dev) for b in range(nb)]
+    y = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
+    p = X.params(N, k, k0, max(m), "total")
+    ws = torch.empty(max(X.moe_workspace_bytes(T, d, f, p),
+                         X.moe_workspace_bytes(T, d, f, X.params(N, k, 0, N, "extra"))),
+                     dtype=torch.uint8, device=dev)
+    led = X.new_ledger(dev)
+
+    def one_pass(b, vanilla=False, ledger=None, **kw):
+        for l in range(L):
+            wset = wsets[l % 2]
+            if vanilla:
+                X.moe_forward(xs[b], logits[l][b], *wset, k, 0, N, "extra", y=y, workspace=ws,
+                              ledger=ledger, **kw)
+            else:
+                X.moe_forward(xs[b], logits[l][b], *wset, k, k0, max(m[l], k), "total", y=y,
+                              workspace=ws, ledger=ledger, **kw)
+
+    totals, totals_v = [], []
+    for b in range(nb):
+        led.zero_()
+        one_pass(b, ledger=led, routing_out=False)
+        totals.append(X.ledger_dict(led))
+        led.zero_()
+        one_pass(b, vanilla=True, ledger=led, routing_out=False)
+        totals_v.append(X.ledger_dict(led))
+    stream = torch.cuda.current_stream()
+
+    def timed(vanilla):
+        for s in range(args.warmup):
+            one_pass(s % nb, vanilla, routing_out=False)
+        torch.cuda.synchronize()
+        e0, e1 = X.HipEvent(), X.HipEvent()
+        e0.record(stream)
+        for s in range(args.steps):
+            one_pass(s % nb, vanilla, ledger=None if vanilla else led, routing_out=False)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_ms(e1) / args.steps
+
+    ms = timed(False)
+    ms_v = None if args.no_vanilla else timed(True)
+    act = float(np.mean([t["active"] for t in totals]))
+    gbs = (act * 3 * f * d * 2 + L * (T * d * 4 + T * N * 4)) / (ms * 1e-3) / 1e9
+    out = {
+        "metric": "MoE layers of a forward pass under a global expert budget K: us per pass "
+                  "+ HBM GB/s; sum of |S_l| against K",
+        "value": round(ms * 1e3, 1),
+        "unit": "us",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}_pass_L{L}_K{K}_k0{k0}", "layers": L,
+                   "global_budget": K, "layer_budgets": [min(m), max(m)], "tokens": T,
+                   "n_experts": N, "top_k": k, "d_model": d, "d_ffn": f, "warmup_k0": k0,
+                   "logits": "per layer: " + LOGITS_RECIPE[cfg["logits"]].format(Q=cfg.get("Q")),
+                   "batches_rotated": nb, "weight_sets": 2},
+        "us_per_layer": round(ms * 1e3 / L, 2),
+        "hbm_gbs": round(gbs, 1),
+        "selected_per_pass": round(float(np.mean([t["selected"] for t in totals])), 2),
+        "selected_per_pass_max": int(max(t["selected"] for t in totals)),
+        "active_per_pass": round(act, 2),
+        "vanilla_active_per_pass": round(float(np.mean([t["active"] for t in totals_v])), 2),
+        "vanilla_us_per_pass": None if ms_v is None else round(ms_v * 1e3, 1),
+        "speedup_vs_vanilla": None if ms_v is None else round(ms_v / ms, 3),
+        "ledger_layers": int(totals[0]["layers"]),
+        "cpu_baseline": None,
     }
     print(json.dumps(out), flush=True)
 

@@ -78,6 +78,23 @@ enum {
                              * order); every expert is a candidate                           */
 };
 
+/*
+ * Running totals over the MoE layers of one forward pass (Section 3.2: the layers share a
+ * global budget K, sum_l |S_l| <= K).  DEVICE memory owned by the caller, who zeroes it at
+ * the start of a pass; each call whose params name it adds its own counts at the end of its
+ * selection kernel (one thread, a plain read-modify-write: calls that share a ledger must
+ * be ordered, e.g. issued on one stream).
+ */
+typedef struct {
+  int32_t layers;           /* calls that added to the ledger                               */
+  int32_t selected;         /* sum of |S_l|                                                 */
+  int32_t active;           /* sum of the experts whose weights the calls streamed          */
+  int32_t vanilla_union;    /* sum of |U_l|: what plain top-k routing would have activated  */
+  int32_t invalid;          /* calls that selected nothing (invalid offsets or group map)   */
+  int32_t max_selected;     /* largest |S_l| of a call                                      */
+  int32_t reserved[2];
+} xshare_budget_ledger;
+
 typedef struct {
   int32_t n_experts;          /* N: routed experts of the layer                             */
   int32_t top_k;              /* k: experts per token (Section 2.2)                         */
@@ -91,6 +108,7 @@ typedef struct {
                                * set's scores in ranking order, then each added expert's, all *
                                * fp32; the target tau * f(E) is one fp32 product; the starting *
                                * set is never cut; tau > 1 takes every candidate              */
+  xshare_budget_ledger* ledger; /* nullable DEVICE: this call's counts are added to it       */
 } xshare_route_params;
 
 /* Per-call statistics, written to DEVICE memory by the kernels.                          */
@@ -328,6 +346,17 @@ xshare_status xshare_moe_layer(const uint16_t* x, const uint16_t* w_gate, int32_
                                uint8_t* sel_mask, int32_t* topk_ids, float* topk_w,
                                xshare_stats* stats, void* ws, size_t ws_bytes,
                                void* const* stage_events, hipStream_t stream);
+
+/*
+ * Uniform per-layer budgets for a global budget of K experts over L MoE layers (the uniform
+ * allocation m_l = K / L of Section 3.2): m[l] = floor(K / L) + (l < K mod L ? 1 : 0), so
+ * the budgets sum to exactly K and differ by at most one (when L divides K every layer gets
+ * K / L).  Each m[l] is then a layer's XSHARE_BUDGET_TOTAL budget; a layer still selects at
+ * least k experts, so the pass exceeds K when K / L < k (the ledger shows it).
+ *   m   HOST [L] int32 output.   XSHARE_EINVAL if L < 1, K < 0 or m is NULL.
+ * Host only: enqueues nothing.
+ */
+xshare_status xshare_layer_budgets(int32_t K, int32_t L, int32_t* m);
 
 /* Static description of a status code (never NULL).                                      */
 const char* xshare_status_string(int32_t status);

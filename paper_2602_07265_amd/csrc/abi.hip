@@ -129,6 +129,7 @@ xs::RouteArgs route_args(const float* logits, int32_t T, const xshare_route_para
   a.ids = ids ? ids : at<int32_t>(ws, L.ids);
   a.w = w ? w : at<float>(ws, L.w);
   a.stats = reinterpret_cast<int32_t*>(stats);
+  a.ledger = reinterpret_cast<int32_t*>(p->ledger);
   a.offsets = at<int32_t>(ws, L.offsets);
   a.perm = at<int32_t>(ws, L.perm);
   a.active = at<int4>(ws, L.active);
@@ -456,6 +457,13 @@ xshare_status xshare_router_logits(const uint16_t* x, const uint16_t* w_gate, in
   const xs::RouterArgs r{x, w_gate, T, d, n_experts, xs::router_parts(T, d, n_experts),
                          static_cast<float*>(ws), logits};
   return xs::launch_router(r, stream) == hipSuccess ? XSHARE_OK : XSHARE_EHIP;
+}
+
+xshare_status xshare_layer_budgets(int32_t K, int32_t L, int32_t* m) {
+  if (L < 1 || K < 0 || !m) return XSHARE_EINVAL;
+  const int32_t base = K / L, extra = K % L;
+  for (int32_t l = 0; l < L; ++l) m[l] = base + (l < extra ? 1 : 0);
+  return XSHARE_OK;
 }
 
 const char* xshare_status_string(int32_t status) {

@@ -190,6 +190,7 @@ struct RouteArgs {
   int32_t* ids;
   float* w;
   int32_t* stats;              // nullable, xshare_stats layout (8 int32)
+  int32_t* ledger;             // nullable, xshare_budget_ledger layout (8 int32), accumulated
   int32_t* offsets;
   int32_t* perm;
   int4* active;

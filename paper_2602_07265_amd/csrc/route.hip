@@ -325,6 +325,10 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
           a.stats[0] = -1;
           for (int s = 1; s < 8; ++s) a.stats[s] = 0;
         }
+        if (a.ledger) {
+          a.ledger[0] += 1;
+          a.ledger[4] += 1;
+        }
       }
       return;
     }
@@ -767,6 +771,13 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
       a.stats[5] = m_eff;
       a.stats[6] = max_load;
       a.stats[7] = 0;
+    }
+    if (a.ledger) {   // running totals over the layers of a pass (global budget K)
+      a.ledger[0] += 1;
+      a.ledger[1] += s_cnt[4];
+      a.ledger[2] += n_active;
+      a.ledger[3] += n_u;
+      a.ledger[5] = max(a.ledger[5], s_cnt[4]);
     }
   }
 }

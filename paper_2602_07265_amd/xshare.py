@@ -32,6 +32,7 @@ class RouteParams(ctypes.Structure):
         ("score_mode", ctypes.c_int32),
         ("per_request_budget", ctypes.c_int32),
         ("threshold", ctypes.c_float),
+        ("ledger", ctypes.c_void_p),
     ]
 
 
@@ -119,6 +120,8 @@ def lib() -> ctypes.CDLL:
         L.xshare_status_string.restype = ctypes.c_char_p
         L.xshare_version.argtypes = []
         L.xshare_version.restype = ctypes.c_char_p
+        L.xshare_layer_budgets.argtypes = [_I32, _I32, _P]
+        L.xshare_layer_budgets.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -132,12 +135,37 @@ def version() -> str:
 
 
 def params(n_experts: int, top_k: int, warmup_k0: int, budget: int, budget_mode="total",
-           score_mode="topk", per_request_budget: int = 0, threshold: float = 0.0) -> RouteParams:
-    """``threshold`` is tau of the "threshold" budget mode (Algorithm 1's stopping rule)."""
+           score_mode="topk", per_request_budget: int = 0, threshold: float = 0.0,
+           ledger=None) -> RouteParams:
+    """``threshold`` is tau of the "threshold" budget mode (Algorithm 1's stopping rule);
+    ``ledger`` an optional device int32 tensor of LEDGER_FIELDS' length that the call adds
+    its counts to."""
+    if ledger is not None:
+        _dev(ledger, torch.int32, (len(LEDGER_FIELDS) + 2,), "ledger")
     return RouteParams(int(n_experts), int(top_k), int(warmup_k0), int(budget),
                        BUDGET[budget_mode] if isinstance(budget_mode, str) else int(budget_mode),
                        SCORE[score_mode] if isinstance(score_mode, str) else int(score_mode),
-                       int(per_request_budget), float(threshold))
+                       int(per_request_budget), float(threshold),
+                       None if ledger is None else ledger.data_ptr())
+
+
+LEDGER_FIELDS = ("layers", "selected", "active", "vanilla_union", "invalid", "max_selected")
+
+
+def new_ledger(device="cuda") -> torch.Tensor:
+    """A zeroed budget ledger (xshare_budget_ledger) in device memory."""
+    return torch.zeros(len(LEDGER_FIELDS) + 2, dtype=torch.int32, device=device)
+
+
+def ledger_dict(ledger: torch.Tensor) -> dict:
+    return dict(zip(LEDGER_FIELDS, ledger.to("cpu").tolist()))
+
+
+def layer_budgets(K: int, L: int) -> list:
+    """Uniform per-layer budgets m_l for a global budget K over L layers (host call)."""
+    m = (ctypes.c_int32 * max(int(L), 1))()
+    _check(lib().xshare_layer_budgets(int(K), int(L), m), "xshare_layer_budgets")
+    return [int(v) for v in m[:int(L)]]
 
 
 def route_workspace_bytes(T: int, p: RouteParams) -> int:
@@ -291,13 +319,13 @@ def _route_impl(logits, p, req_offsets, out, workspace, stream):
 
 
 def select_ep(logits: torch.Tensor, groups: GroupMap, top_k: int, warmup_k0: int,
-              per_group_budget: int, score_mode="topk", *, out=None, workspace=None,
-              stream=None) -> dict:
+              per_group_budget: int, score_mode="topk", *, ledger=None, out=None,
+              workspace=None, stream=None) -> dict:
     """Algorithms 5-6 on the GPU: dict(sel_mask, ids, w, stats, group_load)."""
     T, N = logits.shape
     dev = logits.device
     _dev(logits, torch.float32, (T, N), "logits")
-    p = params(N, top_k, warmup_k0, per_group_budget, "per_group", score_mode)
+    p = params(N, top_k, warmup_k0, per_group_budget, "per_group", score_mode, ledger=ledger)
     G = groups.layout.n_groups
     out = dict(out or {})
     sel = out.get("sel_mask") if out.get("sel_mask") is not None else torch.empty(N, dtype=torch.uint8, device=dev)
@@ -320,26 +348,29 @@ def select_ep(logits: torch.Tensor, groups: GroupMap, top_k: int, warmup_k0: int
 
 
 def route(logits: torch.Tensor, top_k: int, warmup_k0: int, budget: int, budget_mode="total",
-          score_mode="topk", *, tau: float = 0.0, out=None, workspace=None, stream=None) -> dict:
+          score_mode="topk", *, tau: float = 0.0, ledger=None, out=None, workspace=None,
+          stream=None) -> dict:
     """Algorithm 2 on the GPU: returns dict(sel_mask, ids, w, stats) device tensors."""
-    p = params(logits.shape[1], top_k, warmup_k0, budget, budget_mode, score_mode, 0, tau)
+    p = params(logits.shape[1], top_k, warmup_k0, budget, budget_mode, score_mode, 0, tau,
+               ledger)
     return _route_impl(logits, p, None, out, workspace, stream)
 
 
 def select_hier(logits: torch.Tensor, req_offsets, top_k: int, warmup_k0: int,
                 per_request_budget: int, budget: int, budget_mode="total", score_mode="topk", *,
-                tau: float = 0.0, out=None, workspace=None, stream=None) -> dict:
+                tau: float = 0.0, ledger=None, out=None, workspace=None, stream=None) -> dict:
     """Algorithms 3-4 on the GPU; req_offsets as a host sequence (validated) or device tensor."""
     p = params(logits.shape[1], top_k, warmup_k0, budget, budget_mode, score_mode,
-               per_request_budget, tau)
+               per_request_budget, tau, ledger)
     return _route_impl(logits, p, req_offsets, out, workspace, stream)
 
 
 def moe_forward(x: torch.Tensor, logits: torch.Tensor, w1: torch.Tensor, w3: torch.Tensor,
                 w2: torch.Tensor, top_k: int, warmup_k0: int, budget: int, budget_mode="total",
                 score_mode="topk", *, req_offsets=None, per_request_budget: int = 0,
-                groups: GroupMap | None = None, tau: float = 0.0, shared=None, y=None,
-                routing_out=True, workspace=None, stage_events=None, stream=None) -> dict:
+                groups: GroupMap | None = None, tau: float = 0.0, shared=None, ledger=None,
+                y=None, routing_out=True, workspace=None, stage_events=None,
+                stream=None) -> dict:
     """The MoE layer: returns dict(y [T,d] bf16, and sel_mask/ids/w/stats if routing_out).
 
     With ``groups`` the selection is Algorithms 5-6 (``budget`` is m_g, budget_mode is
@@ -355,7 +386,8 @@ def moe_forward(x: torch.Tensor, logits: torch.Tensor, w1: torch.Tensor, w3: tor
     _dev(w2, torch.bfloat16, (N, d, f), "w2")
     if groups is not None:
         budget_mode = "per_group"
-    p = params(N, top_k, warmup_k0, budget, budget_mode, score_mode, per_request_budget, tau)
+    p = params(N, top_k, warmup_k0, budget, budget_mode, score_mode, per_request_budget, tau,
+               ledger)
     ep = None if groups is None else groups.layout
     sh = _shared(shared, d, f, dev)
     if y is None:
@@ -395,8 +427,8 @@ def moe_forward_fp8(x: torch.Tensor, logits: torch.Tensor, q1: torch.Tensor, q3:
                     q2: torch.Tensor, s1: torch.Tensor, s3: torch.Tensor, s2: torch.Tensor,
                     top_k: int, warmup_k0: int, budget: int, budget_mode="total",
                     score_mode="topk", *, req_offsets=None, per_request_budget: int = 0,
-                    groups: GroupMap | None = None, tau: float = 0.0, y=None, routing_out=True,
-                    workspace=None, stage_events=None, stream=None) -> dict:
+                    groups: GroupMap | None = None, tau: float = 0.0, ledger=None, y=None,
+                    routing_out=True, workspace=None, stage_events=None, stream=None) -> dict:
     """The MoE layer with FP8 E4M3FN expert weights (uint8 codes) and per-row fp32 scales."""
     T, d = x.shape
     N = logits.shape[1]
@@ -412,7 +444,8 @@ def moe_forward_fp8(x: torch.Tensor, logits: torch.Tensor, q1: torch.Tensor, q3:
     _dev(s2, torch.float32, (N, d), "w2 scales")
     if groups is not None:
         budget_mode = "per_group"
-    p = params(N, top_k, warmup_k0, budget, budget_mode, score_mode, per_request_budget, tau)
+    p = params(N, top_k, warmup_k0, budget, budget_mode, score_mode, per_request_budget, tau,
+               ledger)
     ep = None if groups is None else groups.layout
     if y is None:
         y = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
@@ -450,8 +483,9 @@ def moe_forward_fp8(x: torch.Tensor, logits: torch.Tensor, q1: torch.Tensor, q3:
 def moe_layer(x: torch.Tensor, w_gate: torch.Tensor, w1: torch.Tensor, w3: torch.Tensor,
               w2: torch.Tensor, top_k: int, warmup_k0: int, budget: int, budget_mode="total",
               score_mode="topk", *, shared=None, req_offsets=None, per_request_budget: int = 0,
-              groups: GroupMap | None = None, tau: float = 0.0, y=None, routing_out=True,
-              logits_out=True, workspace=None, stage_events=None, stream=None) -> dict:
+              groups: GroupMap | None = None, tau: float = 0.0, ledger=None, y=None,
+              routing_out=True, logits_out=True, workspace=None, stage_events=None,
+              stream=None) -> dict:
     """The whole layer from hidden states: router GEMM, selection, routed and shared experts.
     Returns dict(y, and logits/sel_mask/ids/w/stats as requested)."""
     T, d = x.shape
@@ -465,7 +499,8 @@ def moe_layer(x: torch.Tensor, w_gate: torch.Tensor, w1: torch.Tensor, w3: torch
     _dev(w2, torch.bfloat16, (N, d, f), "w2")
     if groups is not None:
         budget_mode = "per_group"
-    p = params(N, top_k, warmup_k0, budget, budget_mode, score_mode, per_request_budget, tau)
+    p = params(N, top_k, warmup_k0, budget, budget_mode, score_mode, per_request_budget, tau,
+               ledger)
     ep = None if groups is None else groups.layout
     sh = _shared(shared, d, f, dev)
     if y is None:

@@ -85,7 +85,7 @@ def _route(p, T=8, ws=FAKE, ws_bytes=1 << 30, logits=FAKE, mask=FAKE, ids=FAKE, 
 ])
 def test_route_parameter_validation(kw, status):
     base = dict(n_experts=16, top_k=2, warmup_k0=1, budget=8, budget_mode=0, score_mode=0,
-                per_request_budget=0, threshold=0.0)
+                per_request_budget=0, threshold=0.0, ledger=None)
     base.update(kw)
     p = X.RouteParams(*[base[f] for f, _ in X.RouteParams._fields_])
     assert _route(p, ws=None) == status             # valid parameters stop at the workspace
