@@ -11,6 +11,14 @@ FP8 expert weights (the paper is silent on precision): OCP FP8 E4M3FN codes
 (1 sign bit, 4 exponent bits with bias 7, 3 mantissa bits; exponent field 0 is
 subnormal, code 0x7F / 0xFF is NaN, no infinities, largest finite 448) with one
 fp32 scale per output row: w[r, c] = decode(q[r, c]) * scale[r].
+
+MXFP4 expert weights (OCP Microscaling formats, MXFP4): FP4 E2M1 element codes
+(1 sign bit, 2 exponent bits with bias 1, 1 mantissa bit; exponent field 0 is
+subnormal with value m / 2; no infinities or NaN; largest 6), two per byte with
+element 2c in the low nibble; every block of 32 consecutive elements of a row
+(along the input index, the reduction dimension) shares one E8M0 scale byte e,
+whose value is 2^(e - 127) (e = 255 is NaN):
+w[r, c] = decode(q[r, c]) * 2^(e[r, c // 32] - 127).
 """
 from __future__ import annotations
 
@@ -48,6 +56,41 @@ def dequant_rows(codes, scale) -> np.ndarray:
         _E4M3_VALUES = decode_e4m3(np.arange(256, dtype=np.uint8))
     return _E4M3_VALUES[np.asarray(codes, dtype=np.uint8)] * \
         np.asarray(scale, dtype=np.float32).astype(np.float64)[:, None]
+
+
+def decode_e2m1(codes) -> np.ndarray:
+    """FP4 E2M1 codes (low 4 bits of each value) -> float64 values."""
+    c = np.asarray(codes, dtype=np.uint8).astype(np.int64) & 15
+    sign = np.where(c >> 3, -1.0, 1.0)
+    e = (c >> 1) & 3
+    m = (c & 1).astype(np.float64)
+    v = np.where(e == 0, m / 2.0, (1.0 + m / 2.0) * np.exp2(e - 1.0))
+    return sign * v
+
+
+def decode_e8m0(codes) -> np.ndarray:
+    """E8M0 scale bytes -> float64 2^(e - 127) (NaN for 255)."""
+    e = np.asarray(codes, dtype=np.uint8).astype(np.int64)
+    return np.where(e == 255, np.nan, np.exp2(e - 127.0))
+
+
+_E2M1_VALUES = None
+
+
+def dequant_mx(packed, scales) -> np.ndarray:
+    """Weights of one MXFP4 matrix, float64 [rows, K] (exact): packed codes [rows, K / 2]
+    (element 2c in the low nibble of byte c), E8M0 scales [rows, K / 32]."""
+    global _E2M1_VALUES
+    if _E2M1_VALUES is None:
+        _E2M1_VALUES = decode_e2m1(np.arange(16, dtype=np.uint8))
+    b = np.asarray(packed, dtype=np.uint8)
+    rows, half = b.shape
+    codes = np.empty((rows, 2 * half), dtype=np.uint8)
+    codes[:, 0::2] = b & 15
+    codes[:, 1::2] = b >> 4
+    scale = decode_e8m0(scales)
+    assert scale.shape == (rows, 2 * half // 32), "one scale per 32 elements of a row"
+    return _E2M1_VALUES[codes] * np.repeat(scale, 32, axis=1)
 
 
 def _as_f64(w) -> np.ndarray:

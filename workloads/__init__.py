@@ -223,6 +223,51 @@ def expert_weights_fp8(N: int, d: int, f: int, seed: int, device="cpu", std: flo
     return (*q, *sc)
 
 
+def quantize_mx_e2m1(w):
+    """Matrix [rows, cols] (cols a multiple of 32) -> MXFP4: (packed E2M1 codes uint8
+    [rows, cols / 2], element 2c in the low nibble; E8M0 scales uint8 [rows, cols / 32]).
+
+    Per block of 32 elements of a row, as the OCP MX conversion does: the shared exponent
+    X = floor(log2(max |v|)) - 2 (2 = the exponent of E2M1's largest value, 6 = 1.5 * 2^2;
+    X = -127 for an all-zero block, clamped to [-127, 127]); each v / 2^X rounded to the
+    nearest E2M1 value, ties to even mantissa, saturating at +-6."""
+    import torch
+
+    v = w.float()
+    rows, cols = v.shape
+    blk = v.reshape(rows, cols // 32, 32)
+    amax = blk.abs().amax(dim=2)
+    _, ex = torch.frexp(amax)                       # amax = m * 2^ex, m in [0.5, 1)
+    X = torch.where(amax > 0, ex - 1 - 2, torch.full_like(ex, -127)).clamp(-127, 127)
+    a = (blk.abs() / torch.exp2(X.float())[:, :, None]).clamp(max=6.0)
+    # the grid spacing is 0.5 below 2, 1 in [2, 4), 2 from 4; an even multiple of the
+    # spacing has an even mantissa, so round-half-even of a / step is the format's rounding
+    step = torch.where(a < 2.0, 0.5, torch.where(a < 4.0, 1.0, 2.0))
+    q = torch.round(a / step) * step
+    idx = torch.where(q < 2.0, q * 2.0, torch.where(q < 4.0, q + 2.0, q / 2.0 + 4.0))
+    code = idx.to(torch.uint8) | (torch.signbit(blk).to(torch.uint8) << 3)
+    code = code.reshape(rows, cols)
+    packed = code[:, 0::2] | (code[:, 1::2] << 4)
+    return packed.contiguous(), (X + 127).to(torch.uint8)
+
+
+def expert_weights_mxfp4(N: int, d: int, f: int, seed: int, device="cpu", std: float = 0.02):
+    """MXFP4 versions of expert_weights: (q1 [N,f,d/2], q3 [N,f,d/2], q2 [N,d,f/2] packed
+    E2M1 codes; e1 [N,f,d/32], e3 [N,f,d/32], e2 [N,d,f/32] E8M0 scales), uint8."""
+    import torch
+
+    q = [torch.empty((N, f, d // 2), dtype=torch.uint8, device=device),
+         torch.empty((N, f, d // 2), dtype=torch.uint8, device=device),
+         torch.empty((N, d, f // 2), dtype=torch.uint8, device=device)]
+    sc = [torch.empty((N, f, d // 32), dtype=torch.uint8, device=device),
+          torch.empty((N, f, d // 32), dtype=torch.uint8, device=device),
+          torch.empty((N, d, f // 32), dtype=torch.uint8, device=device)]
+    for e in range(N):
+        for i, which in enumerate(("w1", "w3", "w2")):
+            q[i][e], sc[i][e] = quantize_mx_e2m1(expert_matrix(e, which, d, f, seed, device, std))
+    return (*q, *sc)
+
+
 def expert_matrix(e: int, which: str, d: int, f: int, seed: int, device="cpu", std: float = 0.02):
     """One expert matrix in nn.Linear [out,in] layout: w1/w3 (s1/s3 for shared experts) are
     [f,d], w2 (s2) is [d,f]."""
