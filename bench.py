@@ -70,9 +70,9 @@ def parse():
     ap.add_argument("--ep-groups", type=int, default=0,
                     help="G > 0: expert-parallel selection and per-group shares")
     ap.add_argument("--per-group-budget", type=int, default=5, help="m_g (with --ep-groups)")
-    ap.add_argument("--weights", choices=("bf16", "fp8"), default="bf16",
+    ap.add_argument("--weights", choices=("bf16", "fp8", "mxfp4"), default="bf16",
                     help="routed-expert weight format (fp8: OCP E4M3FN codes, one fp32 scale "
-                         "per output row)")
+                         "per output row; mxfp4: E2M1 codes, one E8M0 scale per 32 inputs)")
     ap.add_argument("--full-layer", action="store_true",
                     help="the whole layer from hidden states: router GEMM, selection, routed "
                          "and shared experts (xshare_moe_layer)")
@@ -85,18 +85,28 @@ def parse():
     return ap.parse_args()
 
 
+def _scale_bytes(n_active, d, f, wb, gate_up_only=False):
+    """Scale bytes read with the weights: FP8 (wb 1) one fp32 per output row, MXFP4
+    (wb 0.5) one byte per 32 weights, bf16 none."""
+    if wb == 1:
+        return n_active * (2 * f + (0 if gate_up_only else d)) * 4
+    if wb == 0.5:
+        return n_active * (2 if gate_up_only else 3) * f * d // 32
+    return 0
+
+
 def gate_up_bytes(n_active, T, k, d, f, wb=2):
     """Algorithmic HBM bytes of one gate/up launch: W1, W3 of every active expert (wb bytes
-    per weight; FP8 adds its row scales), x, and H written as two bf16 arrays (hi and lo)."""
-    scales = 0 if wb == 2 else n_active * 2 * f * 4
-    return n_active * 2 * f * d * wb + scales + T * d * 2 + T * k * f * 2 * 2
+    per weight, plus the format's scales), x, and H written as two bf16 arrays (hi, lo)."""
+    return (n_active * 2 * f * d * wb + _scale_bytes(n_active, d, f, wb, True) + T * d * 2
+            + T * k * f * 2 * 2)
 
 
 def layer_bytes(n_active, T, N, d, f, wb=2):
-    """Algorithmic HBM bytes of one layer call: active experts' weights (and FP8 row scales),
-    x, logits, y."""
-    scales = 0 if wb == 2 else n_active * (2 * f + d) * 4
-    return n_active * 3 * f * d * wb + scales + T * d * 2 + T * N * 4 + T * d * 2
+    """Algorithmic HBM bytes of one layer call: active experts' weights (and scales), x,
+    logits, y."""
+    return (n_active * 3 * f * d * wb + _scale_bytes(n_active, d, f, wb) + T * d * 2
+            + T * N * 4 + T * d * 2)
 
 
 def counters_traffic():
@@ -144,17 +154,20 @@ def main():
     # small layers would sit in the 256 MB Infinity Cache between steps: rotate weight copies
 
     fp8 = args.weights == "fp8"
-    wb = 1 if fp8 else 2
+    mx4 = args.weights == "mxfp4"
+    wb = 1 if fp8 else (0.5 if mx4 else 2)
     layer_gb = N * 3 * d * f * wb / 1e9
     reps = args.replicas or max(1, min(8, int(np.ceil(4.0 / layer_gb))))
     print(f"[bench] {args.workload}: generating layer weights ({layer_gb:.2f} GB x {reps})",
           file=sys.stderr, flush=True)
     if fp8:
         base = W.expert_weights_fp8(N, d, f, 0, dev)
+    elif mx4:
+        base = W.expert_weights_mxfp4(N, d, f, 0, dev)
     else:
         base = W.expert_weights(N, d, f, 0, dev)
     wsets = [base] + [tuple(t.clone() for t in base) for _ in range(reps - 1)]
-    forward = X.moe_forward_fp8 if fp8 else X.moe_forward
+    forward = X.moe_forward_fp8 if fp8 else (X.moe_forward_mxfp4 if mx4 else X.moe_forward)
     made = [W.make_logits(cfg, s) for s in range(nb)]
     logits = [torch.from_numpy(h).to(dev) for h, _ in made]
     offs = [None if o is None else [int(v) for v in o] for _, o in made]
@@ -228,13 +241,13 @@ def main():
     gbs = float(lay_bytes.mean()) / (ms_step * 1e-3) / 1e9
     gu_achieved = float(gu_bytes.mean()) / (float(gu_ms.mean()) * 1e-3) / 1e9
     # the committed counter record covers the headline workload only
-    traffic = counters_traffic() if (args.workload, M, T, args.tau, fp8) == \
-        ("ds_t32", 48, 32, None, False) else None
+    traffic = counters_traffic() if (args.workload, M, T, args.tau, args.weights) == \
+        ("ds_t32", 48, 32, None, "bf16") else None
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(W, xs, logits, offs if hier else None, m_r, base, fp8, T, N, k, k0,
-                           M, d, f, bmode, args.tau)
+        cpu = cpu_baseline(W, xs, logits, offs if hier else None, m_r, base, args.weights, T,
+                           N, k, k0, M, d, f, bmode, args.tau)
 
     out = {
         "metric": METRIC,
@@ -247,12 +260,14 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "fp8-e4m3 weights, bf16 activations" if fp8 else "bf16",
+        "dtype": ("fp8-e4m3 weights, bf16 activations" if fp8 else
+                  "mxfp4 (e2m1 + e8m0 per 32) weights, bf16 activations" if mx4 else "bf16"),
         "data": "synthetic",
         "config": {"workload": WORKLOAD_NAMES[args.workload].format(T=T, N=N, k=k, d=d, f=f, M=M,
                                                                      k0=k0, m_r=m_r)
                    + ("" if args.tau is None else f"_tau{args.tau:g}")
-                   + ("_fp8" if fp8 else ""), "weights": args.weights,
+                   + ("" if args.weights == "bf16" else "_" + args.weights),
+                   "weights": args.weights,
                    "tokens": T, "n_experts": N, "top_k": k, "d_model": d, "d_ffn": f,
                    "budget": None if args.tau is not None else M, "budget_mode": bmode,
                    "threshold": args.tau, "warmup_k0": k0,
@@ -599,7 +614,7 @@ def run_ep(args, W, X, np, torch):
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(W, xs, logits, offs, m_r, weights, fp8, T, N, k, k0, M, d, f, mode="total",
+def cpu_baseline(W, xs, logits, offs, m_r, weights, fmt, T, N, k, k0, M, d, f, mode="total",
                  tau=None, budget_s=10.0):
     """The oracle on the host cores: routing plus the float64 SwiGLU layer of whole batches,
     over as many of the rotated batches as fit in about budget_s seconds (at least one)."""
@@ -616,7 +631,7 @@ def cpu_baseline(W, xs, logits, offs, m_r, weights, fp8, T, N, k, k0, M, d, f, m
     spent, done, active = 0.0, 0, []
     wall0 = time.perf_counter()
     for b in range(len(xs)):
-        if done and time.perf_counter() - wall0 > 100.0:     # FP8 weight preparation is slow
+        if done and time.perf_counter() - wall0 > 100.0:     # weight decoding is slow
             break
         h = logits[b].cpu().numpy()
         xb = W.bf16_bits(xs[b])
@@ -625,11 +640,12 @@ def cpu_baseline(W, xs, logits, offs, m_r, weights, fp8, T, N, k, k0, M, d, f, m
             OR.select_hier(h, offs[b], k, k0, m_r, M, mode, tau=tau)
         t_route = time.perf_counter() - t0
         used = sorted(set(int(e) for e in r.ids.reshape(-1)))
-        if fp8:                                                             # not timed
+        if fmt != "bf16":                                                   # not timed
             q1, q3, q2, s1, s3, s2 = weights
+            dec = OF.dequant_rows if fmt == "fp8" else OF.dequant_mx
             cache = {}
             for n_done, e in enumerate(used):
-                cache[e] = tuple(OF.dequant_rows(q[e].cpu().numpy(), sc[e].cpu().numpy())
+                cache[e] = tuple(dec(q[e].cpu().numpy(), sc[e].cpu().numpy())
                                  for q, sc in ((q1, s1), (q3, s3), (q2, s2)))
                 if n_done % 8 == 7:
                     print(f"[bench] cpu baseline: batch {b}, {n_done + 1}/{len(used)} experts "
@@ -647,13 +663,15 @@ def cpu_baseline(W, xs, logits, offs, m_r, weights, fp8, T, N, k, k0, M, d, f, m
         if spent >= budget_s:
             break
     t_batch = spent / done
-    bytes_batch = float(np.mean([layer_bytes(a, T, N, d, f, 1 if fp8 else 2) for a in active]))
+    wb = {"bf16": 2, "fp8": 1, "mxfp4": 0.5}[fmt]
+    bytes_batch = float(np.mean([layer_bytes(a, T, N, d, f, wb) for a in active]))
     return {"value": round(bytes_batch / t_batch / 1e9, 3), "unit": "GB/s",
             "us_per_batch": round(t_batch * 1e6, 1), "cores": int(cores), "kind": "oracle",
             "sample": f"full oracle (numpy routing, float64 SwiGLU of all {T} tokens over their "
                       f"{np.mean(active):.0f} active experts) on {done} of the rotated batches, "
                       f"{spent:.1f} s total; BLAS threads = cores, weight conversion "
-                      f"{'(FP8 decode) ' if fp8 else ''}single-threaded and not timed"}
+                      f"{'' if fmt == 'bf16' else '(' + fmt + ' decode) '}single-threaded and "
+                      "not timed"}
 
 
 if __name__ == "__main__":

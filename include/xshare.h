@@ -326,6 +326,36 @@ xshare_status xshare_moe_forward_fp8(const uint16_t* x, const float* logits, int
                                      void* const* stage_events, hipStream_t stream);
 
 /*
+ * xshare_moe_forward_mxfp4 -- xshare_moe_forward with MXFP4 routed-expert weights (OCP
+ * Microscaling MXFP4: a quarter of the bytes of bf16 plus one scale byte per 32 weights;
+ * the paper is silent on precision).
+ *
+ *   w1, w3    [N, f, d/2] uint8: FP4 E2M1 codes (1 sign, 2 exponent bits with bias 1, 1
+ *             mantissa bit; values 0, 0.5, 1, 1.5, 2, 3, 4, 6 and their negatives), two per
+ *             byte along the input index: element 2c in the low nibble of byte c.  16-byte
+ *             aligned.
+ *   w2        [N, d, f/2] uint8, same format.
+ *   w1_scale, w3_scale  [N, f, d/32] uint8; w2_scale [N, d, f/32] uint8: E8M0 scales, one per
+ *             block of 32 consecutive inputs of a row, value 2^(e - 127); the weight is
+ *             decode(code) * 2^(e - 127).  e = 255 (NaN) must not occur, and the decoded
+ *             weights must lie in bf16's normal range (or be zero): the GPU turns each code
+ *             and its scale into the exact bf16 weight before the bf16 MFMA.
+ *   d and f multiples of 32.  Everything else as xshare_moe_forward (workspace from
+ *   xshare_moe_workspace_bytes); shared experts are not taken here.
+ */
+xshare_status xshare_moe_forward_mxfp4(const uint16_t* x, const float* logits, int32_t T,
+                                       int32_t d, int32_t f, const uint8_t* w1,
+                                       const uint8_t* w3, const uint8_t* w2,
+                                       const uint8_t* w1_scale, const uint8_t* w3_scale,
+                                       const uint8_t* w2_scale,
+                                       const xshare_route_params* params,
+                                       const int32_t* req_offsets, const int32_t* host_offsets,
+                                       int32_t R, const xshare_ep_layout* ep, uint16_t* y,
+                                       uint8_t* sel_mask, int32_t* topk_ids, float* topk_w,
+                                       xshare_stats* stats, void* ws, size_t ws_bytes,
+                                       void* const* stage_events, hipStream_t stream);
+
+/*
  * xshare_moe_layer -- the whole MoE layer of Section 2.1 from the hidden states: router
  * logits h = W_g x (as xshare_router_logits), selection, the selected routed experts and
  * the shared experts, combine.

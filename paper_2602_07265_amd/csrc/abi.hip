@@ -203,13 +203,18 @@ struct Weights {
   const float* s1 = nullptr;
   const float* s3 = nullptr;
   const float* s2 = nullptr;
-  bool fp8() const { return q1 != nullptr; }
+  const uint8_t* e1 = nullptr;   // MXFP4 block scales
+  const uint8_t* e3 = nullptr;
+  const uint8_t* e2 = nullptr;
+  int fmt = 0;                   // 0 bf16, 1 FP8, 2 MXFP4
   bool present() const {
-    return fp8() ? (q3 && q2 && s1 && s3 && s2) : (w1 && w3 && w2);
+    if (fmt == 1) return q1 && q3 && q2 && s1 && s3 && s2;
+    if (fmt == 2) return q1 && q3 && q2 && e1 && e3 && e2;
+    return w1 && w3 && w2;
   }
   bool aligned() const {
-    return fp8() ? (aligned16(q1) && aligned16(q3) && aligned16(q2))
-                 : (aligned16(w1) && aligned16(w3) && aligned16(w2));
+    return fmt ? (aligned16(q1) && aligned16(q3) && aligned16(q2))
+               : (aligned16(w1) && aligned16(w3) && aligned16(w2));
   }
 };
 
@@ -235,7 +240,7 @@ xshare_status layer_common(const uint16_t* x, const float* logits, const uint16_
   if (st != XSHARE_OK) return st;
   st = check_shared(shared, ep);
   if (st != XSHARE_OK) return st;
-  if (wt.fp8() && shared && shared->n_shared > 0) return XSHARE_EUNSUPPORTED;
+  if (wt.fmt != 0 && shared && shared->n_shared > 0) return XSHARE_EUNSUPPORTED;
   if (d <= 0 || f <= 0) return XSHARE_EINVAL;
   if (d % xs::kDimAlign != 0 || f % xs::kDimAlign != 0) return XSHARE_EUNSUPPORTED;
   if (T > 0 && (!x || !wt.present() || !y)) return XSHARE_EINVAL;
@@ -283,6 +288,10 @@ xshare_status layer_common(const uint16_t* x, const float* logits, const uint16_
   fa.s1 = wt.s1;
   fa.s3 = wt.s3;
   fa.s2 = wt.s2;
+  fa.e1 = wt.e1;
+  fa.e3 = wt.e3;
+  fa.e2 = wt.e2;
+  fa.wfmt = wt.fmt;
   fa.T = T;
   fa.N = N;
   fa.k = k;
@@ -408,12 +417,38 @@ xshare_status xshare_moe_forward_fp8(const uint16_t* x, const float* logits, int
                                      void* const* stage_events, hipStream_t stream) {
   if (T > 0 && (!logits || !w1)) return XSHARE_EINVAL;
   Weights wt;              // with T == 0 nothing is read and the pointers may be null
+  wt.fmt = 1;
   wt.q1 = w1;
   wt.q3 = w3;
   wt.q2 = w2;
   wt.s1 = w1_scale;
   wt.s3 = w3_scale;
   wt.s2 = w2_scale;
+  return layer_common(x, logits, nullptr, T, d, f, wt, nullptr, params, req_offsets,
+                      host_offsets, R, ep, y, nullptr, sel_mask, topk_ids, topk_w, stats, ws,
+                      ws_bytes, stage_events, stream);
+}
+
+xshare_status xshare_moe_forward_mxfp4(const uint16_t* x, const float* logits, int32_t T,
+                                       int32_t d, int32_t f, const uint8_t* w1,
+                                       const uint8_t* w3, const uint8_t* w2,
+                                       const uint8_t* w1_scale, const uint8_t* w3_scale,
+                                       const uint8_t* w2_scale,
+                                       const xshare_route_params* params,
+                                       const int32_t* req_offsets, const int32_t* host_offsets,
+                                       int32_t R, const xshare_ep_layout* ep, uint16_t* y,
+                                       uint8_t* sel_mask, int32_t* topk_ids, float* topk_w,
+                                       xshare_stats* stats, void* ws, size_t ws_bytes,
+                                       void* const* stage_events, hipStream_t stream) {
+  if (T > 0 && (!logits || !w1)) return XSHARE_EINVAL;
+  Weights wt;
+  wt.fmt = 2;
+  wt.q1 = w1;
+  wt.q3 = w3;
+  wt.q2 = w2;
+  wt.e1 = w1_scale;
+  wt.e3 = w3_scale;
+  wt.e2 = w2_scale;
   return layer_common(x, logits, nullptr, T, d, f, wt, nullptr, params, req_offsets,
                       host_offsets, R, ep, y, nullptr, sel_mask, topk_ids, topk_w, stats, ws,
                       ws_bytes, stage_events, stream);

@@ -72,6 +72,72 @@ __device__ __forceinline__ uint2 load_q8(const uint8_t* p) {
   return *reinterpret_cast<const uint2*>(p);
 }
 
+// Weight formats of the expert GEMMs.
+constexpr int kBf16 = 0;   // bf16
+constexpr int kFp8 = 1;    // OCP FP8 E4M3FN codes, one fp32 scale per output row
+constexpr int kMx4 = 2;    // MXFP4: E2M1 codes, two per byte, one E8M0 scale per 32 elements
+
+// 8U packed E2M1 codes of one lane and step (U words, 8 elements each, low nibble first).
+template <int U>
+struct Q4 {
+  uint32_t w[U];
+};
+template <int U>
+__device__ __forceinline__ Q4<U> load_q4(const uint8_t* p) {
+  Q4<U> r;
+  if constexpr (U == 8) {
+    const uint4 v = *reinterpret_cast<const uint4*>(p);
+    const uint4 w = *reinterpret_cast<const uint4*>(p + 16);
+    r.w[0] = v.x;
+    r.w[1] = v.y;
+    r.w[2] = v.z;
+    r.w[3] = v.w;
+    r.w[4] = w.x;
+    r.w[5] = w.y;
+    r.w[6] = w.z;
+    r.w[7] = w.w;
+  } else if constexpr (U == 4) {
+    const uint4 v = *reinterpret_cast<const uint4*>(p);
+    r.w[0] = v.x;
+    r.w[1] = v.y;
+    r.w[2] = v.z;
+    r.w[3] = v.w;
+  } else if constexpr (U == 2) {
+    const uint2 v = *reinterpret_cast<const uint2*>(p);
+    r.w[0] = v.x;
+    r.w[1] = v.y;
+  } else {
+    r.w[0] = *reinterpret_cast<const uint32_t*>(p);
+  }
+  return r;
+}
+
+// E8M0 scale byte -> 2^(e - 127) as fp32 (e = 0 is the subnormal 2^-127).
+__device__ __forceinline__ float e8m0_scale(uint32_t e) {
+  return e ? __uint_as_float(e << 23) : __uint_as_float(0x00400000u);
+}
+
+// 8 E2M1 codes (one word) times their block scale -> 8 bf16.  The conversion (one byte, two
+// elements, per instruction; low nibble first) multiplies by a power of two, so the result
+// is exact for scales that keep the weights in bf16's normal range.
+__device__ __forceinline__ bf16x8 fp4x8_to_bf16(uint32_t w, float scale) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 p0 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, scale, 0);
+  const bf16x2 p1 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, scale, 1);
+  const bf16x2 p2 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, scale, 2);
+  const bf16x2 p3 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, scale, 3);
+  bf16x8 r;
+  r[0] = p0[0];
+  r[1] = p0[1];
+  r[2] = p1[0];
+  r[3] = p1[1];
+  r[4] = p2[0];
+  r[5] = p2[1];
+  r[6] = p3[0];
+  r[7] = p3[1];
+  return r;
+}
+
 // Stores v = H[p, c] as hi = bf16(v) and lo = bf16(v - hi) in the interleaved rows of 2f
 // elements: hi at 16 (c / 8) + c % 8, lo 8 elements further.
 __device__ __forceinline__ void store_hilo(uint16_t* h2, size_t p, int c, int f, float v) {
@@ -116,6 +182,15 @@ __device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[TL], int
     const bool more = s + KB < K;
     int kn = kb + KB;
     if (kn >= K) kn -= K;
+    // Token loads of this step go out before the next step's weight loads: loads complete
+    // in issue order, so waiting for the tokens then leaves the weight prefetch in flight.
+    if (!ADBL) {
+#pragma unroll
+      for (int rt = 0; rt < TL; ++rt)
+        if (rt < nt)
+#pragma unroll
+          for (int u = 0; u < U; ++u) x[rt][u] = load8(arow[rt] + AS * (kb + 8 * u));
+    }
     if (more) {
 #pragma unroll
       for (int m = 0; m < NM; ++m)
@@ -128,13 +203,6 @@ __device__ __forceinline__ void wave_pass(const uint16_t* const (&arow)[TL], int
 #pragma unroll
             for (int u = 0; u < U; ++u) nx[rt][u] = load8(arow[rt] + AS * (kn + 8 * u));
       }
-    }
-    if (!ADBL) {
-#pragma unroll
-      for (int rt = 0; rt < TL; ++rt)
-        if (rt < nt)
-#pragma unroll
-          for (int u = 0; u < U; ++u) x[rt][u] = load8(arow[rt] + AS * (kb + 8 * u));
     }
 #pragma unroll
     for (int u = 0; u < U; ++u)
@@ -178,17 +246,17 @@ __device__ __forceinline__ void wave_pass_q8(const uint16_t* const (&arow)[TL], 
     const bool more = s + KB < K;
     int kn = kb + KB;
     if (kn >= K) kn -= K;
+#pragma unroll
+    for (int rt = 0; rt < TL; ++rt)       // tokens first: see wave_pass
+      if (rt < nt)
+#pragma unroll
+        for (int u = 0; u < U; ++u) x[rt][u] = load8(arow[rt] + AS * (kb + 8 * u));
     if (more) {
 #pragma unroll
       for (int m = 0; m < NM; ++m)
 #pragma unroll
         for (int u = 0; u < U; ++u) nb[m][u] = load_q8(brow[m] + kn + 8 * u);
     }
-#pragma unroll
-    for (int rt = 0; rt < TL; ++rt)
-      if (rt < nt)
-#pragma unroll
-        for (int u = 0; u < U; ++u) x[rt][u] = load8(arow[rt] + AS * (kb + 8 * u));
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
@@ -203,6 +271,77 @@ __device__ __forceinline__ void wave_pass_q8(const uint16_t* const (&arow)[TL], 
       for (int m = 0; m < NM; ++m)
 #pragma unroll
         for (int u = 0; u < U; ++u) b[m][u] = nb[m][u];
+    }
+    kb = kn;
+  }
+}
+
+// The scale byte(s) of a lane's step: one block for U <= 4, two consecutive blocks (two
+// bytes, the first block's in the low byte) for U = 8.
+template <int U>
+__device__ __forceinline__ uint32_t load_e8m0(const uint8_t* p) {
+  if constexpr (U == 8)
+    return *reinterpret_cast<const uint16_t*>(p);
+  else
+    return *p;
+}
+
+// wave_pass with MXFP4 weights: per step a lane loads 4U bytes of codes (its 8U elements:
+// within one 32-element block for U <= 4, two blocks for U = 8) and their scale bytes, one
+// step ahead; the codes become bf16, scaled, just before use.  `brow[m]` points at the codes
+// of this lane's first element, `srow[m]` at the scale of its first block.
+template <int U, int NM, int TL = kTiles, int AS = 1>
+__device__ __forceinline__ void wave_pass_q4(const uint16_t* const (&arow)[TL], int nt,
+                                             const uint8_t* const (&brow)[NM],
+                                             const uint8_t* const (&srow)[NM], int K,
+                                             floatx4 (&acc)[NM][TL], int k_first = 0) {
+  static_assert(U == 1 || U == 2 || U == 4 || U == 8, "1, 2, 4 or 8 words per lane and step");
+  constexpr int KB = 32 * U;
+  Q4<U> b[NM];
+  uint32_t e[NM];
+  bf16x8 x[TL][U];
+#pragma unroll
+  for (int m = 0; m < NM; ++m) {
+    b[m] = load_q4<U>(brow[m] + k_first / 2);
+    e[m] = load_e8m0<U>(srow[m] + k_first / 32);
+  }
+  int kb = k_first;
+  for (int s = 0; s < K; s += KB) {
+    Q4<U> nb[NM];
+    uint32_t ne[NM];
+    const bool more = s + KB < K;
+    int kn = kb + KB;
+    if (kn >= K) kn -= K;
+#pragma unroll
+    for (int rt = 0; rt < TL; ++rt)       // tokens first: see wave_pass
+      if (rt < nt)
+#pragma unroll
+        for (int u = 0; u < U; ++u) x[rt][u] = load8(arow[rt] + AS * (kb + 8 * u));
+    if (more) {
+#pragma unroll
+      for (int m = 0; m < NM; ++m) {
+        nb[m] = load_q4<U>(brow[m] + kn / 2);
+        ne[m] = load_e8m0<U>(srow[m] + kn / 32);
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < NM; ++m) {
+      const float sc0 = e8m0_scale(e[m] & 0xFFu);
+      const float sc1 = U == 8 ? e8m0_scale(e[m] >> 8) : sc0;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const bf16x8 bv = fp4x8_to_bf16(b[m].w[u], u < 4 ? sc0 : sc1);
+#pragma unroll
+        for (int rt = 0; rt < TL; ++rt)
+          if (rt < nt) acc[m][rt] = mfma(x[rt][u], bv, acc[m][rt]);
+      }
+    }
+    if (more) {
+#pragma unroll
+      for (int m = 0; m < NM; ++m) {
+        b[m] = nb[m];
+        e[m] = ne[m];
+      }
     }
     kb = kn;
   }
@@ -226,6 +365,15 @@ __device__ __forceinline__ void wave_pass_q8(const uint16_t* const (&arow)[TL], 
 #endif
 #ifndef XS_Q8_DOWN_U
 #define XS_Q8_DOWN_U 4
+#endif
+#ifndef XS_Q4_GATE_UP_U
+#define XS_Q4_GATE_UP_U 8
+#endif
+#ifndef XS_Q4_DOWN_U
+#define XS_Q4_DOWN_U 8
+#endif
+#ifndef XS_Q4_DOWN_ROT
+#define XS_Q4_DOWN_ROT 0
 #endif
 // K steps between the starts of consecutive down waves: one with bf16 weights (DeepSeek
 // T=32 down 270 -> 263 us); none with FP8, where it measured no gain.
@@ -280,7 +428,7 @@ __device__ __forceinline__ const uint8_t* slot_q(const FfnArgs& a, const SlotWor
 
 // kSplit: the block covers one part of the reduction (blockIdx.z) and writes fp32 gate and
 // up partials; otherwise it covers all of d and writes H directly.
-template <int U, bool kSplit, bool kQ8>
+template <int U, bool kSplit, int kW>
 __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
   SlotWork sw;
   if (!slot_work(a, blockIdx.y, sw)) return;
@@ -295,7 +443,7 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
   const size_t wrow = (size_t)(j0 + n) * d + k0;
   const size_t plane = (size_t)a.rows * f;     // one fp32 partial plane [rows, f]
   float sc1 = 1.0f, sc3 = 1.0f;                // FP8 per-row scales of this lane's column
-  if (kQ8) {
+  if (kW == kFp8) {
     sc1 = a.s1[(size_t)sw.e * f + j0 + n];
     sc3 = a.s3[(size_t)sw.e * f + j0 + n];
   }
@@ -314,9 +462,16 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
     for (int m = 0; m < 2; ++m)
 #pragma unroll
       for (int rt = 0; rt < kTiles; ++rt) acc[m][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    if (kQ8) {
+    if constexpr (kW == kFp8) {
       const uint8_t* const brow[2] = {slot_q(a, sw, a.q1) + wrow, slot_q(a, sw, a.q3) + wrow};
       wave_pass_q8<U, 2>(arow, nt, brow, Kg, acc);
+    } else if constexpr (kW == kMx4) {
+      // row j0 + n of the expert: d / 2 code bytes, d / 32 scale bytes
+      const size_t r = (size_t)sw.e * f + j0 + n;
+      const uint8_t* const brow[2] = {a.q1 + r * (d / 2) + k0 / 2, a.q3 + r * (d / 2) + k0 / 2};
+      const uint8_t* const srow[2] = {a.e1 + r * (d / 32) + k0 / 32,
+                                      a.e3 + r * (d / 32) + k0 / 32};
+      wave_pass_q4<U, 2>(arow, nt, brow, srow, Kg, acc);
     } else {
       const uint16_t* const brow[2] = {slot_w(a, sw, a.w1, a.sw1) + wrow,
                                        slot_w(a, sw, a.w3, a.sw3) + wrow};
@@ -344,9 +499,10 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
   }
 }
 
-template <int U, bool kQ8>
+template <int U, int kW>
 __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
-  constexpr int NM = kQ8 ? XS_Q8_DOWN_NM : XS_DOWN_NM;   // 16-row W2 tiles per wave
+  constexpr int NM = kW == kBf16 ? XS_DOWN_NM                 // 16-row W2 tiles per wave
+                   : (kW == kFp8 ? XS_Q8_DOWN_NM : XS_Q4_DOWN_NM);
   constexpr int TL = XS_DOWN_TL;  // token tiles per pass, 8 tokens each (hi and lo rows)
   SlotWork sw;
   if (!slot_work(a, blockIdx.y, sw)) return;
@@ -361,12 +517,13 @@ __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
   float* const ypart = a.yslot + (size_t)blockIdx.z * a.rows * d;
   const int lo_off = n < 8 ? 0 : 8;                    // A rows 0-7: hi, rows 8-15: lo
   size_t wrow[NM];
-  float sc[NM];                                        // FP8 per-row scales (1 for bf16)
+  int rowm[NM];
+  float sc[NM];                                        // FP8 per-row scales (else 1)
 #pragma unroll
   for (int m = 0; m < NM; ++m) {
-    const int row = min(n0 + 16 * m, d - 16) + n;
-    wrow[m] = (size_t)row * f + k0;
-    sc[m] = kQ8 ? a.s2[(size_t)sw.e * d + row] : 1.0f;
+    rowm[m] = min(n0 + 16 * m, d - 16) + n;
+    wrow[m] = (size_t)rowm[m] * f + k0;
+    sc[m] = kW == kFp8 ? a.s2[(size_t)sw.e * d + rowm[m]] : 1.0f;
   }
 
   for (int c0 = 0; c0 < te; c0 += 8 * TL) {
@@ -385,13 +542,23 @@ __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
     // Consecutive waves start their pass over K one step apart (and wrap around): W2 rows
     // are f elements apart, often a power of two, so waves that stepped through K in the
     // same order would read the same offsets of every row at the same time.
-    const int rot = kQ8 ? XS_Q8_DOWN_ROT : XS_DOWN_ROT;
+    const int rot = kW == kBf16 ? XS_DOWN_ROT : (kW == kFp8 ? XS_Q8_DOWN_ROT : XS_Q4_DOWN_ROT);
     const int k_first = (int)(((blockIdx.x * kWaves + wave) * rot) % (Ks / (32 * U))) * 32 * U;
-    if (kQ8) {
+    if constexpr (kW == kFp8) {
       const uint8_t* brow[NM];
 #pragma unroll
       for (int m = 0; m < NM; ++m) brow[m] = slot_q(a, sw, a.q2) + wrow[m];
       wave_pass_q8<U, NM, TL, 2>(arow, nt, brow, Ks, acc, k_first);
+    } else if constexpr (kW == kMx4) {
+      const uint8_t* brow[NM];
+      const uint8_t* srow[NM];
+#pragma unroll
+      for (int m = 0; m < NM; ++m) {
+        const size_t r = (size_t)sw.e * d + rowm[m];      // f / 2 code, f / 32 scale bytes
+        brow[m] = a.q2 + r * (f / 2) + k0 / 2;
+        srow[m] = a.e2 + r * (f / 32) + k0 / 32;
+      }
+      wave_pass_q4<U, NM, TL, 2>(arow, nt, brow, srow, Ks, acc, k_first);
     } else {
       const uint16_t* brow[NM];
 #pragma unroll
@@ -549,12 +716,41 @@ __global__ __launch_bounds__(kBlock) void router_sum_kernel(RouterArgs r) {
   r.logits[idx] = v;
 }
 
-template <int U, bool kQ8>
+template <int U, int kW>
 void launch_gu(const FfnArgs& a, bool split, dim3 grid, dim3 block, hipStream_t stream) {
   if (split)
-    hipLaunchKernelGGL((gate_up_kernel<U, true, kQ8>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((gate_up_kernel<U, true, kW>), grid, block, 0, stream, a);
   else
-    hipLaunchKernelGGL((gate_up_kernel<U, false, kQ8>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((gate_up_kernel<U, false, kW>), grid, block, 0, stream, a);
+}
+
+// Unroll U (a power of two <= 8 dividing K / 32) for weight format kW.
+template <int kW>
+void launch_gu_fmt(const FfnArgs& a, int u, bool split, dim3 grid, dim3 block,
+                   hipStream_t stream) {
+  if (u == 8) {
+    launch_gu<8, kW>(a, split, grid, block, stream);
+    return;
+  }
+  if (u >= 4)
+    launch_gu<4, kW>(a, split, grid, block, stream);
+  else if (u == 2)
+    launch_gu<2, kW>(a, split, grid, block, stream);
+  else
+    launch_gu<1, kW>(a, split, grid, block, stream);
+}
+template <int kW>
+void launch_down_fmt(const FfnArgs& a, int u, dim3 grid, dim3 block, hipStream_t stream) {
+  if (u == 8) {
+    hipLaunchKernelGGL((down_kernel<8, kW>), grid, block, 0, stream, a);
+    return;
+  }
+  if (u >= 4)
+    hipLaunchKernelGGL((down_kernel<4, kW>), grid, block, 0, stream, a);
+  else if (u == 2)
+    hipLaunchKernelGGL((down_kernel<2, kW>), grid, block, 0, stream, a);
+  else
+    hipLaunchKernelGGL((down_kernel<1, kW>), grid, block, 0, stream, a);
 }
 
 int unroll_for(int K, int want) {
@@ -570,21 +766,13 @@ hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
                   a.gu_splits),
       block(kBlock);
   const bool split = a.gu_splits > 1;
-  if (a.q1) {
-    switch (unroll_for(a.d / a.gu_splits, XS_Q8_GATE_UP_U)) {
-      case 8: launch_gu<8, true>(a, split, grid, block, stream); break;
-      case 4: launch_gu<4, true>(a, split, grid, block, stream); break;
-      case 2: launch_gu<2, true>(a, split, grid, block, stream); break;
-      default: launch_gu<1, true>(a, split, grid, block, stream); break;
-    }
-  } else {
-    switch (unroll_for(a.d / a.gu_splits, XS_GATE_UP_U)) {
-      case 8: launch_gu<8, false>(a, split, grid, block, stream); break;
-      case 4: launch_gu<4, false>(a, split, grid, block, stream); break;
-      case 2: launch_gu<2, false>(a, split, grid, block, stream); break;
-      default: launch_gu<1, false>(a, split, grid, block, stream); break;
-    }
-  }
+  const int K = a.d / a.gu_splits;
+  if (a.wfmt == kFp8)
+    launch_gu_fmt<kFp8>(a, unroll_for(K, XS_Q8_GATE_UP_U), split, grid, block, stream);
+  else if (a.wfmt == kMx4)
+    launch_gu_fmt<kMx4>(a, unroll_for(K, XS_Q4_GATE_UP_U), split, grid, block, stream);
+  else
+    launch_gu_fmt<kBf16>(a, unroll_for(K, XS_GATE_UP_U), split, grid, block, stream);
   if (split) {
     const dim3 fgrid((a.f + kBlock * 4 - 1) / (kBlock * 4), (unsigned)a.rows);
     hipLaunchKernelGGL(gate_up_finish_kernel, fgrid, block, 0, stream, a);
@@ -593,23 +781,16 @@ hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_down(const FfnArgs& a, hipStream_t stream) {
-  const int cols = kWaves * kCols * (a.q1 ? XS_Q8_DOWN_NM : XS_DOWN_NM);
+  const int nm = a.wfmt == kFp8 ? XS_Q8_DOWN_NM : (a.wfmt == kMx4 ? XS_Q4_DOWN_NM : XS_DOWN_NM);
+  const int cols = kWaves * kCols * nm;
   const dim3 grid((a.d + cols - 1) / cols, a.max_active + a.n_shared, a.splits), block(kBlock);
-  if (a.q1) {
-    switch (unroll_for(a.f / a.splits, XS_Q8_DOWN_U)) {
-      case 8: hipLaunchKernelGGL((down_kernel<8, true>), grid, block, 0, stream, a); break;
-      case 4: hipLaunchKernelGGL((down_kernel<4, true>), grid, block, 0, stream, a); break;
-      case 2: hipLaunchKernelGGL((down_kernel<2, true>), grid, block, 0, stream, a); break;
-      default: hipLaunchKernelGGL((down_kernel<1, true>), grid, block, 0, stream, a); break;
-    }
-  } else {
-    switch (unroll_for(a.f / a.splits, XS_DOWN_U)) {
-      case 8: hipLaunchKernelGGL((down_kernel<8, false>), grid, block, 0, stream, a); break;
-      case 4: hipLaunchKernelGGL((down_kernel<4, false>), grid, block, 0, stream, a); break;
-      case 2: hipLaunchKernelGGL((down_kernel<2, false>), grid, block, 0, stream, a); break;
-      default: hipLaunchKernelGGL((down_kernel<1, false>), grid, block, 0, stream, a); break;
-    }
-  }
+  const int K = a.f / a.splits;
+  if (a.wfmt == kFp8)
+    launch_down_fmt<kFp8>(a, unroll_for(K, XS_Q8_DOWN_U), grid, block, stream);
+  else if (a.wfmt == kMx4)
+    launch_down_fmt<kMx4>(a, unroll_for(K, XS_Q4_DOWN_U), grid, block, stream);
+  else
+    launch_down_fmt<kBf16>(a, unroll_for(K, XS_DOWN_U), grid, block, stream);
   return hipGetLastError();
 }
 

@@ -99,13 +99,16 @@ inline int gate_up_splits(int est_active, int d, int f) {
 }
 // 16-row tiles of W2 per wave of the down GEMM (output rows per wave = 16 * NM): 2 with
 // bf16 weights, 4 with FP8 weights (whose one-byte rows make the shared token operand
-// relatively more expensive).  The split counts below use the bf16 figure for both, so the
+// relatively more expensive), 2 with MXFP4 weights (whose 8-word steps need the registers).  The split counts below use the bf16 figure for both, so the
 // workspace does not depend on the weight format.
 #ifndef XS_DOWN_NM
 #define XS_DOWN_NM 2
 #endif
 #ifndef XS_Q8_DOWN_NM
 #define XS_Q8_DOWN_NM 4
+#endif
+#ifndef XS_Q4_DOWN_NM
+#define XS_Q4_DOWN_NM 2
 #endif
 inline int down_splits(int est_active, int d, int f) {
   return split_for((long)est_active * (d / (16 * XS_DOWN_NM)), f, 128, XS_DN_SPLIT_BELOW,
@@ -205,12 +208,16 @@ struct FfnArgs {
   const uint16_t* w1;          // bf16 weights (nullptr with FP8 weights)
   const uint16_t* w3;
   const uint16_t* w2;
-  const uint8_t* q1;           // FP8 E4M3FN weights, same layout (nullptr with bf16 weights)
+  const uint8_t* q1;           // FP8 / MXFP4 weight codes (nullptr with bf16 weights)
   const uint8_t* q3;
   const uint8_t* q2;
   const float* s1;             // FP8 scales, one per output row: [N, f], [N, f], [N, d]
   const float* s3;
   const float* s2;
+  const uint8_t* e1;           // MXFP4 E8M0 block scales [N, f, d/32], [N, f, d/32], [N, d, f/32]
+  const uint8_t* e3;           //   (q1, q3, q2 then hold packed E2M1 codes, two per byte)
+  const uint8_t* e2;
+  int wfmt;                    // 0 bf16, 1 FP8, 2 MXFP4
   int T, N, k, d, f;
   int max_active;              // host bound on the number of active experts (grid size)
   int splits;                  // K-splits of the down GEMM (partials summed in the combine)

@@ -102,6 +102,11 @@ def lib() -> ctypes.CDLL:
                                              ctypes.POINTER(EpLayout), _P, _P, _P, _P, _P, _P,
                                              _SZ, _P, _P]
         L.xshare_moe_forward_fp8.restype = ctypes.c_int
+        L.xshare_moe_forward_mxfp4.argtypes = [_P, _P, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P,
+                                             ctypes.POINTER(RouteParams), _P, _P, _I32,
+                                             ctypes.POINTER(EpLayout), _P, _P, _P, _P, _P, _P,
+                                             _SZ, _P, _P]
+        L.xshare_moe_forward_mxfp4.restype = ctypes.c_int
         L.xshare_route.argtypes = [_P, _I32, ctypes.POINTER(RouteParams), _P, _P, _P, _P, _P, _SZ,
                                    _P]
         L.xshare_route.restype = ctypes.c_int
@@ -477,6 +482,64 @@ def moe_forward_fp8(x: torch.Tensor, logits: torch.Tensor, q1: torch.Tensor, q3:
         _ptr(res.get("ids")), _ptr(res.get("w")), _ptr(res.get("stats")), _ptr(workspace),
         workspace.numel(), ev, _stream(stream))
     _check(st, "xshare_moe_forward_fp8")
+    return res
+
+
+def moe_forward_mxfp4(x: torch.Tensor, logits: torch.Tensor, q1: torch.Tensor, q3: torch.Tensor,
+                      q2: torch.Tensor, e1: torch.Tensor, e3: torch.Tensor, e2: torch.Tensor,
+                      top_k: int, warmup_k0: int, budget: int, budget_mode="total",
+                      score_mode="topk", *, req_offsets=None, per_request_budget: int = 0,
+                      groups: GroupMap | None = None, tau: float = 0.0, ledger=None, y=None,
+                      routing_out=True, workspace=None, stage_events=None, stream=None) -> dict:
+    """The MoE layer with MXFP4 expert weights: packed E2M1 codes (uint8, two per byte) and
+    one E8M0 scale byte per 32 inputs of a row."""
+    T, d = x.shape
+    N = logits.shape[1]
+    f = q1.shape[1]
+    dev = x.device
+    _dev(x, torch.bfloat16, (T, d), "x")
+    _dev(logits, torch.float32, (T, N), "logits")
+    _dev(q1, torch.uint8, (N, f, d // 2), "w1 codes")
+    _dev(q3, torch.uint8, (N, f, d // 2), "w3 codes")
+    _dev(q2, torch.uint8, (N, d, f // 2), "w2 codes")
+    _dev(e1, torch.uint8, (N, f, d // 32), "w1 scales")
+    _dev(e3, torch.uint8, (N, f, d // 32), "w3 scales")
+    _dev(e2, torch.uint8, (N, d, f // 32), "w2 scales")
+    if groups is not None:
+        budget_mode = "per_group"
+    p = params(N, top_k, warmup_k0, budget, budget_mode, score_mode, per_request_budget, tau,
+               ledger)
+    ep = None if groups is None else groups.layout
+    if y is None:
+        y = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
+    _dev(y, torch.bfloat16, (T, d), "y")
+    res = {"y": y}
+    if routing_out:
+        res.update(sel_mask=torch.empty(N, dtype=torch.uint8, device=dev),
+                   ids=torch.empty((T, top_k), dtype=torch.int32, device=dev),
+                   w=torch.empty((T, top_k), dtype=torch.float32, device=dev),
+                   stats=torch.empty(8, dtype=torch.int32, device=dev))
+    need = moe_workspace_bytes(T, d, f, p, ep)
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    d_off = h_off = None
+    R = 0
+    if req_offsets is not None:
+        d_off, h_off = _offsets(req_offsets, dev)
+        R = d_off.numel() - 1
+    ev = None
+    if stage_events is not None:
+        if len(stage_events) != N_STAGE_EVENTS:
+            raise ValueError(f"stage_events needs {N_STAGE_EVENTS} events")
+        ev = (ctypes.c_void_p * N_STAGE_EVENTS)(*[e.handle for e in stage_events])
+    st = lib().xshare_moe_forward_mxfp4(
+        _ptr(x), _ptr(logits), T, d, f, _ptr(q1), _ptr(q3), _ptr(q2), _ptr(e1), _ptr(e3),
+        _ptr(e2), ctypes.byref(p), _ptr(d_off),
+        None if h_off is None else ctypes.c_void_p(h_off.data_ptr()), R,
+        None if ep is None else ctypes.byref(ep), _ptr(y), _ptr(res.get("sel_mask")),
+        _ptr(res.get("ids")), _ptr(res.get("w")), _ptr(res.get("stats")), _ptr(workspace),
+        workspace.numel(), ev, _stream(stream))
+    _check(st, "xshare_moe_forward_mxfp4")
     return res
 
 

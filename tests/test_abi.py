@@ -27,7 +27,8 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
     assert {"xshare_route", "xshare_select_hier", "xshare_select_ep", "xshare_moe_forward",
-            "xshare_moe_forward_fp8", "xshare_moe_layer", "xshare_router_logits"} <= set(names)
+            "xshare_moe_forward_fp8", "xshare_moe_forward_mxfp4", "xshare_moe_layer",
+            "xshare_router_logits", "xshare_layer_budgets"} <= set(names)
     lib = X.lib()
     for n in names:
         assert hasattr(lib, n), n
@@ -258,3 +259,23 @@ def test_moe_forward_fp8_validation():
     assert call(s3=None) == X.EINVAL                 # scales are required
     assert call(q3=FAKE_ODD) == X.EINVAL             # 16-byte alignment
     assert call(d=40) == X.EUNSUPPORTED
+
+
+def test_moe_forward_mxfp4_validation():
+    L = X.lib()
+    p = X.params(16, 2, 1, 8)
+
+    def call(q1=FAKE, q3=FAKE, q2=FAKE, e1=FAKE, e3=FAKE, e2=FAKE, d=64, f=128, T=8):
+        return L.xshare_moe_forward_mxfp4(FAKE, FAKE, T, d, f, q1, q3, q2, e1, e3, e2,
+                                          ctypes.byref(p), None, None, 0, None, FAKE, None,
+                                          None, None, None, None, 1 << 30, None, None)
+
+    assert call() == X.EWORKSPACE
+    assert call(q1=None) == X.EINVAL
+    assert call(q2=None) == X.EINVAL
+    assert call(e1=None) == X.EINVAL                 # block scales are required
+    assert call(e2=None) == X.EINVAL
+    assert call(q3=FAKE_ODD) == X.EINVAL             # 16-byte alignment of the codes
+    assert call(e3=FAKE_ODD) == X.EWORKSPACE         # scale bytes need no alignment
+    assert call(d=48) == X.EUNSUPPORTED              # d, f multiples of 32
+    assert call(f=80) == X.EUNSUPPORTED
