@@ -59,6 +59,14 @@ def test_ffn_ragged_shapes():
         _run(c, 0, 1, M, label=f"ragged T{T} d{d} f{f}")
 
 
+def test_ffn_largest_batches():
+    """The size limits: T * k = 8192 (token, slot) rows, and T = 4096 tokens; many tokens per
+    expert, so the GEMMs loop over several 32-token passes."""
+    for T, N, k, d, f, M in [(1024, 64, 8, 64, 64, 24), (4096, 16, 2, 32, 64, 4)]:
+        c = dict(N=N, k=k, d=d, f=f, T=T, logits="domains", Q=4)
+        _run(c, 0, 1, M, label=f"largest T{T} k{k}")
+
+
 def test_ffn_split_reduction():
     """Few, wide experts: the down GEMM splits f into 8, 8, 4 and 2 parts and the gate/up
     GEMM splits d into 8 and 4 parts (partials summed in split order); within tolerance."""

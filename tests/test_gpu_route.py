@@ -76,7 +76,8 @@ def test_route_adversarial_ties_and_signed_zero():
 def test_route_shapes_edges():
     rng = np.random.default_rng(1)
     for T, N, k, M in [(0, 16, 2, 8), (1, 256, 8, 8), (37, 200, 6, 30), (5, 1024, 32, 100),
-                       (64, 8, 2, 5), (3, 1, 1, 1), (1024, 256, 8, 96), (2048, 64, 4, 16)]:
+                       (64, 8, 2, 5), (3, 1, 1, 1), (1024, 256, 8, 96), (2048, 64, 4, 16),
+                       (4096, 16, 2, 8)]:
         h = rng.standard_normal((T, N)).astype(F32)
         _case(h, k, min(1, k), M, "total", label=f"edge T{T} N{N}")
         _case(h, k, min(2, k), 3, "extra", label=f"edge T{T} N{N}")
