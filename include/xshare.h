@@ -20,7 +20,9 @@
  *   (size from the matching *_workspace_bytes function, 256-byte aligned).
  * - Calls are asynchronous and stream-ordered on `stream` (a hipStream_t; NULL = the
  *   default stream).  Outputs are valid once the stream has reached the end of the call.
- *   Nothing is copied back to the host and the stream is never synchronised.
+ *   Nothing is copied back to the host and the stream is never synchronised.  A call only
+ *   launches kernels (no memset, copy or allocation), so it can be captured in a HIP graph
+ *   and replayed with the same pointers; calls that share a workspace must be ordered.
  * - Host-checkable errors are returned before anything is enqueued: XSHARE_EINVAL for an
  *   invalid argument, XSHARE_EUNSUPPORTED for a valid size outside the kernels' limits,
  *   XSHARE_EWORKSPACE when ws_bytes is too small.  XSHARE_EHIP reports a failed launch.
