@@ -377,6 +377,12 @@ __device__ __forceinline__ void wave_pass_q4(const uint16_t* const (&arow)[TL], 
 #ifndef XS_Q8_DOWN_U
 #define XS_Q8_DOWN_U 4
 #endif
+// gate/up launches whose grid keeps at least this many blocks with two column tiles per
+// wave use two (measured: DeepSeek T=32 gate/up -1 % bf16, -5 % FP8, -10 % MXFP4; a grid
+// half that size, as at T=8, ran 10-14 % slower).
+#ifndef XS_GU_CT2_MIN_BLOCKS
+#define XS_GU_CT2_MIN_BLOCKS 768
+#endif
 #ifndef XS_Q4_GATE_UP_U
 #define XS_Q4_GATE_UP_U 8
 #endif
@@ -439,25 +445,31 @@ __device__ __forceinline__ const uint8_t* slot_q(const FfnArgs& a, const SlotWor
 
 // kSplit: the block covers one part of the reduction (blockIdx.z) and writes fp32 gate and
 // up partials; otherwise it covers all of d and writes H directly.
-template <int U, bool kSplit, int kW>
+// CT: column tiles (16 weight rows of W1 and of W3 each) per wave; with two, one token load
+// feeds four weight tiles instead of two, at the cost of registers and of half as many
+// blocks (the launch takes two only for grids that stay large).
+template <int U, bool kSplit, int kW, int CT>
 __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
+  constexpr int NM = 2 * CT;                   // weight tiles: W1 and W3 of each column tile
   SlotWork sw;
   if (!slot_work(a, blockIdx.y, sw)) return;
   const int p0 = sw.p0, te = sw.te;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int j0 = (blockIdx.x * kWaves + wave) * kCols;
+  const int j0 = (blockIdx.x * kWaves + wave) * kCols * CT;
   if (j0 >= a.f) return;
   const int n = lane & 15, g = lane >> 4;
   const int d = a.d, f = a.f;
   const int Kg = kSplit ? d / a.gu_splits : d;   // this block's part of the reduction
   const size_t k0 = (kSplit ? (size_t)blockIdx.z * Kg : 0) +
                     (size_t)(kW == kBf16 ? klane<U>(g) : g * 8 * U);
-  const size_t wrow = (size_t)(j0 + n) * d + k0;
   const size_t plane = (size_t)a.rows * f;     // one fp32 partial plane [rows, f]
-  float sc1 = 1.0f, sc3 = 1.0f;                // FP8 per-row scales of this lane's column
-  if (kW == kFp8) {
-    sc1 = a.s1[(size_t)sw.e * f + j0 + n];
-    sc3 = a.s3[(size_t)sw.e * f + j0 + n];
+  int col[CT];                                 // this lane's column of each tile (< f)
+  float sc[NM];                                // FP8 per-row scales (else 1)
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct) {
+    col[ct] = min(j0 + 16 * ct, f - 16) + n;
+    sc[2 * ct] = kW == kFp8 ? a.s1[(size_t)sw.e * f + col[ct]] : 1.0f;
+    sc[2 * ct + 1] = kW == kFp8 ? a.s3[(size_t)sw.e * f + col[ct]] : 1.0f;
   }
 
   for (int c0 = 0; c0 < te; c0 += 16 * kTiles) {
@@ -469,25 +481,42 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
       const int tok = sw.shared ? t : a.perm[p0 + t] / a.k;
       arow[rt] = a.x + (size_t)tok * d + k0;
     }
-    floatx4 acc[2][kTiles];
+    floatx4 acc[NM][kTiles];
 #pragma unroll
-    for (int m = 0; m < 2; ++m)
+    for (int m = 0; m < NM; ++m)
 #pragma unroll
       for (int rt = 0; rt < kTiles; ++rt) acc[m][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
     if constexpr (kW == kFp8) {
-      const uint8_t* const brow[2] = {slot_q(a, sw, a.q1) + wrow, slot_q(a, sw, a.q3) + wrow};
-      wave_pass_q8<U, 2>(arow, nt, brow, Kg, acc);
+      const uint8_t* brow[NM];
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) {
+        const size_t wrow = (size_t)col[ct] * d + k0;
+        brow[2 * ct] = slot_q(a, sw, a.q1) + wrow;
+        brow[2 * ct + 1] = slot_q(a, sw, a.q3) + wrow;
+      }
+      wave_pass_q8<U, NM>(arow, nt, brow, Kg, acc);
     } else if constexpr (kW == kMx4) {
-      // row j0 + n of the expert: d / 2 code bytes, d / 32 scale bytes
-      const size_t r = (size_t)sw.e * f + j0 + n;
-      const uint8_t* const brow[2] = {a.q1 + r * (d / 2) + k0 / 2, a.q3 + r * (d / 2) + k0 / 2};
-      const uint8_t* const srow[2] = {a.e1 + r * (d / 32) + k0 / 32,
-                                      a.e3 + r * (d / 32) + k0 / 32};
-      wave_pass_q4<U, 2>(arow, nt, brow, srow, Kg, acc);
+      // row col of the expert: d / 2 code bytes, d / 32 scale bytes
+      const uint8_t* brow[NM];
+      const uint8_t* srow[NM];
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) {
+        const size_t r = (size_t)sw.e * f + col[ct];
+        brow[2 * ct] = a.q1 + r * (d / 2) + k0 / 2;
+        brow[2 * ct + 1] = a.q3 + r * (d / 2) + k0 / 2;
+        srow[2 * ct] = a.e1 + r * (d / 32) + k0 / 32;
+        srow[2 * ct + 1] = a.e3 + r * (d / 32) + k0 / 32;
+      }
+      wave_pass_q4<U, NM>(arow, nt, brow, srow, Kg, acc);
     } else {
-      const uint16_t* const brow[2] = {slot_w(a, sw, a.w1, a.sw1) + wrow,
-                                       slot_w(a, sw, a.w3, a.sw3) + wrow};
-      wave_pass<U, 2, XS_GATE_UP_ADBL != 0>(arow, nt, brow, Kg, acc);
+      const uint16_t* brow[NM];
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) {
+        const size_t wrow = (size_t)col[ct] * d + k0;
+        brow[2 * ct] = slot_w(a, sw, a.w1, a.sw1) + wrow;
+        brow[2 * ct + 1] = slot_w(a, sw, a.w3, a.sw3) + wrow;
+      }
+      wave_pass<U, NM, XS_GATE_UP_ADBL != 0>(arow, nt, brow, Kg, acc);
     }
 #pragma unroll
     for (int rt = 0; rt < kTiles; ++rt) {
@@ -496,14 +525,19 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
       for (int i = 0; i < 4; ++i) {
         const int t = c0 + rt * 16 + 4 * g + i;
         if (t < te) {
-          const float h1 = acc[0][rt][i] * sc1, h3 = acc[1][rt][i] * sc3;
-          const size_t at = (size_t)(p0 + t) * f + j0 + n;
-          if (!kSplit) {
-            store_hilo(a.h, p0 + t, j0 + n, f, h1 / (1.0f + __expf(-h1)) * h3);
-          } else {
-            float* const part = a.gpart + 2 * blockIdx.z * plane;
-            part[at] = h1;
-            part[plane + at] = h3;
+#pragma unroll
+          for (int ct = 0; ct < CT; ++ct) {
+            if (j0 + 16 * ct >= f) break;
+            const float h1 = acc[2 * ct][rt][i] * sc[2 * ct];
+            const float h3 = acc[2 * ct + 1][rt][i] * sc[2 * ct + 1];
+            const size_t at = (size_t)(p0 + t) * f + col[ct];
+            if (!kSplit) {
+              store_hilo(a.h, p0 + t, col[ct], f, h1 / (1.0f + __expf(-h1)) * h3);
+            } else {
+              float* const part = a.gpart + 2 * blockIdx.z * plane;
+              part[at] = h1;
+              part[plane + at] = h3;
+            }
           }
         }
       }
@@ -730,10 +764,18 @@ __global__ __launch_bounds__(kBlock) void router_sum_kernel(RouterArgs r) {
 
 template <int U, int kW>
 void launch_gu(const FfnArgs& a, bool split, dim3 grid, dim3 block, hipStream_t stream) {
-  if (split)
-    hipLaunchKernelGGL((gate_up_kernel<U, true, kW>), grid, block, 0, stream, a);
+  // column tiles per wave: two if the expected active blocks stay enough with them
+  const bool two = (long)((a.f + 2 * kWaves * kCols - 1) / (2 * kWaves * kCols)) *
+                       (a.est_active + a.n_shared) * grid.z >= XS_GU_CT2_MIN_BLOCKS;
+  if (two) grid.x = (a.f + 2 * kWaves * kCols - 1) / (2 * kWaves * kCols);
+  if (split && two)
+    hipLaunchKernelGGL((gate_up_kernel<U, true, kW, 2>), grid, block, 0, stream, a);
+  else if (split)
+    hipLaunchKernelGGL((gate_up_kernel<U, true, kW, 1>), grid, block, 0, stream, a);
+  else if (two)
+    hipLaunchKernelGGL((gate_up_kernel<U, false, kW, 2>), grid, block, 0, stream, a);
   else
-    hipLaunchKernelGGL((gate_up_kernel<U, false, kW>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((gate_up_kernel<U, false, kW, 1>), grid, block, 0, stream, a);
 }
 
 // Unroll U (a power of two <= 8 dividing K / 32) for weight format kW.
@@ -774,8 +816,8 @@ int unroll_for(int K, int want) {
 }  // namespace
 
 hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
-  const dim3 grid((a.f + kWaves * kCols - 1) / (kWaves * kCols), a.max_active + a.n_shared,
-                  a.gu_splits),
+  const int cols = kWaves * kCols;            // one column tile per wave; launch_gu may take two
+  const dim3 grid((a.f + cols - 1) / cols, a.max_active + a.n_shared, a.gu_splits),
       block(kBlock);
   const bool split = a.gu_splits > 1;
   const int K = a.d / a.gu_splits;

@@ -220,6 +220,7 @@ struct FfnArgs {
   int wfmt;                    // 0 bf16, 1 FP8, 2 MXFP4
   int T, N, k, d, f;
   int max_active;              // host bound on the number of active experts (grid size)
+  int est_active;              // experts expected to be active (0: unknown), for launch shapes
   int splits;                  // K-splits of the down GEMM (partials summed in the combine)
   int gu_splits;               // K-splits of the gate/up GEMM (partials summed by finish)
   float* gpart;                // [gu_splits, 2, T * k, f] when gu_splits > 1
