@@ -380,6 +380,16 @@ __device__ __forceinline__ void wave_pass_q4(const uint16_t* const (&arow)[TL], 
 // gate/up launches whose grid keeps at least this many blocks with two column tiles per
 // wave use two (measured: DeepSeek T=32 gate/up -1 % bf16, -5 % FP8, -10 % MXFP4; a grid
 // half that size, as at T=8, ran 10-14 % slower).
+// bf16 down launches use 2 * XS_DOWN_NM tiles per wave when the routed rows are at least
+// XS_DN_WIDE_TOKENS per expected expert and the grid keeps XS_DN_WIDE_MIN_BLOCKS blocks
+// (measured: DeepSeek T=32 down -1.6 %, speculative -3 %; with 1-3 tokens per expert, as at
+// T=8, it ran 4-20 % slower).
+#ifndef XS_DN_WIDE_TOKENS
+#define XS_DN_WIDE_TOKENS 4
+#endif
+#ifndef XS_DN_WIDE_MIN_BLOCKS
+#define XS_DN_WIDE_MIN_BLOCKS 768
+#endif
 #ifndef XS_GU_CT2_MIN_BLOCKS
 #define XS_GU_CT2_MIN_BLOCKS 768
 #endif
@@ -545,10 +555,9 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
   }
 }
 
-template <int U, int kW>
+// NM: 16-row W2 tiles per wave (the launch picks it per weight format and batch shape).
+template <int U, int kW, int NM>
 __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
-  constexpr int NM = kW == kBf16 ? XS_DOWN_NM                 // 16-row W2 tiles per wave
-                   : (kW == kFp8 ? XS_Q8_DOWN_NM : XS_Q4_DOWN_NM);
   constexpr int TL = XS_DOWN_TL;  // token tiles per pass, 8 tokens each (hi and lo rows)
   SlotWork sw;
   if (!slot_work(a, blockIdx.y, sw)) return;
@@ -793,18 +802,20 @@ void launch_gu_fmt(const FfnArgs& a, int u, bool split, dim3 grid, dim3 block,
   else
     launch_gu<1, kW>(a, split, grid, block, stream);
 }
-template <int kW>
-void launch_down_fmt(const FfnArgs& a, int u, dim3 grid, dim3 block, hipStream_t stream) {
+template <int kW, int NM>
+void launch_down_fmt(const FfnArgs& a, int u, hipStream_t stream) {
+  const int cols = kWaves * kCols * NM;
+  const dim3 grid((a.d + cols - 1) / cols, a.max_active + a.n_shared, a.splits), block(kBlock);
   if (u == 8) {
-    hipLaunchKernelGGL((down_kernel<8, kW>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((down_kernel<8, kW, NM>), grid, block, 0, stream, a);
     return;
   }
   if (u >= 4)
-    hipLaunchKernelGGL((down_kernel<4, kW>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((down_kernel<4, kW, NM>), grid, block, 0, stream, a);
   else if (u == 2)
-    hipLaunchKernelGGL((down_kernel<2, kW>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((down_kernel<2, kW, NM>), grid, block, 0, stream, a);
   else
-    hipLaunchKernelGGL((down_kernel<1, kW>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((down_kernel<1, kW, NM>), grid, block, 0, stream, a);
 }
 
 int unroll_for(int K, int want) {
@@ -835,16 +846,24 @@ hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_down(const FfnArgs& a, hipStream_t stream) {
-  const int nm = a.wfmt == kFp8 ? XS_Q8_DOWN_NM : (a.wfmt == kMx4 ? XS_Q4_DOWN_NM : XS_DOWN_NM);
-  const int cols = kWaves * kCols * nm;
-  const dim3 grid((a.d + cols - 1) / cols, a.max_active + a.n_shared, a.splits), block(kBlock);
   const int K = a.f / a.splits;
-  if (a.wfmt == kFp8)
-    launch_down_fmt<kFp8>(a, unroll_for(K, XS_Q8_DOWN_U), grid, block, stream);
-  else if (a.wfmt == kMx4)
-    launch_down_fmt<kMx4>(a, unroll_for(K, XS_Q4_DOWN_U), grid, block, stream);
-  else
-    launch_down_fmt<kBf16>(a, unroll_for(K, XS_DOWN_U), grid, block, stream);
+  if (a.wfmt == kFp8) {
+    launch_down_fmt<kFp8, XS_Q8_DOWN_NM>(a, unroll_for(K, XS_Q8_DOWN_U), stream);
+  } else if (a.wfmt == kMx4) {
+    launch_down_fmt<kMx4, XS_Q4_DOWN_NM>(a, unroll_for(K, XS_Q4_DOWN_U), stream);
+  } else {
+    // twice the rows per wave (one token load feeding four weight tiles) pays when experts
+    // hold several tokens each and the grid stays large
+    const long est = a.est_active + a.n_shared;
+    const bool wide = est > 0 && (long)a.T * a.k >= XS_DN_WIDE_TOKENS * est &&
+                      (long)((a.d + kWaves * kCols * 2 * XS_DOWN_NM - 1) /
+                             (kWaves * kCols * 2 * XS_DOWN_NM)) * est * a.splits >=
+                          XS_DN_WIDE_MIN_BLOCKS;
+    if (wide)
+      launch_down_fmt<kBf16, 2 * XS_DOWN_NM>(a, unroll_for(K, XS_DOWN_U), stream);
+    else
+      launch_down_fmt<kBf16, XS_DOWN_NM>(a, unroll_for(K, XS_DOWN_U), stream);
+  }
   return hipGetLastError();
 }
 
