@@ -380,10 +380,10 @@ __device__ __forceinline__ void wave_pass_q4(const uint16_t* const (&arow)[TL], 
 // gate/up launches whose grid keeps at least this many blocks with two column tiles per
 // wave use two (measured: DeepSeek T=32 gate/up -1 % bf16, -5 % FP8, -10 % MXFP4; a grid
 // half that size, as at T=8, ran 10-14 % slower).
-// bf16 down launches use 2 * XS_DOWN_NM tiles per wave when the routed rows are at least
-// XS_DN_WIDE_TOKENS per expected expert and the grid keeps XS_DN_WIDE_MIN_BLOCKS blocks
-// (measured: DeepSeek T=32 down -1.6 %, speculative -3 %; with 1-3 tokens per expert, as at
-// T=8, it ran 4-20 % slower).
+// bf16 and FP8 down launches use twice the base tiles per wave when the routed rows are at
+// least XS_DN_WIDE_TOKENS per expected expert and the grid keeps XS_DN_WIDE_MIN_BLOCKS blocks
+// (measured on DeepSeek T=32 and the speculative batch: bf16 down -1.6 % and -3 %, FP8 -10 %
+// and -13 %; with 1-3 tokens per expert, as at T=8, wide waves ran 4-20 % slower).
 #ifndef XS_DN_WIDE_TOKENS
 #define XS_DN_WIDE_TOKENS 4
 #endif
@@ -847,18 +847,23 @@ hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
 
 hipError_t launch_down(const FfnArgs& a, hipStream_t stream) {
   const int K = a.f / a.splits;
-  if (a.wfmt == kFp8) {
-    launch_down_fmt<kFp8, XS_Q8_DOWN_NM>(a, unroll_for(K, XS_Q8_DOWN_U), stream);
-  } else if (a.wfmt == kMx4) {
+  if (a.wfmt == kMx4) {
     launch_down_fmt<kMx4, XS_Q4_DOWN_NM>(a, unroll_for(K, XS_Q4_DOWN_U), stream);
+    return hipGetLastError();
+  }
+  // bf16 and FP8: twice the rows per wave (one token load feeding twice the weight tiles)
+  // pays when experts hold several tokens each and the grid stays large
+  const int nm = a.wfmt == kFp8 ? XS_Q8_DOWN_NM : XS_DOWN_NM;
+  const long est = a.est_active + a.n_shared;
+  const bool wide = est > 0 && (long)a.T * a.k >= XS_DN_WIDE_TOKENS * est &&
+                    (long)((a.d + kWaves * kCols * 2 * nm - 1) / (kWaves * kCols * 2 * nm)) *
+                            est * a.splits >= XS_DN_WIDE_MIN_BLOCKS;
+  if (a.wfmt == kFp8) {
+    if (wide)
+      launch_down_fmt<kFp8, 2 * XS_Q8_DOWN_NM>(a, unroll_for(K, XS_Q8_DOWN_U), stream);
+    else
+      launch_down_fmt<kFp8, XS_Q8_DOWN_NM>(a, unroll_for(K, XS_Q8_DOWN_U), stream);
   } else {
-    // twice the rows per wave (one token load feeding four weight tiles) pays when experts
-    // hold several tokens each and the grid stays large
-    const long est = a.est_active + a.n_shared;
-    const bool wide = est > 0 && (long)a.T * a.k >= XS_DN_WIDE_TOKENS * est &&
-                      (long)((a.d + kWaves * kCols * 2 * XS_DOWN_NM - 1) /
-                             (kWaves * kCols * 2 * XS_DOWN_NM)) * est * a.splits >=
-                          XS_DN_WIDE_MIN_BLOCKS;
     if (wide)
       launch_down_fmt<kBf16, 2 * XS_DOWN_NM>(a, unroll_for(K, XS_DOWN_U), stream);
     else

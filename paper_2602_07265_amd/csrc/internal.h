@@ -97,15 +97,16 @@ inline int gate_up_splits(int est_active, int d, int f) {
   return split_for((long)est_active * (f / 16), d, 128, XS_GU_SPLIT_BELOW, XS_GU_SPLIT_TARGET,
                    XS_GATE_UP_MAX_SPLITS);
 }
-// 16-row tiles of W2 per wave of the down GEMM (output rows per wave = 16 * NM): 2 with
-// bf16 weights, 4 with FP8 weights (whose one-byte rows make the shared token operand
-// relatively more expensive), 2 with MXFP4 weights (whose 8-word steps need the registers).  The split counts below use the bf16 figure for both, so the
-// workspace does not depend on the weight format.
+// 16-row tiles of W2 per wave of the down GEMM (output rows per wave = 16 * NM), the base
+// that the launch doubles for bf16 and FP8 when experts hold several tokens each (the shared
+// token operand then serves more weight rows); MXFP4 keeps 2 (its 8-word steps need the
+// registers).  The split counts below use the bf16 base for every format, so the workspace
+// does not depend on the weight format.
 #ifndef XS_DOWN_NM
 #define XS_DOWN_NM 2
 #endif
 #ifndef XS_Q8_DOWN_NM
-#define XS_Q8_DOWN_NM 4
+#define XS_Q8_DOWN_NM 2
 #endif
 #ifndef XS_Q4_DOWN_NM
 #define XS_Q4_DOWN_NM 2
