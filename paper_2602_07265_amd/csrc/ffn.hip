@@ -414,31 +414,32 @@ __device__ __forceinline__ void wave_pass_q4(const uint16_t* const (&arow)[TL], 
 #define XS_DOWN_TL 4                 // 8-token (hi + lo) tiles per pass of the down GEMM
 #endif
 
-// Work of grid row `slot` of the expert GEMMs: the routed active experts first (their
-// tokens' rows in permuted order), then the shared experts (all T tokens, rows
-// T*k + s*T + t).  False for rows beyond both.  `e` is the routed expert or the shared one.
+// Work of grid row `slot` of the expert GEMMs: the always-on shared experts first (all T
+// tokens, rows T*k + s*T + t; their blocks are the longest, so they start first and do
+// not trail the launch), then the routed active experts (their tokens' rows in permuted
+// order).  False for rows beyond both.  `e` is the shared or the routed expert.
 struct SlotWork {
   int e, p0, te;
   bool shared;
 };
 
 __device__ __forceinline__ bool slot_work(const FfnArgs& a, int slot, SlotWork& w) {
-  // both loads are issued together; the record is used only below the count
-  const int n_active = a.counters[kCntActive];
-  const int4 rec = a.active[slot < a.N ? slot : 0];
-  if (slot < n_active) {
-    w.e = rec.x;
-    w.p0 = rec.y;
-    w.te = rec.z;
-    w.shared = false;
+  if (slot < a.n_shared) {
+    w.e = slot;
+    w.p0 = a.T * a.k + slot * a.T;
+    w.te = a.T;
+    w.shared = true;
     return true;
   }
-  const int sh = slot - n_active;
-  if (sh >= a.n_shared) return false;
-  w.e = sh;
-  w.p0 = a.T * a.k + sh * a.T;
-  w.te = a.T;
-  w.shared = true;
+  const int r = slot - a.n_shared;
+  // both loads are issued together; the record is used only below the count
+  const int n_active = a.counters[kCntActive];
+  const int4 rec = a.active[r < a.N ? r : 0];
+  if (r >= n_active) return false;
+  w.e = rec.x;
+  w.p0 = rec.y;
+  w.te = rec.z;
+  w.shared = false;
   return true;
 }
 
