@@ -24,6 +24,10 @@ namespace {
 constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / 64;
 constexpr uint32_t kNoEntry = 0xFFFFu;   // empty slot of the per-token lists
+#ifndef XS_HEAVY_ROWS
+#define XS_HEAVY_ROWS 8
+#endif
+constexpr int kHeavyRows = XS_HEAVY_ROWS;   // active-list class boundary (routed rows)
 
 // exp(x) for x <= 0 in fp32: n = rint(x log2 e); r = (x - n ln2_hi) - n ln2_lo with a
 // 15-bit ln2_hi (Cody-Waite: n ln2_hi is exact); p = degree-7 Taylor polynomial of e^r
@@ -751,8 +755,15 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   const bool listed = j < N && cnt > 0 &&
                       (a.local_group < 0 ||
                        (a.group ? a.group[j] : j / (N / a.G)) == a.local_group);
-  int n_active = 0;
-  const int arank = block_excl_scan(listed ? 1 : 0, s_wsum, n_active);
+  // The active list puts experts with more than kHeavyRows routed rows first (in expert
+  // order), then the others: their GEMM blocks run longest, so they start first instead of
+  // trailing the launch.  One scan counts both classes (16 bits each).
+  const bool heavy = listed && cnt > kHeavyRows;
+  int packed_total = 0;
+  const int packed = block_excl_scan(listed ? (heavy ? 1 : (1 << 16)) : 0, s_wsum, packed_total);
+  const int n_heavy = packed_total & 0xFFFF;
+  const int n_active = n_heavy + (packed_total >> 16);
+  const int arank = heavy ? (packed & 0xFFFF) : n_heavy + (packed >> 16);
   if (j < N) {
     a.offsets[j] = off;
     if (j == N - 1) a.offsets[N] = off + cnt;
