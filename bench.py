@@ -224,6 +224,7 @@ def main():
     stage_ms = {name: float(np.mean([e[i].elapsed_ms(e[i + 1]) for e in evs]))
                 for i, name in enumerate(X.STAGES)}
     gu_ms = np.array([e[1].elapsed_ms(e[2]) for e in evs])
+    step_us = np.array([e[0].elapsed_ms(e[-1]) for e in evs]) * 1e3
     gu_bytes = np.array([gate_up_bytes(act[s % nb], T, k, d, f, wb) for s in range(args.steps)])
     lay_bytes = np.array([layer_bytes(act[s % nb], T, N, d, f, wb) for s in range(args.steps)])
 
@@ -284,6 +285,8 @@ def main():
         "speedup_vs_vanilla": None if vanilla is None else round(vanilla / ms_step, 3),
         "layer_frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
         "stages_us": {kk: round(v * 1e3, 2) for kk, v in stage_ms.items()},
+        "step_us_percentiles": {f"p{q}": round(float(np.percentile(step_us, q)), 2)
+                                for q in (10, 50, 90)},
         "roofline": {"kernel": "gate_up_kernel", "bound": "hbm", "achieved": round(gu_achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(gu_achieved / HBM_PEAK_GBS, 4),
@@ -628,7 +631,7 @@ def cpu_baseline(W, xs, logits, offs, m_r, weights, fmt, T, N, k, k0, M, d, f, m
     except Exception:
         cores = len(os.sched_getaffinity(0))
     print("[bench] cpu baseline: full oracle on rotated batches", file=sys.stderr, flush=True)
-    spent, done, active = 0.0, 0, []
+    spent, spent_route, done, active = 0.0, 0.0, 0, []
     wall0 = time.perf_counter()
     for b in range(len(xs)):
         if done and time.perf_counter() - wall0 > 100.0:     # weight decoding is slow
@@ -655,6 +658,7 @@ def cpu_baseline(W, xs, logits, offs, m_r, weights, fmt, T, N, k, k0, M, d, f, m
         t0 = time.perf_counter()
         OF.moe_forward(xb, r.ids, r.w, lambda e: cache[e])
         spent += t_route + time.perf_counter() - t0
+        spent_route += t_route
         done += 1
         print(f"[bench] cpu baseline: batch {b} done, {spent:.1f} s timed so far", file=sys.stderr,
               flush=True)
@@ -667,6 +671,7 @@ def cpu_baseline(W, xs, logits, offs, m_r, weights, fmt, T, N, k, k0, M, d, f, m
     bytes_batch = float(np.mean([layer_bytes(a, T, N, d, f, wb) for a in active]))
     return {"value": round(bytes_batch / t_batch / 1e9, 3), "unit": "GB/s",
             "us_per_batch": round(t_batch * 1e6, 1), "cores": int(cores), "kind": "oracle",
+            "route_us_per_batch": round(spent_route / done * 1e6, 1),
             "sample": f"full oracle (numpy routing, float64 SwiGLU of all {T} tokens over their "
                       f"{np.mean(active):.0f} active experts) on {done} of the rotated batches, "
                       f"{spent:.1f} s total; BLAS threads = cores, weight conversion "
