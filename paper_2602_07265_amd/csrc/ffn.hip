@@ -358,6 +358,158 @@ __device__ __forceinline__ void wave_pass_q4(const uint16_t* const (&arow)[TL], 
   }
 }
 
+// MXFP4 weights carry a quarter of bf16's bytes, so with tokens loaded per wave (wave_pass_q4)
+// a step issues as many token loads as weight loads, or more: half-line gathers that every
+// wave of the block repeats.  In both expert GEMMs the four waves of a block share the
+// expert, the token rows and the reduction range: this pass has the block load each step's
+// token rows once, coalesced (16 bytes per thread, P threads per row), into a double-buffered
+// LDS tile, and the waves read their A operands from it.  The loads of step s + 1 (tokens,
+// then weights) are issued before the MFMAs of step s, with no branch around them, so the
+// wait before the LDS write covers the token loads only and the weight loads stay in flight
+// across the barrier.  One barrier per step: the writes into the other buffer come after
+// this step's reads of it were fenced by the previous barrier.
+//   gate/up (kDown false): staged rows are x rows, 16 per MFMA tile (lane row n).
+//   down (kDown true): staged rows are H rows (hi and lo chunks interleaved, two elements
+//   per k), 8 per tile: lanes n < 8 read token n's hi chunk, lanes n >= 8 its lo chunk.
+constexpr int kStageRows = 32;            // token rows per pass
+template <int U, bool kDown>
+struct Q4Stage {
+  static_assert(U >= 2, "a step of at least 64 elements: 256 threads cover 32 rows");
+  static constexpr int KB = 32 * U;                  // reduction elements per step
+  static constexpr int AS = kDown ? 2 : 1;           // staged elements per reduction element
+  static constexpr int P = AS * KB / 8;              // 16-byte pieces per row and step
+  static constexpr int TR = kDown ? 8 : 16;          // token rows per MFMA tile
+  // LDS row stride (elements): the rows of one A read start 16 B (x) or 32 B (H, whose lo
+  // lanes read 16 B past their hi lanes) apart modulo 256 B, so they fall in distinct banks
+  static constexpr int LS = AS * KB + (kDown ? 16 : 8);
+  static constexpr int kElems = 2 * kStageRows * LS; // both buffers
+};
+
+// NT: token tiles of the pass (R <= TR * NT rows); NL: loads per thread and step, at least
+// ceil(R * P / 256) (pieces beyond R * P repeat the last one).  Staged row r (r < R) is
+// x[tok[r] * ld ...], x already offset to this block's reduction range.  brow / srow as in
+// wave_pass_q4; acc[m][rt] as in wave_pass_q4 (gate/up) or the down pass.
+template <int U, bool kDown, int NM, int NT, int NL, int TA>
+__device__ __forceinline__ void block_pass_q4(const uint16_t* x, size_t ld, const int* tok,
+                                              int R, const uint8_t* const (&brow)[NM],
+                                              const uint8_t* const (&srow)[NM], int K,
+                                              floatx4 (&acc)[NM][TA], uint16_t* lds) {
+  using S = Q4Stage<U, kDown>;
+  constexpr int KB = S::KB;
+  static_assert(NT <= TA && S::TR * NT <= kStageRows, "tiles of the pass");
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const int t = threadIdx.x, lane = t & 63;
+  const int n = lane & 15, g = lane >> 4;
+  const uint16_t* src[NL];   // this thread's pieces: global source and LDS offset
+  int wofs[NL];
+#pragma unroll
+  for (int i = 0; i < NL; ++i) {
+    const int q = min(t + i * kBlock, R * S::P - 1);
+    const int row = q / S::P, piece = q % S::P;
+    src[i] = x + (size_t)tok[row] * ld + piece * 8;
+    wofs[i] = row * S::LS + piece * 8;
+  }
+  int rofs[NT];              // this lane's A rows (padding lanes repeat the last token row)
+#pragma unroll
+  for (int rt = 0; rt < NT; ++rt)
+    rofs[rt] = kDown ? min(8 * rt + (n & 7), R - 1) * S::LS + 2 * g * 8 * U + (n & 8)
+                     : min(16 * rt + n, R - 1) * S::LS + g * 8 * U;
+
+  u32x4 v[NL];
+  Q4<U> b[NM];
+  uint16_t e[NM];            // 16 bits: a widening at the end of a step would wait for the load
+#pragma unroll
+  for (int i = 0; i < NL; ++i) v[i] = *reinterpret_cast<const u32x4*>(src[i]);
+#pragma unroll
+  for (int m = 0; m < NM; ++m) {
+    b[m] = load_q4<U>(brow[m]);
+    e[m] = load_e8m0<U>(srow[m]);
+  }
+#pragma unroll
+  for (int i = 0; i < NL; ++i) *reinterpret_cast<u32x4*>(lds + wofs[i]) = v[i];
+  __syncthreads();
+
+  // MFMAs of one step from LDS buffer `cur`
+  auto step = [&](const uint16_t* cur) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      bf16x8 xa[NT];
+#pragma unroll
+      for (int rt = 0; rt < NT; ++rt)
+        xa[rt] = *reinterpret_cast<const bf16x8*>(cur + rofs[rt] + S::AS * 8 * u);
+#pragma unroll
+      for (int m = 0; m < NM; ++m) {
+        const uint32_t em = e[m];
+        const float sc = e8m0_scale(U == 8 && u >= 4 ? em >> 8 : em & 0xFFu);
+        const bf16x8 bv = fp4x8_to_bf16(b[m].w[u], sc);
+#pragma unroll
+        for (int rt = 0; rt < NT; ++rt) acc[m][rt] = mfma(xa[rt], bv, acc[m][rt]);
+      }
+    }
+  };
+  int buf = 0;
+  for (int s = KB; s < K; s += KB) {       // loads of step s, MFMAs of step s - KB
+#pragma unroll
+    for (int i = 0; i < NL; ++i) v[i] = *reinterpret_cast<const u32x4*>(src[i] + S::AS * s);
+    Q4<U> nb[NM];
+    uint16_t ne[NM];
+#pragma unroll
+    for (int m = 0; m < NM; ++m) {
+      nb[m] = load_q4<U>(brow[m] + s / 2);
+      ne[m] = load_e8m0<U>(srow[m] + s / 32);
+    }
+    step(lds + buf * kStageRows * S::LS);
+    uint16_t* const nxt = lds + (buf ^ 1) * kStageRows * S::LS;
+#pragma unroll
+    for (int i = 0; i < NL; ++i) *reinterpret_cast<u32x4*>(nxt + wofs[i]) = v[i];
+#pragma unroll
+    for (int m = 0; m < NM; ++m) {
+      b[m] = nb[m];
+      e[m] = ne[m];
+    }
+    __syncthreads();
+    buf ^= 1;
+  }
+  step(lds + buf * kStageRows * S::LS);
+  __syncthreads();                         // the block's next pass rewrites both buffers
+}
+
+// The staged MXFP4 pass over R token rows, by block-uniform instance: the fewest tiles that
+// hold R rows and the loads per thread that the largest R of that tile count needs.
+template <int U, bool kDown, int NM, int TA>
+__device__ __forceinline__ void staged_pass_q4(const uint16_t* x, size_t ld, const int* tok,
+                                               int R, const uint8_t* const (&brow)[NM],
+                                               const uint8_t* const (&srow)[NM], int K,
+                                               floatx4 (&acc)[NM][TA], uint16_t* lds) {
+  using S = Q4Stage<U, kDown>;
+  constexpr int TR = S::TR;
+  constexpr int L1 = (TR * S::P + kBlock - 1) / kBlock, L2 = (2 * TR * S::P + kBlock - 1) / kBlock;
+  if constexpr (TA == 2) {          // gate/up: up to two 16-row tiles
+    constexpr int L1h = (TR / 2 * S::P + kBlock - 1) / kBlock;
+    constexpr int L2h = (3 * TR / 2 * S::P + kBlock - 1) / kBlock;
+    if (R <= TR / 2)
+      block_pass_q4<U, kDown, NM, 1, L1h, TA>(x, ld, tok, R, brow, srow, K, acc, lds);
+    else if (R <= TR)
+      block_pass_q4<U, kDown, NM, 1, L1, TA>(x, ld, tok, R, brow, srow, K, acc, lds);
+    else if (R <= 3 * TR / 2)
+      block_pass_q4<U, kDown, NM, 2, L2h, TA>(x, ld, tok, R, brow, srow, K, acc, lds);
+    else
+      block_pass_q4<U, kDown, NM, 2, L2, TA>(x, ld, tok, R, brow, srow, K, acc, lds);
+  } else {                          // down: up to four 8-token tiles
+    static_assert(TA == 4, "four 8-token tiles");
+    constexpr int L3 = (3 * TR * S::P + kBlock - 1) / kBlock;
+    constexpr int L4 = (4 * TR * S::P + kBlock - 1) / kBlock;
+    if (R <= TR)
+      block_pass_q4<U, kDown, NM, 1, L1, TA>(x, ld, tok, R, brow, srow, K, acc, lds);
+    else if (R <= 2 * TR)
+      block_pass_q4<U, kDown, NM, 2, L2, TA>(x, ld, tok, R, brow, srow, K, acc, lds);
+    else if (R <= 3 * TR)
+      block_pass_q4<U, kDown, NM, 3, L3, TA>(x, ld, tok, R, brow, srow, K, acc, lds);
+    else
+      block_pass_q4<U, kDown, NM, 4, L4, TA>(x, ld, tok, R, brow, srow, K, acc, lds);
+  }
+}
+
 // Unroll (32-element k-groups per step) and token-operand buffering of the two GEMMs.
 #ifndef XS_GATE_UP_U
 #define XS_GATE_UP_U 4
@@ -392,6 +544,9 @@ __device__ __forceinline__ void wave_pass_q4(const uint16_t* const (&arow)[TL], 
 #endif
 #ifndef XS_GU_CT2_MIN_BLOCKS
 #define XS_GU_CT2_MIN_BLOCKS 768
+#endif
+#ifndef XS_Q4_GU_CT2_MIN_BLOCKS
+#define XS_Q4_GU_CT2_MIN_BLOCKS XS_GU_CT2_MIN_BLOCKS
 #endif
 #ifndef XS_Q4_GATE_UP_U
 #define XS_Q4_GATE_UP_U 8
@@ -459,20 +614,25 @@ __device__ __forceinline__ const uint8_t* slot_q(const FfnArgs& a, const SlotWor
 // CT: column tiles (16 weight rows of W1 and of W3 each) per wave; with two, one token load
 // feeds four weight tiles instead of two, at the cost of registers and of half as many
 // blocks (the launch takes two only for grids that stay large).
+// The MXFP4 one-tile instance is held to 168 registers (3 waves per SIMD): left alone the
+// compiler took 175 and 2 waves, and DeepSeek T=8 gate/up ran 14 % slower.
 template <int U, bool kSplit, int kW, int CT>
-__global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
+__global__ __attribute__((amdgpu_waves_per_eu(kW == kMx4 && CT == 1 ? 3 : 1)))
+__launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
   constexpr int NM = 2 * CT;                   // weight tiles: W1 and W3 of each column tile
   SlotWork sw;
   if (!slot_work(a, blockIdx.y, sw)) return;
   const int p0 = sw.p0, te = sw.te;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int j0 = (blockIdx.x * kWaves + wave) * kCols * CT;
-  if (j0 >= a.f) return;
+  // the MXFP4 pass stages tokens with the whole block: a wave past f stays for the staging
+  // and the barriers (its columns are clamped into range and its stores skipped)
+  if ((kW != kMx4 || U < 2) && j0 >= a.f) return;
   const int n = lane & 15, g = lane >> 4;
   const int d = a.d, f = a.f;
   const int Kg = kSplit ? d / a.gu_splits : d;   // this block's part of the reduction
-  const size_t k0 = (kSplit ? (size_t)blockIdx.z * Kg : 0) +
-                    (size_t)(kW == kBf16 ? klane<U>(g) : g * 8 * U);
+  const size_t kbase = kSplit ? (size_t)blockIdx.z * Kg : 0;
+  const size_t k0 = kbase + (size_t)(kW == kBf16 ? klane<U>(g) : g * 8 * U);
   const size_t plane = (size_t)a.rows * f;     // one fp32 partial plane [rows, f]
   int col[CT];                                 // this lane's column of each tile (< f)
   float sc[NM];                                // FP8 per-row scales (else 1)
@@ -518,7 +678,17 @@ __global__ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
         srow[2 * ct] = a.e1 + r * (d / 32) + k0 / 32;
         srow[2 * ct + 1] = a.e3 + r * (d / 32) + k0 / 32;
       }
-      wave_pass_q4<U, NM>(arow, nt, brow, srow, Kg, acc);
+      if constexpr (U >= 2) {
+        __shared__ __align__(16) uint16_t stage[Q4Stage<U, false>::kElems];
+        __shared__ int s_tok[kStageRows];
+        const int R = min(kStageRows, te - c0);
+        if (threadIdx.x < R)
+          s_tok[threadIdx.x] = sw.shared ? c0 + threadIdx.x : a.perm[p0 + c0 + threadIdx.x] / a.k;
+        __syncthreads();
+        staged_pass_q4<U, false, NM, kTiles>(a.x + kbase, d, s_tok, R, brow, srow, Kg, acc, stage);
+      } else {
+        wave_pass_q4<U, NM>(arow, nt, brow, srow, Kg, acc);
+      }
     } else {
       const uint16_t* brow[NM];
 #pragma unroll
@@ -565,7 +735,8 @@ __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
   const int p0 = sw.p0, te = sw.te;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int n0 = (blockIdx.x * kWaves + wave) * kCols * NM;
-  if (n0 >= a.d) return;
+  // the staged MXFP4 pass needs the whole block (see gate_up_kernel)
+  if ((kW != kMx4 || U < 2) && n0 >= a.d) return;
   const int n = lane & 15, g = lane >> 4;
   const int d = a.d, f = a.f;
   const int Ks = f / a.splits;                 // this block's part of the reduction
@@ -614,7 +785,18 @@ __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
         brow[m] = a.q2 + r * (f / 2) + k0 / 2;
         srow[m] = a.e2 + r * (f / 32) + k0 / 32;
       }
-      wave_pass_q4<U, NM, TL, 2>(arow, nt, brow, srow, Ks, acc, k_first);
+      if constexpr (U >= 2) {
+        static_assert(XS_Q4_DOWN_ROT == 0 && TL == 4, "the staged pass starts at k = 0");
+        __shared__ __align__(16) uint16_t stage[Q4Stage<U, true>::kElems];
+        __shared__ int s_tok[kStageRows];
+        const int R = min(kStageRows, te - c0);
+        if (threadIdx.x < R) s_tok[threadIdx.x] = p0 + c0 + threadIdx.x;   // H rows
+        __syncthreads();
+        staged_pass_q4<U, true, NM, TL>(a.h + 2 * (size_t)blockIdx.z * Ks, 2 * (size_t)f, s_tok,
+                                        R, brow, srow, Ks, acc, stage);
+      } else {
+        wave_pass_q4<U, NM, TL, 2>(arow, nt, brow, srow, Ks, acc, k_first);
+      }
     } else {
       const uint16_t* brow[NM];
 #pragma unroll
@@ -775,8 +957,9 @@ __global__ __launch_bounds__(kBlock) void router_sum_kernel(RouterArgs r) {
 template <int U, int kW>
 void launch_gu(const FfnArgs& a, bool split, dim3 grid, dim3 block, hipStream_t stream) {
   // column tiles per wave: two if the expected active blocks stay enough with them
+  const long min_blocks = kW == kMx4 ? XS_Q4_GU_CT2_MIN_BLOCKS : XS_GU_CT2_MIN_BLOCKS;
   const bool two = (long)((a.f + 2 * kWaves * kCols - 1) / (2 * kWaves * kCols)) *
-                       (a.est_active + a.n_shared) * grid.z >= XS_GU_CT2_MIN_BLOCKS;
+                       (a.est_active + a.n_shared) * grid.z >= min_blocks;
   if (two) grid.x = (a.f + 2 * kWaves * kCols - 1) / (2 * kWaves * kCols);
   if (split && two)
     hipLaunchKernelGGL((gate_up_kernel<U, true, kW, 2>), grid, block, 0, stream, a);
