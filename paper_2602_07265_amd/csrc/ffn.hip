@@ -358,26 +358,27 @@ __device__ __forceinline__ void wave_pass_q4(const uint16_t* const (&arow)[TL], 
   }
 }
 
-// MXFP4 weights carry a quarter of bf16's bytes, so with tokens loaded per wave (wave_pass_q4)
-// a step issues as many token loads as weight loads, or more: half-line gathers that every
-// wave of the block repeats.  In both expert GEMMs the four waves of a block share the
-// expert, the token rows and the reduction range: this pass has the block load each step's
-// token rows once, coalesced (16 bytes per thread, P threads per row), into a double-buffered
-// LDS tile, and the waves read their A operands from it.  The loads of step s + 1 (tokens,
-// then weights) are issued before the MFMAs of step s, with no branch around them, so the
-// wait before the LDS write covers the token loads only and the weight loads stay in flight
-// across the barrier.  One barrier per step: the writes into the other buffer come after
-// this step's reads of it were fenced by the previous barrier.
+// Token rows staged in LDS.  With tokens loaded per wave (wave_pass*), every wave of a block
+// gathers the same token rows again, as half-line loads; with MXFP4 weights (a quarter of
+// bf16's bytes) these were as many load instructions as the weights', or more.  In both
+// expert GEMMs the four waves of a block share the expert, the token rows and the reduction
+// range: this pass has the block load each step's token rows once, coalesced (16 bytes per
+// thread, P threads per row), into a double-buffered LDS tile, and the waves read their A
+// operands from it.  The loads of step s + 1 (tokens, then weights) are issued before the
+// MFMAs of step s, with no branch around them, so the wait before the LDS write covers the
+// token loads only and the weight loads stay in flight across the barrier.  One barrier per
+// step: the writes into the other buffer come after this step's reads of it were fenced by
+// the previous barrier.
 //   gate/up (kDown false): staged rows are x rows, 16 per MFMA tile (lane row n).
 //   down (kDown true): staged rows are H rows (hi and lo chunks interleaved, two elements
 //   per k), 8 per tile: lanes n < 8 read token n's hi chunk, lanes n >= 8 its lo chunk.
 constexpr int kStageRows = 32;            // token rows per pass
 template <int U, bool kDown>
-struct Q4Stage {
-  static_assert(U >= 2, "a step of at least 64 elements: 256 threads cover 32 rows");
+struct Stage {
   static constexpr int KB = 32 * U;                  // reduction elements per step
   static constexpr int AS = kDown ? 2 : 1;           // staged elements per reduction element
   static constexpr int P = AS * KB / 8;              // 16-byte pieces per row and step
+  static_assert(P * kStageRows >= kBlock, "256 threads cover at most the 32 rows of a step");
   static constexpr int TR = kDown ? 8 : 16;          // token rows per MFMA tile
   // LDS row stride (elements): the rows of one A read start 16 B (x) or 32 B (H, whose lo
   // lanes read 16 B past their hi lanes) apart modulo 256 B, so they fall in distinct banks
@@ -385,16 +386,66 @@ struct Q4Stage {
   static constexpr int kElems = 2 * kStageRows * LS; // both buffers
 };
 
+// One lane's weights of one step for one 16-row tile, by format: where they are (w: this
+// lane's first element; sc: MXFP4 scale bytes), the registers that hold them, their loads
+// for step s and the B operand of MFMA u.  `koff(g, u)`: the reduction offset, within a
+// step, of lane group g's elements in MFMA u (the A operand reads the same).
+template <int kW, int U>
+struct WTile;
+template <int U>
+struct WTile<kBf16, U> {
+  struct Ptr { const uint16_t* w; };
+  struct Regs { bf16x8 w[U]; };
+  __device__ static constexpr int koff(int g, int u) { return kstep(u) + klane<U>(g); }
+  __device__ static Regs load(const Ptr& p, int s) {
+    Regs r;
+#pragma unroll
+    for (int u = 0; u < U; ++u) r.w[u] = load8(p.w + s + kstep(u));
+    return r;
+  }
+  __device__ static bf16x8 operand(const Regs& r, int u) { return r.w[u]; }
+};
+template <int U>
+struct WTile<kFp8, U> {
+  struct Ptr { const uint8_t* w; };
+  struct Regs { uint2 w[U]; };
+  __device__ static constexpr int koff(int g, int u) { return 8 * U * g + 8 * u; }
+  __device__ static Regs load(const Ptr& p, int s) {
+    Regs r;
+#pragma unroll
+    for (int u = 0; u < U; ++u) r.w[u] = load_q8(p.w + s + 8 * u);
+    return r;
+  }
+  __device__ static bf16x8 operand(const Regs& r, int u) { return fp8x8_to_bf16(r.w[u]); }
+};
+template <int U>
+struct WTile<kMx4, U> {
+  struct Ptr { const uint8_t* w; const uint8_t* sc; };
+  // 16-bit scales: a widening at the end of a step would wait for their load
+  struct Regs { Q4<U> q; uint16_t e; };
+  __device__ static constexpr int koff(int g, int u) { return 8 * U * g + 8 * u; }
+  __device__ static Regs load(const Ptr& p, int s) {
+    Regs r;
+    r.q = load_q4<U>(p.w + s / 2);
+    r.e = load_e8m0<U>(p.sc + s / 32);
+    return r;
+  }
+  __device__ static bf16x8 operand(const Regs& r, int u) {
+    const uint32_t e = r.e;
+    return fp4x8_to_bf16(r.q.w[u], e8m0_scale(U == 8 && u >= 4 ? e >> 8 : e & 0xFFu));
+  }
+};
+
 // NT: token tiles of the pass (R <= TR * NT rows); NL: loads per thread and step, at least
 // ceil(R * P / 256) (pieces beyond R * P repeat the last one).  Staged row r (r < R) is
-// x[tok[r] * ld ...], x already offset to this block's reduction range.  brow / srow as in
-// wave_pass_q4; acc[m][rt] as in wave_pass_q4 (gate/up) or the down pass.
-template <int U, bool kDown, int NM, int NT, int NL, int TA>
-__device__ __forceinline__ void block_pass_q4(const uint16_t* x, size_t ld, const int* tok,
-                                              int R, const uint8_t* const (&brow)[NM],
-                                              const uint8_t* const (&srow)[NM], int K,
-                                              floatx4 (&acc)[NM][TA], uint16_t* lds) {
-  using S = Q4Stage<U, kDown>;
+// x[tok[r] * ld ...], x already offset to this block's reduction range.  acc[m][rt] as in
+// wave_pass (gate/up) or the down pass.
+template <int kW, int U, bool kDown, int NM, int NT, int NL, int TA>
+__device__ __forceinline__ void block_pass(const uint16_t* x, size_t ld, const int* tok, int R,
+                                           const typename WTile<kW, U>::Ptr (&wp)[NM], int K,
+                                           int k_first, floatx4 (&acc)[NM][TA], uint16_t* lds) {
+  using S = Stage<U, kDown>;
+  using WT = WTile<kW, U>;
   constexpr int KB = S::KB;
   static_assert(NT <= TA && S::TR * NT <= kStageRows, "tiles of the pass");
   typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -412,19 +463,15 @@ __device__ __forceinline__ void block_pass_q4(const uint16_t* x, size_t ld, cons
   int rofs[NT];              // this lane's A rows (padding lanes repeat the last token row)
 #pragma unroll
   for (int rt = 0; rt < NT; ++rt)
-    rofs[rt] = kDown ? min(8 * rt + (n & 7), R - 1) * S::LS + 2 * g * 8 * U + (n & 8)
-                     : min(16 * rt + n, R - 1) * S::LS + g * 8 * U;
+    rofs[rt] = kDown ? min(8 * rt + (n & 7), R - 1) * S::LS + (n & 8)
+                     : min(16 * rt + n, R - 1) * S::LS;
 
   u32x4 v[NL];
-  Q4<U> b[NM];
-  uint16_t e[NM];            // 16 bits: a widening at the end of a step would wait for the load
+  typename WT::Regs b[NM];
 #pragma unroll
-  for (int i = 0; i < NL; ++i) v[i] = *reinterpret_cast<const u32x4*>(src[i]);
+  for (int i = 0; i < NL; ++i) v[i] = *reinterpret_cast<const u32x4*>(src[i] + S::AS * k_first);
 #pragma unroll
-  for (int m = 0; m < NM; ++m) {
-    b[m] = load_q4<U>(brow[m]);
-    e[m] = load_e8m0<U>(srow[m]);
-  }
+  for (int m = 0; m < NM; ++m) b[m] = WT::load(wp[m], k_first);
 #pragma unroll
   for (int i = 0; i < NL; ++i) *reinterpret_cast<u32x4*>(lds + wofs[i]) = v[i];
   __syncthreads();
@@ -433,80 +480,76 @@ __device__ __forceinline__ void block_pass_q4(const uint16_t* x, size_t ld, cons
   auto step = [&](const uint16_t* cur) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
+      const int ka = S::AS * WT::koff(g, u);
       bf16x8 xa[NT];
 #pragma unroll
-      for (int rt = 0; rt < NT; ++rt)
-        xa[rt] = *reinterpret_cast<const bf16x8*>(cur + rofs[rt] + S::AS * 8 * u);
+      for (int rt = 0; rt < NT; ++rt) xa[rt] = *reinterpret_cast<const bf16x8*>(cur + rofs[rt] + ka);
 #pragma unroll
       for (int m = 0; m < NM; ++m) {
-        const uint32_t em = e[m];
-        const float sc = e8m0_scale(U == 8 && u >= 4 ? em >> 8 : em & 0xFFu);
-        const bf16x8 bv = fp4x8_to_bf16(b[m].w[u], sc);
+        const bf16x8 bv = WT::operand(b[m], u);
 #pragma unroll
         for (int rt = 0; rt < NT; ++rt) acc[m][rt] = mfma(xa[rt], bv, acc[m][rt]);
       }
     }
   };
   int buf = 0;
-  for (int s = KB; s < K; s += KB) {       // loads of step s, MFMAs of step s - KB
+  // loads of step kn, MFMAs of the step before it, then kn's tokens into the other buffer
+  auto advance = [&](int kn) {
 #pragma unroll
-    for (int i = 0; i < NL; ++i) v[i] = *reinterpret_cast<const u32x4*>(src[i] + S::AS * s);
-    Q4<U> nb[NM];
-    uint16_t ne[NM];
+    for (int i = 0; i < NL; ++i) v[i] = *reinterpret_cast<const u32x4*>(src[i] + S::AS * kn);
+    typename WT::Regs nb[NM];
 #pragma unroll
-    for (int m = 0; m < NM; ++m) {
-      nb[m] = load_q4<U>(brow[m] + s / 2);
-      ne[m] = load_e8m0<U>(srow[m] + s / 32);
-    }
+    for (int m = 0; m < NM; ++m) nb[m] = WT::load(wp[m], kn);
     step(lds + buf * kStageRows * S::LS);
     uint16_t* const nxt = lds + (buf ^ 1) * kStageRows * S::LS;
 #pragma unroll
     for (int i = 0; i < NL; ++i) *reinterpret_cast<u32x4*>(nxt + wofs[i]) = v[i];
 #pragma unroll
-    for (int m = 0; m < NM; ++m) {
-      b[m] = nb[m];
-      e[m] = ne[m];
-    }
+    for (int m = 0; m < NM; ++m) b[m] = nb[m];
     __syncthreads();
     buf ^= 1;
-  }
+  };
+  // the pass starts at step k_first and wraps around (two plain loops: a wrap test inside
+  // one loop measured slower)
+  for (int kn = k_first + KB; kn < K; kn += KB) advance(kn);
+  for (int kn = 0; kn < k_first; kn += KB) advance(kn);
   step(lds + buf * kStageRows * S::LS);
   __syncthreads();                         // the block's next pass rewrites both buffers
 }
 
-// The staged MXFP4 pass over R token rows, by block-uniform instance: the fewest tiles that
-// hold R rows and the loads per thread that the largest R of that tile count needs.
-template <int U, bool kDown, int NM, int TA>
-__device__ __forceinline__ void staged_pass_q4(const uint16_t* x, size_t ld, const int* tok,
-                                               int R, const uint8_t* const (&brow)[NM],
-                                               const uint8_t* const (&srow)[NM], int K,
-                                               floatx4 (&acc)[NM][TA], uint16_t* lds) {
-  using S = Q4Stage<U, kDown>;
+// The staged pass over R token rows, by block-uniform instance: the fewest tiles that hold
+// R rows and the loads per thread that the largest R of that tile count needs.
+template <int kW, int U, bool kDown, int NM, int TA>
+__device__ __forceinline__ void staged_pass(const uint16_t* x, size_t ld, const int* tok, int R,
+                                            const typename WTile<kW, U>::Ptr (&wp)[NM], int K,
+                                            int k_first, floatx4 (&acc)[NM][TA],
+                                            uint16_t* lds) {
+  using S = Stage<U, kDown>;
   constexpr int TR = S::TR;
   constexpr int L1 = (TR * S::P + kBlock - 1) / kBlock, L2 = (2 * TR * S::P + kBlock - 1) / kBlock;
   if constexpr (TA == 2) {          // gate/up: up to two 16-row tiles
     constexpr int L1h = (TR / 2 * S::P + kBlock - 1) / kBlock;
     constexpr int L2h = (3 * TR / 2 * S::P + kBlock - 1) / kBlock;
     if (R <= TR / 2)
-      block_pass_q4<U, kDown, NM, 1, L1h, TA>(x, ld, tok, R, brow, srow, K, acc, lds);
+      block_pass<kW, U, kDown, NM, 1, L1h, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
     else if (R <= TR)
-      block_pass_q4<U, kDown, NM, 1, L1, TA>(x, ld, tok, R, brow, srow, K, acc, lds);
+      block_pass<kW, U, kDown, NM, 1, L1, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
     else if (R <= 3 * TR / 2)
-      block_pass_q4<U, kDown, NM, 2, L2h, TA>(x, ld, tok, R, brow, srow, K, acc, lds);
+      block_pass<kW, U, kDown, NM, 2, L2h, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
     else
-      block_pass_q4<U, kDown, NM, 2, L2, TA>(x, ld, tok, R, brow, srow, K, acc, lds);
+      block_pass<kW, U, kDown, NM, 2, L2, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
   } else {                          // down: up to four 8-token tiles
     static_assert(TA == 4, "four 8-token tiles");
     constexpr int L3 = (3 * TR * S::P + kBlock - 1) / kBlock;
     constexpr int L4 = (4 * TR * S::P + kBlock - 1) / kBlock;
     if (R <= TR)
-      block_pass_q4<U, kDown, NM, 1, L1, TA>(x, ld, tok, R, brow, srow, K, acc, lds);
+      block_pass<kW, U, kDown, NM, 1, L1, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
     else if (R <= 2 * TR)
-      block_pass_q4<U, kDown, NM, 2, L2, TA>(x, ld, tok, R, brow, srow, K, acc, lds);
+      block_pass<kW, U, kDown, NM, 2, L2, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
     else if (R <= 3 * TR)
-      block_pass_q4<U, kDown, NM, 3, L3, TA>(x, ld, tok, R, brow, srow, K, acc, lds);
+      block_pass<kW, U, kDown, NM, 3, L3, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
     else
-      block_pass_q4<U, kDown, NM, 4, L4, TA>(x, ld, tok, R, brow, srow, K, acc, lds);
+      block_pass<kW, U, kDown, NM, 4, L4, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
   }
 }
 
@@ -557,8 +600,9 @@ __device__ __forceinline__ void staged_pass_q4(const uint16_t* x, size_t ld, con
 #ifndef XS_Q4_DOWN_ROT
 #define XS_Q4_DOWN_ROT 0
 #endif
-// K steps between the starts of consecutive down waves: one with bf16 weights (DeepSeek
-// T=32 down 270 -> 263 us); none with FP8, where it measured no gain.
+// K steps between the starts of consecutive down waves (blocks, when the pass is staged):
+// one with bf16 weights (per wave: DeepSeek T=32 down 270 -> 263 us; per block, staged:
+// 266 -> 258 us, speculative 358 -> 351 us); none with FP8, where it measured no gain.
 #ifndef XS_DOWN_ROT
 #define XS_DOWN_ROT 1
 #endif
@@ -568,6 +612,23 @@ __device__ __forceinline__ void staged_pass_q4(const uint16_t* x, size_t ld, con
 #ifndef XS_DOWN_TL
 #define XS_DOWN_TL 4                 // 8-token (hi + lo) tiles per pass of the down GEMM
 #endif
+
+// Formats whose GEMMs stage the token rows in LDS (bit kW of each mask; all three by
+// default).  Same-box A/B against per-wave token loads, gate/up and down (us):
+//   bf16  DeepSeek T=32 M=48  469 / 262 -> 460 / 258   M=24  250 / 165 -> 245 / 138
+//         Qwen M=32            64 /  40 ->  53 /  32   DeepSeek T=8  236 / 132 -> 237 / 132
+//   FP8   DeepSeek T=32 M=48  249 / 147 -> 249 / 138   speculative  371 / 209 -> 329 / 189
+//   MXFP4 DeepSeek T=32 M=48  193 / 142 -> 170 /  99   Qwen M=32     44 /  32 ->  25 /  19
+// A staged down pass rotates its start by block, not by wave (the waves of a block share
+// one token step).
+#ifndef XS_STAGE_GATE_UP
+#define XS_STAGE_GATE_UP 7
+#endif
+#ifndef XS_STAGE_DOWN
+#define XS_STAGE_DOWN 7
+#endif
+constexpr bool stage_gate_up(int kW, int U) { return ((XS_STAGE_GATE_UP >> kW) & 1) && U >= 2; }
+constexpr bool stage_down(int kW) { return (XS_STAGE_DOWN >> kW) & 1; }
 
 // Work of grid row `slot` of the expert GEMMs: the always-on shared experts first (all T
 // tokens, rows T*k + s*T + t; their blocks are the longest, so they start first and do
@@ -625,9 +686,10 @@ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
   const int p0 = sw.p0, te = sw.te;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int j0 = (blockIdx.x * kWaves + wave) * kCols * CT;
-  // the MXFP4 pass stages tokens with the whole block: a wave past f stays for the staging
-  // and the barriers (its columns are clamped into range and its stores skipped)
-  if ((kW != kMx4 || U < 2) && j0 >= a.f) return;
+  // a staged pass needs the whole block: a wave past f stays for the staging and the
+  // barriers (its columns are clamped into range and its stores skipped)
+  constexpr bool kStaged = stage_gate_up(kW, U);
+  if (!kStaged && j0 >= a.f) return;
   const int n = lane & 15, g = lane >> 4;
   const int d = a.d, f = a.f;
   const int Kg = kSplit ? d / a.gu_splits : d;   // this block's part of the reduction
@@ -657,7 +719,31 @@ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
     for (int m = 0; m < NM; ++m)
 #pragma unroll
       for (int rt = 0; rt < kTiles; ++rt) acc[m][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    if constexpr (kW == kFp8) {
+    if constexpr (kStaged) {
+      typename WTile<kW, U>::Ptr wp[NM];
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) {
+        const size_t wrow = (size_t)col[ct] * d + k0;
+        if constexpr (kW == kBf16) {
+          wp[2 * ct].w = slot_w(a, sw, a.w1, a.sw1) + wrow;
+          wp[2 * ct + 1].w = slot_w(a, sw, a.w3, a.sw3) + wrow;
+        } else if constexpr (kW == kFp8) {
+          wp[2 * ct].w = slot_q(a, sw, a.q1) + wrow;
+          wp[2 * ct + 1].w = slot_q(a, sw, a.q3) + wrow;
+        } else {        // row col of the expert: d / 2 code bytes, d / 32 scale bytes
+          const size_t r = (size_t)sw.e * f + col[ct];
+          wp[2 * ct] = {a.q1 + r * (d / 2) + k0 / 2, a.e1 + r * (d / 32) + k0 / 32};
+          wp[2 * ct + 1] = {a.q3 + r * (d / 2) + k0 / 2, a.e3 + r * (d / 32) + k0 / 32};
+        }
+      }
+      __shared__ __align__(16) uint16_t stage[Stage<U, false>::kElems];
+      __shared__ int s_tok[kStageRows];
+      const int R = min(kStageRows, te - c0);
+      if (threadIdx.x < R)
+        s_tok[threadIdx.x] = sw.shared ? c0 + threadIdx.x : a.perm[p0 + c0 + threadIdx.x] / a.k;
+      __syncthreads();
+      staged_pass<kW, U, false, NM, kTiles>(a.x + kbase, d, s_tok, R, wp, Kg, 0, acc, stage);
+    } else if constexpr (kW == kFp8) {
       const uint8_t* brow[NM];
 #pragma unroll
       for (int ct = 0; ct < CT; ++ct) {
@@ -678,17 +764,7 @@ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
         srow[2 * ct] = a.e1 + r * (d / 32) + k0 / 32;
         srow[2 * ct + 1] = a.e3 + r * (d / 32) + k0 / 32;
       }
-      if constexpr (U >= 2) {
-        __shared__ __align__(16) uint16_t stage[Q4Stage<U, false>::kElems];
-        __shared__ int s_tok[kStageRows];
-        const int R = min(kStageRows, te - c0);
-        if (threadIdx.x < R)
-          s_tok[threadIdx.x] = sw.shared ? c0 + threadIdx.x : a.perm[p0 + c0 + threadIdx.x] / a.k;
-        __syncthreads();
-        staged_pass_q4<U, false, NM, kTiles>(a.x + kbase, d, s_tok, R, brow, srow, Kg, acc, stage);
-      } else {
-        wave_pass_q4<U, NM>(arow, nt, brow, srow, Kg, acc);
-      }
+      wave_pass_q4<U, NM>(arow, nt, brow, srow, Kg, acc);
     } else {
       const uint16_t* brow[NM];
 #pragma unroll
@@ -727,16 +803,20 @@ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
 }
 
 // NM: 16-row W2 tiles per wave (the launch picks it per weight format and batch shape).
+// Staged down instances are held to 2 waves per SIMD: left alone the compiler took 1 for the
+// 64-row bf16 and FP8 instances (FP8 DeepSeek T=32 down 166 -> 138 us with the hint).
 template <int U, int kW, int NM>
-__global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
+__global__ __attribute__((amdgpu_waves_per_eu(stage_down(kW) ? 2 : 1)))
+__launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
   constexpr int TL = XS_DOWN_TL;  // token tiles per pass, 8 tokens each (hi and lo rows)
   SlotWork sw;
   if (!slot_work(a, blockIdx.y, sw)) return;
   const int p0 = sw.p0, te = sw.te;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int n0 = (blockIdx.x * kWaves + wave) * kCols * NM;
-  // the staged MXFP4 pass needs the whole block (see gate_up_kernel)
-  if ((kW != kMx4 || U < 2) && n0 >= a.d) return;
+  // a staged pass needs the whole block (see gate_up_kernel)
+  constexpr bool kStaged = stage_down(kW);
+  if (!kStaged && n0 >= a.d) return;
   const int n = lane & 15, g = lane >> 4;
   const int d = a.d, f = a.f;
   const int Ks = f / a.splits;                 // this block's part of the reduction
@@ -771,7 +851,30 @@ __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
     // same order would read the same offsets of every row at the same time.
     const int rot = kW == kBf16 ? XS_DOWN_ROT : (kW == kFp8 ? XS_Q8_DOWN_ROT : XS_Q4_DOWN_ROT);
     const int k_first = (int)(((blockIdx.x * kWaves + wave) * rot) % (Ks / (32 * U))) * 32 * U;
-    if constexpr (kW == kFp8) {
+    if constexpr (kStaged) {
+      static_assert(TL == 4, "the staged pass takes four 8-token tiles");
+      typename WTile<kW, U>::Ptr wp[NM];
+#pragma unroll
+      for (int m = 0; m < NM; ++m) {
+        if constexpr (kW == kBf16) {
+          wp[m].w = slot_w(a, sw, a.w2, a.sw2) + wrow[m];
+        } else if constexpr (kW == kFp8) {
+          wp[m].w = slot_q(a, sw, a.q2) + wrow[m];
+        } else {
+          const size_t r = (size_t)sw.e * d + rowm[m];      // f / 2 code, f / 32 scale bytes
+          wp[m] = {a.q2 + r * (f / 2) + k0 / 2, a.e2 + r * (f / 32) + k0 / 32};
+        }
+      }
+      __shared__ __align__(16) uint16_t stage[Stage<U, true>::kElems];
+      __shared__ int s_tok[kStageRows];
+      const int R = min(kStageRows, te - c0);
+      if (threadIdx.x < R) s_tok[threadIdx.x] = p0 + c0 + threadIdx.x;   // H rows
+      __syncthreads();
+      // staged: consecutive blocks, not waves, start their pass `rot` steps apart
+      const int kb_first = (int)((blockIdx.x * rot) % (Ks / (32 * U))) * 32 * U;
+      staged_pass<kW, U, true, NM, TL>(a.h + 2 * (size_t)blockIdx.z * Ks, 2 * (size_t)f, s_tok, R,
+                                       wp, Ks, kb_first, acc, stage);
+    } else if constexpr (kW == kFp8) {
       const uint8_t* brow[NM];
 #pragma unroll
       for (int m = 0; m < NM; ++m) brow[m] = slot_q(a, sw, a.q2) + wrow[m];
@@ -785,18 +888,7 @@ __global__ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
         brow[m] = a.q2 + r * (f / 2) + k0 / 2;
         srow[m] = a.e2 + r * (f / 32) + k0 / 32;
       }
-      if constexpr (U >= 2) {
-        static_assert(XS_Q4_DOWN_ROT == 0 && TL == 4, "the staged pass starts at k = 0");
-        __shared__ __align__(16) uint16_t stage[Q4Stage<U, true>::kElems];
-        __shared__ int s_tok[kStageRows];
-        const int R = min(kStageRows, te - c0);
-        if (threadIdx.x < R) s_tok[threadIdx.x] = p0 + c0 + threadIdx.x;   // H rows
-        __syncthreads();
-        staged_pass_q4<U, true, NM, TL>(a.h + 2 * (size_t)blockIdx.z * Ks, 2 * (size_t)f, s_tok,
-                                        R, brow, srow, Ks, acc, stage);
-      } else {
-        wave_pass_q4<U, NM, TL, 2>(arow, nt, brow, srow, Ks, acc, k_first);
-      }
+      wave_pass_q4<U, NM, TL, 2>(arow, nt, brow, srow, Ks, acc, k_first);
     } else {
       const uint16_t* brow[NM];
 #pragma unroll

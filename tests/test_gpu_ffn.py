@@ -67,6 +67,17 @@ def test_ffn_largest_batches():
         _run(c, 0, 1, M, label=f"largest T{T} k{k}")
 
 
+def test_ffn_many_rows_per_expert():
+    """Few experts holding many rows each: the GEMMs stage up to 32 token rows per pass in
+    LDS, so these cases run passes of 32 rows followed by ragged ones (1-8, 9-16, 17-24,
+    25-32 rows), with 128- and 64-element steps, a rotated down pass and blocks whose last
+    waves lie past f or d."""
+    for T, N, k, d, f, M in [(70, 8, 4, 256, 512, 4), (40, 6, 3, 384, 192, 3),
+                             (20, 4, 2, 192, 320, 2), (45, 8, 2, 320, 256, 3)]:
+        c = dict(N=N, k=k, d=d, f=f, T=T, logits="domains", Q=2)
+        _run(c, 0, 1, M, label=f"many rows T{T} d{d} f{f} M{M}")
+
+
 def test_ffn_split_reduction():
     """Few, wide experts: the down GEMM splits f into 8, 8, 4 and 2 parts and the gate/up
     GEMM splits d into 8 and 4 parts (partials summed in split order); within tolerance."""

@@ -76,6 +76,15 @@ def test_fp8_tiny_and_ragged():
              label=f"ragged T{T} d{d} f{f}")
 
 
+def test_fp8_many_rows_per_expert():
+    """Few experts holding many rows each: passes of 32 staged token rows, then ragged ones
+    (1-8, 9-16, 17-24, 25-32 rows), with blocks whose last waves lie past f or d."""
+    for T, N, k, d, f, M in [(70, 8, 4, 256, 512, 4), (40, 6, 3, 384, 192, 3),
+                             (20, 4, 2, 192, 320, 2), (45, 8, 2, 320, 256, 3)]:
+        _run(dict(N=N, k=k, d=d, f=f, T=T, logits="domains", Q=2), 0, 1, M,
+             label=f"many rows T{T} d{d} f{f} M{M}")
+
+
 def test_fp8_every_code():
     """Weights cycling through every finite E4M3FN code (both signs, subnormals, 448) with
     power-of-two scales: the kernels' hardware decode must agree with the format."""
