@@ -213,6 +213,8 @@ struct Weights {
     return w1 && w3 && w2;
   }
   bool aligned() const {
+    auto even = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 1u) == 0; };
+    if (fmt == 2 && !(even(e1) && even(e3) && even(e2))) return false;   // scale pairs
     return fmt ? (aligned16(q1) && aligned16(q3) && aligned16(q2))
                : (aligned16(w1) && aligned16(w3) && aligned16(w2));
   }

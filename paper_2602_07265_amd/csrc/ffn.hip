@@ -21,6 +21,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "internal.h"
 
 namespace xs {
@@ -85,7 +87,16 @@ struct Q4 {
 template <int U>
 __device__ __forceinline__ Q4<U> load_q4(const uint8_t* p) {
   Q4<U> r;
-  if constexpr (U == 8) {
+  if constexpr (U == 16) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint4 v = *reinterpret_cast<const uint4*>(p + 16 * i);
+      r.w[4 * i] = v.x;
+      r.w[4 * i + 1] = v.y;
+      r.w[4 * i + 2] = v.z;
+      r.w[4 * i + 3] = v.w;
+    }
+  } else if constexpr (U == 8) {
     const uint4 v = *reinterpret_cast<const uint4*>(p);
     const uint4 w = *reinterpret_cast<const uint4*>(p + 16);
     r.w[0] = v.x;
@@ -291,7 +302,10 @@ __device__ __forceinline__ void wave_pass_q8(const uint16_t* const (&arow)[TL], 
 // bytes, the first block's in the low byte) for U = 8.
 template <int U>
 __device__ __forceinline__ uint32_t load_e8m0(const uint8_t* p) {
-  if constexpr (U == 8)
+  if constexpr (U == 16)   // four blocks; two 16-bit loads (scale rows are 2-byte aligned)
+    return *reinterpret_cast<const uint16_t*>(p) |
+           ((uint32_t)*reinterpret_cast<const uint16_t*>(p + 2) << 16);
+  else if constexpr (U == 8)
     return *reinterpret_cast<const uint16_t*>(p);
   else
     return *p;
@@ -421,8 +435,10 @@ struct WTile<kFp8, U> {
 template <int U>
 struct WTile<kMx4, U> {
   struct Ptr { const uint8_t* w; const uint8_t* sc; };
-  // 16-bit scales: a widening at the end of a step would wait for their load
-  struct Regs { Q4<U> q; uint16_t e; };
+  // scale bytes (block u / 4 in byte u / 4) in a type no wider than their loads: a
+  // widening at the end of a step would wait for the load
+  using E = typename std::conditional<(U > 8), uint32_t, uint16_t>::type;
+  struct Regs { Q4<U> q; E e; };
   __device__ static constexpr int koff(int g, int u) { return 8 * U * g + 8 * u; }
   __device__ static Regs load(const Ptr& p, int s) {
     Regs r;
@@ -432,7 +448,7 @@ struct WTile<kMx4, U> {
   }
   __device__ static bf16x8 operand(const Regs& r, int u) {
     const uint32_t e = r.e;
-    return fp4x8_to_bf16(r.q.w[u], e8m0_scale(U == 8 && u >= 4 ? e >> 8 : e & 0xFFu));
+    return fp4x8_to_bf16(r.q.w[u], e8m0_scale((e >> (8 * (u >> 2))) & 0xFFu));
   }
 };
 
@@ -592,7 +608,7 @@ __device__ __forceinline__ void staged_pass(const uint16_t* x, size_t ld, const 
 #define XS_Q4_GU_CT2_MIN_BLOCKS XS_GU_CT2_MIN_BLOCKS
 #endif
 #ifndef XS_Q4_GATE_UP_U
-#define XS_Q4_GATE_UP_U 8
+#define XS_Q4_GATE_UP_U 16
 #endif
 #ifndef XS_Q4_DOWN_U
 #define XS_Q4_DOWN_U 8
@@ -1046,28 +1062,47 @@ __global__ __launch_bounds__(kBlock) void router_sum_kernel(RouterArgs r) {
   r.logits[idx] = v;
 }
 
+// Column tiles per wave: two if the expected active blocks stay enough with them.
+bool gu_two_tiles(const FfnArgs& a, int kW, unsigned splits) {
+  const long min_blocks = kW == kMx4 ? XS_Q4_GU_CT2_MIN_BLOCKS : XS_GU_CT2_MIN_BLOCKS;
+  return (long)((a.f + 2 * kWaves * kCols - 1) / (2 * kWaves * kCols)) *
+             (a.est_active + a.n_shared) * splits >= min_blocks;
+}
+
 template <int U, int kW>
 void launch_gu(const FfnArgs& a, bool split, dim3 grid, dim3 block, hipStream_t stream) {
-  // column tiles per wave: two if the expected active blocks stay enough with them
-  const long min_blocks = kW == kMx4 ? XS_Q4_GU_CT2_MIN_BLOCKS : XS_GU_CT2_MIN_BLOCKS;
-  const bool two = (long)((a.f + 2 * kWaves * kCols - 1) / (2 * kWaves * kCols)) *
-                       (a.est_active + a.n_shared) * grid.z >= min_blocks;
+  const bool two = U <= 8 && gu_two_tiles(a, kW, grid.z);   // U = 16: one-tile launches only
   if (two) grid.x = (a.f + 2 * kWaves * kCols - 1) / (2 * kWaves * kCols);
-  if (split && two)
-    hipLaunchKernelGGL((gate_up_kernel<U, true, kW, 2>), grid, block, 0, stream, a);
-  else if (split)
+  if constexpr (U <= 8) {
+    if (split && two) {
+      hipLaunchKernelGGL((gate_up_kernel<U, true, kW, 2>), grid, block, 0, stream, a);
+      return;
+    }
+    if (two) {
+      hipLaunchKernelGGL((gate_up_kernel<U, false, kW, 2>), grid, block, 0, stream, a);
+      return;
+    }
+  }
+  if (split)
     hipLaunchKernelGGL((gate_up_kernel<U, true, kW, 1>), grid, block, 0, stream, a);
-  else if (two)
-    hipLaunchKernelGGL((gate_up_kernel<U, false, kW, 2>), grid, block, 0, stream, a);
   else
     hipLaunchKernelGGL((gate_up_kernel<U, false, kW, 1>), grid, block, 0, stream, a);
 }
 
-// Unroll U (a power of two <= 8 dividing K / 32) for weight format kW.
+// Unroll U (a power of two dividing K / 32; at most 8, or 16 for MXFP4) for weight format kW.
 template <int kW>
 void launch_gu_fmt(const FfnArgs& a, int u, bool split, dim3 grid, dim3 block,
                    hipStream_t stream) {
-  if (u == 8) {
+  if constexpr (kW == kMx4) {
+    // 16-word steps (64 code bytes per lane and tile) for one-tile launches: twice the
+    // weight bytes in flight per wave (DeepSeek T=8 gate/up 92 -> 83 us); two-tile launches
+    // keep 8 (16 words ran at one wave per SIMD: T=32 169 -> 174 us)
+    if (u == 16 && !gu_two_tiles(a, kW, grid.z)) {
+      launch_gu<16, kW>(a, split, grid, block, stream);
+      return;
+    }
+  }
+  if (u >= 8) {
     launch_gu<8, kW>(a, split, grid, block, stream);
     return;
   }

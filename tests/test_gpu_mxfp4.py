@@ -81,10 +81,11 @@ def test_mxfp4_tiny_and_ragged():
 def test_mxfp4_many_rows_per_expert():
     """Few experts holding many rows each: the GEMMs stage up to 32 token rows per pass in
     LDS, so these cases run passes of 32 rows followed by ragged ones (1-8, 9-16, 17-24,
-    25-32 rows), with 256-, 128- and 64-element steps and blocks whose last waves lie past
-    f or d."""
+    25-32 rows), with 512-, 256-, 128- and 64-element steps and blocks whose last waves lie
+    past f or d."""
     for T, N, k, d, f, M in [(70, 8, 4, 256, 512, 4), (40, 6, 3, 384, 192, 3),
-                             (20, 4, 2, 192, 320, 2), (45, 8, 2, 320, 256, 3)]:
+                             (20, 4, 2, 192, 320, 2), (45, 8, 2, 320, 256, 3),
+                             (33, 4, 2, 512, 160, 2), (21, 6, 3, 1024, 256, 3)]:
         _run(dict(N=N, k=k, d=d, f=f, T=T, logits="domains", Q=2), 0, 1, M,
              label=f"many rows T{T} d{d} f{f} M{M}")
 
