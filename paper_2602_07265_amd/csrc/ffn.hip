@@ -608,7 +608,21 @@ __device__ __forceinline__ void staged_pass(const uint16_t* x, size_t ld, const 
 #define XS_Q4_GU_CT2_MIN_BLOCKS XS_GU_CT2_MIN_BLOCKS
 #endif
 #ifndef XS_Q4_GATE_UP_U
-#define XS_Q4_GATE_UP_U 16
+#define XS_Q4_GATE_UP_U 8
+#endif
+// Unroll of one-tile gate/up launches (small grids), twice the two-tile one for bf16 and
+// MXFP4: twice the weight bytes in flight per wave where there are fewer waves.  Same-box
+// A/B: bf16 DeepSeek T=32 M=24 gate/up 246 -> 237 us, Mixtral 232 -> 215, T=8 239 -> 234;
+// MXFP4 DeepSeek T=8 92 -> 83 us (at two tiles, 16 MXFP4 words ran at one wave per SIMD:
+// T=32 169 -> 174 us).  FP8 at 8 words gained on Mixtral and lost on Qwen and T=8.
+#ifndef XS_GATE_UP_U1
+#define XS_GATE_UP_U1 8
+#endif
+#ifndef XS_Q8_GATE_UP_U1
+#define XS_Q8_GATE_UP_U1 XS_Q8_GATE_UP_U
+#endif
+#ifndef XS_Q4_GATE_UP_U1
+#define XS_Q4_GATE_UP_U1 16
 #endif
 #ifndef XS_Q4_DOWN_U
 #define XS_Q4_DOWN_U 8
@@ -1062,6 +1076,8 @@ __global__ __launch_bounds__(kBlock) void router_sum_kernel(RouterArgs r) {
   r.logits[idx] = v;
 }
 
+int unroll_for(int K, int want);
+
 // Column tiles per wave: two if the expected active blocks stay enough with them.
 bool gu_two_tiles(const FfnArgs& a, int kW, unsigned splits) {
   const long min_blocks = kW == kMx4 ? XS_Q4_GU_CT2_MIN_BLOCKS : XS_GU_CT2_MIN_BLOCKS;
@@ -1070,10 +1086,10 @@ bool gu_two_tiles(const FfnArgs& a, int kW, unsigned splits) {
 }
 
 template <int U, int kW>
-void launch_gu(const FfnArgs& a, bool split, dim3 grid, dim3 block, hipStream_t stream) {
-  const bool two = U <= 8 && gu_two_tiles(a, kW, grid.z);   // U = 16: one-tile launches only
+void launch_gu(const FfnArgs& a, bool split, bool two, dim3 grid, dim3 block,
+               hipStream_t stream) {
   if (two) grid.x = (a.f + 2 * kWaves * kCols - 1) / (2 * kWaves * kCols);
-  if constexpr (U <= 8) {
+  if constexpr (U <= 8) {   // U = 16: one-tile launches only
     if (split && two) {
       hipLaunchKernelGGL((gate_up_kernel<U, true, kW, 2>), grid, block, 0, stream, a);
       return;
@@ -1089,29 +1105,27 @@ void launch_gu(const FfnArgs& a, bool split, dim3 grid, dim3 block, hipStream_t 
     hipLaunchKernelGGL((gate_up_kernel<U, false, kW, 1>), grid, block, 0, stream, a);
 }
 
-// Unroll U (a power of two dividing K / 32; at most 8, or 16 for MXFP4) for weight format kW.
+// Unroll U (a power of two dividing K / 32; at most u2 for two-tile launches, u1 for
+// one-tile launches, 16 only for MXFP4) for weight format kW.
 template <int kW>
-void launch_gu_fmt(const FfnArgs& a, int u, bool split, dim3 grid, dim3 block,
+void launch_gu_fmt(const FfnArgs& a, int K, int u2, int u1, bool split, dim3 grid, dim3 block,
                    hipStream_t stream) {
+  const bool two = gu_two_tiles(a, kW, grid.z);
+  const int u = unroll_for(K, two ? u2 : u1);
   if constexpr (kW == kMx4) {
-    // 16-word steps (64 code bytes per lane and tile) for one-tile launches: twice the
-    // weight bytes in flight per wave (DeepSeek T=8 gate/up 92 -> 83 us); two-tile launches
-    // keep 8 (16 words ran at one wave per SIMD: T=32 169 -> 174 us)
-    if (u == 16 && !gu_two_tiles(a, kW, grid.z)) {
-      launch_gu<16, kW>(a, split, grid, block, stream);
+    if (u == 16) {
+      launch_gu<16, kW>(a, split, false, grid, block, stream);
       return;
     }
   }
-  if (u >= 8) {
-    launch_gu<8, kW>(a, split, grid, block, stream);
-    return;
-  }
-  if (u >= 4)
-    launch_gu<4, kW>(a, split, grid, block, stream);
+  if (u >= 8)
+    launch_gu<8, kW>(a, split, two, grid, block, stream);
+  else if (u == 4)
+    launch_gu<4, kW>(a, split, two, grid, block, stream);
   else if (u == 2)
-    launch_gu<2, kW>(a, split, grid, block, stream);
+    launch_gu<2, kW>(a, split, two, grid, block, stream);
   else
-    launch_gu<1, kW>(a, split, grid, block, stream);
+    launch_gu<1, kW>(a, split, two, grid, block, stream);
 }
 template <int kW, int NM>
 void launch_down_fmt(const FfnArgs& a, int u, hipStream_t stream) {
@@ -1144,11 +1158,11 @@ hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
   const bool split = a.gu_splits > 1;
   const int K = a.d / a.gu_splits;
   if (a.wfmt == kFp8)
-    launch_gu_fmt<kFp8>(a, unroll_for(K, XS_Q8_GATE_UP_U), split, grid, block, stream);
+    launch_gu_fmt<kFp8>(a, K, XS_Q8_GATE_UP_U, XS_Q8_GATE_UP_U1, split, grid, block, stream);
   else if (a.wfmt == kMx4)
-    launch_gu_fmt<kMx4>(a, unroll_for(K, XS_Q4_GATE_UP_U), split, grid, block, stream);
+    launch_gu_fmt<kMx4>(a, K, XS_Q4_GATE_UP_U, XS_Q4_GATE_UP_U1, split, grid, block, stream);
   else
-    launch_gu_fmt<kBf16>(a, unroll_for(K, XS_GATE_UP_U), split, grid, block, stream);
+    launch_gu_fmt<kBf16>(a, K, XS_GATE_UP_U, XS_GATE_UP_U1, split, grid, block, stream);
   if (split) {
     const dim3 fgrid((a.f + kBlock * 4 - 1) / (kBlock * 4), (unsigned)a.rows);
     hipLaunchKernelGGL(gate_up_finish_kernel, fgrid, block, 0, stream, a);
