@@ -16,8 +16,11 @@
 // 16 weight rows and the whole reduction dimension; weights go from HBM straight into the
 // B operand of v_mfma_f32_16x16x32_bf16 (lane (n, g) loads 16 contiguous bytes of row n per
 // MFMA, so a wave reads 16 rows x 32*U contiguous elements per step), tokens form the M
-// dimension (16 per tile, up to two tiles per pass), accumulation is fp32.  The next step's
-// loads are issued before the current step's MFMAs (register double buffering).
+// dimension (16 per tile, up to two tiles per pass), accumulation is fp32.  The block's
+// four waves share the expert and its token rows, which the block stages in LDS one step
+// at a time (block_pass); the next step's loads are issued before the current step's
+// MFMAs (register double buffering).  The per-wave passes (wave_pass*) serve the router
+// GEMM and the shapes the staged pass does not take.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
