@@ -85,6 +85,14 @@ def test_fp8_many_rows_per_expert():
              label=f"many rows T{T} d{d} f{f} M{M}")
 
 
+def test_fp8_largest_batches():
+    """The size limits: T * k = 8192 (token, slot) rows, and T = 4096 tokens; experts with
+    hundreds of rows, so the GEMMs loop over many staged 32-row passes."""
+    for T, N, k, d, f, M in [(1024, 64, 8, 64, 64, 24), (4096, 16, 2, 64, 64, 4)]:
+        _run(dict(N=N, k=k, d=d, f=f, T=T, logits="domains", Q=4), 0, 1, M,
+             label=f"largest T{T} k{k}")
+
+
 def test_fp8_every_code():
     """Weights cycling through every finite E4M3FN code (both signs, subnormals, 448) with
     power-of-two scales: the kernels' hardware decode must agree with the format."""

@@ -90,6 +90,14 @@ def test_mxfp4_many_rows_per_expert():
              label=f"many rows T{T} d{d} f{f} M{M}")
 
 
+def test_mxfp4_largest_batches():
+    """The size limits: T * k = 8192 (token, slot) rows, and T = 4096 tokens; experts with
+    hundreds of rows, so the GEMMs loop over many staged 32-row passes."""
+    for T, N, k, d, f, M in [(1024, 64, 8, 64, 64, 24), (4096, 16, 2, 64, 64, 4)]:
+        _run(dict(N=N, k=k, d=d, f=f, T=T, logits="domains", Q=4), 0, 1, M,
+             label=f"largest T{T} k{k}")
+
+
 def test_mxfp4_every_code_and_varied_scales():
     """Weight bytes cycling through all 256 pairs of E2M1 codes, block scales drawn from
     2^-14 .. 2^-6: the kernels' hardware decode and scaling must agree with the format."""
