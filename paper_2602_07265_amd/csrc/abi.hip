@@ -303,7 +303,7 @@ xshare_status layer_common(const uint16_t* x, const float* logits, const uint16_
   // the threshold rule's set size is not known before the selection runs
   fa.est_active = params->budget_mode == XSHARE_BUDGET_THRESHOLD ? 0
                                                                  : layer_estimate(T, params, ep);
-  fa.splits = L.splits;
+  fa.splits = wt.fmt == 2 ? L.q4_splits : L.splits;
   fa.gu_splits = L.gu_splits;
   fa.gpart = at<float>(ws, L.gpart);
   fa.G = ra.G;

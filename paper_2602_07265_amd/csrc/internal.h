@@ -80,13 +80,20 @@ inline int active_bound(int T, int N, int k, int budget_mode, int budget) {
 #define XS_DN_SPLIT_BELOW 1536
 #endif
 #ifndef XS_DN_SPLIT_TARGET
-#define XS_DN_SPLIT_TARGET 4096
+#define XS_DN_SPLIT_TARGET 2048
+#endif
+#ifndef XS_Q4_DN_SPLIT_TARGET
+#define XS_Q4_DN_SPLIT_TARGET 4096
 #endif
 // Splits (a power of two <= max_splits) for a launch of `waves` waves: none at or above
 // `below`, else the fewest that reach `target` waves, each part a multiple of `step`.
 // Measured on MI355X: gate/up pays for its partials and the finish pass, so it splits only
 // below 1024 waves (five DeepSeek experts, 640 waves: 4 splits); down splits below 1536
-// (five experts, 1120 waves: 4 splits; Mixtral's five experts, 640 waves: 8 splits).
+// waves, to reach 2048 with bf16 and FP8 weights (five DeepSeek experts, 1120 waves: 2
+// splits; Mixtral's five, 640 waves: 4) and 4096 with MXFP4 (4 and 8 splits).  With the
+// token rows staged in LDS, bf16 and FP8 down run best with fewer parts (a five-expert
+// DeepSeek share 141 -> 134 us, FP8 Mixtral down 67 -> 64 us); MXFP4 down, with half the
+// weight bytes per wave in flight, kept the larger target (Mixtral down 53 against 61 us).
 inline int split_for(long waves, int K, int step, int below, int target, int max_splits = 8) {
   if (waves >= below) return 1;
   int s = 1;
@@ -111,9 +118,9 @@ inline int gate_up_splits(int est_active, int d, int f) {
 #ifndef XS_Q4_DOWN_NM
 #define XS_Q4_DOWN_NM 2
 #endif
-inline int down_splits(int est_active, int d, int f) {
+inline int down_splits(int est_active, int d, int f, bool mxfp4 = false) {
   return split_for((long)est_active * (d / (16 * XS_DOWN_NM)), f, 128, XS_DN_SPLIT_BELOW,
-                   XS_DN_SPLIT_TARGET);
+                   mxfp4 ? XS_Q4_DN_SPLIT_TARGET : XS_DN_SPLIT_TARGET);
 }
 
 // Hidden and output rows of the expert GEMMs: the T * k routed (token, slot) rows in
@@ -126,12 +133,13 @@ inline size_t ffn_rows(int T, int k, int n_shared) {
 struct FfnLayout {
   RouteLayout route;
   int gu_splits;  // K-splits of the gate/up GEMM
-  int splits;     // K-splits of the down GEMM
+  int splits;     // K-splits of the down GEMM (bf16 and FP8 weights)
+  int q4_splits;  // K-splits of the down GEMM with MXFP4 weights
   size_t gpart;   // fp32 [gu_splits, 2, rows, f] gate and up partial sums (gu_splits > 1)
   size_t h;       // bf16 [rows, 2f]            SwiGLU hidden rows as hi = bf16(H) and
                   //                            lo = bf16(H - hi), interleaved in 8-element
                   //                            chunks: row p holds hi(c..c+7), lo(c..c+7), ...
-  size_t y;       // fp32 [splits, rows, d]     per-row partial expert outputs
+  size_t y;       // fp32 [max(splits, q4_splits), rows, d]  per-row partial expert outputs
   size_t total;
 };
 
@@ -142,12 +150,14 @@ inline FfnLayout ffn_layout(int T, int N, int k, bool dense, int d, int f, int e
   L.route = route_layout(T, N, k, dense);
   L.gu_splits = gate_up_splits(est_active, d, f);
   L.splits = down_splits(est_active, d, f);
+  L.q4_splits = down_splits(est_active, d, f, true);
   const size_t rows = ffn_rows(T, k, n_shared);
   size_t o = L.route.total;
   L.gpart = o;
   if (L.gu_splits > 1) o += align256(sizeof(float) * 2 * size_t(L.gu_splits) * rows * size_t(f));
   L.h = o; o += align256(sizeof(uint16_t) * rows * 2 * size_t(f));
-  L.y = o; o += align256(sizeof(float) * size_t(L.splits) * rows * size_t(d));
+  const int y_planes = L.splits > L.q4_splits ? L.splits : L.q4_splits;   // any format
+  L.y = o; o += align256(sizeof(float) * size_t(y_planes) * rows * size_t(d));
   L.total = o;
   return L;
 }
