@@ -558,17 +558,19 @@ __device__ __forceinline__ void staged_pass(const uint16_t* x, size_t ld, const 
     else
       block_pass<kW, U, kDown, NM, 2, L2, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
   } else {                          // down: up to four 8-token tiles
-    static_assert(TA == 4, "four 8-token tiles");
-    constexpr int L3 = (3 * TR * S::P + kBlock - 1) / kBlock;
-    constexpr int L4 = (4 * TR * S::P + kBlock - 1) / kBlock;
-    if (R <= TR)
+    static_assert(TA == 2 || TA == 4, "two or four 8-token tiles");
+    if (R <= TR) {
       block_pass<kW, U, kDown, NM, 1, L1, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
-    else if (R <= 2 * TR)
+    } else if (TA == 2 || R <= 2 * TR) {
       block_pass<kW, U, kDown, NM, 2, L2, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
-    else if (R <= 3 * TR)
-      block_pass<kW, U, kDown, NM, 3, L3, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
-    else
-      block_pass<kW, U, kDown, NM, 4, L4, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
+    } else if constexpr (TA == 4) {
+      constexpr int L3 = (3 * TR * S::P + kBlock - 1) / kBlock;
+      constexpr int L4 = (4 * TR * S::P + kBlock - 1) / kBlock;
+      if (R <= 3 * TR)
+        block_pass<kW, U, kDown, NM, 3, L3, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
+      else
+        block_pass<kW, U, kDown, NM, 4, L4, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
+    }
   }
 }
 
@@ -629,6 +631,9 @@ __device__ __forceinline__ void staged_pass(const uint16_t* x, size_t ld, const 
 #endif
 #ifndef XS_Q4_DOWN_U
 #define XS_Q4_DOWN_U 8
+#endif
+#ifndef XS_Q4_DN_WIDE
+#define XS_Q4_DN_WIDE 1
 #endif
 #ifndef XS_Q4_DOWN_ROT
 #define XS_Q4_DOWN_ROT 0
@@ -838,10 +843,10 @@ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
 // NM: 16-row W2 tiles per wave (the launch picks it per weight format and batch shape).
 // Staged down instances are held to 2 waves per SIMD: left alone the compiler took 1 for the
 // 64-row bf16 and FP8 instances (FP8 DeepSeek T=32 down 166 -> 138 us with the hint).
-template <int U, int kW, int NM>
+// TL: token tiles per pass, 8 tokens each (hi and lo rows).
+template <int U, int kW, int NM, int TL = XS_DOWN_TL>
 __global__ __attribute__((amdgpu_waves_per_eu(stage_down(kW) ? 2 : 1)))
 __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
-  constexpr int TL = XS_DOWN_TL;  // token tiles per pass, 8 tokens each (hi and lo rows)
   SlotWork sw;
   if (!slot_work(a, blockIdx.y, sw)) return;
   const int p0 = sw.p0, te = sw.te;
@@ -885,7 +890,7 @@ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
     const int rot = kW == kBf16 ? XS_DOWN_ROT : (kW == kFp8 ? XS_Q8_DOWN_ROT : XS_Q4_DOWN_ROT);
     const int k_first = (int)(((blockIdx.x * kWaves + wave) * rot) % (Ks / (32 * U))) * 32 * U;
     if constexpr (kStaged) {
-      static_assert(TL == 4, "the staged pass takes four 8-token tiles");
+      static_assert(TL == 2 || TL == 4, "the staged pass takes two or four 8-token tiles");
       typename WTile<kW, U>::Ptr wp[NM];
 #pragma unroll
       for (int m = 0; m < NM; ++m) {
@@ -900,7 +905,7 @@ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
       }
       __shared__ __align__(16) uint16_t stage[Stage<U, true>::kElems];
       __shared__ int s_tok[kStageRows];
-      const int R = min(kStageRows, te - c0);
+      const int R = min(8 * TL, te - c0);
       if (threadIdx.x < R) s_tok[threadIdx.x] = p0 + c0 + threadIdx.x;   // H rows
       __syncthreads();
       // staged: consecutive blocks, not waves, start their pass `rot` steps apart
@@ -1130,20 +1135,20 @@ void launch_gu_fmt(const FfnArgs& a, int K, int u2, int u1, bool split, dim3 gri
   else
     launch_gu<1, kW>(a, split, two, grid, block, stream);
 }
-template <int kW, int NM>
+template <int kW, int NM, int TL = XS_DOWN_TL>
 void launch_down_fmt(const FfnArgs& a, int u, hipStream_t stream) {
   const int cols = kWaves * kCols * NM;
   const dim3 grid((a.d + cols - 1) / cols, a.max_active + a.n_shared, a.splits), block(kBlock);
   if (u == 8) {
-    hipLaunchKernelGGL((down_kernel<8, kW, NM>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((down_kernel<8, kW, NM, TL>), grid, block, 0, stream, a);
     return;
   }
   if (u >= 4)
-    hipLaunchKernelGGL((down_kernel<4, kW, NM>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((down_kernel<4, kW, NM, TL>), grid, block, 0, stream, a);
   else if (u == 2)
-    hipLaunchKernelGGL((down_kernel<2, kW, NM>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((down_kernel<2, kW, NM, TL>), grid, block, 0, stream, a);
   else
-    hipLaunchKernelGGL((down_kernel<1, kW, NM>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((down_kernel<1, kW, NM, TL>), grid, block, 0, stream, a);
 }
 
 int unroll_for(int K, int want) {
@@ -1175,14 +1180,24 @@ hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
 
 hipError_t launch_down(const FfnArgs& a, hipStream_t stream) {
   const int K = a.f / a.splits;
+  const long est = a.est_active + a.n_shared;
   if (a.wfmt == kMx4) {
-    launch_down_fmt<kMx4, XS_Q4_DOWN_NM>(a, unroll_for(K, XS_Q4_DOWN_U), stream);
+    // twice the rows per wave (twice the weight bytes in flight) over 16-token passes, when
+    // experts hold 8 rows or fewer on average (an expert past 16 rows reads its weights
+    // once per pass) and the grid stays large.  Same-box A/B: DeepSeek T=32 M=48 down
+    // 98.5 -> 93.6 us, speculative 135.6 -> 127.2 us; at T=8 (672 blocks) 50.6 -> 53.2 us.
+    const int wcols = kWaves * kCols * 2 * XS_Q4_DOWN_NM;
+    const bool wide = XS_Q4_DN_WIDE && est > 0 && (long)a.T * a.k <= 8 * est &&
+                      (long)((a.d + wcols - 1) / wcols) * est * a.splits >= XS_DN_WIDE_MIN_BLOCKS;
+    if (wide)
+      launch_down_fmt<kMx4, 2 * XS_Q4_DOWN_NM, 2>(a, unroll_for(K, XS_Q4_DOWN_U), stream);
+    else
+      launch_down_fmt<kMx4, XS_Q4_DOWN_NM>(a, unroll_for(K, XS_Q4_DOWN_U), stream);
     return hipGetLastError();
   }
   // bf16 and FP8: twice the rows per wave (one token load feeding twice the weight tiles)
   // pays when experts hold several tokens each and the grid stays large
   const int nm = a.wfmt == kFp8 ? XS_Q8_DOWN_NM : XS_DOWN_NM;
-  const long est = a.est_active + a.n_shared;
   const bool wide = est > 0 && (long)a.T * a.k >= XS_DN_WIDE_TOKENS * est &&
                     (long)((a.d + kWaves * kCols * 2 * nm - 1) / (kWaves * kCols * 2 * nm)) *
                             est * a.splits >= XS_DN_WIDE_MIN_BLOCKS;
