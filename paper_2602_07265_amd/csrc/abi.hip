@@ -213,8 +213,9 @@ struct Weights {
     return w1 && w3 && w2;
   }
   bool aligned() const {
-    auto even = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 1u) == 0; };
-    if (fmt == 2 && !(even(e1) && even(e3) && even(e2))) return false;   // scale pairs
+    // MXFP4 scale rows are read in pieces of up to 8 bytes
+    auto a8 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; };
+    if (fmt == 2 && !(a8(e1) && a8(e3) && a8(e2))) return false;
     return fmt ? (aligned16(q1) && aligned16(q3) && aligned16(q2))
                : (aligned16(w1) && aligned16(w3) && aligned16(w2));
   }

@@ -411,6 +411,8 @@ template <int kW, int U>
 struct WTile;
 template <int U>
 struct WTile<kBf16, U> {
+  static constexpr bool kGroupScales = false;
+  using GV = uint32_t;
   struct Ptr { const uint16_t* w; };
   struct Regs { bf16x8 w[U]; };
   __device__ static constexpr int koff(int g, int u) { return kstep(u) + klane<U>(g); }
@@ -424,6 +426,8 @@ struct WTile<kBf16, U> {
 };
 template <int U>
 struct WTile<kFp8, U> {
+  static constexpr bool kGroupScales = false;
+  using GV = uint32_t;
   struct Ptr { const uint8_t* w; };
   struct Regs { uint2 w[U]; };
   __device__ static constexpr int koff(int g, int u) { return 8 * U * g + 8 * u; }
@@ -437,6 +441,8 @@ struct WTile<kFp8, U> {
 };
 template <int U>
 struct WTile<kMx4, U> {
+  // w: this lane's codes; sc: this lane's scale bytes (lane group g: its row's scale bytes
+  // from byte U / 4 * g on)
   struct Ptr { const uint8_t* w; const uint8_t* sc; };
   // scale bytes (block u / 4 in byte u / 4) in a type no wider than their loads: a
   // widening at the end of a step would wait for the load
@@ -449,6 +455,34 @@ struct WTile<kMx4, U> {
     r.e = load_e8m0<U>(p.sc + s / 32);
     return r;
   }
+  // Scales by groups of four steps: a row's scale bytes of one step (U bytes) are one
+  // cache-line piece that all four lanes of the row used to load separately, step after
+  // step (a fifth of the GEMM time went to these 2-byte loads, one cache line per row
+  // each).  In group G, lane group g loads its row's U bytes of step 4G + g, and at step
+  // 4G + ph every lane takes its bytes from lane (n, ph) with a cross-lane read: one load
+  // instruction per four steps and tile.
+  static constexpr bool kGroupScales = U == 4 || U == 8;
+  using GV = typename std::conditional<(U == 8), uint2, uint32_t>::type;
+  __device__ static Regs load_codes(const Ptr& p, int s) {
+    Regs r;
+    r.q = load_q4<U>(p.w + s / 2);
+    return r;
+  }
+  // (a group past the pass's last step `last` repeats that step's bytes)
+  __device__ static GV load_group(const Ptr& p, int G, int g, int last) {
+    return *reinterpret_cast<const GV*>(p.sc - U / 4 * g + min(4 * G + g, last) * U);
+  }
+  __device__ static E group_scale(const GV& v, int ph, int lane) {
+    const int src = (lane & 15) + 16 * ph, g = lane >> 4;
+    if constexpr (U == 8) {   // lane group g's two bytes: bytes 2g, 2g + 1 of the step's 8
+      const uint32_t w0 = (uint32_t)__shfl((int)v.x, src, 64);
+      const uint32_t w1 = (uint32_t)__shfl((int)v.y, src, 64);
+      return (E)((g < 2 ? w0 : w1) >> (16 * (g & 1)));
+    } else {                  // U = 4: byte g of the step's 4
+      const uint32_t w = (uint32_t)__shfl((int)v, src, 64);
+      return (E)((w >> (8 * g)) & 0xFFu);
+    }
+  }
   __device__ static bf16x8 operand(const Regs& r, int u) {
     const uint32_t e = r.e;
     return fp4x8_to_bf16(r.q.w[u], e8m0_scale((e >> (8 * (u >> 2))) & 0xFFu));
@@ -459,7 +493,9 @@ struct WTile<kMx4, U> {
 // ceil(R * P / 256) (pieces beyond R * P repeat the last one).  Staged row r (r < R) is
 // x[tok[r] * ld ...], x already offset to this block's reduction range.  acc[m][rt] as in
 // wave_pass (gate/up) or the down pass.
-template <int kW, int U, bool kDown, int NM, int NT, int NL, int TA>
+// kGS: MXFP4 scales loaded by groups of four steps (WTile<kMx4, U>::load_group); needs
+// k_first = 0.
+template <int kW, int U, bool kDown, int NM, int NT, int NL, int TA, bool kGS = false>
 __device__ __forceinline__ void block_pass(const uint16_t* x, size_t ld, const int* tok, int R,
                                            const typename WTile<kW, U>::Ptr (&wp)[NM], int K,
                                            int k_first, floatx4 (&acc)[NM][TA], uint16_t* lds) {
@@ -487,14 +523,31 @@ __device__ __forceinline__ void block_pass(const uint16_t* x, size_t ld, const i
 
   u32x4 v[NL];
   typename WT::Regs b[NM];
+  // kGS: this lane's scale piece of the current group of four steps
+  typename WT::GV gs[kGS ? NM : 1];
 #pragma unroll
   for (int i = 0; i < NL; ++i) v[i] = *reinterpret_cast<const u32x4*>(src[i] + S::AS * k_first);
+  if constexpr (kGS) {
 #pragma unroll
-  for (int m = 0; m < NM; ++m) b[m] = WT::load(wp[m], k_first);
+    for (int m = 0; m < NM; ++m) {
+      gs[m] = WT::load_group(wp[m], 0, g, K / KB - 1);
+      b[m] = WT::load_codes(wp[m], 0);
+    }
+  } else {
+#pragma unroll
+    for (int m = 0; m < NM; ++m) b[m] = WT::load(wp[m], k_first);
+  }
 #pragma unroll
   for (int i = 0; i < NL; ++i) *reinterpret_cast<u32x4*>(lds + wofs[i]) = v[i];
   __syncthreads();
 
+  // kGS: step ks's scales out of the group's pieces
+  auto scales = [&](int ks) {
+    if constexpr (kGS) {
+#pragma unroll
+      for (int m = 0; m < NM; ++m) b[m].e = WT::group_scale(gs[m], ks & 3, lane);
+    }
+  };
   // MFMAs of one step from LDS buffer `cur`
   auto step = [&](const uint16_t* cur) {
 #pragma unroll
@@ -514,17 +567,33 @@ __device__ __forceinline__ void block_pass(const uint16_t* x, size_t ld, const i
   int buf = 0;
   // loads of step kn, MFMAs of the step before it, then kn's tokens into the other buffer
   auto advance = [&](int kn) {
+    const int ks = kn / KB;
+    // kGS: the scales of step ks - 1 out of the pieces, then, when step ks starts a group
+    // (a uniform branch, taken every fourth step), that group's pieces, first of the loads
+    scales(ks - 1);
+    if constexpr (kGS) {
+      if ((ks & 3) == 0) {
+#pragma unroll
+        for (int m = 0; m < NM; ++m) gs[m] = WT::load_group(wp[m], ks >> 2, g, K / KB - 1);
+      }
+    }
 #pragma unroll
     for (int i = 0; i < NL; ++i) v[i] = *reinterpret_cast<const u32x4*>(src[i] + S::AS * kn);
     typename WT::Regs nb[NM];
 #pragma unroll
-    for (int m = 0; m < NM; ++m) nb[m] = WT::load(wp[m], kn);
+    for (int m = 0; m < NM; ++m) {
+      if constexpr (kGS) nb[m] = WT::load_codes(wp[m], kn);
+      else nb[m] = WT::load(wp[m], kn);
+    }
     step(lds + buf * kStageRows * S::LS);
     uint16_t* const nxt = lds + (buf ^ 1) * kStageRows * S::LS;
 #pragma unroll
     for (int i = 0; i < NL; ++i) *reinterpret_cast<u32x4*>(nxt + wofs[i]) = v[i];
 #pragma unroll
-    for (int m = 0; m < NM; ++m) b[m] = nb[m];
+    for (int m = 0; m < NM; ++m) {
+      if constexpr (kGS) b[m].q = nb[m].q;
+      else b[m] = nb[m];
+    }
     __syncthreads();
     buf ^= 1;
   };
@@ -532,17 +601,18 @@ __device__ __forceinline__ void block_pass(const uint16_t* x, size_t ld, const i
   // one loop measured slower)
   for (int kn = k_first + KB; kn < K; kn += KB) advance(kn);
   for (int kn = 0; kn < k_first; kn += KB) advance(kn);
+  scales(K / KB - 1);
   step(lds + buf * kStageRows * S::LS);
   __syncthreads();                         // the block's next pass rewrites both buffers
 }
 
 // The staged pass over R token rows, by block-uniform instance: the fewest tiles that hold
 // R rows and the loads per thread that the largest R of that tile count needs.
-template <int kW, int U, bool kDown, int NM, int TA>
-__device__ __forceinline__ void staged_pass(const uint16_t* x, size_t ld, const int* tok, int R,
-                                            const typename WTile<kW, U>::Ptr (&wp)[NM], int K,
-                                            int k_first, floatx4 (&acc)[NM][TA],
-                                            uint16_t* lds) {
+template <int kW, int U, bool kDown, int NM, int TA, bool kGS>
+__device__ __forceinline__ void staged_pass_as(const uint16_t* x, size_t ld, const int* tok,
+                                               int R, const typename WTile<kW, U>::Ptr (&wp)[NM],
+                                               int K, int k_first, floatx4 (&acc)[NM][TA],
+                                               uint16_t* lds) {
   using S = Stage<U, kDown>;
   constexpr int TR = S::TR;
   constexpr int L1 = (TR * S::P + kBlock - 1) / kBlock, L2 = (2 * TR * S::P + kBlock - 1) / kBlock;
@@ -550,28 +620,43 @@ __device__ __forceinline__ void staged_pass(const uint16_t* x, size_t ld, const 
     constexpr int L1h = (TR / 2 * S::P + kBlock - 1) / kBlock;
     constexpr int L2h = (3 * TR / 2 * S::P + kBlock - 1) / kBlock;
     if (R <= TR / 2)
-      block_pass<kW, U, kDown, NM, 1, L1h, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
+      block_pass<kW, U, kDown, NM, 1, L1h, TA, kGS>(x, ld, tok, R, wp, K, k_first, acc, lds);
     else if (R <= TR)
-      block_pass<kW, U, kDown, NM, 1, L1, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
+      block_pass<kW, U, kDown, NM, 1, L1, TA, kGS>(x, ld, tok, R, wp, K, k_first, acc, lds);
     else if (R <= 3 * TR / 2)
-      block_pass<kW, U, kDown, NM, 2, L2h, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
+      block_pass<kW, U, kDown, NM, 2, L2h, TA, kGS>(x, ld, tok, R, wp, K, k_first, acc, lds);
     else
-      block_pass<kW, U, kDown, NM, 2, L2, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
+      block_pass<kW, U, kDown, NM, 2, L2, TA, kGS>(x, ld, tok, R, wp, K, k_first, acc, lds);
   } else {                          // down: up to four 8-token tiles
     static_assert(TA == 2 || TA == 4, "two or four 8-token tiles");
     if (R <= TR) {
-      block_pass<kW, U, kDown, NM, 1, L1, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
+      block_pass<kW, U, kDown, NM, 1, L1, TA, kGS>(x, ld, tok, R, wp, K, k_first, acc, lds);
     } else if (TA == 2 || R <= 2 * TR) {
-      block_pass<kW, U, kDown, NM, 2, L2, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
+      block_pass<kW, U, kDown, NM, 2, L2, TA, kGS>(x, ld, tok, R, wp, K, k_first, acc, lds);
     } else if constexpr (TA == 4) {
       constexpr int L3 = (3 * TR * S::P + kBlock - 1) / kBlock;
       constexpr int L4 = (4 * TR * S::P + kBlock - 1) / kBlock;
       if (R <= 3 * TR)
-        block_pass<kW, U, kDown, NM, 3, L3, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
+        block_pass<kW, U, kDown, NM, 3, L3, TA, kGS>(x, ld, tok, R, wp, K, k_first, acc, lds);
       else
-        block_pass<kW, U, kDown, NM, 4, L4, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
+        block_pass<kW, U, kDown, NM, 4, L4, TA, kGS>(x, ld, tok, R, wp, K, k_first, acc, lds);
     }
   }
+}
+
+// The staged pass, with MXFP4 scales by groups of four steps where the pass allows it.
+template <int kW, int U, bool kDown, int NM, int TA>
+__device__ __forceinline__ void staged_pass(const uint16_t* x, size_t ld, const int* tok, int R,
+                                            const typename WTile<kW, U>::Ptr (&wp)[NM], int K,
+                                            int k_first, floatx4 (&acc)[NM][TA],
+                                            uint16_t* lds) {
+  if constexpr (WTile<kW, U>::kGroupScales) {
+    if (k_first == 0) {
+      staged_pass_as<kW, U, kDown, NM, TA, true>(x, ld, tok, R, wp, K, k_first, acc, lds);
+      return;
+    }
+  }
+  staged_pass_as<kW, U, kDown, NM, TA, false>(x, ld, tok, R, wp, K, k_first, acc, lds);
 }
 
 // Unroll (32-element k-groups per step) and token-operand buffering of the two GEMMs.
