@@ -341,9 +341,9 @@ xshare_status xshare_moe_forward_fp8(const uint16_t* x, const float* logits, int
  *             block of 32 consecutive inputs of a row, value 2^(e - 127); the weight is
  *             decode(code) * 2^(e - 127).  e = 255 (NaN) must not occur, and the decoded
  *             weights must lie in bf16's normal range (or be zero): the GPU turns each code
- *             and its scale into the exact bf16 weight before the bf16 MFMA.  8-byte
+ *             and its scale into the exact bf16 weight before the bf16 MFMA.  16-byte
  *             aligned (XSHARE_EINVAL otherwise: the kernels read scale rows in pieces of
- *             up to 8 bytes).
+ *             up to 16 bytes).
  *   d and f multiples of 32.  Everything else as xshare_moe_forward (workspace from
  *   xshare_moe_workspace_bytes); shared experts are not taken here.
  */

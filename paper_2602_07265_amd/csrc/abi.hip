@@ -213,9 +213,8 @@ struct Weights {
     return w1 && w3 && w2;
   }
   bool aligned() const {
-    // MXFP4 scale rows are read in pieces of up to 8 bytes
-    auto a8 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; };
-    if (fmt == 2 && !(a8(e1) && a8(e3) && a8(e2))) return false;
+    // MXFP4 scale rows are read in pieces of up to 16 bytes
+    if (fmt == 2 && !(aligned16(e1) && aligned16(e3) && aligned16(e2))) return false;
     return fmt ? (aligned16(q1) && aligned16(q3) && aligned16(q2))
                : (aligned16(w1) && aligned16(w3) && aligned16(w2));
   }

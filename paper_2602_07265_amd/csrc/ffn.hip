@@ -461,8 +461,9 @@ struct WTile<kMx4, U> {
   // each).  In group G, lane group g loads its row's U bytes of step 4G + g, and at step
   // 4G + ph every lane takes its bytes from lane (n, ph) with a cross-lane read: one load
   // instruction per four steps and tile.
-  static constexpr bool kGroupScales = U == 4 || U == 8;
-  using GV = typename std::conditional<(U == 8), uint2, uint32_t>::type;
+  static constexpr bool kGroupScales = U == 4 || U == 8 || U == 16;
+  using GV = typename std::conditional<
+      (U == 16), uint4, typename std::conditional<(U == 8), uint2, uint32_t>::type>::type;
   __device__ static Regs load_codes(const Ptr& p, int s) {
     Regs r;
     r.q = load_q4<U>(p.w + s / 2);
@@ -474,7 +475,13 @@ struct WTile<kMx4, U> {
   }
   __device__ static E group_scale(const GV& v, int ph, int lane) {
     const int src = (lane & 15) + 16 * ph, g = lane >> 4;
-    if constexpr (U == 8) {   // lane group g's two bytes: bytes 2g, 2g + 1 of the step's 8
+    if constexpr (U == 16) {  // lane group g's four bytes: word g of the step's 16 bytes
+      const uint32_t w0 = (uint32_t)__shfl((int)v.x, src, 64);
+      const uint32_t w1 = (uint32_t)__shfl((int)v.y, src, 64);
+      const uint32_t w2 = (uint32_t)__shfl((int)v.z, src, 64);
+      const uint32_t w3 = (uint32_t)__shfl((int)v.w, src, 64);
+      return g < 2 ? (g == 0 ? w0 : w1) : (g == 2 ? w2 : w3);
+    } else if constexpr (U == 8) {   // lane group g's bytes 2g, 2g + 1 of the step's 8
       const uint32_t w0 = (uint32_t)__shfl((int)v.x, src, 64);
       const uint32_t w1 = (uint32_t)__shfl((int)v.y, src, 64);
       return (E)((g < 2 ? w0 : w1) >> (16 * (g & 1)));

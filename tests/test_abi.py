@@ -276,7 +276,7 @@ def test_moe_forward_mxfp4_validation():
     assert call(e1=None) == X.EINVAL                 # block scales are required
     assert call(e2=None) == X.EINVAL
     assert call(q3=FAKE_ODD) == X.EINVAL             # 16-byte alignment of the codes
-    assert call(e3=FAKE_ODD) == X.EINVAL             # scale rows: 8-byte alignment
-    assert call(e2=ctypes.c_void_p((1 << 20) + 4)) == X.EINVAL
+    assert call(e3=FAKE_ODD) == X.EINVAL             # scale rows: 16-byte alignment
+    assert call(e2=ctypes.c_void_p((1 << 20) + 8)) == X.EINVAL
     assert call(d=48) == X.EUNSUPPORTED              # d, f multiples of 32
     assert call(f=80) == X.EUNSUPPORTED
