@@ -707,11 +707,12 @@ __device__ __forceinline__ void staged_pass(const uint16_t* x, size_t ld, const 
 #ifndef XS_Q4_GATE_UP_U
 #define XS_Q4_GATE_UP_U 8
 #endif
-// Unroll of one-tile gate/up launches (small grids), twice the two-tile one for bf16 and
-// MXFP4: twice the weight bytes in flight per wave where there are fewer waves.  Same-box
-// A/B: bf16 DeepSeek T=32 M=24 gate/up 246 -> 237 us, Mixtral 232 -> 215, T=8 239 -> 234;
-// MXFP4 DeepSeek T=8 92 -> 83 us (at two tiles, 16 MXFP4 words ran at one wave per SIMD:
-// T=32 169 -> 174 us).  FP8 at 8 words gained on Mixtral and lost on Qwen and T=8.
+// Unroll of one-tile gate/up launches (small grids), twice the two-tile one for bf16:
+// twice the weight bytes in flight per wave where there are fewer waves.  Same-box A/B:
+// bf16 DeepSeek T=32 M=24 gate/up 246 -> 237 us, Mixtral 232 -> 215, T=8 239 -> 234.  FP8
+// at 8 words gained on Mixtral and lost on Qwen and T=8.  MXFP4 gained from 16 words while
+// every step read its scales; with scales read once per four steps, 8 words are ahead
+// (DeepSeek T=8 M=24 gate/up 76.2 -> 74.5 us, Mixtral 69.1 -> 67.1 us).
 #ifndef XS_GATE_UP_U1
 #define XS_GATE_UP_U1 8
 #endif
@@ -719,7 +720,7 @@ __device__ __forceinline__ void staged_pass(const uint16_t* x, size_t ld, const 
 #define XS_Q8_GATE_UP_U1 XS_Q8_GATE_UP_U
 #endif
 #ifndef XS_Q4_GATE_UP_U1
-#define XS_Q4_GATE_UP_U1 16
+#define XS_Q4_GATE_UP_U1 8
 #endif
 #ifndef XS_Q4_DOWN_U
 #define XS_Q4_DOWN_U 8
@@ -1212,7 +1213,7 @@ void launch_gu_fmt(const FfnArgs& a, int K, int u2, int u1, bool split, dim3 gri
                    hipStream_t stream) {
   const bool two = gu_two_tiles(a, kW, grid.z);
   const int u = unroll_for(K, two ? u2 : u1);
-  if constexpr (kW == kMx4) {
+  if constexpr (kW == kMx4 && (XS_Q4_GATE_UP_U == 16 || XS_Q4_GATE_UP_U1 == 16)) {
     if (u == 16) {
       launch_gu<16, kW>(a, split, false, grid, block, stream);
       return;
