@@ -98,11 +98,15 @@ def test_mxfp4_largest_batches():
              label=f"largest T{T} k{k}")
 
 
-def test_mxfp4_every_code_and_varied_scales():
+@pytest.mark.parametrize("d,f", [(128, 128), (1024, 1280), (1280, 768), (2048, 512)])
+def test_mxfp4_every_code_and_varied_scales(d, f):
     """Weight bytes cycling through all 256 pairs of E2M1 codes, block scales drawn from
-    2^-14 .. 2^-6: the kernels' hardware decode and scaling must agree with the format."""
-    N, k, d, f, T = 8, 2, 128, 128, 12
-    rng = np.random.default_rng(4)
+    2^-14 .. 2^-6: the kernels' hardware decode and scaling must agree with the format.
+    The GEMMs read a row's scales once per four steps and hand each step's bytes to the
+    row's lanes: d, f of 1024-2048 run whole groups of four 256-element steps, 1280 and 768
+    end in a partial group (five and three steps), 512 is split across blocks."""
+    N, k, T = 8, 2, 12
+    rng = np.random.default_rng(4 + d + f)
 
     def codes(r, c):
         return torch.from_numpy(rng.permutation(np.resize(np.arange(256, dtype=np.uint8),
@@ -118,7 +122,7 @@ def test_mxfp4_every_code_and_varied_scales():
     e3 = torch.stack([scales(f, d // 32) for _ in range(N)])
     e2 = torch.stack([scales(d, f // 32) for _ in range(N)])
     c = dict(N=N, k=k, d=d, f=f, T=T, logits="domains", Q=2)
-    _run(c, 0, 1, 4, weights=(q1, q3, q2, e1, e3, e2), label="every code")
+    _run(c, 0, 1, 4, weights=(q1, q3, q2, e1, e3, e2), label=f"every code d{d} f{f}")
 
 
 def test_mxfp4_split_reductions():
