@@ -740,6 +740,12 @@ __device__ __forceinline__ void staged_pass(const uint16_t* x, size_t ld, const 
 #ifndef XS_Q8_DOWN_ROT
 #define XS_Q8_DOWN_ROT 0
 #endif
+// Expert slots from which the down grid keeps each slot's column blocks on one XCD (with
+// fewer, whole XCDs would idle: five experts left three of eight without work).
+#ifndef XS_DOWN_XCD_SLOTS
+#define XS_DOWN_XCD_SLOTS 16
+#endif
+static_assert(XS_DOWN_XCD_SLOTS >= 8 && XS_DOWN_XCD_SLOTS % 8 == 0, "whole rounds of 8 XCDs");
 #ifndef XS_DOWN_TL
 #define XS_DOWN_TL 4                 // 8-token (hi + lo) tiles per pass of the down GEMM
 #endif
@@ -940,11 +946,22 @@ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
 template <int U, int kW, int NM, int TL = XS_DOWN_TL>
 __global__ __attribute__((amdgpu_waves_per_eu(stage_down(kW) ? 2 : 1)))
 __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
+  // (bx, slot): this block's column block and expert slot.  Grids of at least
+  // XS_DOWN_XCD_SLOTS slots (then a multiple of 8) run all column blocks of slot y on XCD
+  // y mod 8 (the dispatcher deals consecutive workgroups to the 8 XCDs in turn), so one L2
+  // serves the slot's H rows to all of them.
+  int bx = blockIdx.x, slot = blockIdx.y;
+  if (gridDim.y >= XS_DOWN_XCD_SLOTS) {
+    const int L = blockIdx.x + gridDim.x * blockIdx.y;
+    const int s = L >> 3;
+    slot = (L & 7) + 8 * (s / gridDim.x);
+    bx = s % gridDim.x;
+  }
   SlotWork sw;
-  if (!slot_work(a, blockIdx.y, sw)) return;
+  if (!slot_work(a, slot, sw)) return;
   const int p0 = sw.p0, te = sw.te;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int n0 = (blockIdx.x * kWaves + wave) * kCols * NM;
+  const int n0 = (bx * kWaves + wave) * kCols * NM;
   // a staged pass needs the whole block (see gate_up_kernel)
   constexpr bool kStaged = stage_down(kW);
   if (!kStaged && n0 >= a.d) return;
@@ -981,7 +998,7 @@ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
     // are f elements apart, often a power of two, so waves that stepped through K in the
     // same order would read the same offsets of every row at the same time.
     const int rot = kW == kBf16 ? XS_DOWN_ROT : (kW == kFp8 ? XS_Q8_DOWN_ROT : XS_Q4_DOWN_ROT);
-    const int k_first = (int)(((blockIdx.x * kWaves + wave) * rot) % (Ks / (32 * U))) * 32 * U;
+    const int k_first = (int)(((bx * kWaves + wave) * rot) % (Ks / (32 * U))) * 32 * U;
     if constexpr (kStaged) {
       static_assert(TL == 2 || TL == 4, "the staged pass takes two or four 8-token tiles");
       typename WTile<kW, U>::Ptr wp[NM];
@@ -1002,7 +1019,7 @@ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
       if (threadIdx.x < R) s_tok[threadIdx.x] = p0 + c0 + threadIdx.x;   // H rows
       __syncthreads();
       // staged: consecutive blocks, not waves, start their pass `rot` steps apart
-      const int kb_first = (int)((blockIdx.x * rot) % (Ks / (32 * U))) * 32 * U;
+      const int kb_first = (int)((bx * rot) % (Ks / (32 * U))) * 32 * U;
       staged_pass<kW, U, true, NM, TL>(a.h + 2 * (size_t)blockIdx.z * Ks, 2 * (size_t)f, s_tok, R,
                                        wp, Ks, kb_first, acc, stage);
     } else if constexpr (kW == kFp8) {
@@ -1231,7 +1248,10 @@ void launch_gu_fmt(const FfnArgs& a, int K, int u2, int u1, bool split, dim3 gri
 template <int kW, int NM, int TL = XS_DOWN_TL>
 void launch_down_fmt(const FfnArgs& a, int u, hipStream_t stream) {
   const int cols = kWaves * kCols * NM;
-  const dim3 grid((a.d + cols - 1) / cols, a.max_active + a.n_shared, a.splits), block(kBlock);
+  const int slots = a.max_active + a.n_shared;
+  const dim3 grid((a.d + cols - 1) / cols,
+                  slots >= XS_DOWN_XCD_SLOTS ? (slots + 7) / 8 * 8 : slots, a.splits),
+      block(kBlock);
   if (u == 8) {
     hipLaunchKernelGGL((down_kernel<8, kW, NM, TL>), grid, block, 0, stream, a);
     return;
