@@ -742,10 +742,13 @@ __device__ __forceinline__ void staged_pass(const uint16_t* x, size_t ld, const 
 #endif
 // Expert slots from which the down grid keeps each slot's column blocks on one XCD (with
 // fewer, whole XCDs would idle: five experts left three of eight without work).
+#ifndef XS_GU_CT2_WPE
+#define XS_GU_CT2_WPE 1
+#endif
 #ifndef XS_DOWN_XCD_SLOTS
 #define XS_DOWN_XCD_SLOTS 16
 #endif
-static_assert(XS_DOWN_XCD_SLOTS >= 8 && XS_DOWN_XCD_SLOTS % 8 == 0, "whole rounds of 8 XCDs");
+static_assert(XS_DOWN_XCD_SLOTS >= 8, "at least one slot per XCD");
 #ifndef XS_DOWN_TL
 #define XS_DOWN_TL 4                 // 8-token (hi + lo) tiles per pass of the down GEMM
 #endif
@@ -815,7 +818,7 @@ __device__ __forceinline__ const uint8_t* slot_q(const FfnArgs& a, const SlotWor
 // The MXFP4 one-tile instance is held to 168 registers (3 waves per SIMD): left alone the
 // compiler took 175 and 2 waves, and DeepSeek T=8 gate/up ran 14 % slower.
 template <int U, bool kSplit, int kW, int CT>
-__global__ __attribute__((amdgpu_waves_per_eu(kW == kMx4 && CT == 1 ? 3 : 1)))
+__global__ __attribute__((amdgpu_waves_per_eu(kW == kMx4 && CT == 1 ? 3 : (kW == kBf16 && CT == 2 ? XS_GU_CT2_WPE : 1))))
 __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
   constexpr int NM = 2 * CT;                   // weight tiles: W1 and W3 of each column tile
   SlotWork sw;
@@ -946,16 +949,21 @@ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
 template <int U, int kW, int NM, int TL = XS_DOWN_TL>
 __global__ __attribute__((amdgpu_waves_per_eu(stage_down(kW) ? 2 : 1)))
 __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
-  // (bx, slot): this block's column block and expert slot.  Grids of at least
-  // XS_DOWN_XCD_SLOTS slots (then a multiple of 8) run all column blocks of slot y on XCD
-  // y mod 8 (the dispatcher deals consecutive workgroups to the 8 XCDs in turn), so one L2
-  // serves the slot's H rows to all of them.
+  // (bx, slot): this block's column block and expert slot.  In grids of at least
+  // XS_DOWN_XCD_SLOTS slots, with `live` slots holding work (shared, then active), all
+  // column blocks of slot y < 8 * (live / 8) run on XCD y mod 8 (the dispatcher deals
+  // consecutive workgroups to the 8 XCDs in turn), so one L2 serves the slot's H rows to
+  // all of them; the blocks of the other slots keep the plain order, which spreads the
+  // last live % 8 slots over all XCDs.
   int bx = blockIdx.x, slot = blockIdx.y;
   if (gridDim.y >= XS_DOWN_XCD_SLOTS) {
     const int L = blockIdx.x + gridDim.x * blockIdx.y;
-    const int s = L >> 3;
-    slot = (L & 7) + 8 * (s / gridDim.x);
-    bx = s % gridDim.x;
+    const int live = a.n_shared + a.counters[kCntActive];   // <= gridDim.y
+    if (L < (int)gridDim.x * (live & ~7)) {
+      const int s = L >> 3;
+      slot = (L & 7) + 8 * (s / gridDim.x);
+      bx = s % gridDim.x;
+    }
   }
   SlotWork sw;
   if (!slot_work(a, slot, sw)) return;
@@ -1249,9 +1257,7 @@ template <int kW, int NM, int TL = XS_DOWN_TL>
 void launch_down_fmt(const FfnArgs& a, int u, hipStream_t stream) {
   const int cols = kWaves * kCols * NM;
   const int slots = a.max_active + a.n_shared;
-  const dim3 grid((a.d + cols - 1) / cols,
-                  slots >= XS_DOWN_XCD_SLOTS ? (slots + 7) / 8 * 8 : slots, a.splits),
-      block(kBlock);
+  const dim3 grid((a.d + cols - 1) / cols, slots, a.splits), block(kBlock);
   if (u == 8) {
     hipLaunchKernelGGL((down_kernel<8, kW, NM, TL>), grid, block, 0, stream, a);
     return;
