@@ -742,9 +742,6 @@ __device__ __forceinline__ void staged_pass(const uint16_t* x, size_t ld, const 
 #endif
 // Expert slots from which the down grid keeps each slot's column blocks on one XCD (with
 // fewer, whole XCDs would idle: five experts left three of eight without work).
-#ifndef XS_GU_CT2_WPE
-#define XS_GU_CT2_WPE 1
-#endif
 #ifndef XS_DOWN_XCD_SLOTS
 #define XS_DOWN_XCD_SLOTS 16
 #endif
@@ -818,7 +815,7 @@ __device__ __forceinline__ const uint8_t* slot_q(const FfnArgs& a, const SlotWor
 // The MXFP4 one-tile instance is held to 168 registers (3 waves per SIMD): left alone the
 // compiler took 175 and 2 waves, and DeepSeek T=8 gate/up ran 14 % slower.
 template <int U, bool kSplit, int kW, int CT>
-__global__ __attribute__((amdgpu_waves_per_eu(kW == kMx4 && CT == 1 ? 3 : (kW == kBf16 && CT == 2 ? XS_GU_CT2_WPE : 1))))
+__global__ __attribute__((amdgpu_waves_per_eu(kW == kMx4 && CT == 1 ? 3 : 1)))
 __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
   constexpr int NM = 2 * CT;                   // weight tiles: W1 and W3 of each column tile
   SlotWork sw;
