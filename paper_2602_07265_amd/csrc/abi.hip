@@ -305,6 +305,8 @@ xshare_status layer_common(const uint16_t* x, const float* logits, const uint16_
                                                                  : layer_estimate(T, params, ep);
   fa.splits = wt.fmt == 2 ? L.q4_splits : L.splits;
   fa.gu_splits = L.gu_splits;
+  fa.gu_tail_splits = L.gu_tail_splits;
+  fa.slot_base = 0;
   fa.gpart = at<float>(ws, L.gpart);
   fa.G = ra.G;
   fa.group = ra.group;

@@ -819,7 +819,7 @@ __global__ __attribute__((amdgpu_waves_per_eu(kW == kMx4 && CT == 1 ? 3 : 1)))
 __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
   constexpr int NM = 2 * CT;                   // weight tiles: W1 and W3 of each column tile
   SlotWork sw;
-  if (!slot_work(a, blockIdx.y, sw)) return;
+  if (!slot_work(a, a.slot_base + blockIdx.y, sw)) return;
   const int p0 = sw.p0, te = sw.te;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int j0 = (blockIdx.x * kWaves + wave) * kCols * CT;
@@ -1100,6 +1100,32 @@ __global__ __launch_bounds__(kBlock) void gate_up_finish_kernel(FfnArgs a) {
   store_hilo(a.h, p, c + 3, a.f, gs.w / (1.0f + __expf(-gs.w)) * us.w);
 }
 
+// The finish pass of the gate/up tail: rows of slots slot_base + blockIdx.y / T (at most T
+// rows a slot: a token takes an expert once; a shared expert takes every token).
+__global__ __launch_bounds__(kBlock) void gate_up_tail_finish_kernel(FfnArgs a) {
+  SlotWork sw;
+  if (!slot_work(a, a.slot_base + blockIdx.y / a.T, sw)) return;
+  const int t = blockIdx.y % a.T;
+  if (t >= sw.te) return;
+  const int p = sw.p0 + t;
+  const int c = (blockIdx.x * kBlock + threadIdx.x) * 4;
+  if (c >= a.f) return;
+  const size_t plane = (size_t)a.rows * a.f;
+  const size_t at = (size_t)p * a.f + c;
+  float4 gs = *reinterpret_cast<const float4*>(a.gpart + at);
+  float4 us = *reinterpret_cast<const float4*>(a.gpart + plane + at);
+  for (int z = 1; z < a.gu_splits; ++z) {
+    const float4 gz = *reinterpret_cast<const float4*>(a.gpart + 2 * z * plane + at);
+    const float4 uz = *reinterpret_cast<const float4*>(a.gpart + (2 * z + 1) * plane + at);
+    gs.x += gz.x; gs.y += gz.y; gs.z += gz.z; gs.w += gz.w;
+    us.x += uz.x; us.y += uz.y; us.z += uz.z; us.w += uz.w;
+  }
+  store_hilo(a.h, p, c + 0, a.f, gs.x / (1.0f + __expf(-gs.x)) * us.x);
+  store_hilo(a.h, p, c + 1, a.f, gs.y / (1.0f + __expf(-gs.y)) * us.y);
+  store_hilo(a.h, p, c + 2, a.f, gs.z / (1.0f + __expf(-gs.z)) * us.z);
+  store_hilo(a.h, p, c + 3, a.f, gs.w / (1.0f + __expf(-gs.w)) * us.w);
+}
+
 __global__ __launch_bounds__(kBlock) void combine_kernel(FfnArgs a) {
   const int i = blockIdx.y;
   const int c = (blockIdx.x * kBlock + threadIdx.x) * 4;
@@ -1208,6 +1234,69 @@ bool gu_two_tiles(const FfnArgs& a, int kW, unsigned splits) {
              (a.est_active + a.n_shared) * splits >= min_blocks;
 }
 
+// Blocks of the unsplit gate/up instance the GPU runs at once (cached per instance; one
+// device type).
+template <int U, int kW, int CT>
+int resident_blocks() {
+  static int cached = 0;
+  if (cached == 0) {
+    int per_cu = 0, dev = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, gate_up_kernel<U, false, kW, CT>,
+                                                     kBlock, 0) != hipSuccess ||
+        hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return 0;
+    cached = per_cu * cus;
+  }
+  return cached;
+}
+
+// An unsplit gate/up launch of grid (B, S): when its last round of blocks holds slots
+// S_main .. S - 1 and under a quarter of the resident blocks, those slots run after the
+// main launch, split `ts` ways along d (partials, then their finish pass).  Returns ts (1:
+// no tail launch) and S_main.
+template <int U>
+int gu_tail_split(const FfnArgs& a, dim3 grid, int resident, int& s_main) {
+  s_main = (int)grid.y;
+  if (a.gu_tail_splits < 2 || a.slot_base != 0 || resident <= 0 || a.T <= 0) return 1;
+  const long B = grid.x, S = grid.y;
+  const long rounds = S * B / resident;
+  if (rounds < 1) return 1;
+  const long main_slots = rounds * resident / B;
+  const long tail = S - main_slots;
+  if (tail <= 0 || 4 * tail * B > resident) return 1;
+  int ts = 1;
+  while (2 * ts <= a.gu_tail_splits && a.d % (2 * ts * 32 * U) == 0 &&
+         tail * B * 2 * ts <= resident)
+    ts *= 2;
+  if (ts < 2) return 1;
+  s_main = (int)main_slots;
+  return ts;
+}
+
+template <int U, int kW, int CT>
+void launch_gu_tail(const FfnArgs& a, dim3 grid, int s_main, int ts, hipStream_t stream) {
+  FfnArgs t = a;
+  t.slot_base = s_main;
+  t.gu_splits = ts;
+  const int tail = (int)grid.y - s_main;
+  const dim3 g(grid.x, tail, ts), block(kBlock);
+  hipLaunchKernelGGL((gate_up_kernel<U, true, kW, CT>), g, block, 0, stream, t);
+  const dim3 fg((a.f + kBlock * 4 - 1) / (kBlock * 4), tail * a.T);
+  hipLaunchKernelGGL(gate_up_tail_finish_kernel, fg, block, 0, stream, t);
+}
+
+// An unsplit launch, with its last round's slots split off when that pays (see
+// gu_tail_split).
+template <int U, int kW, int CT>
+void launch_gu_unsplit(const FfnArgs& a, dim3 grid, dim3 block, hipStream_t stream) {
+  int s_main = 0;
+  const int ts = gu_tail_split<U>(a, grid, resident_blocks<U, kW, CT>(), s_main);
+  const dim3 g(grid.x, s_main, grid.z);
+  if (s_main > 0) hipLaunchKernelGGL((gate_up_kernel<U, false, kW, CT>), g, block, 0, stream, a);
+  if (ts > 1) launch_gu_tail<U, kW, CT>(a, grid, s_main, ts, stream);
+}
+
 template <int U, int kW>
 void launch_gu(const FfnArgs& a, bool split, bool two, dim3 grid, dim3 block,
                hipStream_t stream) {
@@ -1218,14 +1307,14 @@ void launch_gu(const FfnArgs& a, bool split, bool two, dim3 grid, dim3 block,
       return;
     }
     if (two) {
-      hipLaunchKernelGGL((gate_up_kernel<U, false, kW, 2>), grid, block, 0, stream, a);
+      launch_gu_unsplit<U, kW, 2>(a, grid, block, stream);
       return;
     }
   }
   if (split)
     hipLaunchKernelGGL((gate_up_kernel<U, true, kW, 1>), grid, block, 0, stream, a);
   else
-    hipLaunchKernelGGL((gate_up_kernel<U, false, kW, 1>), grid, block, 0, stream, a);
+    launch_gu_unsplit<U, kW, 1>(a, grid, block, stream);
 }
 
 // Unroll U (a power of two dividing K / 32; at most u2 for two-tile launches, u1 for

@@ -130,8 +130,20 @@ inline size_t ffn_rows(int T, int k, int n_shared) {
   return t * size_t(k) + size_t(n_shared) * t;
 }
 
+// The gate/up launch's last, partly filled round of blocks: when it holds under a quarter
+// of the blocks the GPU runs at once, its slots are taken out of the launch and run after
+// it split this many ways along d (a lone block streams its weights several times slower
+// than its share of a full round).  Partial planes for all rows, if within the cap.
+#ifndef XS_GU_TAIL_SPLITS
+#define XS_GU_TAIL_SPLITS 8
+#endif
+#ifndef XS_GU_TAIL_CAP
+#define XS_GU_TAIL_CAP (64L << 20)
+#endif
+
 struct FfnLayout {
   RouteLayout route;
+  int gu_tail_splits;  // K-splits available to the gate/up tail (0: none)
   int gu_splits;  // K-splits of the gate/up GEMM
   int splits;     // K-splits of the down GEMM (bf16 and FP8 weights)
   int q4_splits;  // K-splits of the down GEMM with MXFP4 weights
@@ -153,8 +165,13 @@ inline FfnLayout ffn_layout(int T, int N, int k, bool dense, int d, int f, int e
   L.q4_splits = down_splits(est_active, d, f, true);
   const size_t rows = ffn_rows(T, k, n_shared);
   size_t o = L.route.total;
+  L.gu_tail_splits = 0;
+  if (L.gu_splits == 1 &&
+      sizeof(float) * 2 * size_t(XS_GU_TAIL_SPLITS) * rows * size_t(f) <= size_t(XS_GU_TAIL_CAP))
+    L.gu_tail_splits = XS_GU_TAIL_SPLITS;
+  const int planes = L.gu_splits > 1 ? L.gu_splits : L.gu_tail_splits;
   L.gpart = o;
-  if (L.gu_splits > 1) o += align256(sizeof(float) * 2 * size_t(L.gu_splits) * rows * size_t(f));
+  if (planes > 1) o += align256(sizeof(float) * 2 * size_t(planes) * rows * size_t(f));
   L.h = o; o += align256(sizeof(uint16_t) * rows * 2 * size_t(f));
   const int y_planes = L.splits > L.q4_splits ? L.splits : L.q4_splits;   // any format
   L.y = o; o += align256(sizeof(float) * size_t(y_planes) * rows * size_t(d));
@@ -234,7 +251,9 @@ struct FfnArgs {
   int est_active;              // experts expected to be active (0: unknown), for launch shapes
   int splits;                  // K-splits of the down GEMM (partials summed in the combine)
   int gu_splits;               // K-splits of the gate/up GEMM (partials summed by finish)
-  float* gpart;                // [gu_splits, 2, T * k, f] when gu_splits > 1
+  float* gpart;                // [gu_splits, 2, rows, f] when gu_splits > 1 (or the tail's)
+  int gu_tail_splits;          // partial planes available to the gate/up tail (0: none)
+  int slot_base;               // first expert slot of this launch (the tail's launch: > 0)
   int G;                       // GPU groups, with `group` and `local_group` as in RouteArgs
   const int32_t* group;
   int local_group;

@@ -46,8 +46,16 @@ def test_router_logits_within_the_accumulation_bound():
         say(f"  max |err| / (d u sum|xw|) = {np.max(err / bound):.3e}")
 
 
+def _last_listed(ids, n=2, heavy=8):
+    """The last n experts of the GEMMs' active list (experts with more than `heavy` rows
+    first, then the others, each class in expert order), from the oracle's routing."""
+    e, c = np.unique(ids[ids >= 0], return_counts=True)
+    order = [int(j) for j in e[c > heavy]] + [int(j) for j in e[c <= heavy]]
+    return order[-n:]
+
+
 def _layer(T, N, k, d, f, n_shared, seed, k0=1, M=None, mode="total", tau=0.0, offsets=None,
-           m_r=0, rows=None, label=""):
+           m_r=0, rows=None, tail_rows=0, label=""):
     from paper_2602_07265_amd import xshare as X
     M = M if M is not None else max(k, N // 4)
     x, wg = _router_inputs(T, d, N, seed)
@@ -69,7 +77,10 @@ def _layer(T, N, k, d, f, n_shared, seed, k0=1, M=None, mode="total", tau=0.0, o
     else:
         ref = OR.select_hier(logits, offsets, k, k0, m_r, M, mode)
     assert_route_equal(got, ref, label)
-    rows = list(range(T)) if rows is None else rows
+    rows = list(range(T)) if rows is None else list(rows)
+    for e in _last_listed(ref.ids) if tail_rows else []:   # the launch's last slots
+        rows += [int(i) for i in np.nonzero((ref.ids == e).any(axis=1))[0][:tail_rows]]
+    rows = sorted(set(rows))
     shared_bits = [] if sh is None else [tuple(W.bf16_bits(m[s]) for m in sh)
                                          for s in range(n_shared)]
     y_ref = OF.moe_forward(W.bf16_bits(x), ref.ids, ref.w, expert_fetcher(w1, w3, w2), rows,
@@ -126,8 +137,11 @@ def test_moe_forward_with_shared_experts_from_given_logits():
 
 
 def test_layer_deepseek_sampled():
-    # DeepSeek-R1 shape with its one shared expert, T = 32, total budget 48
-    res = _layer(32, 256, 8, 7168, 2048, 1, 0, M=48, rows=[0, 11, 31], label="deepseek")
+    # DeepSeek-R1 shape with its one shared expert, T = 32, total budget 48: 49 expert
+    # slots, so the gate/up launch's last slot runs apart, split along d; rows of the last
+    # two listed experts are among those checked
+    res = _layer(32, 256, 8, 7168, 2048, 1, 0, M=48, rows=[0, 11, 31], tail_rows=2,
+                 label="deepseek")
     assert int(res["stats"][1]) <= 48
     torch.cuda.empty_cache()
 
