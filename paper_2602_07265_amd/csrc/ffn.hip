@@ -1265,6 +1265,7 @@ int gu_tail_split(const FfnArgs& a, dim3 grid, int resident, int& s_main) {
   const long main_slots = rounds * resident / B;
   const long tail = S - main_slots;
   if (tail <= 0 || 4 * tail * B > resident) return 1;
+  if (tail * a.T > 65535) return 1;                 // the finish pass's grid rows
   int ts = 1;
   while (2 * ts <= a.gu_tail_splits && a.d % (2 * ts * 32 * U) == 0 &&
          tail * B * 2 * ts <= resident)
