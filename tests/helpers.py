@@ -77,3 +77,15 @@ def ffn_error(y_gpu, y_ref):
 
 def bf16_to_f64(t):
     return OF.bf16_to_f64(W.bf16_bits(t))
+
+
+def last_listed_rows(ids, rows, n=2, per=2, heavy=8):
+    """rows plus up to `per` tokens of each of the last n experts of the GEMMs' active list
+    (experts with more than `heavy` rows first, then the others, each class in expert
+    order), from the oracle's routing: the slots that a launch's last round holds."""
+    e, c = np.unique(ids[ids >= 0], return_counts=True)
+    order = [int(j) for j in e[c > heavy]] + [int(j) for j in e[c <= heavy]]
+    out = list(rows)
+    for j in order[-n:]:
+        out += [int(i) for i in np.nonzero((ids == j).any(axis=1))[0][:per]]
+    return sorted(set(out))

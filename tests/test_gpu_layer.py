@@ -12,7 +12,7 @@ import pytest
 import torch
 
 import workloads as W
-from helpers import DEV, assert_route_equal, expert_fetcher, ffn_error, say
+from helpers import DEV, assert_route_equal, expert_fetcher, ffn_error, say, last_listed_rows
 from oracle import ffn as OF
 from oracle import route as OR
 
@@ -46,14 +46,6 @@ def test_router_logits_within_the_accumulation_bound():
         say(f"  max |err| / (d u sum|xw|) = {np.max(err / bound):.3e}")
 
 
-def _last_listed(ids, n=2, heavy=8):
-    """The last n experts of the GEMMs' active list (experts with more than `heavy` rows
-    first, then the others, each class in expert order), from the oracle's routing."""
-    e, c = np.unique(ids[ids >= 0], return_counts=True)
-    order = [int(j) for j in e[c > heavy]] + [int(j) for j in e[c <= heavy]]
-    return order[-n:]
-
-
 def _layer(T, N, k, d, f, n_shared, seed, k0=1, M=None, mode="total", tau=0.0, offsets=None,
            m_r=0, rows=None, tail_rows=0, label=""):
     from paper_2602_07265_amd import xshare as X
@@ -78,9 +70,8 @@ def _layer(T, N, k, d, f, n_shared, seed, k0=1, M=None, mode="total", tau=0.0, o
         ref = OR.select_hier(logits, offsets, k, k0, m_r, M, mode)
     assert_route_equal(got, ref, label)
     rows = list(range(T)) if rows is None else list(rows)
-    for e in _last_listed(ref.ids) if tail_rows else []:   # the launch's last slots
-        rows += [int(i) for i in np.nonzero((ref.ids == e).any(axis=1))[0][:tail_rows]]
-    rows = sorted(set(rows))
+    if tail_rows:                                           # the launch's last slots
+        rows = last_listed_rows(ref.ids, rows, per=tail_rows)
     shared_bits = [] if sh is None else [tuple(W.bf16_bits(m[s]) for m in sh)
                                          for s in range(n_shared)]
     y_ref = OF.moe_forward(W.bf16_bits(x), ref.ids, ref.w, expert_fetcher(w1, w3, w2), rows,
