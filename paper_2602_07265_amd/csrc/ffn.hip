@@ -1131,26 +1131,49 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(FfnArgs a) {
   const int c = (blockIdx.x * kBlock + threadIdx.x) * 4;
   if (c >= a.d) return;
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int r = 0; r < a.k; ++r) {
-    const int slot = i * a.k + r;
-    const int e = a.ids[slot];
-    if (e < 0) continue;
-    if (a.local_group >= 0 && (a.group ? a.group[e] : e / (a.N / a.G)) != a.local_group)
-      continue;   // another GPU group's term of y_i
-    const float wr = a.w[slot];
-    float4 v = *reinterpret_cast<const float4*>(a.yslot + (size_t)slot * a.d + c);
-    for (int s = 1; s < a.splits; ++s) {   // partial sums of a split reduction, in order
-      const float4 u = *reinterpret_cast<const float4*>(
-          a.yslot + ((size_t)s * a.rows + slot) * a.d + c);
-      v.x += u.x;
-      v.y += u.y;
-      v.z += u.z;
-      v.w += u.w;
+  // kR ranks at a time: their ids and weights, then all their row loads, are issued before
+  // any is used (one round trip per group instead of two per rank); the sums keep rank
+  // order and, per rank, split order
+  constexpr int kR = 8;
+  for (int r0 = 0; r0 < a.k; r0 += kR) {
+    int e[kR];
+    float wr[kR];
+#pragma unroll
+    for (int j = 0; j < kR; ++j) {
+      const bool in = r0 + j < a.k;
+      e[j] = in ? a.ids[i * a.k + r0 + j] : -1;
+      wr[j] = in ? a.w[i * a.k + r0 + j] : 0.0f;
     }
-    acc[0] += wr * v.x;
-    acc[1] += wr * v.y;
-    acc[2] += wr * v.z;
-    acc[3] += wr * v.w;
+    bool use[kR];
+    float4 v[kR];
+#pragma unroll
+    for (int j = 0; j < kR; ++j) {
+      use[j] = e[j] >= 0 &&   // another GPU group's terms of y_i are left out
+               (a.local_group < 0 ||
+                (a.group ? a.group[e[j]] : e[j] / (a.N / a.G)) == a.local_group);
+      v[j] = use[j] ? *reinterpret_cast<const float4*>(a.yslot + (size_t)(i * a.k + r0 + j) * a.d + c)
+                    : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    for (int s = 1; s < a.splits; ++s) {   // partial sums of a split reduction, in order
+#pragma unroll
+      for (int j = 0; j < kR; ++j) {
+        if (!use[j]) continue;
+        const float4 u = *reinterpret_cast<const float4*>(
+            a.yslot + ((size_t)s * a.rows + i * a.k + r0 + j) * a.d + c);
+        v[j].x += u.x;
+        v[j].y += u.y;
+        v[j].z += u.z;
+        v[j].w += u.w;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kR; ++j) {
+      if (!use[j]) continue;
+      acc[0] += wr[j] * v[j].x;
+      acc[1] += wr[j] * v[j].y;
+      acc[2] += wr[j] * v[j].z;
+      acc[3] += wr[j] * v[j].w;
+    }
   }
   for (int sh = 0; sh < a.n_shared; ++sh) {  // shared experts, weight 1, after the routed terms
     const size_t row = (size_t)a.T * a.k + (size_t)sh * a.T + i;
