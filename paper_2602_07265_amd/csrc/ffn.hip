@@ -302,10 +302,10 @@ __device__ __forceinline__ void wave_pass_q8(const uint16_t* const (&arow)[TL], 
 }
 
 // The scale byte(s) of a lane's step: one block for U <= 4, two consecutive blocks (two
-// bytes, the first block's in the low byte) for U = 8.
+// bytes, the first block's in the low byte) for U = 8, four for U = 16.
 template <int U>
 __device__ __forceinline__ uint32_t load_e8m0(const uint8_t* p) {
-  if constexpr (U == 16)   // four blocks; two 16-bit loads (scale rows are 2-byte aligned)
+  if constexpr (U == 16)   // as two 16-bit loads
     return *reinterpret_cast<const uint16_t*>(p) |
            ((uint32_t)*reinterpret_cast<const uint16_t*>(p + 2) << 16);
   else if constexpr (U == 8)
