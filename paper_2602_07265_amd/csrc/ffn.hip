@@ -24,6 +24,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
 #include <type_traits>
 
 #include "internal.h"
@@ -1261,17 +1262,19 @@ bool gu_two_tiles(const FfnArgs& a, int kW, unsigned splits) {
 // device type).
 template <int U, int kW, int CT>
 int resident_blocks() {
-  static int cached = 0;
-  if (cached == 0) {
+  static std::atomic<int> cached{0};   // callers on several threads may fill it at once
+  int r = cached.load(std::memory_order_relaxed);
+  if (r == 0) {
     int per_cu = 0, dev = 0, cus = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, gate_up_kernel<U, false, kW, CT>,
                                                      kBlock, 0) != hipSuccess ||
         hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
       return 0;
-    cached = per_cu * cus;
+    r = per_cu * cus;
+    cached.store(r, std::memory_order_relaxed);
   }
-  return cached;
+  return r;
 }
 
 // An unsplit gate/up launch of grid (B, S): when its last round of blocks holds slots
