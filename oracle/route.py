@@ -143,48 +143,48 @@ def scores_over(G, tokens) -> np.ndarray:
 
 # ----------------------------------------------------------------------------- greedy
 
-def greedy_select(scores, start, budget: int, candidates, priority=None) -> set[int]:
-    """Algorithm 1 with a fixed budget: grow ``start`` by the best remaining candidate.
+def greedy_order(scores, start, candidates, priority=None) -> list[int]:
+    """The order in which Algorithm 1's greedy takes experts under the objective of Eq. (2).
 
-    If ``start`` already holds more than ``budget`` experts it is cut to the first
-    ``budget`` under (priority ascending, score descending, index ascending).
+    f(S) = sum of s_j over S is modular (Proposition 3.1): adding e to any set raises f by
+    exactly s_e.  So the argmax of every greedy step is the best remaining candidate by score
+    whatever was taken before, and the greedy takes the candidates in one fixed order, score
+    descending, lowest index first on equal scores (Corollary 3.2).  The starting set comes
+    first, in (priority ascending, score descending, index ascending) order: the order in
+    which a budget smaller than the starting set cuts it.
     """
+    pri = priority or {}
     start = set(int(j) for j in start)
-    if len(start) > budget:
-        pri = priority or {}
-        keep = sorted(start, key=lambda j: (pri.get(j, 0), -float(scores[j]), j))[:budget]
-        return set(keep)
-    S = set(start)
-    while len(S) < budget:
-        rest = [int(e) for e in candidates if int(e) not in S]
-        if not rest:
-            break
-        e_star = max(rest, key=lambda e: (float(scores[e]), -e))   # argmax, lowest index on ties
-        S.add(e_star)
-    return S
+    head = sorted(start, key=lambda j: (pri.get(j, 0), -float(scores[j]), j))
+    rest = sorted(set(int(e) for e in candidates) - start, key=lambda e: (-float(scores[e]), e))
+    return head + rest
+
+
+def greedy_select(scores, start, budget: int, candidates, priority=None) -> set[int]:
+    """Algorithm 1 with a fixed budget (Section 3.4): the first ``budget`` experts of the
+    greedy order, or all of them if there are fewer; a starting set larger than the budget
+    is cut by the order's key."""
+    return set(greedy_order(scores, start, candidates, priority)[:max(int(budget), 0)])
 
 
 def greedy_threshold(scores, start, tau: float, candidates, priority=None) -> set[int]:
-    """Algorithm 1 as printed: from ``start``, add the best remaining candidate while
-    f(S) < tau * f(E), with f(S) = sum of the scores in S (Eq. (2)) in fp32."""
+    """Algorithm 1's own stopping rule: the shortest prefix of the greedy order that holds
+    the whole starting set and reaches f(S) >= tau * f(E), f(S) = sum of the scores in S
+    (Eq. (2)); every candidate if no prefix reaches it.  All in fp32: f(E) adds every s_j in
+    index order, f(S) adds the prefix's scores in order, tau * f(E) is one product."""
     scores = np.asarray(scores, dtype=F32)
     f_E = F32(0.0)
     for j in range(len(scores)):                       # f(E), index order
         f_E = F32(f_E + scores[j])
     target = F32(F32(tau) * f_E)
-    pri = priority or {}
-    S = set(int(j) for j in start)
+    order = greedy_order(scores, start, candidates, priority)
+    n_start = len(set(int(j) for j in start))
     f_S = F32(0.0)
-    for j in sorted(S, key=lambda j: (pri.get(j, 0), -float(scores[j]), j)):
+    for m, j in enumerate(order):
+        if m >= n_start and not f_S < target:          # order[:m] reaches the target
+            return set(order[:m])
         f_S = F32(f_S + scores[j])
-    while f_S < target:
-        rest = [int(e) for e in candidates if int(e) not in S]
-        if not rest:
-            break
-        e_star = max(rest, key=lambda e: (float(scores[e]), -e))   # argmax, lowest index on ties
-        S.add(e_star)
-        f_S = F32(f_S + scores[e_star])
-    return S
+    return set(order)
 
 
 def _effective_budget(base: int, n_cand: int, k: int) -> int:
