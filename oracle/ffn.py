@@ -144,3 +144,21 @@ def moe_forward(x_bits, ids, w, expert, rows=None, local=None, shared=()) -> np.
     for w1, w3, w2 in shared:
         y += expert_ffn(X[rows], w1, w3, w2)
     return y
+
+
+def combine(outputs, ids, w, d, rows=None, local=None) -> np.ndarray:
+    """The routed sum of Section 2.1 from expert outputs on every token of the batch:
+    y[i] = sum_r w[i,r] * outputs[ids[i,r]][i], ranks r in order, for the tokens in ``rows``
+    (default: all).  ``outputs[e]`` is float64 [T, d], expert e applied to every token
+    (expert_ffn over all rows of x); with ``local`` only those experts' terms are summed.
+    Returns float64 [len(rows), d]."""
+    ids = np.asarray(ids)
+    w = np.asarray(w, dtype=np.float64)
+    rows = list(range(ids.shape[0])) if rows is None else [int(i) for i in rows]
+    y = np.zeros((len(rows), d), dtype=np.float64)
+    for p, i in enumerate(rows):
+        for r in range(ids.shape[1]):
+            e = int(ids[i, r])
+            if local is None or e in local:
+                y[p] += w[i, r] * outputs[e][i]
+    return y

@@ -6,7 +6,7 @@ import pytest
 import torch
 
 import workloads as W
-from helpers import DEV, assert_route_equal, expert_fetcher, ffn_error, say
+from helpers import DEV, assert_ffn_close, assert_route_equal, expert_fetcher, say
 from oracle import budget as B
 from oracle import ffn as OF
 from oracle import route as OR
@@ -75,8 +75,7 @@ def test_ledger_through_the_layer_entry_points():
         assert_route_equal({key: v.cpu().numpy() for key, v in res.items() if key != "y"}, ref,
                            f"moe layer {l}")
         y_ref = OF.moe_forward(W.bf16_bits(x), ref.ids, ref.w, expert_fetcher(w1, w3, w2))
-        err, _ = ffn_error(OF.bf16_to_f64(W.bf16_bits(res["y"])), y_ref)
-        assert err <= 2e-2
+        assert_ffn_close(OF.bf16_to_f64(W.bf16_bits(res["y"])), y_ref, f"moe layer {l}")
         refs.append(ref)
     # an expert-parallel selection and a hierarchical call with invalid device-side offsets
     # (it selects nothing) add to the same ledger

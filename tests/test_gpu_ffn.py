@@ -1,25 +1,26 @@
 """MoE layer parity on the GPU: y within 2e-2 * RMS of the float64 oracle (Section 2.1).
 
 The oracle routes independently (bit-exact routing is asserted too) and evaluates the
-SwiGLU experts in float64 from the same bf16 inputs.  Full-size layers are compared on
-sampled tokens, the oracle computing those rows one by one.
+SwiGLU experts in float64 from the same bf16 inputs.  Every workload shape of the layer is
+compared on all of its token rows: the DeepSeek-R1 shape at T = 8 and T = 32 with budgets
+24, 48 and 96 (domain logits) and 48 (iid logits), the speculative 16 x 4 batch, the
+Mixtral and Qwen-MoE shapes.  The oracle evaluates each routed expert once on every token
+of a batch and the budgets' routings share those outputs.
 """
 import numpy as np
 import pytest
 import torch
 
 import workloads as W
-from helpers import (DEV, assert_route_equal, expert_fetcher, ffn_error, make_layer,
-                     oracle_route, say)
+from helpers import (DEV, OracleOutputs, assert_ffn_close, assert_route_equal, bf16_weights_of,
+                     make_layer, oracle_route, say)
 from oracle import ffn as OF
 
 pytestmark = pytest.mark.gpu
 
-TOL = 2e-2   # max |y_gpu - y_ref| <= TOL * RMS(y_ref)
-
 
 def _run(cfg, seed, k0, M, mode="total", score="topk", rows=None, m_r=0, layer=None,
-         label=""):
+         oracle=None, label=""):
     from paper_2602_07265_amd import xshare as X
     h, off, x, w1, w3, w2 = layer if layer is not None else make_layer(cfg, seed)
     hier = cfg.get("logits") == "spec"
@@ -32,14 +33,30 @@ def _run(cfg, seed, k0, M, mode="total", score="topk", rows=None, m_r=0, layer=N
     ref = oracle_route(h, cfg["k"], k0, M, mode, score, off if hier else None, m_r)
     assert_route_equal(got, ref, label)
     rows = list(range(cfg["T"])) if rows is None else rows
-    y_ref = OF.moe_forward(W.bf16_bits(x), ref.ids, ref.w, expert_fetcher(w1, w3, w2), rows)
+    if oracle is None:
+        oracle = OracleOutputs(x, bf16_weights_of(w1, w3, w2))
+    y_ref = oracle.y(ref.ids, ref.w, rows)
     y_gpu = OF.bf16_to_f64(W.bf16_bits(res["y"]))[rows]
-    err, rms = ffn_error(y_gpu, y_ref)
-    say(f"  max err / RMS = {err:.3e} (RMS {rms:.3e}), |S|={got['stats'][0]} "
-        f"active={got['stats'][1]} |U|={got['stats'][2]}")
-    assert np.all(np.isfinite(y_gpu))
-    assert err <= TOL, f"{label}: max error {err:.3e} x RMS exceeds {TOL}"
+    assert_ffn_close(y_gpu, y_ref, label, f", |S|={got['stats'][0]} active={got['stats'][1]} "
+                     f"|U|={got['stats'][2]}, {len(rows)} rows")
     return res, ref
+
+
+@pytest.fixture(scope="module")
+def ds_weights():
+    """The DeepSeek-R1-shaped layer's expert weights (N=256, d=7168, f=2048, seed 0): the
+    T = 8, T = 32 and speculative workloads draw the same weights for seed 0."""
+    say("generating the DeepSeek-shaped expert weights (22.5 GB)")
+    w = W.expert_weights(256, 7168, 2048, 0, DEV)
+    yield w
+    del w
+    torch.cuda.empty_cache()
+
+
+def _ds_layer(cfg, seed, weights):
+    h, off = W.make_logits(cfg, seed)
+    x = W.activations(cfg["T"], cfg["d"], seed, DEV)
+    return (h, off, x, *weights)
 
 
 def test_ffn_tiny_all_modes():
@@ -96,24 +113,45 @@ def test_ffn_qwen_full():
     _run(c, 0, 0, c["N"], "extra", layer=layer, label="qwen vanilla")
 
 
-def test_ffn_mixtral_sampled():
+def test_ffn_mixtral():
     c = W.CONFIGS["mixtral"]
-    _run(c, 0, 1, 5, rows=[0, 7, 15], label="mixtral")
+    _run(c, 0, 1, 5, label="mixtral")
+    torch.cuda.empty_cache()
 
 
-def test_ffn_deepseek_t32_sampled():
+def test_ffn_deepseek_t32(ds_weights):
+    """The headline shape at every budget of its sweep, all 32 rows; M = 96 exceeds |U| on
+    some batches, so the whole union is selected there.  The iid control batch shares x."""
     c = W.CONFIGS["ds_t32"]
-    layer = make_layer(c, 0)
-    for M in (24, 48):
-        _run(c, 0, 1, M, rows=[0, 13, 31], layer=layer, label=f"ds_t32 M{M}")
-    del layer
-    torch.cuda.empty_cache()
+    layer = _ds_layer(c, 0, ds_weights)
+    oracle = OracleOutputs(layer[2], bf16_weights_of(*ds_weights))
+    for M in c["M_sweep"]:
+        _run(c, 0, 1, M, layer=layer, oracle=oracle, label=f"ds_t32 M{M}")
+    ci = W.CONFIGS["ds_iid_t32"]
+    _run(ci, 0, 1, 48, layer=(*W.make_logits(ci, 0), *layer[2:]), oracle=oracle,
+         label="ds_iid_t32 M48")
 
 
-def test_ffn_spec_hier_sampled():
+def test_ffn_deepseek_t8(ds_weights):
+    """T = 8: the narrow down GEMM shape (few rows per expert); M = 48 and 96 reach |U|."""
+    c = W.CONFIGS["ds_t8"]
+    layer = _ds_layer(c, 0, ds_weights)
+    oracle = OracleOutputs(layer[2], bf16_weights_of(*ds_weights))
+    for M in c["M_sweep"]:
+        _run(c, 0, 1, M, layer=layer, oracle=oracle, label=f"ds_t8 M{M}")
+    ci = W.CONFIGS["ds_iid_t8"]
+    _run(ci, 0, 1, 48, layer=(*W.make_logits(ci, 0), *layer[2:]), oracle=oracle,
+         label="ds_iid_t8 M48")
+
+
+def test_ffn_spec_hier(ds_weights):
+    """The speculative 16 x 4 batch, all 64 rows: hierarchical selection with m_r = 4 under a
+    total budget of 64, and the paper's (k0, m, m_r) = (1, 0, 4) as an extra budget of 0."""
     c = W.CONFIGS["spec"]
-    _run(c, 0, 1, 64, m_r=4, rows=[0, 1, 33, 63], label="spec")
-    torch.cuda.empty_cache()
+    layer = _ds_layer(c, 0, ds_weights)
+    oracle = OracleOutputs(layer[2], bf16_weights_of(*ds_weights))
+    _run(c, 0, 1, 64, m_r=4, layer=layer, oracle=oracle, label="spec M64")
+    _run(c, 0, 1, 0, "extra", m_r=4, layer=layer, oracle=oracle, label="spec extra 0")
 
 
 def test_ffn_reads_only_selected_experts_and_is_deterministic():

@@ -12,13 +12,13 @@ import pytest
 import torch
 
 import workloads as W
-from helpers import DEV, assert_route_equal, expert_fetcher, ffn_error, say, last_listed_rows
+from helpers import (DEV, OracleOutputs, assert_ffn_close, assert_route_equal, bf16_weights_of,
+                     expert_fetcher, say)
 from oracle import ffn as OF
 from oracle import route as OR
 
 pytestmark = pytest.mark.gpu
 
-TOL = 2e-2
 
 
 def _router_inputs(T, d, N, seed, Q=4):
@@ -47,7 +47,7 @@ def test_router_logits_within_the_accumulation_bound():
 
 
 def _layer(T, N, k, d, f, n_shared, seed, k0=1, M=None, mode="total", tau=0.0, offsets=None,
-           m_r=0, rows=None, tail_rows=0, label=""):
+           m_r=0, rows=None, label=""):
     from paper_2602_07265_amd import xshare as X
     M = M if M is not None else max(k, N // 4)
     x, wg = _router_inputs(T, d, N, seed)
@@ -70,17 +70,12 @@ def _layer(T, N, k, d, f, n_shared, seed, k0=1, M=None, mode="total", tau=0.0, o
         ref = OR.select_hier(logits, offsets, k, k0, m_r, M, mode)
     assert_route_equal(got, ref, label)
     rows = list(range(T)) if rows is None else list(rows)
-    if tail_rows:                                           # the launch's last slots
-        rows = last_listed_rows(ref.ids, rows, per=tail_rows)
     shared_bits = [] if sh is None else [tuple(W.bf16_bits(m[s]) for m in sh)
                                          for s in range(n_shared)]
-    y_ref = OF.moe_forward(W.bf16_bits(x), ref.ids, ref.w, expert_fetcher(w1, w3, w2), rows,
-                           shared=shared_bits)
+    y_ref = OracleOutputs(x, bf16_weights_of(w1, w3, w2), shared_bits).y(ref.ids, ref.w, rows)
     y_gpu = OF.bf16_to_f64(W.bf16_bits(res["y"]))[rows]
     assert np.all(np.isfinite(y_gpu))
-    err, rms = ffn_error(y_gpu, y_ref)
-    say(f"  max err / RMS = {err:.3e} (RMS {rms:.3e}) |S|={got['stats'][0]}")
-    assert err <= TOL, f"{label}: max error {err:.3e} x RMS exceeds {TOL}"
+    assert_ffn_close(y_gpu, y_ref, label, f" |S|={got['stats'][0]}")
     return res
 
 
@@ -122,17 +117,13 @@ def test_moe_forward_with_shared_experts_from_given_logits():
     assert_route_equal(got, ref, "qwen shared")
     y_ref = OF.moe_forward(W.bf16_bits(x), ref.ids, ref.w, expert_fetcher(w1, w3, w2),
                            shared=[tuple(W.bf16_bits(m[s]) for m in sh) for s in range(4)])
-    err, rms = ffn_error(OF.bf16_to_f64(W.bf16_bits(res["y"])), y_ref)
-    say(f"  max err / RMS = {err:.3e}")
-    assert err <= TOL
+    assert_ffn_close(OF.bf16_to_f64(W.bf16_bits(res["y"])), y_ref, "qwen shared")
 
 
-def test_layer_deepseek_sampled():
-    # DeepSeek-R1 shape with its one shared expert, T = 32, total budget 48: 49 expert
-    # slots, so the gate/up launch's last slot runs apart, split along d; rows of the last
-    # two listed experts are among those checked
-    res = _layer(32, 256, 8, 7168, 2048, 1, 0, M=48, rows=[0, 11, 31], tail_rows=2,
-                 label="deepseek")
+def test_layer_deepseek():
+    # DeepSeek-R1 shape with its one shared expert, T = 32, total budget 48, all rows: 49
+    # expert slots, so the gate/up launch's last slot runs apart, split along d
+    res = _layer(32, 256, 8, 7168, 2048, 1, 0, M=48, label="deepseek")
     assert int(res["stats"][1]) <= 48
     torch.cuda.empty_cache()
 

@@ -7,7 +7,7 @@ import numpy as np
 import pytest
 
 import workloads as W
-from helpers import assert_route_equal, gpu_route, oracle_route, say
+from helpers import assert_route_equal, gpu_route, oracle_route, say, score_order_case
 
 pytestmark = pytest.mark.gpu
 
@@ -71,6 +71,15 @@ def test_route_adversarial_ties_and_signed_zero():
     h[np.arange(16), np.arange(16) * 3 + 1] = -50.0
     _case(h, 4, 1, 20, label="underflow")
     _case(h, 4, 0, 6, "extra", label="underflow")
+
+
+def test_route_score_sum_order_decides_the_set():
+    """The case where the ascending token order of the score sums decides which of two
+    experts takes the last slot (the oracle's pin derives it by hand): bit-exact parity."""
+    h, k, M, A, B = score_order_case()
+    _case(h, k, 0, M, label="score order")
+    got = gpu_route(h, k, 0, M)
+    assert got["sel_mask"][A] == 1 and got["sel_mask"][B] == 0
 
 
 def test_route_shapes_edges():

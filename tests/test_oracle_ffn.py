@@ -85,6 +85,18 @@ def test_dense_gate_formulation_on_tiny_workload():
     # a subset of rows gives the same rows
     sub = O.moe_forward(x, r.ids, r.w, lambda e: ws[e], rows=[5, 1])
     assert np.allclose(sub, y[[5, 1]], rtol=1e-12, atol=1e-15)
+    # the routed sum from every expert's output on all tokens (combine) is the dense form too,
+    # for all rows, a subset, and one group's experts (the dense form over those experts only)
+    outs = {e: O.expert_ffn(X, *ws[e]) for e in range(c["N"])}
+    assert np.allclose(O.combine(outs, r.ids, r.w, c["d"]), dense, rtol=1e-12, atol=1e-14)
+    assert np.allclose(O.combine(outs, r.ids, r.w, c["d"], rows=[6, 0]), dense[[6, 0]],
+                       rtol=1e-12, atol=1e-14)
+    mine = {int(e) for e in r.ids[0][:1]}
+    part = np.zeros_like(dense)
+    for e in mine:
+        part += G[:, e:e + 1] * outs[e]
+    assert np.allclose(O.combine(outs, r.ids, r.w, c["d"], local=mine), part, rtol=1e-12,
+                       atol=1e-14)
 
 
 def test_group_shares_sum_to_the_layer():

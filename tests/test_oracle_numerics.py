@@ -113,3 +113,23 @@ def test_softmax_dense_matches_float64():
         ref = e / e.sum()
         rel = np.abs(g.astype(np.float64) - ref) / ref
         assert rel.max() <= _softmax_rel_bound(h, N)
+
+
+def test_scores_sum_tokens_in_ascending_order():
+    """s_j = sum_i g_ij is summed one token at a time in ascending token order (Eq. (2) in
+    fp32).  Hand-derived: expert A's gates are fp32(1/3), 1/4, fp32(1/6) in token order, so
+    ((1/3 + 1/4) + 1/6) = 0.75000006 (0x3F400001) while the reverse order gives exactly 0.75,
+    which expert B (lower index) has too; with a total budget whose last slot goes to one of
+    them, the ascending order selects A, and the reverse order would select B."""
+    from helpers import score_order_case
+    from oracle import route as R
+    h, k, M, A, B = score_order_case()
+    third, sixth = F32(1) / F32(3), F32(1) / F32(6)          # correctly rounded quotients
+    assert third == F32(0.3333333432674408) and sixth == F32(0.1666666716337204)
+    asc = F32(F32(third + F32(0.25)) + sixth)
+    rev = F32(F32(sixth + F32(0.25)) + third)
+    assert asc.view(np.uint32) == 0x3F400001 and rev == F32(0.75)
+    r = R.route(h, k, 0, M)
+    assert r.scores[A].view(np.uint32) == asc.view(np.uint32)
+    assert r.scores[B] == F32(0.75)
+    assert r.sel_list == [A, 3, 4, 5, 6, 7]

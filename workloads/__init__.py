@@ -104,7 +104,8 @@ def _mul32(x, m: int):
 
 
 def _mix32(x):
-    """32-bit integer hash (xorshift-multiply rounds, constants 0x7feb352d / 0x846ca68b)."""
+    """32-bit integer hash: xorshift-multiply rounds with the published "lowbias32"
+    constants 0x7feb352d / 0x846ca68b (Chris Wellons' hash-prospector search)."""
     x = x ^ (x >> 16)
     x = _mul32(x, 0x7FEB352D)
     x = x ^ (x >> 15)
