@@ -143,7 +143,8 @@ int n_shared_of(const xshare_shared_experts* shared) { return shared ? shared->n
 xs::FfnLayout layer_layout(int32_t T, int32_t d, int32_t f, const xshare_route_params* p,
                            const xshare_ep_layout* ep, int n_shared) {
   return xs::ffn_layout(T, p->n_experts, p->top_k, p->score_mode == XSHARE_SCORE_DENSE, d, f,
-                        layer_estimate(T, p, ep) + n_shared, n_shared);
+                        layer_estimate(T, p, ep) + n_shared, n_shared,
+                        p->budget_mode == XSHARE_BUDGET_TOTAL);
 }
 
 // Router scratch: its fp32 part planes [parts, T, N].
@@ -316,6 +317,8 @@ xshare_status layer_common(const uint16_t* x, const float* logits, const uint16_
   fa.sw3 = n_shared ? shared->w3 : nullptr;
   fa.sw2 = n_shared ? shared->w2 : nullptr;
   fa.rows = (long)xs::ffn_rows(T, k, n_shared);
+  fa.part_rows = fa.rows;
+  fa.part_compact = 0;
   fa.offsets = ra.offsets;
   fa.perm = ra.perm;
   fa.active = ra.active;

@@ -24,6 +24,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <atomic>
 #include <type_traits>
 
@@ -833,7 +834,7 @@ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
   const int Kg = kSplit ? d / a.gu_splits : d;   // this block's part of the reduction
   const size_t kbase = kSplit ? (size_t)blockIdx.z * Kg : 0;
   const size_t k0 = kbase + (size_t)(kW == kBf16 ? klane<U>(g) : g * 8 * U);
-  const size_t plane = (size_t)a.rows * f;     // one fp32 partial plane [rows, f]
+  const size_t plane = (size_t)a.part_rows * f;   // one fp32 partial plane [part_rows, f]
   int col[CT];                                 // this lane's column of each tile (< f)
   float sc[NM];                                // FP8 per-row scales (else 1)
 #pragma unroll
@@ -925,10 +926,12 @@ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
             if (j0 + 16 * ct >= f) break;
             const float h1 = acc[2 * ct][rt][i] * sc[2 * ct];
             const float h3 = acc[2 * ct + 1][rt][i] * sc[2 * ct + 1];
-            const size_t at = (size_t)(p0 + t) * f + col[ct];
             if (!kSplit) {
               store_hilo(a.h, p0 + t, col[ct], f, h1 / (1.0f + __expf(-h1)) * h3);
             } else {
+              // the tail's planes hold its slots' rows only
+              const size_t prow = a.part_compact ? (size_t)blockIdx.y * a.T + t : (size_t)(p0 + t);
+              const size_t at = prow * f + col[ct];
               float* const part = a.gpart + 2 * blockIdx.z * plane;
               part[at] = h1;
               part[plane + at] = h3;
@@ -1072,21 +1075,11 @@ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
   }
 }
 
-// Split gate/up reduction: sums the gate and up partials in split order, then
-// H = silu(gate) * up in bf16.  One block row per hidden row; routed rows beyond the routed
-// count, and rows whose expert the GEMMs did not cover (another GPU group's), are skipped.
-__global__ __launch_bounds__(kBlock) void gate_up_finish_kernel(FfnArgs a) {
-  const int p = blockIdx.y;
-  const bool shared_row = p >= a.T * a.k;
-  if (!shared_row && p >= a.offsets[a.N]) return;
-  if (!shared_row && a.local_group >= 0) {
-    const int e = a.ids[a.perm[p]];
-    if ((a.group ? a.group[e] : e / (a.N / a.G)) != a.local_group) return;
-  }
-  const int c = (blockIdx.x * kBlock + threadIdx.x) * 4;
-  if (c >= a.f) return;
-  const size_t plane = (size_t)a.rows * a.f;
-  const size_t at = (size_t)p * a.f + c;
+// Sums the gate and up partials of hidden element c..c+3 of partial row `prow` in split
+// order, then H[hrow] = silu(gate) * up as bf16 hi and lo.
+__device__ __forceinline__ void finish_row(const FfnArgs& a, size_t prow, size_t hrow, int c) {
+  const size_t plane = (size_t)a.part_rows * a.f;
+  const size_t at = prow * a.f + c;
   float4 gs = *reinterpret_cast<const float4*>(a.gpart + at);
   float4 us = *reinterpret_cast<const float4*>(a.gpart + plane + at);
   for (int z = 1; z < a.gu_splits; ++z) {
@@ -1095,36 +1088,41 @@ __global__ __launch_bounds__(kBlock) void gate_up_finish_kernel(FfnArgs a) {
     gs.x += gz.x; gs.y += gz.y; gs.z += gz.z; gs.w += gz.w;
     us.x += uz.x; us.y += uz.y; us.z += uz.z; us.w += uz.w;
   }
-  store_hilo(a.h, p, c + 0, a.f, gs.x / (1.0f + __expf(-gs.x)) * us.x);
-  store_hilo(a.h, p, c + 1, a.f, gs.y / (1.0f + __expf(-gs.y)) * us.y);
-  store_hilo(a.h, p, c + 2, a.f, gs.z / (1.0f + __expf(-gs.z)) * us.z);
-  store_hilo(a.h, p, c + 3, a.f, gs.w / (1.0f + __expf(-gs.w)) * us.w);
+  store_hilo(a.h, hrow, c + 0, a.f, gs.x / (1.0f + __expf(-gs.x)) * us.x);
+  store_hilo(a.h, hrow, c + 1, a.f, gs.y / (1.0f + __expf(-gs.y)) * us.y);
+  store_hilo(a.h, hrow, c + 2, a.f, gs.z / (1.0f + __expf(-gs.z)) * us.z);
+  store_hilo(a.h, hrow, c + 3, a.f, gs.w / (1.0f + __expf(-gs.w)) * us.w);
 }
 
-// The finish pass of the gate/up tail: rows of slots slot_base + blockIdx.y / T (at most T
-// rows a slot: a token takes an expert once; a shared expert takes every token).
+// Split gate/up reduction: H for every hidden row from its partials.  Block row y takes
+// hidden rows y, y + gridDim.y, ... (the grid keeps at most 65535 rows); routed rows beyond
+// the routed count, and rows whose expert the GEMMs did not cover (another GPU group's),
+// are skipped.
+__global__ __launch_bounds__(kBlock) void gate_up_finish_kernel(FfnArgs a) {
+  const int c = (blockIdx.x * kBlock + threadIdx.x) * 4;
+  if (c >= a.f) return;
+  for (long p = blockIdx.y; p < a.rows; p += gridDim.y) {
+    const bool shared_row = p >= (long)a.T * a.k;
+    if (!shared_row && p >= a.offsets[a.N]) continue;
+    if (!shared_row && a.local_group >= 0) {
+      const int e = a.ids[a.perm[p]];
+      if ((a.group ? a.group[e] : e / (a.N / a.G)) != a.local_group) continue;
+    }
+    finish_row(a, (size_t)p, (size_t)p, c);
+  }
+}
+
+// The finish pass of the gate/up tail: block row y is partial row y of the tail's compact
+// planes, token y % T of slot slot_base + y / T (at most T rows a slot: a token takes an
+// expert once; a shared expert takes every token).
 __global__ __launch_bounds__(kBlock) void gate_up_tail_finish_kernel(FfnArgs a) {
   SlotWork sw;
   if (!slot_work(a, a.slot_base + blockIdx.y / a.T, sw)) return;
   const int t = blockIdx.y % a.T;
   if (t >= sw.te) return;
-  const int p = sw.p0 + t;
   const int c = (blockIdx.x * kBlock + threadIdx.x) * 4;
   if (c >= a.f) return;
-  const size_t plane = (size_t)a.rows * a.f;
-  const size_t at = (size_t)p * a.f + c;
-  float4 gs = *reinterpret_cast<const float4*>(a.gpart + at);
-  float4 us = *reinterpret_cast<const float4*>(a.gpart + plane + at);
-  for (int z = 1; z < a.gu_splits; ++z) {
-    const float4 gz = *reinterpret_cast<const float4*>(a.gpart + 2 * z * plane + at);
-    const float4 uz = *reinterpret_cast<const float4*>(a.gpart + (2 * z + 1) * plane + at);
-    gs.x += gz.x; gs.y += gz.y; gs.z += gz.z; gs.w += gz.w;
-    us.x += uz.x; us.y += uz.y; us.z += uz.z; us.w += uz.w;
-  }
-  store_hilo(a.h, p, c + 0, a.f, gs.x / (1.0f + __expf(-gs.x)) * us.x);
-  store_hilo(a.h, p, c + 1, a.f, gs.y / (1.0f + __expf(-gs.y)) * us.y);
-  store_hilo(a.h, p, c + 2, a.f, gs.z / (1.0f + __expf(-gs.z)) * us.z);
-  store_hilo(a.h, p, c + 3, a.f, gs.w / (1.0f + __expf(-gs.w)) * us.w);
+  finish_row(a, blockIdx.y, (size_t)(sw.p0 + t), c);
 }
 
 __global__ __launch_bounds__(kBlock) void combine_kernel(FfnArgs a) {
@@ -1290,7 +1288,7 @@ int gu_tail_split(const FfnArgs& a, dim3 grid, int resident, int& s_main) {
   if (rounds < 1) return 1;
   const long main_slots = rounds * resident / B;
   const long tail = S - main_slots;
-  if (tail <= 0 || 4 * tail * B > resident) return 1;
+  if (tail <= 0 || 4 * tail * B > resident || tail > XS_GU_TAIL_MAX_SLOTS) return 1;
   if (tail * a.T > 65535) return 1;                 // the finish pass's grid rows
   int ts = 1;
   while (2 * ts <= a.gu_tail_splits && a.d % (2 * ts * 32 * U) == 0 &&
@@ -1306,6 +1304,8 @@ void launch_gu_tail(const FfnArgs& a, dim3 grid, int s_main, int ts, hipStream_t
   FfnArgs t = a;
   t.slot_base = s_main;
   t.gu_splits = ts;
+  t.part_rows = (long)gu_tail_rows(a.T);     // compact planes: (slot - s_main) * T + t
+  t.part_compact = 1;
   const int tail = (int)grid.y - s_main;
   const dim3 g(grid.x, tail, ts), block(kBlock);
   hipLaunchKernelGGL((gate_up_kernel<U, true, kW, CT>), g, block, 0, stream, t);
@@ -1404,7 +1404,7 @@ hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
   else
     launch_gu_fmt<kBf16>(a, K, XS_GATE_UP_U, XS_GATE_UP_U1, split, grid, block, stream);
   if (split) {
-    const dim3 fgrid((a.f + kBlock * 4 - 1) / (kBlock * 4), (unsigned)a.rows);
+    const dim3 fgrid((a.f + kBlock * 4 - 1) / (kBlock * 4), (unsigned)std::min(a.rows, 65535L));
     hipLaunchKernelGGL(gate_up_finish_kernel, fgrid, block, 0, stream, a);
   }
   return hipGetLastError();

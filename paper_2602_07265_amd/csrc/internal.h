@@ -131,15 +131,22 @@ inline size_t ffn_rows(int T, int k, int n_shared) {
 }
 
 // The gate/up launch's last, partly filled round of blocks: when it holds under a quarter
-// of the blocks the GPU runs at once, its slots are taken out of the launch and run after
-// it split this many ways along d (a lone block streams its weights several times slower
-// than its share of a full round).  Partial planes for all rows, if within the cap.
+// of the blocks the GPU runs at once and at most XS_GU_TAIL_MAX_SLOTS expert slots, its
+// slots are taken out of the launch and run after it split up to XS_GU_TAIL_SPLITS ways
+// along d (a lone block streams its weights several times slower than its share of a full
+// round).  Only under a total budget, where the active experts usually fill the budget and
+// the launch's rounds are known on the host.  The tail's partial planes hold its rows only,
+// (slot - first tail slot) * T + t, if within the cap.
 #ifndef XS_GU_TAIL_SPLITS
 #define XS_GU_TAIL_SPLITS 8
+#endif
+#ifndef XS_GU_TAIL_MAX_SLOTS
+#define XS_GU_TAIL_MAX_SLOTS 4
 #endif
 #ifndef XS_GU_TAIL_CAP
 #define XS_GU_TAIL_CAP (64L << 20)
 #endif
+inline size_t gu_tail_rows(int T) { return size_t(XS_GU_TAIL_MAX_SLOTS) * size_t(T > 0 ? T : 1); }
 
 struct FfnLayout {
   RouteLayout route;
@@ -147,7 +154,8 @@ struct FfnLayout {
   int gu_splits;  // K-splits of the gate/up GEMM
   int splits;     // K-splits of the down GEMM (bf16 and FP8 weights)
   int q4_splits;  // K-splits of the down GEMM with MXFP4 weights
-  size_t gpart;   // fp32 [gu_splits, 2, rows, f] gate and up partial sums (gu_splits > 1)
+  size_t gpart;   // fp32 [gu_splits, 2, rows, f] gate and up partial sums (gu_splits > 1),
+                  //      or the tail's [gu_tail_splits, 2, gu_tail_rows(T), f]
   size_t h;       // bf16 [rows, 2f]            SwiGLU hidden rows as hi = bf16(H) and
                   //                            lo = bf16(H - hi), interleaved in 8-element
                   //                            chunks: row p holds hi(c..c+7), lo(c..c+7), ...
@@ -155,9 +163,10 @@ struct FfnLayout {
   size_t total;
 };
 
-// est_active: experts expected to be active (routed plus shared), for the split counts.
+// est_active: experts expected to be active (routed plus shared), for the split counts;
+// tail_ok: the gate/up tail may run (a total budget).
 inline FfnLayout ffn_layout(int T, int N, int k, bool dense, int d, int f, int est_active,
-                            int n_shared) {
+                            int n_shared, bool tail_ok) {
   FfnLayout L{};
   L.route = route_layout(T, N, k, dense);
   L.gu_splits = gate_up_splits(est_active, d, f);
@@ -165,13 +174,15 @@ inline FfnLayout ffn_layout(int T, int N, int k, bool dense, int d, int f, int e
   L.q4_splits = down_splits(est_active, d, f, true);
   const size_t rows = ffn_rows(T, k, n_shared);
   size_t o = L.route.total;
+  const size_t tail_plane = sizeof(float) * 2 * gu_tail_rows(T) * size_t(f);
   L.gu_tail_splits = 0;
-  if (L.gu_splits == 1 &&
-      sizeof(float) * 2 * size_t(XS_GU_TAIL_SPLITS) * rows * size_t(f) <= size_t(XS_GU_TAIL_CAP))
+  if (tail_ok && L.gu_splits == 1 && size_t(XS_GU_TAIL_SPLITS) * tail_plane <= size_t(XS_GU_TAIL_CAP))
     L.gu_tail_splits = XS_GU_TAIL_SPLITS;
-  const int planes = L.gu_splits > 1 ? L.gu_splits : L.gu_tail_splits;
   L.gpart = o;
-  if (planes > 1) o += align256(sizeof(float) * 2 * size_t(planes) * rows * size_t(f));
+  if (L.gu_splits > 1)
+    o += align256(sizeof(float) * 2 * size_t(L.gu_splits) * rows * size_t(f));
+  else if (L.gu_tail_splits > 1)
+    o += align256(size_t(L.gu_tail_splits) * tail_plane);
   L.h = o; o += align256(sizeof(uint16_t) * rows * 2 * size_t(f));
   const int y_planes = L.splits > L.q4_splits ? L.splits : L.q4_splits;   // any format
   L.y = o; o += align256(sizeof(float) * size_t(y_planes) * rows * size_t(d));
@@ -251,7 +262,9 @@ struct FfnArgs {
   int est_active;              // experts expected to be active (0: unknown), for launch shapes
   int splits;                  // K-splits of the down GEMM (partials summed in the combine)
   int gu_splits;               // K-splits of the gate/up GEMM (partials summed by finish)
-  float* gpart;                // [gu_splits, 2, rows, f] when gu_splits > 1 (or the tail's)
+  float* gpart;                // [gu_splits, 2, part_rows, f] when gu_splits > 1 (or the tail's)
+  long part_rows;              // rows of one partial plane: rows, or gu_tail_rows(T) in the tail
+  int part_compact;            // the tail's partial rows: (slot - slot_base) * T + t
   int gu_tail_splits;          // partial planes available to the gate/up tail (0: none)
   int slot_base;               // first expert slot of this launch (the tail's launch: > 0)
   int G;                       // GPU groups, with `group` and `local_group` as in RouteArgs
