@@ -303,6 +303,42 @@ xshare_status xshare_moe_forward(const uint16_t* x, const float* logits, int32_t
                                  xshare_stats* stats, void* ws, size_t ws_bytes,
                                  void* const* stage_events, hipStream_t stream);
 
+/* Size of the scratch array that xshare_moe_forward_noalloc uses on each GPU (64 MiB).     */
+#define XSHARE_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/*
+ * xshare_moe_forward_noalloc -- xshare_moe_forward for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same layer, the same kernels and the same results, with no workspace
+ * argument.  Its scratch is a fixed array of XSHARE_NOALLOC_SCRATCH_BYTES inside the
+ * library, one per GPU, which that GPU holds from the first call on it until the process
+ * ends.  Nothing is allocated or freed, by the library or any library it calls.
+ *
+ *   Arguments as xshare_moe_forward, without ws / ws_bytes.
+ *   Limit: xshare_moe_workspace_bytes(T, d, f, params, ep, shared) <= the array's size
+ *          (for instance the DeepSeek-R1 shape, d = 7168, f = 2048, N = 256, k = 8, up to
+ *          T = 64 under a total budget); larger calls return XSHARE_EWORKSPACE before
+ *          anything is enqueued.
+ *   The array used is the current device's; a non-NULL stream must belong to it
+ *   (XSHARE_EINVAL otherwise).  XSHARE_EHIP if its address cannot be obtained.
+ *   Every call on one GPU shares that GPU's array and it keeps the last call's contents (no
+ *   kernel reads scratch it has not written in the same call, so nothing needs clearing).
+ *   Calls that overlap on one GPU -- on different streams, or from threads without an
+ *   ordering between them -- race on the array and give wrong results: order them, e.g. on
+ *   one stream.
+ */
+xshare_status xshare_moe_forward_noalloc(const uint16_t* x, const float* logits, int32_t T,
+                                         int32_t d, int32_t f, const uint16_t* w1,
+                                         const uint16_t* w3, const uint16_t* w2,
+                                         const xshare_route_params* params,
+                                         const int32_t* req_offsets,
+                                         const int32_t* host_offsets, int32_t R,
+                                         const xshare_ep_layout* ep,
+                                         const xshare_shared_experts* shared, uint16_t* y,
+                                         uint8_t* sel_mask, int32_t* topk_ids, float* topk_w,
+                                         xshare_stats* stats, void* const* stage_events,
+                                         hipStream_t stream);
+
 /*
  * xshare_moe_forward_fp8 -- xshare_moe_forward with FP8 routed-expert weights (half the
  * bytes of bf16 on the stream that bounds the layer; the paper is silent on precision).

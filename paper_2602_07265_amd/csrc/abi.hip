@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 
 #include "internal.h"
 #include "xshare.h"
@@ -334,6 +335,35 @@ xshare_status layer_common(const uint16_t* x, const float* logits, const uint16_
   return XSHARE_OK;
 }
 
+// Scratch of xshare_moe_forward_noalloc: one fixed array per GPU, for callers that cannot
+// allocate.  Host code never names the array in a kernel argument or a copy (its host-side
+// name is not a device address): each device's address comes from hipGetSymbolAddress, taken
+// once per device with that device current, and only that address is passed on.
+static __device__ __align__(256) unsigned char scratch[XSHARE_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's scratch address (nullptr, with the HIP error in *err, on failure).
+void* scratch_for_current_device(hipError_t* err) {
+  int dev = 0;
+  *err = hipGetDevice(&dev);
+  if (*err != hipSuccess) return nullptr;
+  if (dev < 0 || dev >= kMaxDevices) {
+    *err = hipErrorInvalidDevice;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    *err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (*err != hipSuccess) return nullptr;
+    g_scratch_ptr[dev] = p;
+  }
+  return g_scratch_ptr[dev];
+}
+
 }  // namespace
 
 extern "C" {
@@ -413,6 +443,48 @@ xshare_status xshare_moe_forward(const uint16_t* x, const float* logits, int32_t
   return layer_common(x, logits, nullptr, T, d, f, wt, shared, params, req_offsets,
                       host_offsets, R, ep, y, nullptr, sel_mask, topk_ids, topk_w, stats, ws,
                       ws_bytes, stage_events, stream);
+}
+
+xshare_status xshare_moe_forward_noalloc(const uint16_t* x, const float* logits, int32_t T,
+                                         int32_t d, int32_t f, const uint16_t* w1,
+                                         const uint16_t* w3, const uint16_t* w2,
+                                         const xshare_route_params* params,
+                                         const int32_t* req_offsets,
+                                         const int32_t* host_offsets, int32_t R,
+                                         const xshare_ep_layout* ep,
+                                         const xshare_shared_experts* shared, uint16_t* y,
+                                         uint8_t* sel_mask, int32_t* topk_ids, float* topk_w,
+                                         xshare_stats* stats, void* const* stage_events,
+                                         hipStream_t stream) {
+  // host checks first (the same as xshare_moe_forward's), then the size limit
+  if (T > 0 && !logits) return XSHARE_EINVAL;
+  const size_t need = xshare_moe_workspace_bytes(T, d, f, params, ep, shared);
+  if (need == 0) {          // invalid parameters: let the full checks name the error
+    Weights wt;
+    wt.w1 = w1;
+    wt.w3 = w3;
+    wt.w2 = w2;
+    return layer_common(x, logits, nullptr, T, d, f, wt, shared, params, req_offsets,
+                        host_offsets, R, ep, y, nullptr, sel_mask, topk_ids, topk_w, stats,
+                        nullptr, 0, stage_events, stream);
+  }
+  if (need > size_t(XSHARE_NOALLOC_SCRATCH_BYTES)) return XSHARE_EWORKSPACE;
+  if (stream) {             // the array used is the current device's
+    int cur = 0, sdev = 0;
+    if (hipGetDevice(&cur) != hipSuccess || hipStreamGetDevice(stream, &sdev) != hipSuccess)
+      return XSHARE_EHIP;
+    if (sdev != cur) return XSHARE_EINVAL;
+  }
+  hipError_t err = hipSuccess;
+  void* ws = scratch_for_current_device(&err);
+  if (!ws) return XSHARE_EHIP;
+  Weights wt;
+  wt.w1 = w1;
+  wt.w3 = w3;
+  wt.w2 = w2;
+  return layer_common(x, logits, nullptr, T, d, f, wt, shared, params, req_offsets,
+                      host_offsets, R, ep, y, nullptr, sel_mask, topk_ids, topk_w, stats, ws,
+                      size_t(XSHARE_NOALLOC_SCRATCH_BYTES), stage_events, stream);
 }
 
 xshare_status xshare_moe_forward_fp8(const uint16_t* x, const float* logits, int32_t T,

@@ -19,6 +19,7 @@ OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP = 0, 1, 2, 3, 4
 BUDGET = {"total": 0, "extra": 1, "per_group": 2, "threshold": 3}
 SCORE = {"topk": 0, "dense": 1}
 N_STAGE_EVENTS = 5
+NOALLOC_SCRATCH_BYTES = 64 << 20     # XSHARE_NOALLOC_SCRATCH_BYTES
 STAGES = ("route", "gate_up", "down", "combine")
 
 
@@ -121,6 +122,12 @@ def lib() -> ctypes.CDLL:
                                          ctypes.POINTER(EpLayout), ctypes.POINTER(SharedExperts),
                                          _P, _P, _P, _P, _P, _P, _SZ, _P, _P]
         L.xshare_moe_forward.restype = ctypes.c_int
+        L.xshare_moe_forward_noalloc.argtypes = [_P, _P, _I32, _I32, _I32, _P, _P, _P,
+                                                 ctypes.POINTER(RouteParams), _P, _P, _I32,
+                                                 ctypes.POINTER(EpLayout),
+                                                 ctypes.POINTER(SharedExperts), _P, _P, _P, _P,
+                                                 _P, _P, _P]
+        L.xshare_moe_forward_noalloc.restype = ctypes.c_int
         L.xshare_status_string.argtypes = [_I32]
         L.xshare_status_string.restype = ctypes.c_char_p
         L.xshare_version.argtypes = []
@@ -425,6 +432,47 @@ def moe_forward(x: torch.Tensor, logits: torch.Tensor, w1: torch.Tensor, w3: tor
         _ptr(res.get("sel_mask")), _ptr(res.get("ids")), _ptr(res.get("w")),
         _ptr(res.get("stats")), _ptr(workspace), workspace.numel(), ev, _stream(stream))
     _check(st, "xshare_moe_forward")
+    return res
+
+
+def moe_forward_noalloc(x: torch.Tensor, logits: torch.Tensor, w1: torch.Tensor,
+                        w3: torch.Tensor, w2: torch.Tensor, top_k: int, warmup_k0: int,
+                        budget: int, budget_mode="total", score_mode="topk", *, y=None,
+                        out=None, stage_events=None, stream=None) -> dict:
+    """xshare_moe_forward_noalloc: the layer with the library's own fixed scratch array (no
+    workspace).  ``y`` and ``out`` (a dict of sel_mask / ids / w / stats tensors) are
+    preallocated outputs; with them the call allocates nothing here either.  Flat selection
+    (Algorithm 2) only in this binding."""
+    T, d = x.shape
+    N = logits.shape[1]
+    f = w1.shape[1]
+    dev = x.device
+    _dev(x, torch.bfloat16, (T, d), "x")
+    _dev(logits, torch.float32, (T, N), "logits")
+    _dev(w1, torch.bfloat16, (N, f, d), "w1")
+    _dev(w3, torch.bfloat16, (N, f, d), "w3")
+    _dev(w2, torch.bfloat16, (N, d, f), "w2")
+    p = params(N, top_k, warmup_k0, budget, budget_mode, score_mode)
+    if y is None:
+        y = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
+    _dev(y, torch.bfloat16, (T, d), "y")
+    res = {"y": y}
+    if out is not None:
+        res.update(out)
+        _dev(res["sel_mask"], torch.uint8, (N,), "sel_mask")
+        _dev(res["ids"], torch.int32, (T, top_k), "ids")
+        _dev(res["w"], torch.float32, (T, top_k), "w")
+        _dev(res["stats"], torch.int32, (8,), "stats")
+    ev = None
+    if stage_events is not None:
+        if len(stage_events) != N_STAGE_EVENTS:
+            raise ValueError(f"stage_events needs {N_STAGE_EVENTS} events")
+        ev = (ctypes.c_void_p * N_STAGE_EVENTS)(*[e.handle for e in stage_events])
+    st = lib().xshare_moe_forward_noalloc(
+        _ptr(x), _ptr(logits), T, d, f, _ptr(w1), _ptr(w3), _ptr(w2), ctypes.byref(p), None,
+        None, 0, None, None, _ptr(y), _ptr(res.get("sel_mask")), _ptr(res.get("ids")),
+        _ptr(res.get("w")), _ptr(res.get("stats")), ev, _stream(stream))
+    _check(st, "xshare_moe_forward_noalloc")
     return res
 
 
