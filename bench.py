@@ -78,6 +78,9 @@ def parse():
                          "and shared experts (xshare_moe_layer)")
     ap.add_argument("--shared", type=int, default=None,
                     help="shared experts with --full-layer (default: 1 for DeepSeek shapes, else 0)")
+    ap.add_argument("--stream-probe", action="store_true",
+                    help="only the streaming-read probe: a plain coalesced read of 4 GiB, "
+                         "over several grid sizes")
     ap.add_argument("--layers", type=int, default=0,
                     help="L > 0: a pass over L MoE layers sharing the global budget K")
     ap.add_argument("--global-budget", type=int, default=None,
@@ -109,6 +112,64 @@ def layer_bytes(n_active, T, N, d, f, wb=2):
             + T * N * 4 + T * d * 2)
 
 
+PROBE_BYTES = 4 << 30       # well beyond the 256 MB Infinity Cache
+
+
+PROBE_MODES = {0: "grid stride, 4 loads", 1: "grid stride, 8 loads",
+               2: "chunk per block, 4 loads", 3: "chunk per block, 8 loads"}
+
+
+def stream_rates(X, torch, runs, blocks, mode, buf):
+    """GB/s of ``runs`` timed streaming reads of ``buf`` (xshare_probe_stream_read) after two
+    untimed ones, HIP events on the launch stream."""
+    sink = torch.zeros(1, dtype=torch.int32, device=buf.device)
+    stream = torch.cuda.current_stream()
+    for _ in range(2):
+        X.probe_stream_read(buf, blocks, mode, sink)
+    rates = []
+    for _ in range(runs):
+        e0, e1 = X.HipEvent(), X.HipEvent()
+        e0.record(stream)
+        X.probe_stream_read(buf, blocks, mode, sink)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        rates.append(buf.numel() / (e0.elapsed_ms(e1) * 1e-3) / 1e9)
+    return rates
+
+
+# the probe configurations the default bench run measures (the best of a sweep on MI355X)
+PROBE_CONFIGS = ((256, 1), (512, 0), (4096, 3), (8192, 2))
+
+
+def stream_peak(X, np, torch, configs=PROBE_CONFIGS, runs=6):
+    """The streaming-read ceiling: the best median over a few probe configurations of a
+    4 GiB read.  Returns (median GB/s, best single read GB/s, (blocks, mode))."""
+    buf = torch.empty(PROBE_BYTES, dtype=torch.uint8, device="cuda:0")
+    best = None
+    for blocks, mode in configs:
+        r = stream_rates(X, torch, runs, blocks, mode, buf)
+        m = float(np.median(r))
+        if best is None or m > best[0]:
+            best = (m, float(np.max(r)), (blocks, mode))
+    del buf
+    return best
+
+
+def run_stream_probe(X, np, torch):
+    """The probe alone: GB/s over grid sizes and access patterns (median and best of 10)."""
+    buf = torch.empty(PROBE_BYTES, dtype=torch.uint8, device="cuda:0")
+    out = {}
+    for mode in PROBE_MODES:
+        for blocks in (256, 512, 1024, 2048, 4096, 8192):
+            r = stream_rates(X, torch, 10, blocks, mode, buf)
+            out[f"{blocks} blocks, {PROBE_MODES[mode]}"] = {
+                "median_GBs": round(float(np.median(r)), 1), "max_GBs": round(float(np.max(r)), 1)}
+            print(f"[probe] mode {mode} ({PROBE_MODES[mode]}), {blocks} blocks: median "
+                  f"{np.median(r):.1f} GB/s, best {np.max(r):.1f}", file=sys.stderr, flush=True)
+    print(json.dumps({"metric": "streaming read of 4 GiB (HBM read ceiling)", "unit": "GB/s",
+                      "bytes": PROBE_BYTES, "runs": out, "peak_GBs": HBM_PEAK_GBS}), flush=True)
+
+
 def counters_traffic():
     """HBM bytes per gate/up launch from committed rocprofv3 counters, if still current."""
     try:
@@ -138,6 +199,8 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     X.lib()
+    if args.stream_probe:
+        return run_stream_probe(X, np, torch)
     if args.ep_groups > 0:
         return run_ep(args, W, X, np, torch)
     if args.full_layer:
@@ -241,6 +304,8 @@ def main():
 
     gbs = float(lay_bytes.mean()) / (ms_step * 1e-3) / 1e9
     gu_achieved = float(gu_bytes.mean()) / (float(gu_ms.mean()) * 1e-3) / 1e9
+    # the HBM read ceiling on this GPU, measured in the same run (4 GiB streaming read)
+    stream_gbs, stream_best, probe_cfg = stream_peak(X, np, torch)
     # the committed counter record covers the headline workload only
     traffic = counters_traffic() if (args.workload, M, T, args.tau, args.weights) == \
         ("ds_t32", 48, 32, None, "bf16") else None
@@ -291,7 +356,14 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(gu_achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "algorithmic_bytes": round(float(gu_bytes.mean())),
-                     "avg_launch_us": round(float(gu_ms.mean()) * 1e3, 2)},
+                     "avg_launch_us": round(float(gu_ms.mean()) * 1e3, 2),
+                     "frac_of_stream": round(gu_achieved / stream_gbs, 4)},
+        "stream_peak_GBs": round(stream_gbs, 1),
+        "stream_peak_best_GBs": round(stream_best, 1),
+        "stream_probe": f"4 GiB read, {probe_cfg[0]} blocks of 256 threads, "
+                        f"{PROBE_MODES[probe_cfg[1]]}; median of 6 reads, best of "
+                        f"{len(PROBE_CONFIGS)} configurations",
+        "layer_frac_of_stream": round(gbs / stream_gbs, 4),
         "cpu_baseline": cpu,
         "wall_s_timed": round(wall, 3),
     }

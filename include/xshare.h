@@ -303,6 +303,74 @@ xshare_status xshare_moe_forward(const uint16_t* x, const float* logits, int32_t
                                  xshare_stats* stats, void* ws, size_t ws_bytes,
                                  void* const* stage_events, hipStream_t stream);
 
+/* Weight formats of the routed experts (xshare_layer_args.weight_format).                  */
+enum {
+  XSHARE_WEIGHTS_BF16 = 0,  /* w1, w3 [N, f, d] and w2 [N, d, f] bf16; no scales             */
+  XSHARE_WEIGHTS_FP8 = 1,   /* as xshare_moe_forward_fp8: E4M3FN codes, fp32 row scales      */
+  XSHARE_WEIGHTS_MXFP4 = 2  /* as xshare_moe_forward_mxfp4: E2M1 codes, E8M0 block scales    */
+};
+
+/*
+ * Every argument of a layer call, for xshare_moe_forward_v2.  The fixed-signature layer
+ * calls (xshare_moe_forward, _fp8, _mxfp4, xshare_moe_layer) fill one of these and run the
+ * same code.  Zero-initialise it, set struct_size = sizeof(xshare_layer_args), then the
+ * fields the call uses; pointer conventions as in those calls.
+ *
+ *   x, T, d, f        hidden states [T, d] bf16 and the layer's sizes.
+ *   logits / w_gate   exactly one when T > 0: fp32 router logits [T, N] (xshare_moe_forward),
+ *                     or bf16 router weights [N, d], the logits then computed on the device
+ *                     (xshare_moe_layer; logits_out optionally receives them).
+ *   weight_format     XSHARE_WEIGHTS_*; w1, w3, w2 and the three scale arrays as the
+ *                     matching fixed-signature call takes them (scales NULL for bf16).
+ *   params, req_offsets / host_offsets / R, ep, shared: as xshare_moe_forward (shared
+ *                     experts with bf16 weights only).
+ *   y, sel_mask, topk_ids, topk_w, stats: outputs as xshare_moe_forward.
+ *   ws, ws_bytes      workspace of xshare_moe_forward_v2_workspace_bytes bytes.
+ *   stage_events, stream: as xshare_moe_forward.
+ */
+typedef struct {
+  size_t struct_size;
+  int32_t T, d, f;
+  const uint16_t* x;
+  const float* logits;
+  const uint16_t* w_gate;
+  int32_t weight_format;
+  const void* w1;
+  const void* w3;
+  const void* w2;
+  const void* w1_scale;
+  const void* w3_scale;
+  const void* w2_scale;
+  const xshare_route_params* params;
+  const int32_t* req_offsets;
+  const int32_t* host_offsets;
+  int32_t R;
+  const xshare_ep_layout* ep;
+  const xshare_shared_experts* shared;
+  uint16_t* y;
+  float* logits_out;
+  uint8_t* sel_mask;
+  int32_t* topk_ids;
+  float* topk_w;
+  xshare_stats* stats;
+  void* ws;
+  size_t ws_bytes;
+  void* const* stage_events;
+  hipStream_t stream;
+} xshare_layer_args;
+
+/* Workspace of xshare_moe_forward_v2 for these arguments (sizes, modes, ep, shared, whether *
+ * w_gate is given); 0 if they are invalid.                                                   */
+size_t xshare_moe_forward_v2_workspace_bytes(const xshare_layer_args* args);
+
+/*
+ * xshare_moe_forward_v2 -- the MoE layer of Sections 2.1-5 (selection by Algorithm 2, 3-4 or
+ * 5-6, the selected routed experts, the shared experts, combine) from one argument struct.
+ * XSHARE_EINVAL also for a struct_size other than sizeof(xshare_layer_args), both or neither
+ * of logits and w_gate (T > 0), or an unknown weight format.
+ */
+xshare_status xshare_moe_forward_v2(const xshare_layer_args* args);
+
 /* Size of the scratch array that xshare_moe_forward_noalloc uses on each GPU (64 MiB).     */
 #define XSHARE_NOALLOC_SCRATCH_BYTES (64u << 20)
 
@@ -427,6 +495,20 @@ xshare_status xshare_moe_layer(const uint16_t* x, const uint16_t* w_gate, int32_
  * Host only: enqueues nothing.
  */
 xshare_status xshare_layer_budgets(int32_t K, int32_t L, int32_t* m);
+
+/*
+ * xshare_probe_stream_read -- measurement only: a plain coalesced read of `bytes` bytes at
+ * `buf` (16-byte aligned, a multiple of 16) by `blocks` workgroups of 256 threads, lanes
+ * reading consecutive 16-byte pieces.  mode 0 / 1: the whole grid strides through the
+ * buffer with 4 / 8 loads in flight per thread; mode 2 / 3: each workgroup reads its own
+ * contiguous chunk, 4 / 8 loads in flight.  Timing it gives the HBM read rate a simple
+ * kernel reaches on this GPU, the practical ceiling for the expert GEMMs' weight streams
+ * (decode is bound by reading expert weights, Section 2.3).  `sink`: DEVICE uint32, written
+ * at most once (it keeps the loads).  Asynchronous on `stream`; XSHARE_EINVAL for bad
+ * arguments.
+ */
+xshare_status xshare_probe_stream_read(const void* buf, size_t bytes, int32_t blocks,
+                                       int32_t mode, uint32_t* sink, hipStream_t stream);
 
 /* Static description of a status code (never NULL).                                      */
 const char* xshare_status_string(int32_t status);

@@ -6,7 +6,8 @@ Translation units:
 * route.hip -- expert selection; -ffp-contract=off and correctly rounded fp32 division, so
                the gate arithmetic is exactly the documented sequence of fp32 operations;
 * ffn.hip   -- expert GEMMs (bf16 MFMA) and the combine;
-* abi.hip   -- the extern "C" entry points declared in include/xshare.h.
+* abi.hip   -- the extern "C" entry points declared in include/xshare.h;
+* probe.hip -- the streaming-read probe (measurement of the HBM read ceiling).
 Every HIP compile disables packed-fp32 instruction selection.
 """
 from __future__ import annotations
@@ -33,6 +34,7 @@ UNITS = {
                   "-fno-fast-math"],
     "ffn.hip": [],
     "abi.hip": [],
+    "probe.hip": [],
 }
 
 

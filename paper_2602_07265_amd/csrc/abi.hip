@@ -194,7 +194,8 @@ xshare_status route_common(const float* logits, int32_t T, const int32_t* req_of
   return xs::launch_route(a, stream) == hipSuccess ? XSHARE_OK : XSHARE_EHIP;
 }
 
-// Routed expert weights: bf16 matrices, or FP8 E4M3FN codes with one fp32 scale per row.
+// Routed expert weights of a layer call, by format: bf16 matrices, FP8 E4M3FN codes with
+// one fp32 scale per row, or MXFP4 E2M1 codes with one E8M0 scale per 32 inputs.
 struct Weights {
   const uint16_t* w1 = nullptr;
   const uint16_t* w3 = nullptr;
@@ -208,69 +209,112 @@ struct Weights {
   const uint8_t* e1 = nullptr;   // MXFP4 block scales
   const uint8_t* e3 = nullptr;
   const uint8_t* e2 = nullptr;
-  int fmt = 0;                   // 0 bf16, 1 FP8, 2 MXFP4
+  int fmt = 0;                   // XSHARE_WEIGHTS_*
+  explicit Weights(const xshare_layer_args& a) : fmt(a.weight_format) {
+    if (fmt == XSHARE_WEIGHTS_BF16) {
+      w1 = static_cast<const uint16_t*>(a.w1);
+      w3 = static_cast<const uint16_t*>(a.w3);
+      w2 = static_cast<const uint16_t*>(a.w2);
+      return;
+    }
+    q1 = static_cast<const uint8_t*>(a.w1);
+    q3 = static_cast<const uint8_t*>(a.w3);
+    q2 = static_cast<const uint8_t*>(a.w2);
+    if (fmt == XSHARE_WEIGHTS_FP8) {
+      s1 = static_cast<const float*>(a.w1_scale);
+      s3 = static_cast<const float*>(a.w3_scale);
+      s2 = static_cast<const float*>(a.w2_scale);
+    } else {
+      e1 = static_cast<const uint8_t*>(a.w1_scale);
+      e3 = static_cast<const uint8_t*>(a.w3_scale);
+      e2 = static_cast<const uint8_t*>(a.w2_scale);
+    }
+  }
   bool present() const {
-    if (fmt == 1) return q1 && q3 && q2 && s1 && s3 && s2;
-    if (fmt == 2) return q1 && q3 && q2 && e1 && e3 && e2;
+    if (fmt == XSHARE_WEIGHTS_FP8) return q1 && q3 && q2 && s1 && s3 && s2;
+    if (fmt == XSHARE_WEIGHTS_MXFP4) return q1 && q3 && q2 && e1 && e3 && e2;
     return w1 && w3 && w2;
   }
   bool aligned() const {
     // MXFP4 scale rows are read in pieces of up to 16 bytes
-    if (fmt == 2 && !(aligned16(e1) && aligned16(e3) && aligned16(e2))) return false;
-    return fmt ? (aligned16(q1) && aligned16(q3) && aligned16(q2))
-               : (aligned16(w1) && aligned16(w3) && aligned16(w2));
+    if (fmt == XSHARE_WEIGHTS_MXFP4 && !(aligned16(e1) && aligned16(e3) && aligned16(e2)))
+      return false;
+    return fmt != XSHARE_WEIGHTS_BF16 ? (aligned16(q1) && aligned16(q3) && aligned16(q2))
+                                      : (aligned16(w1) && aligned16(w3) && aligned16(w2));
   }
 };
 
-// The layer: optional router GEMM (w_gate given: logits computed on the device), selection,
-// expert GEMMs (routed and shared), combine.
-xshare_status layer_common(const uint16_t* x, const float* logits, const uint16_t* w_gate,
-                           int32_t T, int32_t d, int32_t f, const Weights& wt,
-                           const xshare_shared_experts* shared, const xshare_route_params* params,
-                           const int32_t* req_offsets, const int32_t* host_offsets, int32_t R,
-                           const xshare_ep_layout* ep, uint16_t* y, float* logits_out,
-                           uint8_t* sel_mask, int32_t* topk_ids, float* topk_w,
-                           xshare_stats* stats, void* ws, size_t ws_bytes,
-                           void* const* stage_events, hipStream_t stream) {
-  const bool hier = req_offsets != nullptr;
-  if (hier && ep) return XSHARE_EUNSUPPORTED;
-  xshare_status st = check_params(T, params, hier, ep != nullptr);
+// Checks of a layer call that do not depend on the workspace; XSHARE_OK if it may run.
+xshare_status check_layer(const xshare_layer_args& a) {
+  const bool hier = a.req_offsets != nullptr;
+  if (hier && a.ep) return XSHARE_EUNSUPPORTED;
+  xshare_status st = check_params(a.T, a.params, hier, a.ep != nullptr);
   if (st != XSHARE_OK) return st;
   if (hier) {
-    st = check_offsets(T, req_offsets, host_offsets, R);
+    st = check_offsets(a.T, a.req_offsets, a.host_offsets, a.R);
     if (st != XSHARE_OK) return st;
   }
-  st = check_ep(params->n_experts, ep, true);
+  st = check_ep(a.params->n_experts, a.ep, true);
   if (st != XSHARE_OK) return st;
-  st = check_shared(shared, ep);
+  st = check_shared(a.shared, a.ep);
   if (st != XSHARE_OK) return st;
-  if (wt.fmt != 0 && shared && shared->n_shared > 0) return XSHARE_EUNSUPPORTED;
-  if (d <= 0 || f <= 0) return XSHARE_EINVAL;
-  if (d % xs::kDimAlign != 0 || f % xs::kDimAlign != 0) return XSHARE_EUNSUPPORTED;
-  if (T > 0 && (!x || !wt.present() || !y)) return XSHARE_EINVAL;
-  if (!aligned16(x) || !wt.aligned() || !aligned16(y) || (w_gate && !aligned16(w_gate)))
+  if (a.weight_format != XSHARE_WEIGHTS_BF16 && a.weight_format != XSHARE_WEIGHTS_FP8 &&
+      a.weight_format != XSHARE_WEIGHTS_MXFP4)
     return XSHARE_EINVAL;
+  if (a.weight_format != XSHARE_WEIGHTS_BF16 && a.shared && a.shared->n_shared > 0)
+    return XSHARE_EUNSUPPORTED;
+  if (a.d <= 0 || a.f <= 0) return XSHARE_EINVAL;
+  if (a.d % xs::kDimAlign != 0 || a.f % xs::kDimAlign != 0) return XSHARE_EUNSUPPORTED;
+  const Weights wt(a);
+  if (a.T > 0) {
+    if (!a.x || !wt.present() || !a.y) return XSHARE_EINVAL;
+    if ((a.logits != nullptr) == (a.w_gate != nullptr)) return XSHARE_EINVAL;  // exactly one
+  }
+  if (!aligned16(a.x) || !wt.aligned() || !aligned16(a.y) || (a.w_gate && !aligned16(a.w_gate)))
+    return XSHARE_EINVAL;
+  return XSHARE_OK;
+}
+
+// Workspace of a layer call (valid arguments): the routing and expert regions, then the
+// router's scratch when the logits are computed on the device.
+size_t layer_workspace(const xshare_layer_args& a) {
+  const xs::FfnLayout L = layer_layout(a.T, a.d, a.f, a.params, a.ep, n_shared_of(a.shared));
+  return L.total + (a.w_gate ? layer_router_bytes(a.T, a.d, a.params->n_experts) : 0);
+}
+
+// The layer: optional router GEMM (w_gate given: logits computed on the device), selection,
+// expert GEMMs (routed and shared), combine.
+xshare_status layer_common(const xshare_layer_args& a) {
+  if (a.struct_size != sizeof(xshare_layer_args)) return XSHARE_EINVAL;
+  xshare_status st = check_layer(a);
+  if (st != XSHARE_OK) return st;
+  const xshare_route_params* params = a.params;
+  const int32_t T = a.T, d = a.d, f = a.f;
+  const hipStream_t stream = a.stream;
+  const bool hier = a.req_offsets != nullptr;
+  const Weights wt(a);
   const int N = params->n_experts, k = params->top_k;
-  const int n_shared = n_shared_of(shared);
-  const int bound = layer_bound(T, params, ep);
-  const xs::FfnLayout L = layer_layout(T, d, f, params, ep, n_shared);
-  const size_t need = L.total + (w_gate ? layer_router_bytes(T, d, N) : 0);
-  if (!ws || ws_bytes < need) return XSHARE_EWORKSPACE;
+  const int n_shared = n_shared_of(a.shared);
+  const int bound = layer_bound(T, params, a.ep);
+  const xs::FfnLayout L = layer_layout(T, d, f, params, a.ep, n_shared);
+  void* const ws = a.ws;
+  if (!ws || a.ws_bytes < layer_workspace(a)) return XSHARE_EWORKSPACE;
 
   // The selection kernel always writes a mask; keep it in the workspace if not wanted.
-  uint8_t* mask = sel_mask ? sel_mask : at<uint8_t>(ws, L.route.mask);
+  uint8_t* mask = a.sel_mask ? a.sel_mask : at<uint8_t>(ws, L.route.mask);
   auto record = [&](int s) -> bool {
-    if (!stage_events) return true;
-    return hipEventRecord(static_cast<hipEvent_t>(stage_events[s]), stream) == hipSuccess;
+    if (!a.stage_events) return true;
+    return hipEventRecord(static_cast<hipEvent_t>(a.stage_events[s]), stream) == hipSuccess;
   };
   if (!record(0)) return XSHARE_EHIP;
-  xs::RouteArgs ra = route_args(logits, T, params, hier ? req_offsets : nullptr, R, ep, nullptr,
-                                mask, topk_ids, topk_w, stats, ws, L.route);
-  if (ep) ra.local_group = ep->local_group;
-  if (w_gate && T > 0) {
+  xs::RouteArgs ra = route_args(a.logits, T, params, hier ? a.req_offsets : nullptr, a.R, a.ep,
+                                nullptr, mask, a.topk_ids, a.topk_w, a.stats, ws, L.route);
+  if (a.ep) ra.local_group = a.ep->local_group;
+  if (a.w_gate && T > 0) {
     float* planes = at<float>(ws, L.total);
-    float* h = logits_out ? logits_out : at<float>(ws, L.total + router_planes_bytes(T, d, N));
-    const xs::RouterArgs r{x, w_gate, T, d, N, xs::router_parts(T, d, N), planes, h};
+    float* h = a.logits_out ? a.logits_out
+                            : at<float>(ws, L.total + router_planes_bytes(T, d, N));
+    const xs::RouterArgs r{a.x, a.w_gate, T, d, N, xs::router_parts(T, d, N), planes, h};
     if (xs::launch_router(r, stream) != hipSuccess) return XSHARE_EHIP;
     ra.logits = h;
   }
@@ -282,7 +326,7 @@ xshare_status layer_common(const uint16_t* x, const float* logits, const uint16_
   }
 
   xs::FfnArgs fa{};
-  fa.x = x;
+  fa.x = a.x;
   fa.w1 = wt.w1;
   fa.w3 = wt.w3;
   fa.w2 = wt.w2;
@@ -303,9 +347,10 @@ xshare_status layer_common(const uint16_t* x, const float* logits, const uint16_
   fa.f = f;
   fa.max_active = bound;
   // the threshold rule's set size is not known before the selection runs
-  fa.est_active = params->budget_mode == XSHARE_BUDGET_THRESHOLD ? 0
-                                                                 : layer_estimate(T, params, ep);
-  fa.splits = wt.fmt == 2 ? L.q4_splits : L.splits;
+  fa.est_active = params->budget_mode == XSHARE_BUDGET_THRESHOLD
+                      ? 0
+                      : layer_estimate(T, params, a.ep);
+  fa.splits = wt.fmt == XSHARE_WEIGHTS_MXFP4 ? L.q4_splits : L.splits;
   fa.gu_splits = L.gu_splits;
   fa.gu_tail_splits = L.gu_tail_splits;
   fa.slot_base = 0;
@@ -314,9 +359,9 @@ xshare_status layer_common(const uint16_t* x, const float* logits, const uint16_
   fa.group = ra.group;
   fa.local_group = ra.local_group;
   fa.n_shared = n_shared;
-  fa.sw1 = n_shared ? shared->w1 : nullptr;
-  fa.sw3 = n_shared ? shared->w3 : nullptr;
-  fa.sw2 = n_shared ? shared->w2 : nullptr;
+  fa.sw1 = n_shared ? a.shared->w1 : nullptr;
+  fa.sw3 = n_shared ? a.shared->w3 : nullptr;
+  fa.sw2 = n_shared ? a.shared->w2 : nullptr;
   fa.rows = (long)xs::ffn_rows(T, k, n_shared);
   fa.part_rows = fa.rows;
   fa.part_compact = 0;
@@ -328,11 +373,55 @@ xshare_status layer_common(const uint16_t* x, const float* logits, const uint16_
   fa.w = ra.w;
   fa.h = at<uint16_t>(ws, L.h);
   fa.yslot = at<float>(ws, L.y);
-  fa.y = y;
+  fa.y = a.y;
   if (xs::launch_gate_up(fa, stream) != hipSuccess || !record(2)) return XSHARE_EHIP;
   if (xs::launch_down(fa, stream) != hipSuccess || !record(3)) return XSHARE_EHIP;
   if (xs::launch_combine(fa, stream) != hipSuccess || !record(4)) return XSHARE_EHIP;
   return XSHARE_OK;
+}
+
+// A layer call of the fixed-signature entry points (no second stream).
+xshare_layer_args layer_args(const uint16_t* x, const float* logits, const uint16_t* w_gate,
+                             int32_t T, int32_t d, int32_t f, int32_t fmt, const void* w1,
+                             const void* w3, const void* w2, const void* s1, const void* s3,
+                             const void* s2, const xshare_shared_experts* shared,
+                             const xshare_route_params* params, const int32_t* req_offsets,
+                             const int32_t* host_offsets, int32_t R, const xshare_ep_layout* ep,
+                             uint16_t* y, float* logits_out, uint8_t* sel_mask,
+                             int32_t* topk_ids, float* topk_w, xshare_stats* stats, void* ws,
+                             size_t ws_bytes, void* const* stage_events, hipStream_t stream) {
+  xshare_layer_args a{};
+  a.struct_size = sizeof(xshare_layer_args);
+  a.T = T;
+  a.d = d;
+  a.f = f;
+  a.x = x;
+  a.logits = logits;
+  a.w_gate = w_gate;
+  a.weight_format = fmt;
+  a.w1 = w1;
+  a.w3 = w3;
+  a.w2 = w2;
+  a.w1_scale = s1;
+  a.w3_scale = s3;
+  a.w2_scale = s2;
+  a.params = params;
+  a.req_offsets = req_offsets;
+  a.host_offsets = host_offsets;
+  a.R = R;
+  a.ep = ep;
+  a.shared = shared;
+  a.y = y;
+  a.logits_out = logits_out;
+  a.sel_mask = sel_mask;
+  a.topk_ids = topk_ids;
+  a.topk_w = topk_w;
+  a.stats = stats;
+  a.ws = ws;
+  a.ws_bytes = ws_bytes;
+  a.stage_events = stage_events;
+  a.stream = stream;
+  return a;
 }
 
 // Scratch of xshare_moe_forward_noalloc: one fixed array per GPU, for callers that cannot
@@ -426,6 +515,21 @@ xshare_status xshare_select_ep(const float* logits, int32_t T, const xshare_rout
   return xs::launch_route(a, stream) == hipSuccess ? XSHARE_OK : XSHARE_EHIP;
 }
 
+xshare_status xshare_moe_forward_v2(const xshare_layer_args* args) {
+  if (!args) return XSHARE_EINVAL;
+  return layer_common(*args);
+}
+
+size_t xshare_moe_forward_v2_workspace_bytes(const xshare_layer_args* args) {
+  if (!args || args->struct_size != sizeof(xshare_layer_args)) return 0;
+  const xshare_layer_args& a = *args;
+  if (check_params(a.T, a.params, a.req_offsets != nullptr, a.ep != nullptr) != XSHARE_OK ||
+      check_ep(a.params->n_experts, a.ep, true) != XSHARE_OK || a.d <= 0 || a.f <= 0 ||
+      a.d % xs::kDimAlign != 0 || a.f % xs::kDimAlign != 0)
+    return 0;
+  return layer_workspace(a);
+}
+
 xshare_status xshare_moe_forward(const uint16_t* x, const float* logits, int32_t T, int32_t d,
                                  int32_t f, const uint16_t* w1, const uint16_t* w3,
                                  const uint16_t* w2, const xshare_route_params* params,
@@ -436,13 +540,10 @@ xshare_status xshare_moe_forward(const uint16_t* x, const float* logits, int32_t
                                  xshare_stats* stats, void* ws, size_t ws_bytes,
                                  void* const* stage_events, hipStream_t stream) {
   if (T > 0 && !logits) return XSHARE_EINVAL;
-  Weights wt;
-  wt.w1 = w1;
-  wt.w3 = w3;
-  wt.w2 = w2;
-  return layer_common(x, logits, nullptr, T, d, f, wt, shared, params, req_offsets,
-                      host_offsets, R, ep, y, nullptr, sel_mask, topk_ids, topk_w, stats, ws,
-                      ws_bytes, stage_events, stream);
+  return layer_common(layer_args(x, logits, nullptr, T, d, f, XSHARE_WEIGHTS_BF16, w1, w3, w2,
+                                 nullptr, nullptr, nullptr, shared, params, req_offsets,
+                                 host_offsets, R, ep, y, nullptr, sel_mask, topk_ids, topk_w,
+                                 stats, ws, ws_bytes, stage_events, stream));
 }
 
 xshare_status xshare_moe_forward_noalloc(const uint16_t* x, const float* logits, int32_t T,
@@ -456,19 +557,15 @@ xshare_status xshare_moe_forward_noalloc(const uint16_t* x, const float* logits,
                                          uint8_t* sel_mask, int32_t* topk_ids, float* topk_w,
                                          xshare_stats* stats, void* const* stage_events,
                                          hipStream_t stream) {
-  // host checks first (the same as xshare_moe_forward's), then the size limit
   if (T > 0 && !logits) return XSHARE_EINVAL;
-  const size_t need = xshare_moe_workspace_bytes(T, d, f, params, ep, shared);
-  if (need == 0) {          // invalid parameters: let the full checks name the error
-    Weights wt;
-    wt.w1 = w1;
-    wt.w3 = w3;
-    wt.w2 = w2;
-    return layer_common(x, logits, nullptr, T, d, f, wt, shared, params, req_offsets,
-                        host_offsets, R, ep, y, nullptr, sel_mask, topk_ids, topk_w, stats,
-                        nullptr, 0, stage_events, stream);
-  }
-  if (need > size_t(XSHARE_NOALLOC_SCRATCH_BYTES)) return XSHARE_EWORKSPACE;
+  xshare_layer_args a = layer_args(x, logits, nullptr, T, d, f, XSHARE_WEIGHTS_BF16, w1, w3, w2,
+                                   nullptr, nullptr, nullptr, shared, params, req_offsets,
+                                   host_offsets, R, ep, y, nullptr, sel_mask, topk_ids, topk_w,
+                                   stats, nullptr, 0, stage_events, stream);
+  // host checks first (the same as xshare_moe_forward's), then the size limit
+  xshare_status st = check_layer(a);
+  if (st != XSHARE_OK) return st;
+  if (layer_workspace(a) > size_t(XSHARE_NOALLOC_SCRATCH_BYTES)) return XSHARE_EWORKSPACE;
   if (stream) {             // the array used is the current device's
     int cur = 0, sdev = 0;
     if (hipGetDevice(&cur) != hipSuccess || hipStreamGetDevice(stream, &sdev) != hipSuccess)
@@ -476,15 +573,10 @@ xshare_status xshare_moe_forward_noalloc(const uint16_t* x, const float* logits,
     if (sdev != cur) return XSHARE_EINVAL;
   }
   hipError_t err = hipSuccess;
-  void* ws = scratch_for_current_device(&err);
-  if (!ws) return XSHARE_EHIP;
-  Weights wt;
-  wt.w1 = w1;
-  wt.w3 = w3;
-  wt.w2 = w2;
-  return layer_common(x, logits, nullptr, T, d, f, wt, shared, params, req_offsets,
-                      host_offsets, R, ep, y, nullptr, sel_mask, topk_ids, topk_w, stats, ws,
-                      size_t(XSHARE_NOALLOC_SCRATCH_BYTES), stage_events, stream);
+  a.ws = scratch_for_current_device(&err);
+  if (!a.ws) return XSHARE_EHIP;
+  a.ws_bytes = size_t(XSHARE_NOALLOC_SCRATCH_BYTES);
+  return layer_common(a);
 }
 
 xshare_status xshare_moe_forward_fp8(const uint16_t* x, const float* logits, int32_t T,
@@ -497,18 +589,11 @@ xshare_status xshare_moe_forward_fp8(const uint16_t* x, const float* logits, int
                                      uint8_t* sel_mask, int32_t* topk_ids, float* topk_w,
                                      xshare_stats* stats, void* ws, size_t ws_bytes,
                                      void* const* stage_events, hipStream_t stream) {
-  if (T > 0 && (!logits || !w1)) return XSHARE_EINVAL;
-  Weights wt;              // with T == 0 nothing is read and the pointers may be null
-  wt.fmt = 1;
-  wt.q1 = w1;
-  wt.q3 = w3;
-  wt.q2 = w2;
-  wt.s1 = w1_scale;
-  wt.s3 = w3_scale;
-  wt.s2 = w2_scale;
-  return layer_common(x, logits, nullptr, T, d, f, wt, nullptr, params, req_offsets,
-                      host_offsets, R, ep, y, nullptr, sel_mask, topk_ids, topk_w, stats, ws,
-                      ws_bytes, stage_events, stream);
+  if (T > 0 && !logits) return XSHARE_EINVAL;
+  return layer_common(layer_args(x, logits, nullptr, T, d, f, XSHARE_WEIGHTS_FP8, w1, w3, w2,
+                                 w1_scale, w3_scale, w2_scale, nullptr, params, req_offsets,
+                                 host_offsets, R, ep, y, nullptr, sel_mask, topk_ids, topk_w,
+                                 stats, ws, ws_bytes, stage_events, stream));
 }
 
 xshare_status xshare_moe_forward_mxfp4(const uint16_t* x, const float* logits, int32_t T,
@@ -522,18 +607,11 @@ xshare_status xshare_moe_forward_mxfp4(const uint16_t* x, const float* logits, i
                                        uint8_t* sel_mask, int32_t* topk_ids, float* topk_w,
                                        xshare_stats* stats, void* ws, size_t ws_bytes,
                                        void* const* stage_events, hipStream_t stream) {
-  if (T > 0 && (!logits || !w1)) return XSHARE_EINVAL;
-  Weights wt;
-  wt.fmt = 2;
-  wt.q1 = w1;
-  wt.q3 = w3;
-  wt.q2 = w2;
-  wt.e1 = w1_scale;
-  wt.e3 = w3_scale;
-  wt.e2 = w2_scale;
-  return layer_common(x, logits, nullptr, T, d, f, wt, nullptr, params, req_offsets,
-                      host_offsets, R, ep, y, nullptr, sel_mask, topk_ids, topk_w, stats, ws,
-                      ws_bytes, stage_events, stream);
+  if (T > 0 && !logits) return XSHARE_EINVAL;
+  return layer_common(layer_args(x, logits, nullptr, T, d, f, XSHARE_WEIGHTS_MXFP4, w1, w3, w2,
+                                 w1_scale, w3_scale, w2_scale, nullptr, params, req_offsets,
+                                 host_offsets, R, ep, y, nullptr, sel_mask, topk_ids, topk_w,
+                                 stats, ws, ws_bytes, stage_events, stream));
 }
 
 xshare_status xshare_moe_layer(const uint16_t* x, const uint16_t* w_gate, int32_t T, int32_t d,
@@ -546,13 +624,10 @@ xshare_status xshare_moe_layer(const uint16_t* x, const uint16_t* w_gate, int32_
                                xshare_stats* stats, void* ws, size_t ws_bytes,
                                void* const* stage_events, hipStream_t stream) {
   if (T > 0 && !w_gate) return XSHARE_EINVAL;
-  Weights wt;
-  wt.w1 = w1;
-  wt.w3 = w3;
-  wt.w2 = w2;
-  return layer_common(x, nullptr, w_gate, T, d, f, wt, shared, params, req_offsets,
-                      host_offsets, R, ep, y, logits_out, sel_mask, topk_ids, topk_w, stats, ws,
-                      ws_bytes, stage_events, stream);
+  return layer_common(layer_args(x, nullptr, w_gate, T, d, f, XSHARE_WEIGHTS_BF16, w1, w3, w2,
+                                 nullptr, nullptr, nullptr, shared, params, req_offsets,
+                                 host_offsets, R, ep, y, logits_out, sel_mask, topk_ids, topk_w,
+                                 stats, ws, ws_bytes, stage_events, stream));
 }
 
 size_t xshare_router_workspace_bytes(int32_t T, int32_t d, int32_t n_experts) {

@@ -12,6 +12,12 @@ copy reads and writes a known number of bytes, so it calibrates what the counter
 per byte.  Prints, per batch, the active experts and the algorithmic bytes of one gate/up
 launch (weights of the active experts, x, H as bf16 hi and lo) to compare with the
 counters.
+
+    python -m paper_2602_07265_amd.profiling --summarize OUT
+
+summarises the counter CSVs that rocprofv3 wrote under OUT: per kernel of this library
+(and the calibration copy) and counter, the dispatches and their mean value, as one JSON
+line.
 """
 from __future__ import annotations
 
@@ -25,7 +31,38 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 
+def summarize(out_dir: str) -> dict:
+    """{kernel: {counter: {"dispatches": n, "mean": m}}} over rocprofv3's counter CSVs."""
+    import csv
+    import glob
+
+    acc: dict = {}
+    for path in glob.glob(os.path.join(out_dir, "**", "*counter_collection.csv"), recursive=True):
+        with open(path) as fh:
+            for row in csv.DictReader(fh):
+                name = row["Kernel_Name"]
+                if "xs::" not in name and "copy" not in name:
+                    continue
+                ours = "xs::" in name
+                short = name.replace("void ", "").replace("xs::(anonymous namespace)::", "")
+                short = short.split("(")[0] if ours else "copy: " + short[:80]
+                per = acc.setdefault(short, {}).setdefault(row["Counter_Name"], [])
+                per.append(float(row["Counter_Value"]))
+    out = {}
+    for k, cs in acc.items():
+        out[k] = {}
+        for c, v in cs.items():
+            out[k][c] = {"dispatches": len(v), "mean": sum(v) / len(v)}
+            if k.startswith("copy: "):
+                # copies: the calibration copies are the largest dispatches of the run
+                out[k][c]["largest"] = sorted(v)[-4:]
+    return out
+
+
 def main():
+    if len(sys.argv) == 3 and sys.argv[1] == "--summarize":
+        print(json.dumps(summarize(sys.argv[2])))
+        return
     ap = argparse.ArgumentParser()
     ap.add_argument("--calls", type=int, default=8)
     ap.add_argument("--batches", type=int, default=8)

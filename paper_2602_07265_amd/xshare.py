@@ -55,6 +55,30 @@ class SharedExperts(ctypes.Structure):
     ]
 
 
+class LayerArgs(ctypes.Structure):
+    """xshare_layer_args (include/xshare.h), the argument struct of xshare_moe_forward_v2."""
+    _fields_ = [
+        ("struct_size", ctypes.c_size_t),
+        ("T", ctypes.c_int32), ("d", ctypes.c_int32), ("f", ctypes.c_int32),
+        ("x", ctypes.c_void_p), ("logits", ctypes.c_void_p), ("w_gate", ctypes.c_void_p),
+        ("weight_format", ctypes.c_int32),
+        ("w1", ctypes.c_void_p), ("w3", ctypes.c_void_p), ("w2", ctypes.c_void_p),
+        ("w1_scale", ctypes.c_void_p), ("w3_scale", ctypes.c_void_p),
+        ("w2_scale", ctypes.c_void_p),
+        ("params", ctypes.POINTER(RouteParams)),
+        ("req_offsets", ctypes.c_void_p), ("host_offsets", ctypes.c_void_p),
+        ("R", ctypes.c_int32),
+        ("ep", ctypes.POINTER(EpLayout)), ("shared", ctypes.POINTER(SharedExperts)),
+        ("y", ctypes.c_void_p), ("logits_out", ctypes.c_void_p), ("sel_mask", ctypes.c_void_p),
+        ("topk_ids", ctypes.c_void_p), ("topk_w", ctypes.c_void_p), ("stats", ctypes.c_void_p),
+        ("ws", ctypes.c_void_p), ("ws_bytes", ctypes.c_size_t),
+        ("stage_events", ctypes.c_void_p),
+        ("stream", ctypes.c_void_p),
+    ]
+
+
+WEIGHTS = {"bf16": 0, "fp8": 1, "mxfp4": 2}
+
 STATS_FIELDS = ("n_selected", "n_active", "n_vanilla_union", "n_warmup", "n_start",
                 "budget_eff", "max_group_load")
 
@@ -128,6 +152,12 @@ def lib() -> ctypes.CDLL:
                                                  ctypes.POINTER(SharedExperts), _P, _P, _P, _P,
                                                  _P, _P, _P]
         L.xshare_moe_forward_noalloc.restype = ctypes.c_int
+        L.xshare_moe_forward_v2.argtypes = [ctypes.POINTER(LayerArgs)]
+        L.xshare_moe_forward_v2.restype = ctypes.c_int
+        L.xshare_moe_forward_v2_workspace_bytes.argtypes = [ctypes.POINTER(LayerArgs)]
+        L.xshare_moe_forward_v2_workspace_bytes.restype = _SZ
+        L.xshare_probe_stream_read.argtypes = [_P, _SZ, _I32, _I32, _P, _P]
+        L.xshare_probe_stream_read.restype = ctypes.c_int
         L.xshare_status_string.argtypes = [_I32]
         L.xshare_status_string.restype = ctypes.c_char_p
         L.xshare_version.argtypes = []
@@ -660,6 +690,7 @@ class HipEvent:
         if cls._hip is None:
             h = ctypes.CDLL("libamdhip64.so")
             h.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+            h.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
             h.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
             h.hipEventSynchronize.argtypes = [ctypes.c_void_p]
             h.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
@@ -668,10 +699,12 @@ class HipEvent:
             cls._hip = h
         return cls._hip
 
-    def __init__(self):
+    def __init__(self, timing: bool = True):
         self.handle = ctypes.c_void_p()
-        if self._rt().hipEventCreate(ctypes.byref(self.handle)) != 0:
-            raise RuntimeError("hipEventCreate failed")
+        rt = self._rt()
+        flags = 0 if timing else 2                 # hipEventDisableTiming
+        if rt.hipEventCreateWithFlags(ctypes.byref(self.handle), flags) != 0:
+            raise RuntimeError("hipEventCreateWithFlags failed")
         self.handle = self.handle.value
 
     def record(self, stream=None):
@@ -694,3 +727,93 @@ class HipEvent:
                 self._hip.hipEventDestroy(self.handle)
         except Exception:
             pass
+
+
+def moe_forward_v2(x: torch.Tensor, top_k: int, warmup_k0: int, budget: int,
+                   budget_mode="total", score_mode="topk", *, logits=None, w_gate=None,
+                   weights=(), scales=(None, None, None), weight_format="bf16",
+                   req_offsets=None, per_request_budget: int = 0,
+                   groups: GroupMap | None = None, tau: float = 0.0, shared=None, ledger=None,
+                   y=None, routing_out=True, logits_out=False, workspace=None,
+                   stage_events=None, stream=None) -> dict:
+    """xshare_moe_forward_v2: the layer from one argument struct.  ``logits`` (fp32 [T, N]) or
+    ``w_gate`` (bf16 [N, d], logits computed on the device); ``weights`` = (w1, w3, w2) in
+    ``weight_format`` with ``scales`` for FP8 / MXFP4.  Shapes are checked by the library;
+    this only marshals pointers."""
+    T, d = x.shape
+    w1, w3, w2 = weights
+    N = (logits if logits is not None else w_gate).shape[0 if logits is None else 1]
+    f = w1.shape[1]
+    dev = x.device
+    if groups is not None:
+        budget_mode = "per_group"
+    p = params(N, top_k, warmup_k0, budget, budget_mode, score_mode, per_request_budget, tau,
+               ledger)
+    ep = None if groups is None else groups.layout
+    sh = _shared(shared, d, f, dev)
+    if y is None:
+        y = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
+    res = {"y": y}
+    if logits_out:
+        res["logits"] = torch.empty((T, N), dtype=torch.float32, device=dev)
+    if routing_out:
+        res.update(sel_mask=torch.empty(N, dtype=torch.uint8, device=dev),
+                   ids=torch.empty((T, top_k), dtype=torch.int32, device=dev),
+                   w=torch.empty((T, top_k), dtype=torch.float32, device=dev),
+                   stats=torch.empty(8, dtype=torch.int32, device=dev))
+    d_off = h_off = None
+    R = 0
+    if req_offsets is not None:
+        d_off, h_off = _offsets(req_offsets, dev)
+        R = d_off.numel() - 1
+    ev = None
+    if stage_events is not None:
+        if len(stage_events) != N_STAGE_EVENTS:
+            raise ValueError(f"stage_events needs {N_STAGE_EVENTS} events")
+        ev = (ctypes.c_void_p * N_STAGE_EVENTS)(*[e.handle for e in stage_events])
+    s1, s3, s2 = scales
+    a = LayerArgs()
+    a.struct_size = ctypes.sizeof(LayerArgs)
+    a.T, a.d, a.f = T, d, f
+    a.x = x.data_ptr()
+    a.logits = None if logits is None else logits.data_ptr()
+    a.w_gate = None if w_gate is None else w_gate.data_ptr()
+    a.weight_format = WEIGHTS[weight_format]
+    a.w1, a.w3, a.w2 = w1.data_ptr(), w3.data_ptr(), w2.data_ptr()
+    a.w1_scale = None if s1 is None else s1.data_ptr()
+    a.w3_scale = None if s3 is None else s3.data_ptr()
+    a.w2_scale = None if s2 is None else s2.data_ptr()
+    a.params = ctypes.pointer(p)
+    a.req_offsets = None if d_off is None else d_off.data_ptr()
+    a.host_offsets = None if h_off is None else h_off.data_ptr()
+    a.R = R
+    a.ep = None if ep is None else ctypes.pointer(ep)
+    a.shared = None if sh is None else ctypes.pointer(sh)
+    a.y = y.data_ptr()
+    for field, key in (("logits_out", "logits"), ("sel_mask", "sel_mask"), ("topk_ids", "ids"),
+                       ("topk_w", "w"), ("stats", "stats")):
+        setattr(a, field, None if res.get(key) is None else res[key].data_ptr())
+    a.stage_events = None if ev is None else ctypes.cast(ev, ctypes.c_void_p)
+    a.stream = _stream(stream).value
+    need = int(lib().xshare_moe_forward_v2_workspace_bytes(ctypes.byref(a)))
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    a.ws, a.ws_bytes = workspace.data_ptr(), workspace.numel()
+    _check(lib().xshare_moe_forward_v2(ctypes.byref(a)), "xshare_moe_forward_v2")
+    return res
+
+
+def probe_stream_read(buf: torch.Tensor, blocks: int = 2048, mode: int = 0, sink=None,
+                      stream=None):
+    """Enqueues one streaming read of ``buf`` (a contiguous GPU tensor, 16-byte aligned,
+    size a multiple of 16 bytes; ``mode`` as xshare_probe_stream_read); time it with
+    HipEvents on the same stream."""
+    if not buf.is_cuda or not buf.is_contiguous():
+        raise ValueError("buf must be a contiguous GPU tensor")
+    if sink is None:
+        sink = torch.zeros(1, dtype=torch.int32, device=buf.device)
+    _check(lib().xshare_probe_stream_read(_ptr(buf), buf.numel() * buf.element_size(),
+                                          int(blocks), int(mode), _ptr(sink),
+                                          _stream(stream)),
+           "xshare_probe_stream_read")
+    return sink

@@ -280,3 +280,85 @@ def test_moe_forward_mxfp4_validation():
     assert call(e2=ctypes.c_void_p((1 << 20) + 8)) == X.EINVAL
     assert call(d=48) == X.EUNSUPPORTED              # d, f multiples of 32
     assert call(f=80) == X.EUNSUPPORTED
+
+
+def _args(**kw):
+    """An xshare_layer_args for a bf16 layer with fake device pointers (never dereferenced:
+    every call below stops in validation)."""
+    p = X.params(16, 2, 1, 8)
+    a = X.LayerArgs()
+    a.struct_size = ctypes.sizeof(X.LayerArgs)
+    a.T, a.d, a.f = 8, 64, 128
+    a.x = a.logits = a.y = FAKE.value
+    a.w1 = a.w3 = a.w2 = FAKE.value
+    a.weight_format = X.WEIGHTS["bf16"]
+    a.params = ctypes.pointer(p)
+    a._keep = p
+    for key, v in kw.items():
+        setattr(a, key, v)
+    return a
+
+
+def test_layer_args_struct_matches_the_header():
+    # offsets of the C struct (x86-64): size_t, three int32, pointers 8-aligned
+    assert ctypes.sizeof(X.LayerArgs) == 232
+    assert X.LayerArgs.weight_format.offset == 48 and X.LayerArgs.R.offset == 128
+    src = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    end = src.index("} xshare_layer_args;")
+    body = src[src.rindex("typedef struct {", 0, end) + len("typedef struct {"):end]
+    names = re.findall(r"(\w+)(?:\s*,\s*(\w+))?(?:\s*,\s*(\w+))?;", body)
+    fields = [n for group in names for n in group if n]
+    assert fields == [f for f, _ in X.LayerArgs._fields_]
+
+
+def test_moe_forward_v2_validation():
+    L = X.lib()
+    v2 = lambda a: L.xshare_moe_forward_v2(ctypes.byref(a))
+    assert L.xshare_moe_forward_v2(None) == X.EINVAL
+    assert v2(_args()) == X.EWORKSPACE                       # valid: fails on the workspace
+    assert v2(_args(struct_size=ctypes.sizeof(X.LayerArgs) - 8)) == X.EINVAL
+    assert v2(_args(w_gate=FAKE.value)) == X.EINVAL          # both logits and w_gate
+    assert v2(_args(logits=None)) == X.EINVAL                # neither
+    assert v2(_args(logits=None, w_gate=FAKE.value)) == X.EWORKSPACE
+    assert v2(_args(weight_format=3)) == X.EINVAL
+    assert v2(_args(weight_format=X.WEIGHTS["fp8"])) == X.EINVAL      # scales missing
+    assert v2(_args(weight_format=X.WEIGHTS["fp8"], w1_scale=FAKE.value, w3_scale=FAKE.value,
+                    w2_scale=FAKE.value)) == X.EWORKSPACE
+    assert v2(_args(weight_format=X.WEIGHTS["mxfp4"], w1_scale=FAKE.value,
+                    w3_scale=FAKE.value, w2_scale=FAKE_ODD.value)) == X.EINVAL   # alignment
+    assert v2(_args(d=48)) == X.EUNSUPPORTED
+    assert v2(_args(x=FAKE_ODD.value)) == X.EINVAL
+    assert v2(_args(T=0, x=None, logits=None, y=None)) == X.EWORKSPACE   # empty batch: no inputs
+    assert v2(_args(ws=FAKE.value, ws_bytes=16)) == X.EWORKSPACE
+    sh = X.SharedExperts(1, 1 << 20, 1 << 20, 1 << 20)
+    assert v2(_args(shared=ctypes.pointer(sh), weight_format=X.WEIGHTS["fp8"],
+                    w1_scale=FAKE.value, w3_scale=FAKE.value,
+                    w2_scale=FAKE.value)) == X.EUNSUPPORTED          # shared experts: bf16 only
+
+
+def test_moe_forward_v2_workspace_equals_the_fixed_calls():
+    L = X.lib()
+    ws2 = lambda a: int(L.xshare_moe_forward_v2_workspace_bytes(ctypes.byref(a)))
+    for T, N, k, M, d, f in [(32, 256, 8, 48, 7168, 2048), (8, 16, 2, 8, 64, 128),
+                             (64, 128, 8, 32, 2048, 768)]:
+        p = X.params(N, k, 1, M)
+        a = _args(T=T, d=d, f=f, params=ctypes.pointer(p))
+        assert ws2(a) == X.moe_workspace_bytes(T, d, f, p) > 0
+        a = _args(T=T, d=d, f=f, params=ctypes.pointer(p), logits=None, w_gate=FAKE.value)
+        assert ws2(a) == X.layer_workspace_bytes(T, d, f, p) > 0
+    assert L.xshare_moe_forward_v2_workspace_bytes(None) == 0
+    assert ws2(_args(struct_size=8)) == 0
+    assert ws2(_args(d=0)) == 0
+
+
+def test_stream_probe_validation():
+    L = X.lib()
+    call = lambda buf=FAKE, n=1 << 20, blocks=64, sink=FAKE, mode=0: L.xshare_probe_stream_read(
+        buf, n, blocks, mode, sink, None)
+    assert call(buf=None) == X.EINVAL
+    assert call(buf=FAKE_ODD) == X.EINVAL
+    assert call(n=0) == X.EINVAL
+    assert call(n=(1 << 20) + 8) == X.EINVAL
+    assert call(blocks=0) == X.EINVAL
+    assert call(sink=None) == X.EINVAL
+    assert call(mode=4) == X.EINVAL
