@@ -110,11 +110,11 @@ __device__ __forceinline__ int wave_pick(uint32_t (&key)[Q], int lane, uint32_t&
   uint32_t bk = 0;
   uint32_t bj = 0xFFFFFFFFu;
 #pragma unroll
-  for (int q = 0; q < Q; ++q)
-    if (key[q] > bk) {  // strict: the lower q (lower index) wins inside a lane
-      bk = key[q];
-      bj = (uint32_t)(lane + 64 * q);
-    }
+  for (int q = 0; q < Q; ++q) {  // strict: the lower q (lower index) wins inside a lane
+    const bool up = key[q] > bk;
+    bk = up ? key[q] : bk;
+    bj = up ? (uint32_t)(lane + 64 * q) : bj;
+  }
   kbest = wave_max(bk);
   if (kbest == 0) return -1;
   const uint64_t holders = __ballot(bk == kbest);
@@ -123,11 +123,11 @@ __device__ __forceinline__ int wave_pick(uint32_t (&key)[Q], int lane, uint32_t&
     jmin = (uint32_t)__builtin_amdgcn_readlane((int)bj, __ffsll((long long)holders) - 1);
   else
     jmin = wave_min(bk == kbest ? bj : 0xFFFFFFFFu);
-  if ((int)(jmin & 63) == lane) {
+  // the holder lane drops the key: selects, not a branch around the holder lane
+  const bool mine = (int)(jmin & 63) == lane;
+  const int qsel = (int)(jmin >> 6);
 #pragma unroll
-    for (int q = 0; q < Q; ++q)
-      if (q == (int)(jmin >> 6)) key[q] = 0;
-  }
+  for (int q = 0; q < Q; ++q) key[q] = (mine && q == qsel) ? 0u : key[q];
   return (int)jmin;
 }
 
@@ -144,10 +144,9 @@ __device__ __forceinline__ void wave_topk(uint32_t (&key)[Q], int r0, int k, int
     uint32_t kb;
     const int jb = wave_pick<Q>(key, lane, kb);
     if (jb < 0) break;
-    if (lane == r) {
-      my_h = unord(kb);
-      my_j = jb;
-    }
+    const bool at = lane == r;
+    my_h = at ? unord(kb) : my_h;
+    my_j = at ? jb : my_j;
   }
 }
 
