@@ -751,6 +751,9 @@ static_assert(XS_DOWN_XCD_SLOTS >= 8, "at least one slot per XCD");
 #ifndef XS_DOWN_TL
 #define XS_DOWN_TL 4                 // 8-token (hi + lo) tiles per pass of the down GEMM
 #endif
+#ifndef XS_DOWN_WAVES_PER_EU
+#define XS_DOWN_WAVES_PER_EU 2       // waves per SIMD of the staged down instances (3: spills)
+#endif
 
 // Formats whose GEMMs stage the token rows in LDS (bit kW of each mask; all three by
 // default).  Same-box A/B against per-wave token loads, gate/up and down (us):
@@ -948,7 +951,7 @@ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
 // 64-row bf16 and FP8 instances (FP8 DeepSeek T=32 down 166 -> 138 us with the hint).
 // TL: token tiles per pass, 8 tokens each (hi and lo rows).
 template <int U, int kW, int NM, int TL = XS_DOWN_TL>
-__global__ __attribute__((amdgpu_waves_per_eu(stage_down(kW) ? 2 : 1)))
+__global__ __attribute__((amdgpu_waves_per_eu(stage_down(kW) ? XS_DOWN_WAVES_PER_EU : 1)))
 __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
   // (bx, slot): this block's column block and expert slot.  In grids of at least
   // XS_DOWN_XCD_SLOTS slots, with `live` slots holding work (shared, then active), all

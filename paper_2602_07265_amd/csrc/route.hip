@@ -160,6 +160,113 @@ __device__ __forceinline__ float ranked_gate(float my_h, int lane, int k) {
   return lane < k ? e / z : 0.0f;
 }
 
+// ---- Two tokens per wave: each 32-lane half ranks its own token (lane l of half h holds
+//      experts l, l + 32, ... of token 2p + h), so one chain of dependent reductions
+//      serves two tokens.  Used where a token's experts fit 8 per lane (N <= 256).
+
+// Max / min over each 32-lane half (lanes 0-31 and 32-63), returned to every lane: four
+// DPP steps give every lane its 16-lane row's value, then the two rows of each half
+// exchange (v_permlane16_swap pairs rows 0 and 1, and rows 2 and 3).
+__device__ __forceinline__ uint32_t half_max(uint32_t v) {
+  v = max(v, dpp<0xB1, 0xF, 0u>(v));   // quad_perm [1,0,3,2]
+  v = max(v, dpp<0x4E, 0xF, 0u>(v));   // quad_perm [2,3,0,1]
+  v = max(v, dpp<0x141, 0xF, 0u>(v));  // row_half_mirror
+  v = max(v, dpp<0x140, 0xF, 0u>(v));  // row_mirror
+  const auto s = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  return max((uint32_t)s[0], (uint32_t)s[1]);
+}
+__device__ __forceinline__ uint32_t half_min(uint32_t v) {
+  constexpr uint32_t kId = 0xFFFFFFFFu;
+  v = min(v, dpp<0xB1, 0xF, kId>(v));
+  v = min(v, dpp<0x4E, 0xF, kId>(v));
+  v = min(v, dpp<0x141, 0xF, kId>(v));
+  v = min(v, dpp<0x140, 0xF, kId>(v));
+  const auto s = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  return min((uint32_t)s[0], (uint32_t)s[1]);
+}
+
+// wave_pick for both halves at once: each half takes its largest key (lowest expert index
+// on equal keys), drops it and returns its expert (-1 if the half has no key left or is
+// not active this round); kbest receives the half's largest key.  sl: lane within the half.
+template <int Q2>
+__device__ __forceinline__ int half_pick(uint32_t (&key)[Q2], int sl, int h, bool act,
+                                         uint32_t& kbest) {
+  uint32_t bk = 0;
+  uint32_t bj = 0xFFFFFFFFu;
+#pragma unroll
+  for (int q = 0; q < Q2; ++q) {  // strict: the lower q (lower index) wins inside a lane
+    const bool up = key[q] > bk;
+    bk = up ? key[q] : bk;
+    bj = up ? (uint32_t)(sl + 32 * q) : bj;
+  }
+  const uint32_t kb = half_max(bk);
+  kbest = kb;
+  const bool got = act && kb != 0;
+  const bool holder = got && bk == kb;
+  const uint64_t hol = __ballot(holder);
+  const uint32_t lo = (uint32_t)hol, hi = (uint32_t)(hol >> 32);
+  const int nlo = __popc(lo), nhi = __popc(hi);
+  uint32_t j0 = 0xFFFFFFFFu, j1 = 0xFFFFFFFFu;
+  if (nlo == 1) j0 = (uint32_t)__builtin_amdgcn_readlane((int)bj, __ffs(lo) - 1);
+  if (nhi == 1) j1 = (uint32_t)__builtin_amdgcn_readlane((int)bj, 31 + __ffs(hi));
+  uint32_t jb = h ? j1 : j0;
+  if (nlo > 1 || nhi > 1) {   // equal largest keys in several lanes of a half
+    const uint32_t m = half_min(holder ? bj : 0xFFFFFFFFu);
+    jb = (h ? nhi > 1 : nlo > 1) ? m : jb;
+  }
+  const bool mine = got && (int)(jb & 31) == sl;
+  const int qsel = (int)(jb >> 5);
+#pragma unroll
+  for (int q = 0; q < Q2; ++q) key[q] = (mine && q == qsel) ? 0u : key[q];
+  return got ? (int)jb : -1;
+}
+
+// wave_topk for both halves: ranks [r0, k) of each half's keys (r0 uniform within a half);
+// lane sl of a half receives rank sl as (logit, expert).  Lanes below r0 keep what they hold.
+template <int Q2>
+__device__ __forceinline__ void half_topk(uint32_t (&key)[Q2], int r0, int k, int sl, int h,
+                                          float& my_h, int& my_j) {
+  if (sl >= r0) {
+    my_h = -INFINITY;
+    my_j = -1;
+  }
+  const int rs = min(__builtin_amdgcn_readlane(r0, 0), __builtin_amdgcn_readlane(r0, 32));
+  for (int r = rs; r < k; ++r) {
+    uint32_t kb;
+    const int jb = half_pick<Q2>(key, sl, h, r >= r0, kb);
+    const bool at = jb >= 0 && sl == r;
+    my_h = at ? unord(kb) : my_h;
+    my_j = at ? jb : my_j;
+  }
+}
+
+// ranked_gate for both halves: e_r = exp(h_r - h_0), Z summed in rank order, g_r = e_r / Z.
+__device__ __forceinline__ float half_gate(float my_h, int sl, int h, int k) {
+  const float m = h ? lane_value(my_h, 32) : lane_value(my_h, 0);
+  const float e = sl < k ? exp_fixed(my_h - m) : 0.0f;
+  float z0 = 0.0f, z1 = 0.0f;
+  for (int r = 0; r < k; ++r) {
+    z0 = z0 + lane_value(e, r);
+    z1 = z1 + lane_value(e, 32 + r);
+  }
+  const float z = h ? z1 : z0;
+  return sl < k ? e / z : 0.0f;
+}
+
+// Raw logits of token pair p: lane sl of half h holds experts sl, sl + 32, ... of token
+// 2p + h (0 beyond the batch or beyond N).
+template <int Q2>
+__device__ __forceinline__ void load_pair(const RouteArgs& a, int p, int sl, int h,
+                                          float (&raw)[Q2]) {
+  const int i = 2 * p + h;
+  const size_t row = (size_t)i * a.N;
+#pragma unroll
+  for (int q = 0; q < Q2; ++q) {
+    const int j = sl + 32 * q;
+    raw[q] = (i < a.T && j < a.N) ? a.logits[row + j] : 0.0f;
+  }
+}
+
 // Raw logits of token i, lane l holding experts l, l + 64, ...
 template <int Q>
 __device__ __forceinline__ void load_row(const RouteArgs& a, int i, int lane, float (&raw)[Q]) {
@@ -264,8 +371,8 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   __shared__ int s_off[kMaxExperts + 1];
   __shared__ uint8_t s_tier1[kMaxExperts];                   // picked by some request
   __shared__ uint8_t s_sel[kMaxExperts];
-  __shared__ uint32_t s_seed[kWaves][kMaxTopK];              // refinement seeds per wave
-  __shared__ float s_seed_h[kWaves][kMaxTopK];
+  __shared__ uint32_t s_seed[kWaves][2 * kMaxTopK];          // refinement seeds per wave
+  __shared__ float s_seed_h[kWaves][2 * kMaxTopK];            //   (and per half of a wave)
   __shared__ int s_wsum[kWaves];
   __shared__ int s_cnt[8];
   __shared__ int s_gload[kMaxExperts];   // GPU groups: warm-up experts per group, then |S| per group
@@ -344,9 +451,24 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   // tokens per wave whose keys stay in registers (1024 threads allow 128 VGPRs each)
   constexpr int kCache = Q <= 4 ? 4 : (Q <= 8 ? 2 : 1);
   const bool cached = T <= kCache * kWaves;
+  // Two tokens per wave (one per half) where a token's experts fit 8 per lane and the batch
+  // gives a wave more than one token, except with dense scores (their softmax sums every
+  // expert of the token in index order): token pairs p = wave, wave + 16, ..., pair p
+  // holding tokens 2p and 2p + 1.  Measured (selection us, one token per wave -> halves):
+  // DeepSeek T=32 25.8 -> 25.0, Qwen T=64 34.4 -> 30.7, speculative T=64 40.0 -> 37.5; with
+  // at most one token per wave (T <= 16) the half-wave rounds only add: T=8 18.0 -> 19.5.
+  constexpr bool kHalves = Q <= 4;
+  constexpr int Q2 = 2 * Q;
+  constexpr int kCacheP = Q2 <= 4 ? 4 : (Q2 <= 8 ? 2 : 1);   // pairs per wave in registers
+  const bool halves = kHalves && !dense && T > kWaves;
+  const int hh = lane >> 5, sl = lane & 31;
+  const int n_pairs = (T + 1) >> 1;
+  const bool cached_p = n_pairs <= kCacheP * kWaves;
   uint32_t kc[kCache][Q];
+  uint32_t kcp[kHalves ? kCacheP : 1][kHalves ? Q2 : 1];
   float raw_next[Q];
-  if (wave < T) load_row<Q>(a, wave, lane, raw_next);
+  float rawp_next[kHalves ? Q2 : 1];
+  if (!halves && wave < T) load_row<Q>(a, wave, lane, raw_next);
   // Token i: its plain top-k, gates and entries; `left` receives the keys that remain
   // after the top-k.  The wave's next row is loaded meanwhile.
   auto plain_topk = [&](int i, uint32_t (&left)[Q]) {
@@ -380,7 +502,44 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
         if (lane + 64 * q < N) a.dense[(size_t)i * N + lane + 64 * q] = e[q] / z;
     }
   };
-  if (cached) {
+  // Token pair p (halves): the plain top-k of both tokens, as plain_topk.
+  auto plain_topk_pair = [&](int p, uint32_t (&left)[kHalves ? Q2 : 1]) {
+    if constexpr (kHalves) {
+      float raw[Q2];
+#pragma unroll
+      for (int q = 0; q < Q2; ++q) raw[q] = rawp_next[q];
+      if (p + kWaves < n_pairs) load_pair<Q2>(a, p + kWaves, sl, hh, rawp_next);
+      const int i = 2 * p + hh;
+      const bool valid = i < T;
+#pragma unroll
+      for (int q = 0; q < Q2; ++q)
+        left[q] = (valid && sl + 32 * q < N) ? ord(raw[q] + 0.0f) : 0u;
+      float my_h;
+      int my_j;
+      half_topk<Q2>(left, 0, k, sl, hh, my_h, my_j);
+      const float g = half_gate(my_h, sl, hh, k);
+      if (valid && sl < k) {
+        s_ent[i * k + sl] = (uint16_t)(my_j < 0 ? kNoEntry : (uint32_t)((sl << 10) | my_j));
+        s_g[i * k + sl] = g;
+        s_vh[i * k + sl] = my_h;
+      }
+    }
+  };
+  if (halves) {
+    if constexpr (kHalves) {
+      if (wave < n_pairs) load_pair<Q2>(a, wave, sl, hh, rawp_next);
+      if (cached_p) {
+#pragma unroll
+        for (int it = 0; it < kCacheP; ++it)
+          if (wave + it * kWaves < n_pairs) plain_topk_pair(wave + it * kWaves, kcp[it]);
+      } else {
+        for (int p = wave; p < n_pairs; p += kWaves) {
+          uint32_t left[Q2];
+          plain_topk_pair(p, left);
+        }
+      }
+    }
+  } else if (cached) {
     // compile-time slots keep the cache in registers
 #pragma unroll
     for (int it = 0; it < kCache; ++it)
@@ -691,7 +850,76 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
       s_ent[i * k + lane] = (uint16_t)(my_j < 0 ? kNoEntry : (uint32_t)((lane << 10) | my_j));
     }
   };
-  if (cached) {
+  // Token pair p (halves): as refine, each half with its own token and seeds.
+  auto refine_pair = [&](int p, uint32_t (&key)[kHalves ? Q2 : 1]) {
+    if constexpr (kHalves) {
+      const int i = 2 * p + hh;
+      const bool valid = i < T;
+      const uint32_t vent = (valid && sl < k) ? (uint32_t)s_ent[i * k + sl] : kNoEntry;
+      const int vid = vent == kNoEntry ? -1 : (int)(vent & 1023u);
+#pragma unroll
+      for (int q = 0; q < Q2; ++q) {
+        const int jq = sl + 32 * q;
+        if (jq >= N || !s_sel[jq]) key[q] = 0;
+      }
+      const bool keep = vid >= 0 && s_sel[vid];
+      const uint64_t kept = __ballot(keep);
+      const uint32_t kh = hh ? (uint32_t)(kept >> 32) : (uint32_t)kept;
+      const int m = __popc(kh);
+      if (keep) {
+        const int dst = __popc(kh & ((1u << sl) - 1u));
+        s_seed[wave][hh * kMaxTopK + dst] = (uint32_t)vid;
+        s_seed_h[wave][hh * kMaxTopK + dst] = s_vh[i * k + sl];
+      }
+      float my_h = -INFINITY;
+      int my_j = -1;
+      if (sl < m) {
+        my_j = (int)s_seed[wave][hh * kMaxTopK + sl];
+        my_h = s_seed_h[wave][hh * kMaxTopK + sl];
+      }
+      half_topk<Q2>(key, m, k, sl, hh, my_h, my_j);
+      const float g = half_gate(my_h, sl, hh, k);
+      if (valid && sl < k) {
+        a.ids[i * k + sl] = my_j;
+        a.w[i * k + sl] = g;
+        s_ent[i * k + sl] = (uint16_t)(my_j < 0 ? kNoEntry : (uint32_t)((sl << 10) | my_j));
+      }
+    }
+  };
+  if (halves) {
+    if constexpr (kHalves) {
+      if (cached_p) {
+#pragma unroll
+        for (int it = 0; it < kCacheP; ++it)
+          if (wave + it * kWaves < n_pairs) refine_pair(wave + it * kWaves, kcp[it]);
+      } else {
+        if (wave < n_pairs) load_pair<Q2>(a, wave, sl, hh, rawp_next);
+        for (int p = wave; p < n_pairs; p += kWaves) {
+          float raw[Q2];
+          uint32_t key[Q2];
+#pragma unroll
+          for (int q = 0; q < Q2; ++q) raw[q] = rawp_next[q];
+          if (p + kWaves < n_pairs) load_pair<Q2>(a, p + kWaves, sl, hh, rawp_next);
+          const int i = 2 * p + hh;
+          const bool valid = i < T;
+#pragma unroll
+          for (int q = 0; q < Q2; ++q)
+            key[q] = (valid && sl + 32 * q < N) ? ord(raw[q] + 0.0f) : 0u;
+          const uint32_t vent = (valid && sl < k) ? (uint32_t)s_ent[i * k + sl] : kNoEntry;
+          const int vid = vent == kNoEntry ? -1 : (int)(vent & 1023u);
+          for (int r = 0; r < k; ++r) {   // the plain top-k is not searched again
+            const int v0 = __builtin_amdgcn_readlane(vid, r);
+            const int v1 = __builtin_amdgcn_readlane(vid, 32 + r);
+            const int vr = hh ? v1 : v0;
+            const bool drop = vr >= 0 && (vr & 31) == sl;
+#pragma unroll
+            for (int q = 0; q < Q2; ++q) key[q] = (drop && q == (vr >> 5)) ? 0u : key[q];
+          }
+          refine_pair(p, key);
+        }
+      }
+    }
+  } else if (cached) {
 #pragma unroll
     for (int it = 0; it < kCache; ++it)
       if (wave + it * kWaves < T) refine(wave + it * kWaves, kc[it]);
