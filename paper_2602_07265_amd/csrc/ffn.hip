@@ -441,6 +441,12 @@ struct WTile<kFp8, U> {
   }
   __device__ static bf16x8 operand(const Regs& r, int u) { return fp8x8_to_bf16(r.w[u]); }
 };
+// Steps per MXFP4 scale group of the 8-word (U = 8) weight tiles: 4, 8 or 16.
+#ifndef XS_Q4_SCALE_STEPS
+#define XS_Q4_SCALE_STEPS 8
+#endif
+static_assert(XS_Q4_SCALE_STEPS == 4 || XS_Q4_SCALE_STEPS == 8 || XS_Q4_SCALE_STEPS == 16,
+              "4, 8 or 16 steps per scale group");
 template <int U>
 struct WTile<kMx4, U> {
   // w: this lane's codes; sc: this lane's scale bytes (lane group g: its row's scale bytes
@@ -457,37 +463,61 @@ struct WTile<kMx4, U> {
     r.e = load_e8m0<U>(p.sc + s / 32);
     return r;
   }
-  // Scales by groups of four steps: a row's scale bytes of one step (U bytes) are one
+  // Scales by groups of steps: a row's scale bytes of one step (U bytes) are one
   // cache-line piece that all four lanes of the row used to load separately, step after
   // step (a fifth of the GEMM time went to these 2-byte loads, one cache line per row
-  // each).  In group G, lane group g loads its row's U bytes of step 4G + g, and at step
-  // 4G + ph every lane takes its bytes from lane (n, ph) with a cross-lane read: one load
-  // instruction per four steps and tile.
+  // each).  In group G of kSG steps, lane group g loads its row's U bytes of the kP steps
+  // kSG G + kP g ..., and at step kSG G + ph every lane takes its bytes from lane (n, ph /
+  // kP) with a cross-lane read: one load per kP steps and tile.  For U = 8 a group spans
+  // XS_Q4_SCALE_STEPS steps.  A row's scale lines are evicted by the weight stream between
+  // its groups, so each group visits them again: with four steps, a row's 224 scale bytes
+  // (d = 7168) came in seven 32-byte pieces and the gate/up fetched 18.4 % more than its
+  // bytes (down, 64 bytes a row: 5.8 %); with eight, 11.3 % and 0.3 % (DeepSeek T=32 M=48
+  // gate/up 145.6 -> 143.4 us, down 82.0 -> 81.4 us).  Sixteen would leave the two-tile
+  // gate/up one wave per SIMD.
   static constexpr bool kGroupScales = U == 4 || U == 8 || U == 16;
+  static constexpr int kP = U == 8 ? XS_Q4_SCALE_STEPS / 4 : 1;   // steps per lane piece
+  static constexpr int kSG = 4 * kP;                               // steps per group
+  struct GV8 { uint2 w[kP]; };
   using GV = typename std::conditional<
-      (U == 16), uint4, typename std::conditional<(U == 8), uint2, uint32_t>::type>::type;
+      (U == 16), uint4, typename std::conditional<(U == 8), GV8, uint32_t>::type>::type;
   __device__ static Regs load_codes(const Ptr& p, int s) {
     Regs r;
     r.q = load_q4<U>(p.w + s / 2);
     return r;
   }
-  // (a group past the pass's last step `last` repeats that step's bytes)
+  // (a step past the pass's last step `last` repeats that step's bytes)
   __device__ static GV load_group(const Ptr& p, int G, int g, int last) {
-    return *reinterpret_cast<const GV*>(p.sc - U / 4 * g + min(4 * G + g, last) * U);
+    const uint8_t* const row = p.sc - U / 4 * g;       // the row's bytes of step 0
+    if constexpr (U == 8) {
+      GV v;
+#pragma unroll
+      for (int i = 0; i < kP; ++i)
+        v.w[i] = *reinterpret_cast<const uint2*>(row + min(kSG * G + kP * g + i, last) * U);
+      return v;
+    } else {
+      return *reinterpret_cast<const GV*>(row + min(4 * G + g, last) * U);
+    }
   }
   __device__ static E group_scale(const GV& v, int ph, int lane) {
-    const int src = (lane & 15) + 16 * ph, g = lane >> 4;
+    const int g = lane >> 4;
     if constexpr (U == 16) {  // lane group g's four bytes: word g of the step's 16 bytes
+      const int src = (lane & 15) + 16 * ph;
       const uint32_t w0 = (uint32_t)__shfl((int)v.x, src, 64);
       const uint32_t w1 = (uint32_t)__shfl((int)v.y, src, 64);
       const uint32_t w2 = (uint32_t)__shfl((int)v.z, src, 64);
       const uint32_t w3 = (uint32_t)__shfl((int)v.w, src, 64);
       return g < 2 ? (g == 0 ? w0 : w1) : (g == 2 ? w2 : w3);
     } else if constexpr (U == 8) {   // lane group g's bytes 2g, 2g + 1 of the step's 8
-      const uint32_t w0 = (uint32_t)__shfl((int)v.x, src, 64);
-      const uint32_t w1 = (uint32_t)__shfl((int)v.y, src, 64);
+      const int src = (lane & 15) + 16 * (ph / kP), i = ph % kP;   // i: uniform
+      uint2 w = v.w[0];
+#pragma unroll
+      for (int j = 1; j < kP; ++j) w = i == j ? v.w[j] : w;
+      const uint32_t w0 = (uint32_t)__shfl((int)w.x, src, 64);
+      const uint32_t w1 = (uint32_t)__shfl((int)w.y, src, 64);
       return (E)((g < 2 ? w0 : w1) >> (16 * (g & 1)));
     } else {                  // U = 4: byte g of the step's 4
+      const int src = (lane & 15) + 16 * ph;
       const uint32_t w = (uint32_t)__shfl((int)v, src, 64);
       return (E)((w >> (8 * g)) & 0xFFu);
     }
@@ -502,7 +532,7 @@ struct WTile<kMx4, U> {
 // ceil(R * P / 256) (pieces beyond R * P repeat the last one).  Staged row r (r < R) is
 // x[tok[r] * ld ...], x already offset to this block's reduction range.  acc[m][rt] as in
 // wave_pass (gate/up) or the down pass.
-// kGS: MXFP4 scales loaded by groups of four steps (WTile<kMx4, U>::load_group); needs
+// kGS: MXFP4 scales loaded by groups of steps (WTile<kMx4, U>::load_group); needs
 // k_first = 0.
 template <int kW, int U, bool kDown, int NM, int NT, int NL, int TA, bool kGS = false>
 __device__ __forceinline__ void block_pass(const uint16_t* x, size_t ld, const int* tok, int R,
@@ -554,7 +584,7 @@ __device__ __forceinline__ void block_pass(const uint16_t* x, size_t ld, const i
   auto scales = [&](int ks) {
     if constexpr (kGS) {
 #pragma unroll
-      for (int m = 0; m < NM; ++m) b[m].e = WT::group_scale(gs[m], ks & 3, lane);
+      for (int m = 0; m < NM; ++m) b[m].e = WT::group_scale(gs[m], ks % WT::kSG, lane);
     }
   };
   // MFMAs of one step from LDS buffer `cur`
@@ -581,9 +611,9 @@ __device__ __forceinline__ void block_pass(const uint16_t* x, size_t ld, const i
     // (a uniform branch, taken every fourth step), that group's pieces, first of the loads
     scales(ks - 1);
     if constexpr (kGS) {
-      if ((ks & 3) == 0) {
+      if (ks % WT::kSG == 0) {
 #pragma unroll
-        for (int m = 0; m < NM; ++m) gs[m] = WT::load_group(wp[m], ks >> 2, g, K / KB - 1);
+        for (int m = 0; m < NM; ++m) gs[m] = WT::load_group(wp[m], ks / WT::kSG, g, K / KB - 1);
       }
     }
 #pragma unroll

@@ -296,16 +296,24 @@ __device__ __forceinline__ void copy_keys(uint32_t (&dst)[Q], const uint32_t (&s
   for (int q = 0; q < Q; ++q) dst[q] = src[q];
 }
 
+// Wave-wide inclusive prefix sum with DPP: shifts by 1, 2, 4 and 8 lanes inside each row
+// of 16 (lanes without a source add 0), then each row's total added to the rows above it
+// (row_bcast:15 into rows 1 and 3, row_bcast:31 into rows 2 and 3).
+__device__ __forceinline__ int wave_incl_scan(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);  // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);  // row_bcast:31
+  return v;
+}
+
 // Block-wide exclusive prefix sum of one int per thread; every thread must call it.
 __device__ int block_excl_scan(int v, int* s_wsum, int& total) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  int inc = v;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const int y = __shfl_up(inc, off, 64);
-    if (lane >= off) inc += y;
-  }
+  const int inc = wave_incl_scan(v);
   if (lane == 63) s_wsum[wave] = inc;
   __syncthreads();
   int pre = 0;
@@ -560,11 +568,25 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
     int total;
     const int cnt = group_by_expert(s_ent, s_occ, s_off, s_list, s_wsum, TK, k, N, total);
     if (j < N) {
+      // eight entries' loads, then their adds in token order (the loads do not wait for the
+      // sum, so a long list costs one LDS round trip per eight tokens)
       const int o = s_off[j];
-      for (int q = 0; q < cnt; ++q) {
-        const int p = s_list[o + q];
-        if (!dense) s = s + s_g[p];
-        if ((int)((s_ent[p] >> 10) & 31u) < k0) inS0 = true;
+      for (int q0 = 0; q0 < cnt; q0 += 8) {
+        float gq[8];
+        uint32_t eq[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int p = s_list[o + min(q0 + u, cnt - 1)];
+          gq[u] = s_g[p];
+          eq[u] = s_ent[p];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          if (q0 + u < cnt) {
+            if (!dense) s = s + gq[u];
+            if ((int)((eq[u] >> 10) & 31u) < k0) inS0 = true;
+          }
+        }
       }
       inU = cnt > 0;
     }
@@ -604,10 +626,22 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
           const uint64_t m = s_occ[jq];
           const int n = __popcll(m & range);
           const int o = s_off[jq] + __popcll(m & below(lo));
-          for (int t = 0; t < n; ++t) {
-            const int p = s_list[o + t];
-            if ((int)((s_ent[p] >> 10) & 31u) < k0) inS0r |= 1u << q;
-            if (!dense) sr[q] = sr[q] + s_g[p];
+          for (int t0 = 0; t0 < n; t0 += 8) {   // loads ahead of the ordered adds, as in (b)
+            float gq[8];
+            uint32_t eq[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+              const int p = s_list[o + min(t0 + u, n - 1)];
+              gq[u] = s_g[p];
+              eq[u] = s_ent[p];
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+              if (t0 + u < n) {
+                if ((int)((eq[u] >> 10) & 31u) < k0) inS0r |= 1u << q;
+                if (!dense) sr[q] = sr[q] + gq[u];
+              }
+            }
           }
           if (n > 0) inUr |= 1u << q;
         }

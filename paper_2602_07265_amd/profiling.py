@@ -6,12 +6,13 @@
         python -m paper_2602_07265_amd.profiling
 
 Runs the DeepSeek-R1-shaped layer (N=256, k=8, d=7168, f=2048, T=32 tokens, total budget
-48, warm-up 1; seeded domain-centroid logits) for --calls calls over rotating batches, then
+48, warm-up 1; seeded domain-centroid logits; --weights bf16, fp8 or mxfp4) for --calls
+calls over rotating batches, then
 a plain device-to-device copy of --copy-mib MiB (torch's copy kernel) --copies times.  The
 copy reads and writes a known number of bytes, so it calibrates what the counters report
 per byte.  Prints, per batch, the active experts and the algorithmic bytes of one gate/up
-launch (weights of the active experts, x, H as bf16 hi and lo) to compare with the
-counters.
+launch (weights and scales of the active experts, x, H as bf16 hi and lo) to compare with
+the counters.
 
     python -m paper_2602_07265_amd.profiling --summarize OUT
 
@@ -69,6 +70,7 @@ def main():
     ap.add_argument("--copy-mib", type=int, default=1024)
     ap.add_argument("--copies", type=int, default=4)
     ap.add_argument("--budget", type=int, default=48)
+    ap.add_argument("--weights", choices=("bf16", "fp8", "mxfp4"), default="bf16")
     args = ap.parse_args()
 
     import torch
@@ -79,7 +81,15 @@ def main():
     dev = "cuda:0"
     c = W.CONFIGS["ds_t32"]
     T, N, k, d, f, k0, M = c["T"], c["N"], c["k"], c["d"], c["f"], c["k0"], args.budget
-    w1, w3, w2 = W.expert_weights(N, d, f, 0, dev)
+    if args.weights == "fp8":
+        wset = W.expert_weights_fp8(N, d, f, 0, dev)
+        wb, sb = 1.0, None              # one byte per weight, one fp32 scale per row
+    elif args.weights == "mxfp4":
+        wset = W.expert_weights_mxfp4(N, d, f, 0, dev)
+        wb, sb = 0.5, 1.0 / 32          # half a byte per weight, one scale byte per 32
+    else:
+        wset = W.expert_weights(N, d, f, 0, dev)
+        wb, sb = 2.0, 0.0
     logits = [torch.from_numpy(W.logits_domains(T, N, c["Q"], s)).to(dev) for s in range(args.batches)]
     xs = [W.activations(T, d, s, dev) for s in range(args.batches)]
     p = X.params(N, k, k0, M)
@@ -89,18 +99,25 @@ def main():
     per_call = []
     for s in range(args.calls):
         b = s % args.batches
-        r = X.moe_forward(xs[b], logits[b], w1, w3, w2, k, k0, M, y=y, workspace=ws)
+        r = X.moe_forward_v2(xs[b], k, k0, M, logits=logits[b], weights=wset[:3],
+                             scales=tuple(wset[3:6]) if len(wset) > 3 else (None,) * 3,
+                             weight_format=args.weights, y=y, workspace=ws)
         st = X.stats_dict(r["stats"])
-        per_call.append({"call": s, "n_active": st["n_active"],
-                         "gate_up_bytes": st["n_active"] * 2 * f * d * 2 + T * d * 2 + T * k * f * 4,
-                         "down_bytes": st["n_active"] * f * d * 2 + T * k * f * 4 + T * k * d * 4})
+        n = st["n_active"]
+        # one matrix of each active expert: W1 or W3 ([f, d]: f rows), W2 ([d, f]: d rows)
+        gu_w = n * (f * d * wb + (f * 4 if sb is None else f * d * sb))
+        dn_w = n * (f * d * wb + (d * 4 if sb is None else f * d * sb))
+        per_call.append({"call": s, "n_active": n,
+                         "gate_up_bytes": round(2 * gu_w + T * d * 2 + T * k * f * 4),
+                         "down_bytes": round(dn_w + T * k * f * 4 + T * k * d * 4)})
     nbytes = args.copy_mib << 20
     src = torch.empty(nbytes, dtype=torch.uint8, device=dev)
     dst = torch.empty_like(src)
     for _ in range(args.copies):
         dst.copy_(src)
     torch.cuda.synchronize()
-    print(json.dumps({"workload": f"ds_t32 M={M}", "copy_bytes": nbytes, "calls": per_call}))
+    print(json.dumps({"workload": f"ds_t32 M={M} {args.weights}", "copy_bytes": nbytes,
+                      "calls": per_call}))
 
 
 if __name__ == "__main__":
