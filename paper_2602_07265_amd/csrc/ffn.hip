@@ -1163,29 +1163,29 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(FfnArgs a) {
   const int c = (blockIdx.x * kBlock + threadIdx.x) * 4;
   if (c >= a.d) return;
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
-  // kR ranks at a time: their ids and weights, then all their row loads, are issued before
-  // any is used (one round trip per group instead of two per rank); the sums keep rank
-  // order and, per rank, split order
+  // kR ranks at a time: their ids, weights and rows are loaded together (the rows of the
+  // ranks that turn out unused, empty slots and other GPU groups' experts, hold stale
+  // values and are left out of the sums), so a group costs one round trip; the sums keep
+  // rank order and, per rank, split order
   constexpr int kR = 8;
   for (int r0 = 0; r0 < a.k; r0 += kR) {
     int e[kR];
     float wr[kR];
+    float4 v[kR];
 #pragma unroll
     for (int j = 0; j < kR; ++j) {
       const bool in = r0 + j < a.k;
       e[j] = in ? a.ids[i * a.k + r0 + j] : -1;
       wr[j] = in ? a.w[i * a.k + r0 + j] : 0.0f;
+      v[j] = *reinterpret_cast<const float4*>(a.yslot +
+                                              (size_t)(i * a.k + min(r0 + j, a.k - 1)) * a.d + c);
     }
     bool use[kR];
-    float4 v[kR];
 #pragma unroll
-    for (int j = 0; j < kR; ++j) {
+    for (int j = 0; j < kR; ++j)
       use[j] = e[j] >= 0 &&   // another GPU group's terms of y_i are left out
                (a.local_group < 0 ||
                 (a.group ? a.group[e[j]] : e[j] / (a.N / a.G)) == a.local_group);
-      v[j] = use[j] ? *reinterpret_cast<const float4*>(a.yslot + (size_t)(i * a.k + r0 + j) * a.d + c)
-                    : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
     for (int s = 1; s < a.splits; ++s) {   // partial sums of a split reduction, in order
 #pragma unroll
       for (int j = 0; j < kR; ++j) {

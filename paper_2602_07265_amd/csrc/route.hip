@@ -400,6 +400,34 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   const int TK = T * k;
   const int TK8 = (TK + 7) & ~7;
 
+  // tokens per wave whose keys stay in registers (1024 threads allow 128 VGPRs each)
+  constexpr int kCache = Q <= 4 ? 4 : (Q <= 8 ? 2 : 1);
+  const bool cached = T <= kCache * kWaves;
+  // Two tokens per wave (one per half) where a token's experts fit 8 per lane and the batch
+  // gives a wave more than one token, except with dense scores (their softmax sums every
+  // expert of the token in index order): token pairs p = wave, wave + 16, ..., pair p
+  // holding tokens 2p and 2p + 1.  Measured (selection us, one token per wave -> halves):
+  // DeepSeek T=32 25.8 -> 25.0, Qwen T=64 34.4 -> 30.7, speculative T=64 40.0 -> 37.5; with
+  // at most one token per wave (T <= 16) the half-wave rounds only add: T=8 18.0 -> 19.5.
+  constexpr bool kHalves = Q <= 4;
+  constexpr int Q2 = 2 * Q;
+  constexpr int kCacheP = Q2 <= 4 ? 4 : (Q2 <= 8 ? 2 : 1);   // pairs per wave in registers
+  const bool halves = kHalves && !dense && T > kWaves;
+  const int hh = lane >> 5, sl = lane & 31;
+  const int n_pairs = (T + 1) >> 1;
+  const bool cached_p = n_pairs <= kCacheP * kWaves;
+  uint32_t kc[kCache][Q];
+  uint32_t kcp[kHalves ? kCacheP : 1][kHalves ? Q2 : 1];
+  float raw_next[Q];
+  float rawp_next[kHalves ? Q2 : 1];
+  // the wave's first logits row is on its way while the workgroup clears its tables
+  if (halves) {
+    if constexpr (kHalves)
+      if (wave < n_pairs) load_pair<Q2>(a, wave, sl, hh, rawp_next);
+  } else if (wave < T) {
+    load_row<Q>(a, wave, lane, raw_next);
+  }
+
   if (tid < 8) s_cnt[tid] = 0;
   for (int j = tid; j < kMaxExperts; j += kThreads) {
     s_tier1[j] = 0;
@@ -456,27 +484,6 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   //      The next token's row is loaded while the current one is ranked; for batches of
   //      up to four tokens per wave the keys left after the top-k (all experts but the
   //      token's top-k) stay in registers for the refinement.
-  // tokens per wave whose keys stay in registers (1024 threads allow 128 VGPRs each)
-  constexpr int kCache = Q <= 4 ? 4 : (Q <= 8 ? 2 : 1);
-  const bool cached = T <= kCache * kWaves;
-  // Two tokens per wave (one per half) where a token's experts fit 8 per lane and the batch
-  // gives a wave more than one token, except with dense scores (their softmax sums every
-  // expert of the token in index order): token pairs p = wave, wave + 16, ..., pair p
-  // holding tokens 2p and 2p + 1.  Measured (selection us, one token per wave -> halves):
-  // DeepSeek T=32 25.8 -> 25.0, Qwen T=64 34.4 -> 30.7, speculative T=64 40.0 -> 37.5; with
-  // at most one token per wave (T <= 16) the half-wave rounds only add: T=8 18.0 -> 19.5.
-  constexpr bool kHalves = Q <= 4;
-  constexpr int Q2 = 2 * Q;
-  constexpr int kCacheP = Q2 <= 4 ? 4 : (Q2 <= 8 ? 2 : 1);   // pairs per wave in registers
-  const bool halves = kHalves && !dense && T > kWaves;
-  const int hh = lane >> 5, sl = lane & 31;
-  const int n_pairs = (T + 1) >> 1;
-  const bool cached_p = n_pairs <= kCacheP * kWaves;
-  uint32_t kc[kCache][Q];
-  uint32_t kcp[kHalves ? kCacheP : 1][kHalves ? Q2 : 1];
-  float raw_next[Q];
-  float rawp_next[kHalves ? Q2 : 1];
-  if (!halves && wave < T) load_row<Q>(a, wave, lane, raw_next);
   // Token i: its plain top-k, gates and entries; `left` receives the keys that remain
   // after the top-k.  The wave's next row is loaded meanwhile.
   auto plain_topk = [&](int i, uint32_t (&left)[Q]) {
@@ -535,7 +542,6 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   };
   if (halves) {
     if constexpr (kHalves) {
-      if (wave < n_pairs) load_pair<Q2>(a, wave, sl, hh, rawp_next);
       if (cached_p) {
 #pragma unroll
         for (int it = 0; it < kCacheP; ++it)
