@@ -189,7 +189,7 @@ __device__ __forceinline__ uint32_t half_min(uint32_t v) {
 // on equal keys), drops it and returns its expert (-1 if the half has no key left or is
 // not active this round); kbest receives the half's largest key.  sl: lane within the half.
 template <int Q2>
-__device__ __forceinline__ int half_pick(uint32_t (&key)[Q2], int sl, int h, bool act,
+__device__ __forceinline__ int half_pick(uint32_t (&key)[Q2], int sl, bool act,
                                          uint32_t& kbest) {
   uint32_t bk = 0;
   uint32_t bj = 0xFFFFFFFFu;
@@ -202,18 +202,8 @@ __device__ __forceinline__ int half_pick(uint32_t (&key)[Q2], int sl, int h, boo
   const uint32_t kb = half_max(bk);
   kbest = kb;
   const bool got = act && kb != 0;
-  const bool holder = got && bk == kb;
-  const uint64_t hol = __ballot(holder);
-  const uint32_t lo = (uint32_t)hol, hi = (uint32_t)(hol >> 32);
-  const int nlo = __popc(lo), nhi = __popc(hi);
-  uint32_t j0 = 0xFFFFFFFFu, j1 = 0xFFFFFFFFu;
-  if (nlo == 1) j0 = (uint32_t)__builtin_amdgcn_readlane((int)bj, __ffs(lo) - 1);
-  if (nhi == 1) j1 = (uint32_t)__builtin_amdgcn_readlane((int)bj, 31 + __ffs(hi));
-  uint32_t jb = h ? j1 : j0;
-  if (nlo > 1 || nhi > 1) {   // equal largest keys in several lanes of a half
-    const uint32_t m = half_min(holder ? bj : 0xFFFFFFFFu);
-    jb = (h ? nhi > 1 : nlo > 1) ? m : jb;
-  }
+  // the lowest expert index among the half's holders of the largest key
+  const uint32_t jb = half_min(got && bk == kb ? bj : 0xFFFFFFFFu);
   const bool mine = got && (int)(jb & 31) == sl;
   const int qsel = (int)(jb >> 5);
 #pragma unroll
@@ -233,7 +223,7 @@ __device__ __forceinline__ void half_topk(uint32_t (&key)[Q2], int r0, int k, in
   const int rs = min(__builtin_amdgcn_readlane(r0, 0), __builtin_amdgcn_readlane(r0, 32));
   for (int r = rs; r < k; ++r) {
     uint32_t kb;
-    const int jb = half_pick<Q2>(key, sl, h, r >= r0, kb);
+    const int jb = half_pick<Q2>(key, sl, r >= r0, kb);
     const bool at = jb >= 0 && sl == r;
     my_h = at ? unord(kb) : my_h;
     my_j = at ? jb : my_j;
@@ -251,6 +241,112 @@ __device__ __forceinline__ float half_gate(float my_h, int sl, int h, int k) {
   }
   const float z = h ? z1 : z0;
   return sl < k ? e / z : 0.0f;
+}
+
+// ---- Four tokens per wave: each 16-lane row ranks its own token (lane l of row r holds
+//      experts l, l + 16, ... of token 4p + r).  Used where a token's experts fit 8 per lane
+//      (N <= 128) and its k ranks fit in a row (k <= 16).
+
+// Max / min over each 16-lane row, returned to every lane of the row (the first four steps
+// of half_max).
+__device__ __forceinline__ uint32_t row_max(uint32_t v) {
+  v = max(v, dpp<0xB1, 0xF, 0u>(v));   // quad_perm [1,0,3,2]
+  v = max(v, dpp<0x4E, 0xF, 0u>(v));   // quad_perm [2,3,0,1]
+  v = max(v, dpp<0x141, 0xF, 0u>(v));  // row_half_mirror
+  v = max(v, dpp<0x140, 0xF, 0u>(v));  // row_mirror
+  return v;
+}
+__device__ __forceinline__ uint32_t row_min(uint32_t v) {
+  constexpr uint32_t kId = 0xFFFFFFFFu;
+  v = min(v, dpp<0xB1, 0xF, kId>(v));
+  v = min(v, dpp<0x4E, 0xF, kId>(v));
+  v = min(v, dpp<0x141, 0xF, kId>(v));
+  v = min(v, dpp<0x140, 0xF, kId>(v));
+  return v;
+}
+
+// The value of `v` in lane 16 r + c for this lane's row r (c uniform).
+__device__ __forceinline__ int row_lane(int v, int r, int c) {
+  const int v0 = __builtin_amdgcn_readlane(v, c);
+  const int v1 = __builtin_amdgcn_readlane(v, 16 + c);
+  const int v2 = __builtin_amdgcn_readlane(v, 32 + c);
+  const int v3 = __builtin_amdgcn_readlane(v, 48 + c);
+  return r < 2 ? (r == 0 ? v0 : v1) : (r == 2 ? v2 : v3);
+}
+
+// wave_pick for the four rows at once: each row takes its largest key (lowest expert index
+// on equal keys), drops it and returns its expert (-1 if the row has no key left or is not
+// active this round); kbest receives the row's largest key.  ql: lane within the row.
+template <int Q4>
+__device__ __forceinline__ int row_pick(uint32_t (&key)[Q4], int ql, bool act, uint32_t& kbest) {
+  uint32_t bk = 0;
+  uint32_t bj = 0xFFFFFFFFu;
+#pragma unroll
+  for (int q = 0; q < Q4; ++q) {  // strict: the lower q (lower index) wins inside a lane
+    const bool up = key[q] > bk;
+    bk = up ? key[q] : bk;
+    bj = up ? (uint32_t)(ql + 16 * q) : bj;
+  }
+  const uint32_t kb = row_max(bk);
+  kbest = kb;
+  const bool got = act && kb != 0;
+  // the lowest expert index among the row's holders of the largest key: a second row
+  // reduction, cheaper than a ballot and a lane read per row
+  const uint32_t jb = row_min(got && bk == kb ? bj : 0xFFFFFFFFu);
+  const bool mine = got && (int)(jb & 15) == ql;
+  const int qsel = (int)(jb >> 4);
+#pragma unroll
+  for (int q = 0; q < Q4; ++q) key[q] = (mine && q == qsel) ? 0u : key[q];
+  return got ? (int)jb : -1;
+}
+
+// wave_topk for the four rows: ranks [r0, k) of each row's keys (r0 uniform within a row);
+// lane ql of a row receives rank ql as (logit, expert).  Lanes below r0 keep what they hold.
+template <int Q4>
+__device__ __forceinline__ void row_topk(uint32_t (&key)[Q4], int r0, int k, int ql, int qr,
+                                         float& my_h, int& my_j) {
+  if (ql >= r0) {
+    my_h = -INFINITY;
+    my_j = -1;
+  }
+  const int rs = min(min(__builtin_amdgcn_readlane(r0, 0), __builtin_amdgcn_readlane(r0, 16)),
+                     min(__builtin_amdgcn_readlane(r0, 32), __builtin_amdgcn_readlane(r0, 48)));
+  for (int r = rs; r < k; ++r) {
+    uint32_t kb;
+    const int jb = row_pick<Q4>(key, ql, r >= r0, kb);
+    const bool at = jb >= 0 && ql == r;
+    my_h = at ? unord(kb) : my_h;
+    my_j = at ? jb : my_j;
+  }
+}
+
+// ranked_gate for the four rows: e_r = exp(h_r - h_0), Z summed in rank order, g_r = e_r / Z.
+__device__ __forceinline__ float row_gate(float my_h, int ql, int qr, int k) {
+  const float m = __int_as_float(row_lane(__float_as_int(my_h), qr, 0));
+  const float e = ql < k ? exp_fixed(my_h - m) : 0.0f;
+  float z0 = 0.0f, z1 = 0.0f, z2 = 0.0f, z3 = 0.0f;
+  for (int r = 0; r < k; ++r) {
+    z0 = z0 + lane_value(e, r);
+    z1 = z1 + lane_value(e, 16 + r);
+    z2 = z2 + lane_value(e, 32 + r);
+    z3 = z3 + lane_value(e, 48 + r);
+  }
+  const float z = qr < 2 ? (qr == 0 ? z0 : z1) : (qr == 2 ? z2 : z3);
+  return ql < k ? e / z : 0.0f;
+}
+
+// Raw logits of token quad p: lane ql of row qr holds experts ql, ql + 16, ... of token
+// 4p + qr (0 beyond the batch or beyond N).
+template <int Q4>
+__device__ __forceinline__ void load_quad(const RouteArgs& a, int p, int ql, int qr,
+                                          float (&raw)[Q4]) {
+  const int i = 4 * p + qr;
+  const size_t row = (size_t)i * a.N;
+#pragma unroll
+  for (int q = 0; q < Q4; ++q) {
+    const int j = ql + 16 * q;
+    raw[q] = (i < a.T && j < a.N) ? a.logits[row + j] : 0.0f;
+  }
 }
 
 // Raw logits of token pair p: lane sl of half h holds experts sl, sl + 32, ... of token
@@ -409,19 +505,34 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   // holding tokens 2p and 2p + 1.  Measured (selection us, one token per wave -> halves):
   // DeepSeek T=32 25.8 -> 25.0, Qwen T=64 34.4 -> 30.7, speculative T=64 40.0 -> 37.5; with
   // at most one token per wave (T <= 16) the half-wave rounds only add: T=8 18.0 -> 19.5.
+  // Four tokens per wave (one per 16-lane row) where a token's experts fit 8 per lane, its
+  // ranks fit in a row and the batch gives a wave more than two tokens, with every quad's
+  // remaining keys kept in registers (token quads p = wave, wave + 16, ...).
   constexpr bool kHalves = Q <= 4;
   constexpr int Q2 = 2 * Q;
   constexpr int kCacheP = Q2 <= 4 ? 4 : (Q2 <= 8 ? 2 : 1);   // pairs per wave in registers
-  const bool halves = kHalves && !dense && T > kWaves;
+  constexpr bool kQuads = Q <= 2;
+  constexpr int Q4 = 4 * Q;
+  constexpr int kCacheQ = Q4 <= 4 ? 4 : 2;                    // quads per wave in registers
+  const int n_quads = (T + 3) >> 2;
+  const bool quads = kQuads && !dense && k <= 16 && T > 2 * kWaves &&
+                     n_quads <= kCacheQ * kWaves;
+  const bool halves = kHalves && !dense && T > kWaves && !quads;
   const int hh = lane >> 5, sl = lane & 31;
+  const int qr = lane >> 4, ql = lane & 15;
   const int n_pairs = (T + 1) >> 1;
   const bool cached_p = n_pairs <= kCacheP * kWaves;
   uint32_t kc[kCache][Q];
   uint32_t kcp[kHalves ? kCacheP : 1][kHalves ? Q2 : 1];
+  uint32_t kcq[kQuads ? kCacheQ : 1][kQuads ? Q4 : 1];
   float raw_next[Q];
   float rawp_next[kHalves ? Q2 : 1];
+  float rawq_next[kQuads ? Q4 : 1];
   // the wave's first logits row is on its way while the workgroup clears its tables
-  if (halves) {
+  if (quads) {
+    if constexpr (kQuads)
+      if (wave < n_quads) load_quad<Q4>(a, wave, ql, qr, rawq_next);
+  } else if (halves) {
     if constexpr (kHalves)
       if (wave < n_pairs) load_pair<Q2>(a, wave, sl, hh, rawp_next);
   } else if (wave < T) {
@@ -540,7 +651,36 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
       }
     }
   };
-  if (halves) {
+  // Token quad p (rows): the plain top-k of four tokens, as plain_topk.
+  auto plain_topk_quad = [&](int p, uint32_t (&left)[kQuads ? Q4 : 1]) {
+    if constexpr (kQuads) {
+      float raw[Q4];
+#pragma unroll
+      for (int q = 0; q < Q4; ++q) raw[q] = rawq_next[q];
+      if (p + kWaves < n_quads) load_quad<Q4>(a, p + kWaves, ql, qr, rawq_next);
+      const int i = 4 * p + qr;
+      const bool valid = i < T;
+#pragma unroll
+      for (int q = 0; q < Q4; ++q)
+        left[q] = (valid && ql + 16 * q < N) ? ord(raw[q] + 0.0f) : 0u;
+      float my_h;
+      int my_j;
+      row_topk<Q4>(left, 0, k, ql, qr, my_h, my_j);
+      const float g = row_gate(my_h, ql, qr, k);
+      if (valid && ql < k) {
+        s_ent[i * k + ql] = (uint16_t)(my_j < 0 ? kNoEntry : (uint32_t)((ql << 10) | my_j));
+        s_g[i * k + ql] = g;
+        s_vh[i * k + ql] = my_h;
+      }
+    }
+  };
+  if (quads) {
+    if constexpr (kQuads) {
+#pragma unroll
+      for (int it = 0; it < kCacheQ; ++it)
+        if (wave + it * kWaves < n_quads) plain_topk_quad(wave + it * kWaves, kcq[it]);
+    }
+  } else if (halves) {
     if constexpr (kHalves) {
       if (cached_p) {
 #pragma unroll
@@ -926,7 +1066,49 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
       }
     }
   };
-  if (halves) {
+  // Token quad p (rows): as refine, each row with its own token and seeds.
+  auto refine_quad = [&](int p, uint32_t (&key)[kQuads ? Q4 : 1]) {
+    if constexpr (kQuads) {
+      const int i = 4 * p + qr;
+      const bool valid = i < T;
+      const uint32_t vent = (valid && ql < k) ? (uint32_t)s_ent[i * k + ql] : kNoEntry;
+      const int vid = vent == kNoEntry ? -1 : (int)(vent & 1023u);
+#pragma unroll
+      for (int q = 0; q < Q4; ++q) {
+        const int jq = ql + 16 * q;
+        if (jq >= N || !s_sel[jq]) key[q] = 0;
+      }
+      const bool keep = vid >= 0 && s_sel[vid];
+      const uint64_t kept = __ballot(keep);
+      const uint32_t kq = (uint32_t)(kept >> (16 * qr)) & 0xFFFFu;
+      const int m = __popc(kq);
+      if (keep) {
+        const int dst = __popc(kq & ((1u << ql) - 1u));
+        s_seed[wave][qr * 16 + dst] = (uint32_t)vid;
+        s_seed_h[wave][qr * 16 + dst] = s_vh[i * k + ql];
+      }
+      float my_h = -INFINITY;
+      int my_j = -1;
+      if (ql < m) {
+        my_j = (int)s_seed[wave][qr * 16 + ql];
+        my_h = s_seed_h[wave][qr * 16 + ql];
+      }
+      row_topk<Q4>(key, m, k, ql, qr, my_h, my_j);
+      const float g = row_gate(my_h, ql, qr, k);
+      if (valid && ql < k) {
+        a.ids[i * k + ql] = my_j;
+        a.w[i * k + ql] = g;
+        s_ent[i * k + ql] = (uint16_t)(my_j < 0 ? kNoEntry : (uint32_t)((ql << 10) | my_j));
+      }
+    }
+  };
+  if (quads) {
+    if constexpr (kQuads) {
+#pragma unroll
+      for (int it = 0; it < kCacheQ; ++it)
+        if (wave + it * kWaves < n_quads) refine_quad(wave + it * kWaves, kcq[it]);
+    }
+  } else if (halves) {
     if constexpr (kHalves) {
       if (cached_p) {
 #pragma unroll

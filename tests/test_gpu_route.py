@@ -73,6 +73,29 @@ def test_route_adversarial_ties_and_signed_zero():
     _case(h, 4, 0, 6, "extra", label="underflow")
 
 
+def test_route_ties_four_tokens_per_wave():
+    """Batches of 33-128 tokens over at most 128 experts rank four tokens per wave (one per
+    16-lane row), with up to 16 ranks a row: quarter-step ties, signed zeros, rows with fewer
+    keys than k, a batch just past the register cache (129 tokens), bit-exact parity."""
+    rng = np.random.default_rng(7)
+    shapes = [(33, 16, 4), (40, 64, 8), (64, 128, 8), (100, 50, 16), (128, 128, 12),
+              (64, 8, 8), (48, 100, 9), (129, 128, 8), (96, 12, 16)]
+    for it, (T, N, k) in enumerate(shapes):
+        h = (np.round(rng.standard_normal((T, N)) * 3) / 4).astype(F32)
+        h[rng.random(h.shape) < 0.15] = F32(-0.0)
+        h[rng.random(h.shape) < 0.15] = F32(0.0)
+        k = min(k, N)
+        M = int(rng.integers(k, N + 1))
+        _case(h, k, int(rng.integers(0, k + 1)), M, "total", label=f"rows{it}")
+        _case(h, k, int(rng.integers(0, k + 1)), int(rng.integers(0, 6)), "extra",
+              label=f"rows{it}")
+    c = W.CONFIGS["qwen"]
+    for seed in range(4):
+        h, _ = W.make_logits(c, seed)
+        for M in (8, 32, 64):
+            _case(h, c["k"], 1, M, "total", label=f"qwen/s{seed}")
+
+
 def test_route_score_sum_order_decides_the_set():
     """The case where the ascending token order of the score sums decides which of two
     experts takes the last slot (the oracle's pin derives it by hand): bit-exact parity."""
