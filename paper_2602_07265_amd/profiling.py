@@ -6,8 +6,9 @@
         python -m paper_2602_07265_amd.profiling
 
 Runs the DeepSeek-R1-shaped layer (N=256, k=8, d=7168, f=2048, T=32 tokens, total budget
-48, warm-up 1; seeded domain-centroid logits; --weights bf16, fp8 or mxfp4) for --calls
-calls over rotating batches, then
+48, warm-up 1; seeded domain-centroid logits; --weights bf16, fp8 or mxfp4; --workload and
+--budget for another flat workload of workloads.CONFIGS) for --calls calls over rotating
+batches, then
 a plain device-to-device copy of --copy-mib MiB (torch's copy kernel) --copies times.  The
 copy reads and writes a known number of bytes, so it calibrates what the counters report
 per byte.  Prints, per batch, the active experts and the algorithmic bytes of one gate/up
@@ -71,6 +72,7 @@ def main():
     ap.add_argument("--copies", type=int, default=4)
     ap.add_argument("--budget", type=int, default=48)
     ap.add_argument("--weights", choices=("bf16", "fp8", "mxfp4"), default="bf16")
+    ap.add_argument("--workload", default="ds_t32", help="a flat workload of workloads.CONFIGS")
     args = ap.parse_args()
 
     import torch
@@ -79,7 +81,7 @@ def main():
     from paper_2602_07265_amd import xshare as X
 
     dev = "cuda:0"
-    c = W.CONFIGS["ds_t32"]
+    c = W.CONFIGS[args.workload]
     T, N, k, d, f, k0, M = c["T"], c["N"], c["k"], c["d"], c["f"], c["k0"], args.budget
     if args.weights == "fp8":
         wset = W.expert_weights_fp8(N, d, f, 0, dev)
@@ -90,7 +92,7 @@ def main():
     else:
         wset = W.expert_weights(N, d, f, 0, dev)
         wb, sb = 2.0, 0.0
-    logits = [torch.from_numpy(W.logits_domains(T, N, c["Q"], s)).to(dev) for s in range(args.batches)]
+    logits = [torch.from_numpy(W.make_logits(c, s)[0]).to(dev) for s in range(args.batches)]
     xs = [W.activations(T, d, s, dev) for s in range(args.batches)]
     p = X.params(N, k, k0, M)
     ws = torch.empty(X.moe_workspace_bytes(T, d, f, p), dtype=torch.uint8, device=dev)
@@ -107,16 +109,17 @@ def main():
         # one matrix of each active expert: W1 or W3 ([f, d]: f rows), W2 ([d, f]: d rows)
         gu_w = n * (f * d * wb + (f * 4 if sb is None else f * d * sb))
         dn_w = n * (f * d * wb + (d * 4 if sb is None else f * d * sb))
+        rows = T * k   # routed rows: x read once, H written (hi and lo) and read, Y written
         per_call.append({"call": s, "n_active": n,
-                         "gate_up_bytes": round(2 * gu_w + T * d * 2 + T * k * f * 4),
-                         "down_bytes": round(dn_w + T * k * f * 4 + T * k * d * 4)})
+                         "gate_up_bytes": round(2 * gu_w + T * d * 2 + rows * f * 4),
+                         "down_bytes": round(dn_w + rows * f * 4 + rows * d * 4)})
     nbytes = args.copy_mib << 20
     src = torch.empty(nbytes, dtype=torch.uint8, device=dev)
     dst = torch.empty_like(src)
     for _ in range(args.copies):
         dst.copy_(src)
     torch.cuda.synchronize()
-    print(json.dumps({"workload": f"ds_t32 M={M} {args.weights}", "copy_bytes": nbytes,
+    print(json.dumps({"workload": f"{args.workload} M={M} {args.weights}", "copy_bytes": nbytes,
                       "calls": per_call}))
 
 
