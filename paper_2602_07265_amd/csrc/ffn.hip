@@ -1399,6 +1399,31 @@ void launch_gu_fmt(const FfnArgs& a, int K, int u2, int u1, bool split, dim3 gri
   else
     launch_gu<1, kW>(a, split, two, grid, block, stream);
 }
+// Blocks of the down instance (unroll u) that the GPU runs at once (cached per instance).
+template <int U, int kW, int NM, int TL>
+int down_resident_u() {
+  static std::atomic<int> cached{0};
+  int r = cached.load(std::memory_order_relaxed);
+  if (r == 0) {
+    int per_cu = 0, dev = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, down_kernel<U, kW, NM, TL>, kBlock,
+                                                     0) != hipSuccess ||
+        hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return 0;
+    r = per_cu * cus;
+    cached.store(r, std::memory_order_relaxed);
+  }
+  return r;
+}
+template <int kW, int NM, int TL = XS_DOWN_TL>
+int down_resident(int u) {
+  if (u == 8) return down_resident_u<8, kW, NM, TL>();
+  if (u >= 4) return down_resident_u<4, kW, NM, TL>();
+  if (u == 2) return down_resident_u<2, kW, NM, TL>();
+  return down_resident_u<1, kW, NM, TL>();
+}
+
 template <int kW, int NM, int TL = XS_DOWN_TL>
 void launch_down_fmt(const FfnArgs& a, int u, hipStream_t stream) {
   const int cols = kWaves * kCols * NM;
@@ -1461,11 +1486,21 @@ hipError_t launch_down(const FfnArgs& a, hipStream_t stream) {
     return hipGetLastError();
   }
   // bf16 and FP8: twice the rows per wave (one token load feeding twice the weight tiles)
-  // pays when experts hold several tokens each and the grid stays large
+  // pays when experts hold several tokens each and the grid stays large, or fills whole
+  // rounds of the blocks the GPU runs at once: the Qwen-MoE shape at M=64 (512 wide blocks,
+  // one round) ran down 53.6 -> 45.8 us wide, while 672 wide blocks (DeepSeek T=32 M=24,
+  // 1.3 rounds) ran 137 -> 158 us.
   const int nm = a.wfmt == kFp8 ? XS_Q8_DOWN_NM : XS_DOWN_NM;
-  const bool wide = est > 0 && (long)a.T * a.k >= XS_DN_WIDE_TOKENS * est &&
-                    (long)((a.d + kWaves * kCols * 2 * nm - 1) / (kWaves * kCols * 2 * nm)) *
-                            est * a.splits >= XS_DN_WIDE_MIN_BLOCKS;
+  const long wide_blocks =
+      (long)((a.d + kWaves * kCols * 2 * nm - 1) / (kWaves * kCols * 2 * nm)) * est * a.splits;
+  bool wide = est > 0 && (long)a.T * a.k >= XS_DN_WIDE_TOKENS * est &&
+              wide_blocks >= XS_DN_WIDE_MIN_BLOCKS;
+  if (!wide && est > 0 && (long)a.T * a.k >= XS_DN_WIDE_TOKENS * est) {
+    const int r = a.wfmt == kFp8
+                      ? down_resident<kFp8, 2 * XS_Q8_DOWN_NM>(unroll_for(K, XS_Q8_DOWN_U))
+                      : down_resident<kBf16, 2 * XS_DOWN_NM>(unroll_for(K, XS_DOWN_U));
+    wide = r > 0 && wide_blocks >= r && wide_blocks % r == 0;
+  }
   if (a.wfmt == kFp8) {
     if (wide)
       launch_down_fmt<kFp8, 2 * XS_Q8_DOWN_NM>(a, unroll_for(K, XS_Q8_DOWN_U), stream);
