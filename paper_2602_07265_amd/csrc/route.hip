@@ -103,8 +103,7 @@ __device__ __forceinline__ float lane_value(float v, int lane) {
 // One round of a wave-wide selection over keys held Q per lane (expert lane + 64 q):
 // returns the expert with the largest key, lowest index on equal keys (key 0 = not
 // available), removes it from its lane, and reports its key; -1 if nothing is left.
-// Usually one lane holds the maximum and a ballot finds it; equal maxima in several
-// lanes take a second (min-index) reduction.
+// A second (min-index) reduction over the holders of the largest key finds the expert.
 template <int Q>
 __device__ __forceinline__ int wave_pick(uint32_t (&key)[Q], int lane, uint32_t& kbest) {
   uint32_t bk = 0;
@@ -117,12 +116,8 @@ __device__ __forceinline__ int wave_pick(uint32_t (&key)[Q], int lane, uint32_t&
   }
   kbest = wave_max(bk);
   if (kbest == 0) return -1;
-  const uint64_t holders = __ballot(bk == kbest);
-  uint32_t jmin;
-  if (__popcll(holders) == 1)
-    jmin = (uint32_t)__builtin_amdgcn_readlane((int)bj, __ffsll((long long)holders) - 1);
-  else
-    jmin = wave_min(bk == kbest ? bj : 0xFFFFFFFFu);
+  // the lowest expert index among the holders of the largest key
+  const uint32_t jmin = wave_min(bk == kbest ? bj : 0xFFFFFFFFu);
   // the holder lane drops the key: selects, not a branch around the holder lane
   const bool mine = (int)(jmin & 63) == lane;
   const int qsel = (int)(jmin >> 6);
