@@ -781,6 +781,27 @@ static_assert(XS_DOWN_XCD_SLOTS >= 8, "at least one slot per XCD");
 #ifndef XS_DOWN_TL
 #define XS_DOWN_TL 4                 // 8-token (hi + lo) tiles per pass of the down GEMM
 #endif
+// Seven 16-row W2 tiles per wave (448 output rows per block, one block per CU) for the bf16
+// down GEMM when that grid is a whole number of rounds: at d = 7168 the DeepSeek layer's 48
+// slots give 768 blocks, three rounds, where 64-row waves leave 2.6 rounds of 512.  With
+// U = 4 a wave keeps 28 KB of weights in flight.  Same-box A/B, down us (64-row waves ->
+// seven tiles): DeepSeek T=32 M=48 256 -> 245, iid logits 257 -> 245, speculative 347 ->
+// 333; M=96 (six rounds against 5.25) 464 -> 464; at U = 2 M=48 ran 260, and on grids
+// that leave a partial round the seven tiles lose (M=24 138 -> 148, the layer with its
+// shared expert 262 -> 295).  FP8 weights gained nothing (DeepSeek 137 -> 136, speculative
+// 188 -> 191) and keep their waves.
+#ifndef XS_DOWN_NM7
+#define XS_DOWN_NM7 1
+#endif
+#ifndef XS_DOWN_NM7_U
+#define XS_DOWN_NM7_U 4
+#endif
+#ifndef XS_Q8_DOWN_NM7
+#define XS_Q8_DOWN_NM7 0
+#endif
+#ifndef XS_Q8_DOWN_NM7_U
+#define XS_Q8_DOWN_NM7_U 4
+#endif
 #ifndef XS_DOWN_WAVES_PER_EU
 #define XS_DOWN_WAVES_PER_EU 2       // waves per SIMD of the staged down instances (3: spills)
 #endif
@@ -981,7 +1002,8 @@ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
 // 64-row bf16 and FP8 instances (FP8 DeepSeek T=32 down 166 -> 138 us with the hint).
 // TL: token tiles per pass, 8 tokens each (hi and lo rows).
 template <int U, int kW, int NM, int TL = XS_DOWN_TL>
-__global__ __attribute__((amdgpu_waves_per_eu(stage_down(kW) ? XS_DOWN_WAVES_PER_EU : 1)))
+__global__ __attribute__((amdgpu_waves_per_eu(stage_down(kW) && NM <= 4 ? XS_DOWN_WAVES_PER_EU
+                                                                          : 1)))
 __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
   // (bx, slot): this block's column block and expert slot.  In grids of at least
   // XS_DOWN_XCD_SLOTS slots, with `live` slots holding work (shared, then active), all
@@ -1501,6 +1523,21 @@ hipError_t launch_down(const FfnArgs& a, hipStream_t stream) {
                       : down_resident<kBf16, 2 * XS_DOWN_NM>(unroll_for(K, XS_DOWN_U));
     wide = r > 0 && wide_blocks >= r && wide_blocks % r == 0;
   }
+#if XS_DOWN_NM7
+  // seven tiles per wave where that grid fills whole rounds (see XS_DOWN_NM7)
+  if (est > 0 && (long)a.T * a.k >= XS_DN_WIDE_TOKENS * est) {
+    const long b7 = (long)((a.d + kWaves * kCols * 7 - 1) / (kWaves * kCols * 7)) * est * a.splits;
+    const int u7 = unroll_for(K, a.wfmt == kFp8 ? XS_Q8_DOWN_NM7_U : XS_DOWN_NM7_U);
+    const int r7 = a.wfmt == kFp8 ? down_resident<kFp8, 7>(u7) : down_resident<kBf16, 7>(u7);
+    if ((a.wfmt == kBf16 || XS_Q8_DOWN_NM7) && r7 > 0 && b7 >= r7 && b7 % r7 == 0) {
+      if (a.wfmt == kFp8)
+        launch_down_fmt<kFp8, 7>(a, u7, stream);
+      else
+        launch_down_fmt<kBf16, 7>(a, u7, stream);
+      return hipGetLastError();
+    }
+  }
+#endif
   if (a.wfmt == kFp8) {
     if (wide)
       launch_down_fmt<kFp8, 2 * XS_Q8_DOWN_NM>(a, unroll_for(K, XS_Q8_DOWN_U), stream);
