@@ -788,20 +788,15 @@ static_assert(XS_DOWN_XCD_SLOTS >= 8, "at least one slot per XCD");
 // seven tiles): DeepSeek T=32 M=48 256 -> 245, iid logits 257 -> 245, speculative 347 ->
 // 333; M=96 (six rounds against 5.25) 464 -> 464; at U = 2 M=48 ran 260, and on grids
 // that leave a partial round the seven tiles lose (M=24 138 -> 148, the layer with its
-// shared expert 262 -> 295).  FP8 weights gained nothing (DeepSeek 137 -> 136, speculative
-// 188 -> 191) and keep their waves.
+// shared expert 262 -> 295).  FP8 gained nothing (DeepSeek 137 -> 136, speculative 188 ->
+// 191) and MXFP4 lost (81 -> 85 us), so they keep their waves.
 #ifndef XS_DOWN_NM7
 #define XS_DOWN_NM7 1
 #endif
 #ifndef XS_DOWN_NM7_U
 #define XS_DOWN_NM7_U 4
 #endif
-#ifndef XS_Q8_DOWN_NM7
-#define XS_Q8_DOWN_NM7 0
-#endif
-#ifndef XS_Q8_DOWN_NM7_U
-#define XS_Q8_DOWN_NM7_U 4
-#endif
+
 #ifndef XS_DOWN_WAVES_PER_EU
 #define XS_DOWN_WAVES_PER_EU 2       // waves per SIMD of the staged down instances (3: spills)
 #endif
@@ -1524,16 +1519,13 @@ hipError_t launch_down(const FfnArgs& a, hipStream_t stream) {
     wide = r > 0 && wide_blocks >= r && wide_blocks % r == 0;
   }
 #if XS_DOWN_NM7
-  // seven tiles per wave where that grid fills whole rounds (see XS_DOWN_NM7)
-  if (est > 0 && (long)a.T * a.k >= XS_DN_WIDE_TOKENS * est) {
+  // bf16: seven tiles per wave where that grid fills whole rounds (see XS_DOWN_NM7)
+  if (a.wfmt == kBf16 && est > 0 && (long)a.T * a.k >= XS_DN_WIDE_TOKENS * est) {
     const long b7 = (long)((a.d + kWaves * kCols * 7 - 1) / (kWaves * kCols * 7)) * est * a.splits;
-    const int u7 = unroll_for(K, a.wfmt == kFp8 ? XS_Q8_DOWN_NM7_U : XS_DOWN_NM7_U);
-    const int r7 = a.wfmt == kFp8 ? down_resident<kFp8, 7>(u7) : down_resident<kBf16, 7>(u7);
-    if ((a.wfmt == kBf16 || XS_Q8_DOWN_NM7) && r7 > 0 && b7 >= r7 && b7 % r7 == 0) {
-      if (a.wfmt == kFp8)
-        launch_down_fmt<kFp8, 7>(a, u7, stream);
-      else
-        launch_down_fmt<kBf16, 7>(a, u7, stream);
+    const int u7 = unroll_for(K, XS_DOWN_NM7_U);
+    const int r7 = down_resident<kBf16, 7>(u7);
+    if (r7 > 0 && b7 >= r7 && b7 % r7 == 0) {
+      launch_down_fmt<kBf16, 7>(a, u7, stream);
       return hipGetLastError();
     }
   }
