@@ -796,6 +796,16 @@ static_assert(XS_DOWN_XCD_SLOTS >= 8, "at least one slot per XCD");
 #ifndef XS_DOWN_NM7_U
 #define XS_DOWN_NM7_U 4
 #endif
+// The seven-tile bf16 down launch as a persistent grid (down_seq_kernel).  Same-box A/B,
+// down us (grid of rounds -> persistent): DeepSeek T=32 M=48 246.0 / 245.8 -> 243.5 / 242.5,
+// speculative 333.2 / 334.9 -> 331.9 / 333.1.  With 2 waves per SIMD (FP8 and bf16 64- and
+// 32-row waves) it lost: FP8 DeepSeek T=32 137.4 -> 147.0, bf16 T=8 M=24 130 -> 133.5 (a
+// CU's second block already overlaps the first one's start there), so only this launch
+// takes it.
+#ifndef XS_DOWN_SEQ
+#define XS_DOWN_SEQ 1
+#endif
+
 
 #ifndef XS_DOWN_WAVES_PER_EU
 #define XS_DOWN_WAVES_PER_EU 2       // waves per SIMD of the staged down instances (3: spills)
@@ -1122,6 +1132,249 @@ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
         }
       }
     }
+  }
+}
+
+// ---- Persistent down GEMM, for launches of whole rounds with one block per CU (the
+// seven-tile bf16 waves).  Such a launch runs its rounds in lock step: the blocks of a round
+// stream the same bytes, so they end together, and every CU then spends the next block's
+// start (dispatch, its slot record, then the first weight loads) with no reads in flight, at
+// the same moment.  Here the grid holds one block per CU and each block walks a fixed list
+// of work units: units b, b + G, b + 2G, ... (G blocks), a unit being one column block of
+// one expert slot, taken in passes of up to 8 * TL token rows.  The block reads its units'
+// slot records once, into LDS; the first step's loads of its next pass are issued in the
+// last step of the current one, so a CU's weight stream does not drain between units.  The
+// MFMAs always cover TL token tiles (one code path for every pass; rows past the pass repeat
+// its last row and are not stored).  Units map to (slot, column block) as in down_kernel's
+// grid, so with G a multiple of 8 every unit of a slot below 8 * (live / 8) runs on the XCD
+// of that slot.  Blocks share nothing: no counters, no flags, no block waits for another.
+constexpr int kSeqUnits = 32;     // units per block of a persistent launch, at most
+
+__device__ __forceinline__ void down_unit(int L, int CB, int live, bool xcd, int& slot, int& bx) {
+  if (xcd && L < CB * (live & ~7)) {
+    const int s = L >> 3;
+    slot = (L & 7) + 8 * (s / CB);
+    bx = s % CB;
+  } else {
+    slot = L / CB;
+    bx = L % CB;
+  }
+}
+
+// Lane state of one pass that its loads need: weight pointers, token pieces and the pass's
+// first reduction step.
+template <int kW, int U, int NM, int NLM>
+struct DnLoads {
+  typename WTile<kW, U>::Ptr wp[NM];
+  const uint16_t* src[NLM];
+  int wofs[NLM];
+  int kb;
+};
+
+// A pass: unit record {expert | shared << 30, first permuted row, rows, column block} and
+// the pass's first row.
+struct DnPass {
+  int4 rec;
+  int c0;
+  __device__ int e() const { return rec.x & 0x3FFFFFFF; }
+  __device__ bool shared() const { return (rec.x >> 30) & 1; }
+};
+
+template <int kW, int U, int NM, int NLM, int TL>
+__device__ __forceinline__ void dn_loads(const FfnArgs& a, const DnPass& ps, int wave, int n,
+                                         size_t kl, int nsteps, int rot,
+                                         DnLoads<kW, U, NM, NLM>& L) {
+  using S = Stage<U, true>;
+  const int d = a.d, f = a.f;
+  const int bx = ps.rec.w, p0 = ps.rec.y, te = ps.rec.z;
+  const int n0 = (bx * kWaves + wave) * kCols * NM;
+  const size_t ebase = (size_t)ps.e() * d * f;
+#pragma unroll
+  for (int m = 0; m < NM; ++m) {
+    const size_t wrow = (size_t)(min(n0 + 16 * m, d - 16) + n) * f + kl;
+    if constexpr (kW == kBf16) L.wp[m].w = (ps.shared() ? a.sw2 : a.w2) + ebase + wrow;
+    else L.wp[m].w = a.q2 + ebase + wrow;
+  }
+  const int R = max(1, min(8 * TL, te - ps.c0));
+#pragma unroll
+  for (int i = 0; i < NLM; ++i) {
+    const int q = min((int)threadIdx.x + i * kBlock, R * S::P - 1);
+    const int row = q / S::P, piece = q % S::P;
+    L.src[i] = a.h + (size_t)(p0 + ps.c0 + row) * 2 * f + piece * 8;
+    L.wofs[i] = row * S::LS + piece * 8;
+  }
+  L.kb = ((bx * rot) % nsteps) * S::KB;
+}
+
+template <int U, int kW, int NM, int TL>
+__global__ __attribute__((amdgpu_waves_per_eu(NM <= 4 ? XS_DOWN_WAVES_PER_EU : 1)))
+__launch_bounds__(kBlock) void down_seq_kernel(FfnArgs a) {
+  using S = Stage<U, true>;
+  using WT = WTile<kW, U>;
+  static_assert(!WT::kGroupScales && kW != kMx4, "bf16 and FP8 weights");
+  constexpr int KB = S::KB;
+  constexpr int NLM = (TL * S::TR * S::P + kBlock - 1) / kBlock;
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int n = lane & 15, g = lane >> 4;
+  const int d = a.d, f = a.f;
+  const int CB = (d + kWaves * kCols * NM - 1) / (kWaves * kCols * NM);
+  const int live = a.n_shared + a.counters[kCntActive];
+  const int units = live * CB;
+  const int G = (int)gridDim.x;
+  const int nu = (int)blockIdx.x < units ? min((units - (int)blockIdx.x + G - 1) / G, kSeqUnits) : 0;
+  if (nu == 0) return;   // uniform: the whole block leaves before any barrier
+  const bool xcd = a.max_active + a.n_shared >= XS_DOWN_XCD_SLOTS;
+  const int nsteps = f / KB;                    // unsplit: the launch takes one K part
+  const int rot = kW == kBf16 ? XS_DOWN_ROT : XS_Q8_DOWN_ROT;
+  const size_t kl = (size_t)(kW == kBf16 ? klane<U>(g) : g * 8 * U);
+
+  // the block's unit records, one thread each
+  __shared__ int4 s_rec[kSeqUnits];
+  if (tid < nu) {
+    int slot, bx;
+    down_unit((int)blockIdx.x + tid * G, CB, live, xcd, slot, bx);
+    SlotWork sw;
+    const bool ok = slot_work(a, slot, sw);   // slot < live: always work
+    s_rec[tid] = ok ? make_int4(sw.e | (sw.shared ? 1 << 30 : 0), sw.p0, sw.te, bx)
+                    : make_int4(0, 0, 0, bx);
+  }
+  __syncthreads();
+
+  int j = 0;                                    // current unit
+  DnPass cur{s_rec[0], 0};
+  __shared__ __align__(16) uint16_t lds[S::kElems];
+  DnLoads<kW, U, NM, NLM> L;
+  dn_loads<kW, U, NM, NLM, TL>(a, cur, wave, n, kl, nsteps, rot, L);
+
+  u32x4 v[NLM];
+  typename WT::Regs b[NM];
+#pragma unroll
+  for (int i = 0; i < NLM; ++i) v[i] = *reinterpret_cast<const u32x4*>(L.src[i] + S::AS * L.kb);
+#pragma unroll
+  for (int m = 0; m < NM; ++m) b[m] = WT::load(L.wp[m], L.kb);
+#pragma unroll
+  for (int i = 0; i < NLM; ++i) *reinterpret_cast<u32x4*>(lds + L.wofs[i]) = v[i];
+  __syncthreads();
+
+  floatx4 acc[NM][TL];
+#pragma unroll
+  for (int m = 0; m < NM; ++m)
+#pragma unroll
+    for (int rt = 0; rt < TL; ++rt) acc[m][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  int buf = 0;
+  // MFMAs of one step from LDS buffer `buf`: all TL tiles (rows past the pass repeat its last
+  // row; their sums are not stored), so every pass runs the same code
+  auto mfma_step = [&](const int (&rofs)[TL]) {
+    const uint16_t* const cl = lds + buf * kStageRows * S::LS;
+#pragma unroll
+    for (int uu = 0; uu < U; ++uu) {
+      const int ka = S::AS * WT::koff(g, uu);
+      bf16x8 xa[TL];
+#pragma unroll
+      for (int rt = 0; rt < TL; ++rt) xa[rt] = *reinterpret_cast<const bf16x8*>(cl + rofs[rt] + ka);
+#pragma unroll
+      for (int rt = 0; rt < TL; ++rt)
+#pragma unroll
+        for (int m = 0; m < NM; ++m) acc[m][rt] = mfma(xa[rt], WT::operand(b[m], uu), acc[m][rt]);
+    }
+  };
+  while (true) {
+    const int te = cur.rec.z, p0 = cur.rec.y;
+    const int R = max(1, min(8 * TL, te - cur.c0));
+    const int nt = (R + 7) >> 3;
+    const int n0 = (cur.rec.w * kWaves + wave) * kCols * NM;
+    int rofs[TL];
+#pragma unroll
+    for (int rt = 0; rt < TL; ++rt) rofs[rt] = min(8 * rt + (n & 7), R - 1) * S::LS + (n & 8);
+    // every step but the last: loads of the next step, MFMAs of this one
+    for (int ks = 0; ks < nsteps - 1; ++ks) {
+      int kn = L.kb + KB;
+      if (kn >= f) kn -= f;
+#pragma unroll
+      for (int i = 0; i < NLM; ++i) v[i] = *reinterpret_cast<const u32x4*>(L.src[i] + S::AS * kn);
+      typename WT::Regs nb[NM];
+#pragma unroll
+      for (int m = 0; m < NM; ++m) nb[m] = WT::load(L.wp[m], kn);
+      mfma_step(rofs);
+      uint16_t* const nl = lds + (buf ^ 1) * kStageRows * S::LS;
+#pragma unroll
+      for (int i = 0; i < NLM; ++i) *reinterpret_cast<u32x4*>(nl + L.wofs[i]) = v[i];
+#pragma unroll
+      for (int m = 0; m < NM; ++m) b[m] = nb[m];
+      __syncthreads();
+      buf ^= 1;
+      L.kb = kn;
+    }
+    // the last step: the loads of the block's next pass (the unit's next rows, else its next
+    // unit; after the block's last pass the same loads again), then this step's MFMAs and the
+    // pass's epilogue
+    DnPass nxt = cur;
+    int jn = j;
+    bool has_nxt = true;
+    if (cur.c0 + 8 * TL < te) {
+      nxt.c0 += 8 * TL;
+    } else {
+      jn = j + 1;
+      has_nxt = jn < nu;
+      if (has_nxt) nxt = DnPass{s_rec[jn], 0};
+    }
+    DnLoads<kW, U, NM, NLM> Ln = L;
+    if (has_nxt) dn_loads<kW, U, NM, NLM, TL>(a, nxt, wave, n, kl, nsteps, rot, Ln);
+    int yrow[TL][4];
+#pragma unroll
+    for (int rt = 0; rt < TL; ++rt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t = max(0, min(cur.c0 + rt * 8 + 4 * (g & 1) + i, te - 1));
+        yrow[rt][i] = cur.shared() ? p0 + t : a.perm[p0 + t];
+      }
+    float sc[NM];
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+      sc[m] = kW == kFp8 ? a.s2[(size_t)cur.e() * d + min(n0 + 16 * m, d - 16) + n] : 1.0f;
+#pragma unroll
+    for (int i = 0; i < NLM; ++i) v[i] = *reinterpret_cast<const u32x4*>(Ln.src[i] + S::AS * Ln.kb);
+    typename WT::Regs nb[NM];
+#pragma unroll
+    for (int m = 0; m < NM; ++m) nb[m] = WT::load(Ln.wp[m], Ln.kb);
+    mfma_step(rofs);
+    // lanes g = 0, 1 hold the hi rows of tokens 4g + i, lanes 32 above them the lo rows;
+    // routed rows go to their (token, slot) row, shared rows keep their own
+#pragma unroll
+    for (int rt = 0; rt < TL; ++rt) {
+      if (rt >= nt) break;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float o[NM];
+#pragma unroll
+        for (int m = 0; m < NM; ++m)
+          o[m] = (acc[m][rt][i] + __shfl_xor(acc[m][rt][i], 32, 64)) * sc[m];
+        const int t = cur.c0 + rt * 8 + 4 * g + i;
+        if (g < 2 && t < te) {
+          float* const yr = a.yslot + (size_t)yrow[rt][i] * d;
+#pragma unroll
+          for (int m = 0; m < NM; ++m)
+            if (n0 + 16 * m < d) yr[n0 + 16 * m + n] = o[m];
+        }
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int rt = 0; rt < TL; ++rt) acc[m][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    uint16_t* const nl = lds + (buf ^ 1) * kStageRows * S::LS;
+#pragma unroll
+    for (int i = 0; i < NLM; ++i) *reinterpret_cast<u32x4*>(nl + Ln.wofs[i]) = v[i];
+#pragma unroll
+    for (int m = 0; m < NM; ++m) b[m] = nb[m];
+    __syncthreads();
+    buf ^= 1;
+    if (!has_nxt) break;
+    cur = nxt;
+    j = jn;
+    L = Ln;
   }
 }
 
@@ -1458,6 +1711,33 @@ void launch_down_fmt(const FfnArgs& a, int u, hipStream_t stream) {
     hipLaunchKernelGGL((down_kernel<1, kW, NM, TL>), grid, block, 0, stream, a);
 }
 
+// The persistent down launch (down_seq_kernel): one block per resident slot, rounded up to a
+// multiple of 8 (one XCD per slot's units) and to at least the unit bound / kSeqUnits.
+// False if the instance's residency is unknown.
+template <int U, int kW, int NM, int TL = XS_DOWN_TL>
+bool launch_down_seq(const FfnArgs& a, hipStream_t stream) {
+  static std::atomic<int> cached{0};
+  int r = cached.load(std::memory_order_relaxed);
+  if (r == 0) {
+    int per_cu = 0, dev = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, down_seq_kernel<U, kW, NM, TL>,
+                                                     kBlock, 0) != hipSuccess ||
+        hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        per_cu <= 0)
+      return false;
+    r = per_cu * cus;
+    cached.store(r, std::memory_order_relaxed);
+  }
+  const int CB = (a.d + kWaves * kCols * NM - 1) / (kWaves * kCols * NM);
+  const long max_units = (long)(a.max_active + a.n_shared) * CB;
+  long G = std::max<long>(r, (max_units + kSeqUnits - 1) / kSeqUnits);
+  G = (G + 7) & ~7L;
+  hipLaunchKernelGGL((down_seq_kernel<U, kW, NM, TL>), dim3((unsigned)G), dim3(kBlock), 0, stream,
+                     a);
+  return true;
+}
+
 int unroll_for(int K, int want) {
   for (int u = want; u > 1; u >>= 1)
     if (K % (32 * u) == 0) return u;
@@ -1525,6 +1805,10 @@ hipError_t launch_down(const FfnArgs& a, hipStream_t stream) {
     const int u7 = unroll_for(K, XS_DOWN_NM7_U);
     const int r7 = down_resident<kBf16, 7>(u7);
     if (r7 > 0 && b7 >= r7 && b7 % r7 == 0) {
+#if XS_DOWN_SEQ
+      if (a.splits == 1 && u7 == 4 && launch_down_seq<4, kBf16, 7>(a, stream))
+        return hipGetLastError();
+#endif
       launch_down_fmt<kBf16, 7>(a, u7, stream);
       return hipGetLastError();
     }
