@@ -225,8 +225,8 @@ def main():
           file=sys.stderr, flush=True)
     if fp8:
         base = W.expert_weights_fp8(N, d, f, 0, dev)
-    elif mx4:
-        base = W.expert_weights_mxfp4(N, d, f, 0, dev)
+    elif mx4:        # scales in the tiled layout of the GEMMs (once, at load time)
+        base = X.mx_tiled(W.expert_weights_mxfp4(N, d, f, 0, dev))
     else:
         base = W.expert_weights(N, d, f, 0, dev)
     wsets = [base] + [tuple(t.clone() for t in base) for _ in range(reps - 1)]

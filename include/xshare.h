@@ -307,7 +307,7 @@ xshare_status xshare_moe_forward(const uint16_t* x, const float* logits, int32_t
 enum {
   XSHARE_WEIGHTS_BF16 = 0,  /* w1, w3 [N, f, d] and w2 [N, d, f] bf16; no scales             */
   XSHARE_WEIGHTS_FP8 = 1,   /* as xshare_moe_forward_fp8: E4M3FN codes, fp32 row scales      */
-  XSHARE_WEIGHTS_MXFP4 = 2  /* as xshare_moe_forward_mxfp4: E2M1 codes, E8M0 block scales    */
+  XSHARE_WEIGHTS_MXFP4 = 2  /* as xshare_moe_forward_mxfp4: E2M1 codes, tiled E8M0 scales     */
 };
 
 /*
@@ -432,6 +432,26 @@ xshare_status xshare_moe_forward_fp8(const uint16_t* x, const float* logits, int
                                      void* const* stage_events, hipStream_t stream);
 
 /*
+ * xshare_mx_scales_tile -- lays out MXFP4 block scales for the expert GEMMs (done once, when
+ * the weights are loaded; not part of a layer call).  The GEMMs read one 16-row weight tile
+ * over 256 inputs per load step: in the tiled layout that tile's scale bytes are one
+ * contiguous 128-byte piece, read once, where the row-major layout scatters them over 16
+ * rows (and the weight stream evicted those lines between steps).
+ *
+ *   scales  [n_mat, rows, k/32] uint8: E8M0 scales, one per block of 32 consecutive inputs
+ *           of a row (row-major, as the OCP MX format lists them).
+ *   tiled   [n_mat, rows/16, G, 16, 8] uint8 with G = ceil(k / 256):
+ *           tiled[m][r / 16][c / 8][r % 16][c % 8] = scales[m][r][c]; bytes past a row's
+ *           last block are 127 (scale 1) and never read.  Size:
+ *           xshare_mx_scales_tiled_bytes(n_mat, rows, k).  Caller-owned device memory.
+ *   rows a multiple of 16, k a multiple of 32 (XSHARE_EINVAL otherwise).  Asynchronous on
+ *   `stream`; `scales` and `tiled` must not overlap.
+ */
+size_t xshare_mx_scales_tiled_bytes(int32_t n_mat, int32_t rows, int32_t k);
+xshare_status xshare_mx_scales_tile(const uint8_t* scales, uint8_t* tiled, int32_t n_mat,
+                                    int32_t rows, int32_t k, hipStream_t stream);
+
+/*
  * xshare_moe_forward_mxfp4 -- xshare_moe_forward with MXFP4 routed-expert weights (OCP
  * Microscaling MXFP4: a quarter of the bytes of bf16 plus one scale byte per 32 weights;
  * the paper is silent on precision).
@@ -441,13 +461,14 @@ xshare_status xshare_moe_forward_fp8(const uint16_t* x, const float* logits, int
  *             byte along the input index: element 2c in the low nibble of byte c.  16-byte
  *             aligned.
  *   w2        [N, d, f/2] uint8, same format.
- *   w1_scale, w3_scale  [N, f, d/32] uint8; w2_scale [N, d, f/32] uint8: E8M0 scales, one per
- *             block of 32 consecutive inputs of a row, value 2^(e - 127); the weight is
- *             decode(code) * 2^(e - 127).  e = 255 (NaN) must not occur, and the decoded
- *             weights must lie in bf16's normal range (or be zero): the GPU turns each code
- *             and its scale into the exact bf16 weight before the bf16 MFMA.  16-byte
- *             aligned (XSHARE_EINVAL otherwise: the kernels read scale rows in pieces of
- *             up to 16 bytes).
+ *   w1_scale, w3_scale  E8M0 scales of W1 and W3 ([N, f, d/32] row-major) in the tiled
+ *             layout of xshare_mx_scales_tile (n_mat = N, rows = f, k = d); w2_scale those
+ *             of W2 ([N, d, f/32]: rows = d, k = f).  One scale per block of 32 consecutive
+ *             inputs of a row, value 2^(e - 127); the weight is decode(code) * 2^(e - 127).
+ *             e = 255 (NaN) must not occur, and the decoded weights must lie in bf16's
+ *             normal range (or be zero): the GPU turns each code and its scale into the
+ *             exact bf16 weight before the bf16 MFMA.  16-byte aligned (XSHARE_EINVAL
+ *             otherwise).
  *   d and f multiples of 32.  Everything else as xshare_moe_forward (workspace from
  *   xshare_moe_workspace_bytes); shared experts are not taken here.
  */

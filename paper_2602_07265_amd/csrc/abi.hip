@@ -651,6 +651,21 @@ xshare_status xshare_router_logits(const uint16_t* x, const uint16_t* w_gate, in
   return xs::launch_router(r, stream) == hipSuccess ? XSHARE_OK : XSHARE_EHIP;
 }
 
+size_t xshare_mx_scales_tiled_bytes(int32_t n_mat, int32_t rows, int32_t k) {
+  if (n_mat < 0 || rows < 0 || k < 0) return 0;
+  return xs::mx_scales_tiled_bytes(n_mat, rows, k);
+}
+
+xshare_status xshare_mx_scales_tile(const uint8_t* scales, uint8_t* tiled, int32_t n_mat,
+                                    int32_t rows, int32_t k, hipStream_t stream) {
+  if (n_mat < 0 || rows < 0 || k < 0 || rows % 16 != 0 || k % 32 != 0) return XSHARE_EINVAL;
+  if (n_mat == 0 || rows == 0 || k == 0) return XSHARE_OK;
+  if (!scales || !tiled) return XSHARE_EINVAL;
+  return xs::launch_mx_scales_tile(scales, tiled, n_mat, rows, k, stream) == hipSuccess
+             ? XSHARE_OK
+             : XSHARE_EHIP;
+}
+
 xshare_status xshare_layer_budgets(int32_t K, int32_t L, int32_t* m) {
   if (L < 1 || K < 0 || !m) return XSHARE_EINVAL;
   const int32_t base = K / L, extra = K % L;

@@ -303,27 +303,38 @@ __device__ __forceinline__ void wave_pass_q8(const uint16_t* const (&arow)[TL], 
   }
 }
 
-// The scale byte(s) of a lane's step: one block for U <= 4, two consecutive blocks (two
-// bytes, the first block's in the low byte) for U = 8, four for U = 16.
+// MXFP4 block scales in the tiled layout (xshare_mx_scales_tile): per matrix of R rows and K
+// inputs, [R / 16][G][16 rows][8 bytes] with G = ceil(K / 256) granules of 8 blocks of 32
+// inputs, so the scale bytes of one 16-row weight tile over 256 inputs are one 128-byte
+// piece, read once and whole: the byte of row r and block c sits at ((r / 16) G + c / 8) 128
+// + (r % 16) 8 + c % 8.  mx_row: where row r's bytes of its tile start (granule 0).
+__device__ __forceinline__ int mx_granules(int K) { return (K + 255) >> 8; }
+__device__ __forceinline__ const uint8_t* mx_row(const uint8_t* mat, int r, int G) {
+  return mat + (size_t)(r >> 4) * G * 128 + (r & 15) * 8;
+}
+// The scale bytes of a lane whose step starts at input k (8U inputs: one block for U <= 4,
+// two for U = 8, four for U = 16; a lane's blocks share one granule since k is a multiple of
+// 8U), from its row `row` (mx_row).
 template <int U>
-__device__ __forceinline__ uint32_t load_e8m0(const uint8_t* p) {
-  if constexpr (U == 16)   // as two 16-bit loads
-    return *reinterpret_cast<const uint16_t*>(p) |
-           ((uint32_t)*reinterpret_cast<const uint16_t*>(p + 2) << 16);
+__device__ __forceinline__ uint32_t load_mx_scales(const uint8_t* row, int k) {
+  const int c = k >> 5;
+  const uint8_t* const p = row + ((c >> 3) << 7) + (c & 7);
+  if constexpr (U >= 16)
+    return *reinterpret_cast<const uint32_t*>(p);
   else if constexpr (U == 8)
     return *reinterpret_cast<const uint16_t*>(p);
   else
     return *p;
 }
 
-// wave_pass with MXFP4 weights: per step a lane loads 4U bytes of codes (its 8U elements:
-// within one 32-element block for U <= 4, two blocks for U = 8) and their scale bytes, one
-// step ahead; the codes become bf16, scaled, just before use.  `brow[m]` points at the codes
-// of this lane's first element, `srow[m]` at the scale of its first block.
+// wave_pass with MXFP4 weights: per step a lane loads 4U bytes of codes (its 8U elements)
+// and their scale bytes, one step ahead; the codes become bf16, scaled, just before use.
+// `brow[m]` points at the codes of this lane's first element, `srow[m]` at its row's tiled
+// scales (mx_row); `kl`: this lane's first input (absolute, for the scale bytes).
 template <int U, int NM, int TL = kTiles, int AS = 1>
 __device__ __forceinline__ void wave_pass_q4(const uint16_t* const (&arow)[TL], int nt,
                                              const uint8_t* const (&brow)[NM],
-                                             const uint8_t* const (&srow)[NM], int K,
+                                             const uint8_t* const (&srow)[NM], int kl, int K,
                                              floatx4 (&acc)[NM][TL], int k_first = 0) {
   static_assert(U == 1 || U == 2 || U == 4 || U == 8, "1, 2, 4 or 8 words per lane and step");
   constexpr int KB = 32 * U;
@@ -333,7 +344,7 @@ __device__ __forceinline__ void wave_pass_q4(const uint16_t* const (&arow)[TL], 
 #pragma unroll
   for (int m = 0; m < NM; ++m) {
     b[m] = load_q4<U>(brow[m] + k_first / 2);
-    e[m] = load_e8m0<U>(srow[m] + k_first / 32);
+    e[m] = load_mx_scales<U>(srow[m], kl + k_first);
   }
   int kb = k_first;
   for (int s = 0; s < K; s += KB) {
@@ -351,13 +362,13 @@ __device__ __forceinline__ void wave_pass_q4(const uint16_t* const (&arow)[TL], 
 #pragma unroll
       for (int m = 0; m < NM; ++m) {
         nb[m] = load_q4<U>(brow[m] + kn / 2);
-        ne[m] = load_e8m0<U>(srow[m] + kn / 32);
+        ne[m] = load_mx_scales<U>(srow[m], kl + kn);
       }
     }
 #pragma unroll
     for (int m = 0; m < NM; ++m) {
       const float sc0 = e8m0_scale(e[m] & 0xFFu);
-      const float sc1 = U == 8 ? e8m0_scale(e[m] >> 8) : sc0;
+      const float sc1 = U == 8 ? e8m0_scale((e[m] >> 8) & 0xFFu) : sc0;
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const bf16x8 bv = fp4x8_to_bf16(b[m].w[u], u < 4 ? sc0 : sc1);
@@ -413,7 +424,6 @@ template <int kW, int U>
 struct WTile;
 template <int U>
 struct WTile<kBf16, U> {
-  static constexpr bool kGroupScales = false;
   using GV = uint32_t;
   struct Ptr { const uint16_t* w; };
   struct Regs { bf16x8 w[U]; };
@@ -428,7 +438,6 @@ struct WTile<kBf16, U> {
 };
 template <int U>
 struct WTile<kFp8, U> {
-  static constexpr bool kGroupScales = false;
   using GV = uint32_t;
   struct Ptr { const uint8_t* w; };
   struct Regs { uint2 w[U]; };
@@ -441,86 +450,20 @@ struct WTile<kFp8, U> {
   }
   __device__ static bf16x8 operand(const Regs& r, int u) { return fp8x8_to_bf16(r.w[u]); }
 };
-// Steps per MXFP4 scale group of the 8-word (U = 8) weight tiles: 4, 8 or 16.
-#ifndef XS_Q4_SCALE_STEPS
-#define XS_Q4_SCALE_STEPS 8
-#endif
-static_assert(XS_Q4_SCALE_STEPS == 4 || XS_Q4_SCALE_STEPS == 8 || XS_Q4_SCALE_STEPS == 16,
-              "4, 8 or 16 steps per scale group");
 template <int U>
 struct WTile<kMx4, U> {
-  // w: this lane's codes; sc: this lane's scale bytes (lane group g: its row's scale bytes
-  // from byte U / 4 * g on)
-  struct Ptr { const uint8_t* w; const uint8_t* sc; };
-  // scale bytes (block u / 4 in byte u / 4) in a type no wider than their loads: a
-  // widening at the end of a step would wait for the load
+  // w: this lane's codes; sc: its row's tiled scales (mx_row); k: its first input (absolute)
+  struct Ptr { const uint8_t* w; const uint8_t* sc; int k; };
+  // scale bytes (block u / 4 in byte u / 4) in a type no wider than their load: a widening
+  // at the end of a step would wait for the load
   using E = typename std::conditional<(U > 8), uint32_t, uint16_t>::type;
   struct Regs { Q4<U> q; E e; };
   __device__ static constexpr int koff(int g, int u) { return 8 * U * g + 8 * u; }
   __device__ static Regs load(const Ptr& p, int s) {
     Regs r;
     r.q = load_q4<U>(p.w + s / 2);
-    r.e = load_e8m0<U>(p.sc + s / 32);
+    r.e = (E)load_mx_scales<U>(p.sc, p.k + s);
     return r;
-  }
-  // Scales by groups of steps: a row's scale bytes of one step (U bytes) are one
-  // cache-line piece that all four lanes of the row used to load separately, step after
-  // step (a fifth of the GEMM time went to these 2-byte loads, one cache line per row
-  // each).  In group G of kSG steps, lane group g loads its row's U bytes of the kP steps
-  // kSG G + kP g ..., and at step kSG G + ph every lane takes its bytes from lane (n, ph /
-  // kP) with a cross-lane read: one load per kP steps and tile.  For U = 8 a group spans
-  // XS_Q4_SCALE_STEPS steps.  A row's scale lines are evicted by the weight stream between
-  // its groups, so each group visits them again: with four steps, a row's 224 scale bytes
-  // (d = 7168) came in seven 32-byte pieces and the gate/up fetched 18.4 % more than its
-  // bytes (down, 64 bytes a row: 5.8 %); with eight, 11.3 % and 0.3 % (DeepSeek T=32 M=48
-  // gate/up 145.6 -> 143.4 us, down 82.0 -> 81.4 us).  Sixteen would leave the two-tile
-  // gate/up one wave per SIMD.
-  static constexpr bool kGroupScales = U == 4 || U == 8 || U == 16;
-  static constexpr int kP = U == 8 ? XS_Q4_SCALE_STEPS / 4 : 1;   // steps per lane piece
-  static constexpr int kSG = 4 * kP;                               // steps per group
-  struct GV8 { uint2 w[kP]; };
-  using GV = typename std::conditional<
-      (U == 16), uint4, typename std::conditional<(U == 8), GV8, uint32_t>::type>::type;
-  __device__ static Regs load_codes(const Ptr& p, int s) {
-    Regs r;
-    r.q = load_q4<U>(p.w + s / 2);
-    return r;
-  }
-  // (a step past the pass's last step `last` repeats that step's bytes)
-  __device__ static GV load_group(const Ptr& p, int G, int g, int last) {
-    const uint8_t* const row = p.sc - U / 4 * g;       // the row's bytes of step 0
-    if constexpr (U == 8) {
-      GV v;
-#pragma unroll
-      for (int i = 0; i < kP; ++i)
-        v.w[i] = *reinterpret_cast<const uint2*>(row + min(kSG * G + kP * g + i, last) * U);
-      return v;
-    } else {
-      return *reinterpret_cast<const GV*>(row + min(4 * G + g, last) * U);
-    }
-  }
-  __device__ static E group_scale(const GV& v, int ph, int lane) {
-    const int g = lane >> 4;
-    if constexpr (U == 16) {  // lane group g's four bytes: word g of the step's 16 bytes
-      const int src = (lane & 15) + 16 * ph;
-      const uint32_t w0 = (uint32_t)__shfl((int)v.x, src, 64);
-      const uint32_t w1 = (uint32_t)__shfl((int)v.y, src, 64);
-      const uint32_t w2 = (uint32_t)__shfl((int)v.z, src, 64);
-      const uint32_t w3 = (uint32_t)__shfl((int)v.w, src, 64);
-      return g < 2 ? (g == 0 ? w0 : w1) : (g == 2 ? w2 : w3);
-    } else if constexpr (U == 8) {   // lane group g's bytes 2g, 2g + 1 of the step's 8
-      const int src = (lane & 15) + 16 * (ph / kP), i = ph % kP;   // i: uniform
-      uint2 w = v.w[0];
-#pragma unroll
-      for (int j = 1; j < kP; ++j) w = i == j ? v.w[j] : w;
-      const uint32_t w0 = (uint32_t)__shfl((int)w.x, src, 64);
-      const uint32_t w1 = (uint32_t)__shfl((int)w.y, src, 64);
-      return (E)((g < 2 ? w0 : w1) >> (16 * (g & 1)));
-    } else {                  // U = 4: byte g of the step's 4
-      const int src = (lane & 15) + 16 * ph;
-      const uint32_t w = (uint32_t)__shfl((int)v, src, 64);
-      return (E)((w >> (8 * g)) & 0xFFu);
-    }
   }
   __device__ static bf16x8 operand(const Regs& r, int u) {
     const uint32_t e = r.e;
@@ -532,9 +475,7 @@ struct WTile<kMx4, U> {
 // ceil(R * P / 256) (pieces beyond R * P repeat the last one).  Staged row r (r < R) is
 // x[tok[r] * ld ...], x already offset to this block's reduction range.  acc[m][rt] as in
 // wave_pass (gate/up) or the down pass.
-// kGS: MXFP4 scales loaded by groups of steps (WTile<kMx4, U>::load_group); needs
-// k_first = 0.
-template <int kW, int U, bool kDown, int NM, int NT, int NL, int TA, bool kGS = false>
+template <int kW, int U, bool kDown, int NM, int NT, int NL, int TA>
 __device__ __forceinline__ void block_pass(const uint16_t* x, size_t ld, const int* tok, int R,
                                            const typename WTile<kW, U>::Ptr (&wp)[NM], int K,
                                            int k_first, floatx4 (&acc)[NM][TA], uint16_t* lds) {
@@ -562,31 +503,14 @@ __device__ __forceinline__ void block_pass(const uint16_t* x, size_t ld, const i
 
   u32x4 v[NL];
   typename WT::Regs b[NM];
-  // kGS: this lane's scale piece of the current group of four steps
-  typename WT::GV gs[kGS ? NM : 1];
 #pragma unroll
   for (int i = 0; i < NL; ++i) v[i] = *reinterpret_cast<const u32x4*>(src[i] + S::AS * k_first);
-  if constexpr (kGS) {
 #pragma unroll
-    for (int m = 0; m < NM; ++m) {
-      gs[m] = WT::load_group(wp[m], 0, g, K / KB - 1);
-      b[m] = WT::load_codes(wp[m], 0);
-    }
-  } else {
-#pragma unroll
-    for (int m = 0; m < NM; ++m) b[m] = WT::load(wp[m], k_first);
-  }
+  for (int m = 0; m < NM; ++m) b[m] = WT::load(wp[m], k_first);
 #pragma unroll
   for (int i = 0; i < NL; ++i) *reinterpret_cast<u32x4*>(lds + wofs[i]) = v[i];
   __syncthreads();
 
-  // kGS: step ks's scales out of the group's pieces
-  auto scales = [&](int ks) {
-    if constexpr (kGS) {
-#pragma unroll
-      for (int m = 0; m < NM; ++m) b[m].e = WT::group_scale(gs[m], ks % WT::kSG, lane);
-    }
-  };
   // MFMAs of one step from LDS buffer `cur`
   auto step = [&](const uint16_t* cur) {
 #pragma unroll
@@ -606,33 +530,17 @@ __device__ __forceinline__ void block_pass(const uint16_t* x, size_t ld, const i
   int buf = 0;
   // loads of step kn, MFMAs of the step before it, then kn's tokens into the other buffer
   auto advance = [&](int kn) {
-    const int ks = kn / KB;
-    // kGS: the scales of step ks - 1 out of the pieces, then, when step ks starts a group
-    // (a uniform branch, taken every fourth step), that group's pieces, first of the loads
-    scales(ks - 1);
-    if constexpr (kGS) {
-      if (ks % WT::kSG == 0) {
-#pragma unroll
-        for (int m = 0; m < NM; ++m) gs[m] = WT::load_group(wp[m], ks / WT::kSG, g, K / KB - 1);
-      }
-    }
 #pragma unroll
     for (int i = 0; i < NL; ++i) v[i] = *reinterpret_cast<const u32x4*>(src[i] + S::AS * kn);
     typename WT::Regs nb[NM];
 #pragma unroll
-    for (int m = 0; m < NM; ++m) {
-      if constexpr (kGS) nb[m] = WT::load_codes(wp[m], kn);
-      else nb[m] = WT::load(wp[m], kn);
-    }
+    for (int m = 0; m < NM; ++m) nb[m] = WT::load(wp[m], kn);
     step(lds + buf * kStageRows * S::LS);
     uint16_t* const nxt = lds + (buf ^ 1) * kStageRows * S::LS;
 #pragma unroll
     for (int i = 0; i < NL; ++i) *reinterpret_cast<u32x4*>(nxt + wofs[i]) = v[i];
 #pragma unroll
-    for (int m = 0; m < NM; ++m) {
-      if constexpr (kGS) b[m].q = nb[m].q;
-      else b[m] = nb[m];
-    }
+    for (int m = 0; m < NM; ++m) b[m] = nb[m];
     __syncthreads();
     buf ^= 1;
   };
@@ -640,15 +548,14 @@ __device__ __forceinline__ void block_pass(const uint16_t* x, size_t ld, const i
   // one loop measured slower)
   for (int kn = k_first + KB; kn < K; kn += KB) advance(kn);
   for (int kn = 0; kn < k_first; kn += KB) advance(kn);
-  scales(K / KB - 1);
   step(lds + buf * kStageRows * S::LS);
   __syncthreads();                         // the block's next pass rewrites both buffers
 }
 
 // The staged pass over R token rows, by block-uniform instance: the fewest tiles that hold
 // R rows and the loads per thread that the largest R of that tile count needs.
-template <int kW, int U, bool kDown, int NM, int TA, bool kGS>
-__device__ __forceinline__ void staged_pass_as(const uint16_t* x, size_t ld, const int* tok,
+template <int kW, int U, bool kDown, int NM, int TA>
+__device__ __forceinline__ void staged_pass(const uint16_t* x, size_t ld, const int* tok,
                                                int R, const typename WTile<kW, U>::Ptr (&wp)[NM],
                                                int K, int k_first, floatx4 (&acc)[NM][TA],
                                                uint16_t* lds) {
@@ -659,43 +566,28 @@ __device__ __forceinline__ void staged_pass_as(const uint16_t* x, size_t ld, con
     constexpr int L1h = (TR / 2 * S::P + kBlock - 1) / kBlock;
     constexpr int L2h = (3 * TR / 2 * S::P + kBlock - 1) / kBlock;
     if (R <= TR / 2)
-      block_pass<kW, U, kDown, NM, 1, L1h, TA, kGS>(x, ld, tok, R, wp, K, k_first, acc, lds);
+      block_pass<kW, U, kDown, NM, 1, L1h, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
     else if (R <= TR)
-      block_pass<kW, U, kDown, NM, 1, L1, TA, kGS>(x, ld, tok, R, wp, K, k_first, acc, lds);
+      block_pass<kW, U, kDown, NM, 1, L1, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
     else if (R <= 3 * TR / 2)
-      block_pass<kW, U, kDown, NM, 2, L2h, TA, kGS>(x, ld, tok, R, wp, K, k_first, acc, lds);
+      block_pass<kW, U, kDown, NM, 2, L2h, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
     else
-      block_pass<kW, U, kDown, NM, 2, L2, TA, kGS>(x, ld, tok, R, wp, K, k_first, acc, lds);
+      block_pass<kW, U, kDown, NM, 2, L2, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
   } else {                          // down: up to four 8-token tiles
     static_assert(TA == 2 || TA == 4, "two or four 8-token tiles");
     if (R <= TR) {
-      block_pass<kW, U, kDown, NM, 1, L1, TA, kGS>(x, ld, tok, R, wp, K, k_first, acc, lds);
+      block_pass<kW, U, kDown, NM, 1, L1, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
     } else if (TA == 2 || R <= 2 * TR) {
-      block_pass<kW, U, kDown, NM, 2, L2, TA, kGS>(x, ld, tok, R, wp, K, k_first, acc, lds);
+      block_pass<kW, U, kDown, NM, 2, L2, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
     } else if constexpr (TA == 4) {
       constexpr int L3 = (3 * TR * S::P + kBlock - 1) / kBlock;
       constexpr int L4 = (4 * TR * S::P + kBlock - 1) / kBlock;
       if (R <= 3 * TR)
-        block_pass<kW, U, kDown, NM, 3, L3, TA, kGS>(x, ld, tok, R, wp, K, k_first, acc, lds);
+        block_pass<kW, U, kDown, NM, 3, L3, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
       else
-        block_pass<kW, U, kDown, NM, 4, L4, TA, kGS>(x, ld, tok, R, wp, K, k_first, acc, lds);
+        block_pass<kW, U, kDown, NM, 4, L4, TA>(x, ld, tok, R, wp, K, k_first, acc, lds);
     }
   }
-}
-
-// The staged pass, with MXFP4 scales by groups of four steps where the pass allows it.
-template <int kW, int U, bool kDown, int NM, int TA>
-__device__ __forceinline__ void staged_pass(const uint16_t* x, size_t ld, const int* tok, int R,
-                                            const typename WTile<kW, U>::Ptr (&wp)[NM], int K,
-                                            int k_first, floatx4 (&acc)[NM][TA],
-                                            uint16_t* lds) {
-  if constexpr (WTile<kW, U>::kGroupScales) {
-    if (k_first == 0) {
-      staged_pass_as<kW, U, kDown, NM, TA, true>(x, ld, tok, R, wp, K, k_first, acc, lds);
-      return;
-    }
-  }
-  staged_pass_as<kW, U, kDown, NM, TA, false>(x, ld, tok, R, wp, K, k_first, acc, lds);
 }
 
 // Unroll (32-element k-groups per step) and token-operand buffering of the two GEMMs.
@@ -928,10 +820,13 @@ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
         } else if constexpr (kW == kFp8) {
           wp[2 * ct].w = slot_q(a, sw, a.q1) + wrow;
           wp[2 * ct + 1].w = slot_q(a, sw, a.q3) + wrow;
-        } else {        // row col of the expert: d / 2 code bytes, d / 32 scale bytes
+        } else {        // row col of the expert: d / 2 code bytes; its tiled scale row
           const size_t r = (size_t)sw.e * f + col[ct];
-          wp[2 * ct] = {a.q1 + r * (d / 2) + k0 / 2, a.e1 + r * (d / 32) + k0 / 32};
-          wp[2 * ct + 1] = {a.q3 + r * (d / 2) + k0 / 2, a.e3 + r * (d / 32) + k0 / 32};
+          const int G = mx_granules(d);
+          const size_t emat = (size_t)sw.e * f * G * 8;     // the expert's scale matrix
+          wp[2 * ct] = {a.q1 + r * (d / 2) + k0 / 2, mx_row(a.e1 + emat, col[ct], G), (int)k0};
+          wp[2 * ct + 1] = {a.q3 + r * (d / 2) + k0 / 2, mx_row(a.e3 + emat, col[ct], G),
+                            (int)k0};
         }
       }
       __shared__ __align__(16) uint16_t stage[Stage<U, false>::kElems];
@@ -951,18 +846,20 @@ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
       }
       wave_pass_q8<U, NM>(arow, nt, brow, Kg, acc);
     } else if constexpr (kW == kMx4) {
-      // row col of the expert: d / 2 code bytes, d / 32 scale bytes
+      // row col of the expert: d / 2 code bytes; its tiled scale row
       const uint8_t* brow[NM];
       const uint8_t* srow[NM];
+      const int G = mx_granules(d);
+      const size_t emat = (size_t)sw.e * f * G * 8;
 #pragma unroll
       for (int ct = 0; ct < CT; ++ct) {
         const size_t r = (size_t)sw.e * f + col[ct];
         brow[2 * ct] = a.q1 + r * (d / 2) + k0 / 2;
         brow[2 * ct + 1] = a.q3 + r * (d / 2) + k0 / 2;
-        srow[2 * ct] = a.e1 + r * (d / 32) + k0 / 32;
-        srow[2 * ct + 1] = a.e3 + r * (d / 32) + k0 / 32;
+        srow[2 * ct] = mx_row(a.e1 + emat, col[ct], G);
+        srow[2 * ct + 1] = mx_row(a.e3 + emat, col[ct], G);
       }
-      wave_pass_q4<U, NM>(arow, nt, brow, srow, Kg, acc);
+      wave_pass_q4<U, NM>(arow, nt, brow, srow, (int)k0, Kg, acc);
     } else {
       const uint16_t* brow[NM];
 #pragma unroll
@@ -1077,9 +974,11 @@ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
           wp[m].w = slot_w(a, sw, a.w2, a.sw2) + wrow[m];
         } else if constexpr (kW == kFp8) {
           wp[m].w = slot_q(a, sw, a.q2) + wrow[m];
-        } else {
-          const size_t r = (size_t)sw.e * d + rowm[m];      // f / 2 code, f / 32 scale bytes
-          wp[m] = {a.q2 + r * (f / 2) + k0 / 2, a.e2 + r * (f / 32) + k0 / 32};
+        } else {         // f / 2 code bytes of row rowm; its tiled scale row
+          const size_t r = (size_t)sw.e * d + rowm[m];
+          const int G = mx_granules(f);
+          wp[m] = {a.q2 + r * (f / 2) + k0 / 2,
+                   mx_row(a.e2 + (size_t)sw.e * d * G * 8, rowm[m], G), (int)k0};
         }
       }
       __shared__ __align__(16) uint16_t stage[Stage<U, true>::kElems];
@@ -1099,13 +998,14 @@ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
     } else if constexpr (kW == kMx4) {
       const uint8_t* brow[NM];
       const uint8_t* srow[NM];
+      const int G = mx_granules(f);
 #pragma unroll
       for (int m = 0; m < NM; ++m) {
-        const size_t r = (size_t)sw.e * d + rowm[m];      // f / 2 code, f / 32 scale bytes
+        const size_t r = (size_t)sw.e * d + rowm[m];      // f / 2 code bytes; tiled scale row
         brow[m] = a.q2 + r * (f / 2) + k0 / 2;
-        srow[m] = a.e2 + r * (f / 32) + k0 / 32;
+        srow[m] = mx_row(a.e2 + (size_t)sw.e * d * G * 8, rowm[m], G);
       }
-      wave_pass_q4<U, NM, TL, 2>(arow, nt, brow, srow, Ks, acc, k_first);
+      wave_pass_q4<U, NM, TL, 2>(arow, nt, brow, srow, (int)k0, Ks, acc, k_first);
     } else {
       const uint16_t* brow[NM];
 #pragma unroll
@@ -1211,7 +1111,7 @@ __global__ __attribute__((amdgpu_waves_per_eu(NM <= 4 ? XS_DOWN_WAVES_PER_EU : 1
 __launch_bounds__(kBlock) void down_seq_kernel(FfnArgs a) {
   using S = Stage<U, true>;
   using WT = WTile<kW, U>;
-  static_assert(!WT::kGroupScales && kW != kMx4, "bf16 and FP8 weights");
+  static_assert(kW != kMx4, "bf16 and FP8 weights");
   constexpr int KB = S::KB;
   constexpr int NLM = (TL * S::TR * S::P + kBlock - 1) / kBlock;
   typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -1840,6 +1740,31 @@ hipError_t launch_router(const RouterArgs& r, hipStream_t stream) {
   const size_t n = (size_t)r.T * r.N;
   hipLaunchKernelGGL(router_sum_kernel, dim3((unsigned)((n + kBlock - 1) / kBlock)), block, 0,
                      stream, r);
+  return hipGetLastError();
+}
+
+// MXFP4 scales [n_mat, rows, K / 32] -> the tiled layout [n_mat, rows / 16, G, 16, 8] (G =
+// ceil(K / 256)); bytes past the last block of a row are 127 (scale 1), never read.
+__global__ __launch_bounds__(kBlock) void mx_scales_tile_kernel(const uint8_t* src, uint8_t* dst,
+                                                                long total, int rows, int K) {
+  const long i = (long)blockIdx.x * kBlock + threadIdx.x;
+  if (i >= total) return;
+  const int G = (K + 255) >> 8, nb = K >> 5;
+  const long per_mat = (long)rows * G * 8;
+  const long mat = i / per_mat;
+  const int r = (int)(i % per_mat);
+  const int tile = r / (G * 128), in_tile = r % (G * 128);
+  const int gran = in_tile >> 7, row = tile * 16 + ((in_tile >> 3) & 15);
+  const int c = gran * 8 + (in_tile & 7);
+  dst[i] = c < nb ? src[(mat * rows + row) * nb + c] : (uint8_t)127;
+}
+
+hipError_t launch_mx_scales_tile(const uint8_t* src, uint8_t* dst, int n_mat, int rows, int K,
+                                 hipStream_t stream) {
+  const long total = (long)n_mat * rows * ((K + 255) / 256) * 8;
+  if (total == 0) return hipSuccess;
+  hipLaunchKernelGGL(mx_scales_tile_kernel, dim3((unsigned)((total + kBlock - 1) / kBlock)),
+                     dim3(kBlock), 0, stream, src, dst, total, rows, K);
   return hipGetLastError();
 }
 

@@ -253,7 +253,9 @@ struct FfnArgs {
   const float* s1;             // FP8 scales, one per output row: [N, f], [N, f], [N, d]
   const float* s3;
   const float* s2;
-  const uint8_t* e1;           // MXFP4 E8M0 block scales [N, f, d/32], [N, f, d/32], [N, d, f/32]
+  const uint8_t* e1;           // MXFP4 E8M0 block scales, tiled (mx_scales_tile_kernel):
+                               //   [N, f/16, G(d), 16, 8], [N, f/16, G(d), 16, 8],
+                               //   [N, d/16, G(f), 16, 8] with G(K) = ceil(K / 256)
   const uint8_t* e3;           //   (q1, q3, q2 then hold packed E2M1 codes, two per byte)
   const uint8_t* e2;
   int wfmt;                    // 0 bf16, 1 FP8, 2 MXFP4
@@ -287,6 +289,12 @@ struct FfnArgs {
 };
 
 hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream);  // + finish if split
+// MXFP4 scales [n_mat, rows, K/32] -> tiled [n_mat, rows/16, ceil(K/256), 16, 8]
+hipError_t launch_mx_scales_tile(const uint8_t* src, uint8_t* dst, int n_mat, int rows, int K,
+                                 hipStream_t stream);
+inline size_t mx_scales_tiled_bytes(int n_mat, int rows, int K) {
+  return size_t(n_mat) * size_t(rows) * size_t((K + 255) / 256) * 8;
+}
 hipError_t launch_down(const FfnArgs& a, hipStream_t stream);
 hipError_t launch_combine(const FfnArgs& a, hipStream_t stream);
 

@@ -87,7 +87,7 @@ def main():
         wset = W.expert_weights_fp8(N, d, f, 0, dev)
         wb, sb = 1.0, None              # one byte per weight, one fp32 scale per row
     elif args.weights == "mxfp4":
-        wset = W.expert_weights_mxfp4(N, d, f, 0, dev)
+        wset = X.mx_tiled(W.expert_weights_mxfp4(N, d, f, 0, dev))
         wb, sb = 0.5, 1.0 / 32          # half a byte per weight, one scale byte per 32
     else:
         wset = W.expert_weights(N, d, f, 0, dev)

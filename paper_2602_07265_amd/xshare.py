@@ -132,6 +132,10 @@ def lib() -> ctypes.CDLL:
                                              ctypes.POINTER(EpLayout), _P, _P, _P, _P, _P, _P,
                                              _SZ, _P, _P]
         L.xshare_moe_forward_mxfp4.restype = ctypes.c_int
+        L.xshare_mx_scales_tiled_bytes.argtypes = [_I32, _I32, _I32]
+        L.xshare_mx_scales_tiled_bytes.restype = _SZ
+        L.xshare_mx_scales_tile.argtypes = [_P, _P, _I32, _I32, _I32, _P]
+        L.xshare_mx_scales_tile.restype = ctypes.c_int
         L.xshare_route.argtypes = [_P, _I32, ctypes.POINTER(RouteParams), _P, _P, _P, _P, _P, _SZ,
                                    _P]
         L.xshare_route.restype = ctypes.c_int
@@ -563,6 +567,33 @@ def moe_forward_fp8(x: torch.Tensor, logits: torch.Tensor, q1: torch.Tensor, q3:
     return res
 
 
+def mx_granules(k: int) -> int:
+    """Granules of 8 scale blocks (256 inputs) per row in the tiled MXFP4 scale layout."""
+    return (k + 255) // 256
+
+
+def tile_mx_scales(scales: torch.Tensor, stream=None) -> torch.Tensor:
+    """xshare_mx_scales_tile: E8M0 scales [n, rows, k/32] (row-major) -> the tiled layout
+    the MXFP4 GEMMs read, [n, rows/16, ceil(k/256), 16, 8] uint8 (a new tensor)."""
+    n, rows, nb = scales.shape
+    k = 32 * nb
+    if scales.dtype != torch.uint8 or not scales.is_cuda:
+        raise ValueError("scales: a uint8 device tensor [n, rows, k/32]")
+    src = scales.contiguous()
+    out = torch.empty((n, rows // 16, mx_granules(k), 16, 8), dtype=torch.uint8,
+                      device=scales.device)
+    assert out.numel() == lib().xshare_mx_scales_tiled_bytes(n, rows, k)
+    _check(lib().xshare_mx_scales_tile(_ptr(src), _ptr(out), n, rows, k, _stream(stream)),
+           "xshare_mx_scales_tile")
+    return out
+
+
+def mx_tiled(weights):
+    """(q1, q3, q2, e1, e3, e2) with row-major scales -> the same with tiled scales."""
+    q1, q3, q2, e1, e3, e2 = weights
+    return q1, q3, q2, tile_mx_scales(e1), tile_mx_scales(e3), tile_mx_scales(e2)
+
+
 def moe_forward_mxfp4(x: torch.Tensor, logits: torch.Tensor, q1: torch.Tensor, q3: torch.Tensor,
                       q2: torch.Tensor, e1: torch.Tensor, e3: torch.Tensor, e2: torch.Tensor,
                       top_k: int, warmup_k0: int, budget: int, budget_mode="total",
@@ -570,7 +601,7 @@ def moe_forward_mxfp4(x: torch.Tensor, logits: torch.Tensor, q1: torch.Tensor, q
                       groups: GroupMap | None = None, tau: float = 0.0, ledger=None, y=None,
                       routing_out=True, workspace=None, stage_events=None, stream=None) -> dict:
     """The MoE layer with MXFP4 expert weights: packed E2M1 codes (uint8, two per byte) and
-    one E8M0 scale byte per 32 inputs of a row."""
+    one E8M0 scale byte per 32 inputs of a row, in the tiled layout (tile_mx_scales)."""
     T, d = x.shape
     N = logits.shape[1]
     f = q1.shape[1]
@@ -580,9 +611,9 @@ def moe_forward_mxfp4(x: torch.Tensor, logits: torch.Tensor, q1: torch.Tensor, q
     _dev(q1, torch.uint8, (N, f, d // 2), "w1 codes")
     _dev(q3, torch.uint8, (N, f, d // 2), "w3 codes")
     _dev(q2, torch.uint8, (N, d, f // 2), "w2 codes")
-    _dev(e1, torch.uint8, (N, f, d // 32), "w1 scales")
-    _dev(e3, torch.uint8, (N, f, d // 32), "w3 scales")
-    _dev(e2, torch.uint8, (N, d, f // 32), "w2 scales")
+    _dev(e1, torch.uint8, (N, f // 16, mx_granules(d), 16, 8), "w1 tiled scales")
+    _dev(e3, torch.uint8, (N, f // 16, mx_granules(d), 16, 8), "w3 tiled scales")
+    _dev(e2, torch.uint8, (N, d // 16, mx_granules(f), 16, 8), "w2 tiled scales")
     if groups is not None:
         budget_mode = "per_group"
     p = params(N, top_k, warmup_k0, budget, budget_mode, score_mode, per_request_budget, tau,

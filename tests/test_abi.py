@@ -282,6 +282,21 @@ def test_moe_forward_mxfp4_validation():
     assert call(f=80) == X.EUNSUPPORTED
 
 
+def test_mx_scales_tile_validation():
+    """The tiled MXFP4 scale layout: ceil(k / 256) granules of 8 bytes per row; rows a
+    multiple of 16 and k of 32, checked before any HIP call."""
+    L = X.lib()
+    assert L.xshare_mx_scales_tiled_bytes(2, 32, 7168) == 2 * 32 * 28 * 8
+    assert L.xshare_mx_scales_tiled_bytes(1, 16, 96) == 16 * 1 * 8      # one partial granule
+    assert L.xshare_mx_scales_tiled_bytes(1, 16, 288) == 16 * 2 * 8
+    assert L.xshare_mx_scales_tiled_bytes(-1, 16, 256) == 0
+    assert L.xshare_mx_scales_tile(FAKE, FAKE, 1, 24, 256, None) == X.EINVAL   # rows % 16
+    assert L.xshare_mx_scales_tile(FAKE, FAKE, 1, 32, 48, None) == X.EINVAL    # k % 32
+    assert L.xshare_mx_scales_tile(None, FAKE, 1, 32, 64, None) == X.EINVAL
+    assert L.xshare_mx_scales_tile(FAKE, None, 1, 32, 64, None) == X.EINVAL
+    assert L.xshare_mx_scales_tile(None, None, 0, 32, 64, None) == X.OK        # nothing to do
+
+
 def _args(**kw):
     """An xshare_layer_args for a bf16 layer with fake device pointers (never dereferenced:
     every call below stops in validation)."""

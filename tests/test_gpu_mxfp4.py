@@ -29,7 +29,7 @@ def _run(cfg, seed, k0, M, mode="total", weights=None, rows=None, offsets=None, 
     wts = weights if weights is not None else W.expert_weights_mxfp4(N, d, f, seed, DEV)
     say(f"mxfp4 case {label} T={T} N={N} k={k} d={d} f={f} k0={k0} M={M} {mode}")
     gm = None if groups is None else X.GroupMap(groups, None, local_group=local, device=DEV)
-    res = X.moe_forward_mxfp4(x, torch.from_numpy(h).to(DEV), *wts, k, k0, M, mode,
+    res = X.moe_forward_mxfp4(x, torch.from_numpy(h).to(DEV), *X.mx_tiled(wts), k, k0, M, mode,
                               req_offsets=None if offsets is None else list(offsets),
                               per_request_budget=m_r, groups=gm)
     torch.cuda.synchronize()
@@ -90,13 +90,32 @@ def test_mxfp4_largest_batches():
              label=f"largest T{T} k{k}")
 
 
+def test_mx_scales_tile_layout():
+    """xshare_mx_scales_tile against the layout written out with numpy, byte for byte:
+    tiled[m][r / 16][c / 8][r % 16][c % 8] = scales[m][r][c], 127 past a row's last block
+    (k = 96 and 288 end in a partial granule of 8 blocks)."""
+    from paper_2602_07265_amd import xshare as X
+    rng = np.random.default_rng(11)
+    for n, rows, k in [(3, 32, 256), (2, 48, 96), (1, 16, 288), (2, 64, 7168)]:
+        say(f"mx scale tiling n={n} rows={rows} k={k}")
+        sc = rng.integers(0, 255, size=(n, rows, k // 32), dtype=np.uint8)
+        got = X.tile_mx_scales(torch.from_numpy(sc).to(DEV)).cpu().numpy()
+        G = (k + 255) // 256
+        want = np.full((n, rows // 16, G, 16, 8), 127, dtype=np.uint8)
+        for m in range(n):
+            for r in range(rows):
+                for c in range(k // 32):
+                    want[m, r // 16, c // 8, r % 16, c % 8] = sc[m, r, c]
+        assert np.array_equal(got, want), (n, rows, k)
+
+
 @pytest.mark.parametrize("d,f", [(128, 128), (1024, 1280), (1280, 768), (2048, 512)])
 def test_mxfp4_every_code_and_varied_scales(d, f):
     """Weight bytes cycling through all 256 pairs of E2M1 codes, block scales drawn from
     2^-14 .. 2^-6: the kernels' hardware decode and scaling must agree with the format.
-    The GEMMs read a row's scales once per four steps and hand each step's bytes to the
-    row's lanes: d, f of 1024-2048 run whole groups of four 256-element steps, 1280 and 768
-    end in a partial group (five and three steps), 512 is split across blocks."""
+    The GEMMs read each step's scale bytes from the tiled layout (granules of 256 inputs):
+    d, f of 1024-2048 are whole granules, 1280 and 768 have 5 and 3, 128 half of one, and
+    512 is split across blocks."""
     N, k, T = 8, 2, 12
     rng = np.random.default_rng(4 + d + f)
 
@@ -157,11 +176,12 @@ def test_mxfp4_deterministic_and_empty():
     wts = W.expert_weights_mxfp4(c["N"], c["d"], c["f"], 5, DEV)
     hd = torch.from_numpy(h).to(DEV)
     say("mxfp4 case determinism and empty batch")
-    a = X.moe_forward_mxfp4(x, hd, *wts, 2, 1, 8)["y"]
-    b = X.moe_forward_mxfp4(x, hd, *wts, 2, 1, 8)["y"]
+    tiled = X.mx_tiled(wts)
+    a = X.moe_forward_mxfp4(x, hd, *tiled, 2, 1, 8)["y"]
+    b = X.moe_forward_mxfp4(x, hd, *tiled, 2, 1, 8)["y"]
     torch.cuda.synchronize()
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
     x0 = torch.empty((0, c["d"]), dtype=torch.bfloat16, device=DEV)
-    r = X.moe_forward_mxfp4(x0, torch.empty((0, c["N"]), device=DEV), *wts, 2, 1, 8)
+    r = X.moe_forward_mxfp4(x0, torch.empty((0, c["N"]), device=DEV), *tiled, 2, 1, 8)
     torch.cuda.synchronize()
     assert r["y"].shape == (0, c["d"]) and int(r["sel_mask"].sum()) == 0

@@ -66,7 +66,7 @@ def test_v2_equals_the_fixed_calls():
                          weight_format="fp8")
     torch.cuda.synchronize()
     _same(a, b, "fp8")
-    q = W.expert_weights_mxfp4(N, d, f, 0, DEV)
+    q = X.mx_tiled(W.expert_weights_mxfp4(N, d, f, 0, DEV))
     a = X.moe_forward_mxfp4(x, hd, *q, k, 1, 32)
     b = X.moe_forward_v2(x, k, 1, 32, logits=hd, weights=q[:3], scales=q[3:],
                          weight_format="mxfp4")
