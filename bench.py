@@ -225,11 +225,14 @@ def main():
           file=sys.stderr, flush=True)
     if fp8:
         base = W.expert_weights_fp8(N, d, f, 0, dev)
-    elif mx4:        # scales in the tiled layout of the GEMMs (once, at load time)
-        base = X.mx_tiled(W.expert_weights_mxfp4(N, d, f, 0, dev))
+    elif mx4:
+        base = W.expert_weights_mxfp4(N, d, f, 0, dev)
     else:
         base = W.expert_weights(N, d, f, 0, dev)
-    wsets = [base] + [tuple(t.clone() for t in base) for _ in range(reps - 1)]
+    # the layer's own copies: MXFP4 scales in the GEMMs' tiled layout (once, at load time);
+    # the CPU baseline reads the format's row-major scales
+    gpu_base = X.mx_tiled(base) if mx4 else base
+    wsets = [gpu_base] + [tuple(t.clone() for t in gpu_base) for _ in range(reps - 1)]
     forward = X.moe_forward_fp8 if fp8 else (X.moe_forward_mxfp4 if mx4 else X.moe_forward)
     made = [W.make_logits(cfg, s) for s in range(nb)]
     logits = [torch.from_numpy(h).to(dev) for h, _ in made]

@@ -20,6 +20,12 @@ the counters.
 summarises the counter CSVs that rocprofv3 wrote under OUT: per kernel of this library
 (and the calibration copy) and counter, the dispatches and their mean value, as one JSON
 line.
+
+    python -m paper_2602_07265_amd.profiling --counters-json OUT_F OUT_W DRIVER_LOG
+
+writes the traffic record of the expert GEMMs (profiles/gate_up_ds_t32_m48_counters.json,
+read by bench.py) from a FETCH_SIZE run (OUT_F), a WRITE_SIZE run (OUT_W) and the
+driver's own printed line (DRIVER_LOG).
 """
 from __future__ import annotations
 
@@ -61,9 +67,64 @@ def summarize(out_dir: str) -> dict:
     return out
 
 
+def counters_json(fetch: dict, write: dict, driver: dict) -> dict:
+    """The traffic record bench.py reads: per launch of the expert GEMMs, FETCH_SIZE and
+    WRITE_SIZE (KiB per dispatch, summaries of two counter runs of this driver) scaled by
+    what the same counters read for the driver's device copy of known size, against the
+    algorithmic bytes the driver printed; stamped with the sha256 of ffn.hip (bench.py
+    ignores the record once that file changes)."""
+    import hashlib
+
+    nbytes = driver["copy_bytes"]
+    copies = [k for k in fetch if k.startswith("copy: ")]
+    fk = max((fetch[k]["FETCH_SIZE"]["largest"] for k in copies), key=lambda v: v[-1])
+    wk = max((write[k]["WRITE_SIZE"]["largest"] for k in copies if k in write
+              and "WRITE_SIZE" in write[k]), key=lambda v: v[-1])
+    ff = round(nbytes / 1024 / (sum(fk) / len(fk)), 4)        # bytes read per FETCH KiB
+    wf = round(nbytes / 1024 / (sum(wk) / len(wk)), 4)
+    ffn = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc", "ffn.hip")
+
+    def pick(prefixes):
+        names = [k for k in fetch if any(k.startswith(p) for p in prefixes) and "true" not in k]
+        return max(names, key=lambda k: fetch[k]["FETCH_SIZE"]["dispatches"])
+
+    def rec(name, alg_key):
+        fkib = fetch[name]["FETCH_SIZE"]["mean"]
+        wkib = write[name]["WRITE_SIZE"]["mean"]
+        alg = sum(c[alg_key] for c in driver["calls"]) / len(driver["calls"])
+        return {"fetch_kib_per_dispatch": fkib, "write_kib_per_dispatch": wkib,
+                "traffic_bytes_per_launch": round(fkib * 1024 * ff + wkib * 1024 * wf),
+                "algorithmic_bytes_per_launch": round(alg)}
+
+    gu = pick(("gate_up_kernel<",))
+    dn = pick(("down_kernel<", "down_seq_kernel<"))
+    out = {"kernel": gu, "workload": driver["workload"],
+           "commands": [
+               "rocprofv3 --pmc FETCH_SIZE -d OUT_F -o fetch --output-format csv -- "
+               "python -u paper_2602_07265_amd/profiling.py",
+               "rocprofv3 --pmc WRITE_SIZE -d OUT_W -o write --output-format csv -- "
+               "python -u paper_2602_07265_amd/profiling.py",
+               "python -m paper_2602_07265_amd.profiling --counters-json OUT_F OUT_W DRIVER"],
+           "ffn_source_sha256": hashlib.sha256(open(ffn, "rb").read()).hexdigest(),
+           "copy_calibration": {"bytes_copied": nbytes, "fetch_kib": fk, "write_kib": wk,
+                                "fetch_factor": ff, "write_factor": wf}}
+    out.update(rec(gu, "gate_up_bytes"))
+    out["down_kernel"] = dict(name=dn, **rec(dn, "down_bytes"))
+    return out
+
+
 def main():
     if len(sys.argv) == 3 and sys.argv[1] == "--summarize":
         print(json.dumps(summarize(sys.argv[2])))
+        return
+    if len(sys.argv) == 5 and sys.argv[1] == "--counters-json":
+        # OUT_F, OUT_W: the two counter runs' directories; DRIVER: this driver's printed line
+        drv = None
+        for line in open(sys.argv[4]):
+            if line.startswith("{"):
+                drv = json.loads(line)
+        print(json.dumps(counters_json(summarize(sys.argv[2]), summarize(sys.argv[3]), drv),
+                         indent=1))
         return
     ap = argparse.ArgumentParser()
     ap.add_argument("--calls", type=int, default=8)
