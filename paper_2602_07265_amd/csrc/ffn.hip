@@ -1699,8 +1699,12 @@ hipError_t launch_down(const FfnArgs& a, hipStream_t stream) {
     wide = r > 0 && wide_blocks >= r && wide_blocks % r == 0;
   }
 #if XS_DOWN_NM7
-  // bf16: seven tiles per wave where that grid fills whole rounds (see XS_DOWN_NM7)
-  if (a.wfmt == kBf16 && est > 0 && (long)a.T * a.k >= XS_DN_WIDE_TOKENS * est) {
+  // bf16: seven tiles per wave where that grid fills whole rounds (see XS_DOWN_NM7); not
+  // for one GPU group's share, whose expected count (the group's experts under plain top-k)
+  // overstates its live slots: the plain top-k share of DeepSeek T=32 (about 12 live of 32
+  // slots) ran down 296 us with 64-row waves and 324 us with seven tiles
+  if (a.wfmt == kBf16 && est > 0 && a.local_group < 0 &&
+      (long)a.T * a.k >= XS_DN_WIDE_TOKENS * est) {
     const long b7 = (long)((a.d + kWaves * kCols * 7 - 1) / (kWaves * kCols * 7)) * est * a.splits;
     const int u7 = unroll_for(K, XS_DOWN_NM7_U);
     const int r7 = down_resident<kBf16, 7>(u7);
