@@ -105,6 +105,20 @@ def test_ffn_split_reduction():
         _run(c, 0, 1, M, label=f"split T{T} d{d} f{f} M{M}")
 
 
+def test_ffn_persistent_down_multi_pass():
+    """The persistent seven-tile down launch (448 output rows per block, one block per CU)
+    on experts that hold more than 32 routed rows, so a unit runs in several passes of up
+    to 32 H rows, and blocks with one and with two units: N=64, k=8, T=64, d=7168 (16
+    column blocks), f=256; budgets 16 and 32 make one and two whole rounds of 256 blocks."""
+    c = dict(N=64, k=8, d=7168, f=256, T=64, logits="domains", Q=4)
+    layer = make_layer(c, 2)
+    oracle = OracleOutputs(layer[2], bf16_weights_of(*layer[3:]))
+    for M in (16, 32):
+        _, ref = _run(c, 2, 1, M, layer=layer, oracle=oracle, label=f"persistent down M{M}")
+        rows = np.bincount(ref.ids.ravel(), minlength=c["N"])
+        assert rows.max() > 32, f"M{M}: no expert above 32 rows ({rows.max()})"
+
+
 def test_ffn_qwen_full():
     c = W.CONFIGS["qwen"]
     layer = make_layer(c, 0)
