@@ -643,6 +643,15 @@ __device__ __forceinline__ void staged_pass(const uint16_t* x, size_t ld, const 
 #ifndef XS_Q8_GATE_UP_U1
 #define XS_Q8_GATE_UP_U1 XS_Q8_GATE_UP_U
 #endif
+// FP8 gate/up instances of up to 4 words a step held to 3 waves per SIMD (168 registers, no
+// spills; left alone the compiler kept 2).  Same-box A/B, gate/up us (2 -> 3 waves):
+// DeepSeek T=32 M=48 252.0 -> 246.6, speculative 335.5 -> 331.8, T=8 M=24 127.0 -> 124.5,
+// Qwen 32.9 -> 32.4, Mixtral 137.8 -> 135.0.  Not kept at 3 waves: the two-tile MXFP4
+// gate/up (72 bytes spilled; DeepSeek T=32 138 -> 152 us) and the 32-row FP8 down (no
+// change).
+#ifndef XS_Q8_GU_W3
+#define XS_Q8_GU_W3 1
+#endif
 #ifndef XS_Q4_GATE_UP_U1
 #define XS_Q4_GATE_UP_U1 8
 #endif
@@ -766,9 +775,11 @@ __device__ __forceinline__ const uint8_t* slot_q(const FfnArgs& a, const SlotWor
 // feeds four weight tiles instead of two, at the cost of registers and of half as many
 // blocks (the launch takes two only for grids that stay large).
 // The MXFP4 one-tile instance is held to 168 registers (3 waves per SIMD): left alone the
-// compiler took 175 and 2 waves, and DeepSeek T=8 gate/up ran 14 % slower.
+// compiler took 175 and 2 waves, and DeepSeek T=8 gate/up ran 14 % slower.  So are the FP8
+// instances of up to 4 words a step (XS_Q8_GU_W3).
 template <int U, bool kSplit, int kW, int CT>
-__global__ __attribute__((amdgpu_waves_per_eu(kW == kMx4 && CT == 1 ? 3 : 1)))
+__global__ __attribute__((amdgpu_waves_per_eu((kW == kMx4 && CT == 1) ||
+                                               (kW == kFp8 && U <= 4 && XS_Q8_GU_W3) ? 3 : 1)))
 __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
   constexpr int NM = 2 * CT;                   // weight tiles: W1 and W3 of each column tile
   SlotWork sw;
