@@ -95,6 +95,19 @@ def test_ffn_many_rows_per_expert():
         _run(c, 0, 1, M, label=f"many rows T{T} d{d} f{f} M{M}")
 
 
+def test_ffn_edge_shapes():
+    """Top-1 and top-32 routing, the largest expert count (N = 1024), a budget of exactly
+    k, a budget above N, and one expert per token."""
+    for T, N, k, d, f, M, label in [(24, 16, 1, 128, 256, 4, "k=1"),
+                                    (8, 64, 32, 64, 128, 40, "k=32"),
+                                    (16, 1024, 8, 64, 64, 64, "N=1024"),
+                                    (8, 32, 4, 128, 128, 4, "M=k"),
+                                    (12, 64, 4, 96, 64, 200, "M>N"),
+                                    (9, 9, 1, 64, 96, 9, "N=9 k=1")]:
+        c = dict(N=N, k=k, d=d, f=f, T=T, logits="domains", Q=3)
+        _run(c, 0, 1, M, label=label)
+
+
 def test_ffn_split_reduction():
     """Few, wide experts: the down GEMM splits f into 8, 8, 4 and 2 parts and the gate/up
     GEMM splits d into 8 and 4 parts (partials summed in split order); within tolerance."""
@@ -156,6 +169,14 @@ def test_ffn_deepseek_t8(ds_weights):
     ci = W.CONFIGS["ds_iid_t8"]
     _run(ci, 0, 1, 48, layer=(*W.make_logits(ci, 0), *layer[2:]), oracle=oracle,
          label="ds_iid_t8 M48")
+
+
+def test_ffn_deepseek_one_token(ds_weights):
+    """A single decoding token at the DeepSeek shape: S is its own top-k."""
+    c = dict(W.CONFIGS["ds_t8"], T=1)
+    layer = _ds_layer(c, 3, ds_weights)
+    for M in (8, 48):
+        _run(c, 3, 1, M, layer=layer, label=f"ds T=1 M{M}")
 
 
 def test_ffn_spec_hier(ds_weights):
