@@ -531,6 +531,30 @@ xshare_status xshare_layer_budgets(int32_t K, int32_t L, int32_t* m);
 xshare_status xshare_probe_stream_read(const void* buf, size_t bytes, int32_t blocks,
                                        int32_t mode, uint32_t* sink, hipStream_t stream);
 
+/*
+ * xshare_block_times -- measurement only: the block timeline of the expert GEMMs, from the
+ * profiling build of this library (libxshare_timeline.so, compiled with XS_BLOCK_TIMES=1;
+ * the product build returns XSHARE_EUNSUPPORTED and touches nothing).  That build stamps,
+ * from the GPU's 100 MHz global clock, the start and end of every block of the last gate/up
+ * and down launches, and the start and the end of each unit of every block of the last
+ * persistent down launch; this call copies the stamps, asynchronously on `stream`, into
+ * DEVICE uint64 arrays owned by the caller:
+ *   gate_up     [2 * XSHARE_TIME_BLOCKS]: start, end of block b at 2b, 2b + 1, where
+ *               b = (blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x;
+ *   down        [2 * XSHARE_TIME_BLOCKS]: the same for the down launch's grid;
+ *   down_units  [XSHARE_TIME_SEQ_BLOCKS * XSHARE_TIME_SEQ_STRIDE]: block b of a persistent
+ *               down launch at b * XSHARE_TIME_SEQ_STRIDE: its start, then its units' ends.
+ * A launch overwrites only the entries of its own blocks (blocks past the array sizes are
+ * not stamped), and blocks with no work stamp nothing; with `clear` nonzero the call zeroes
+ * the stamps after copying them (hipMemsetAsync: a measurement call, not for capture in a
+ * HIP graph).  XSHARE_EINVAL for a NULL pointer.
+ */
+#define XSHARE_TIME_BLOCKS 16384
+#define XSHARE_TIME_SEQ_BLOCKS 1024
+#define XSHARE_TIME_SEQ_STRIDE 33
+xshare_status xshare_block_times(uint64_t* gate_up, uint64_t* down, uint64_t* down_units,
+                                 int32_t clear, hipStream_t stream);
+
 /* Static description of a status code (never NULL).                                      */
 const char* xshare_status_string(int32_t status);
 

@@ -8,7 +8,9 @@ Translation units:
 * ffn.hip   -- expert GEMMs (bf16 MFMA) and the combine;
 * abi.hip   -- the extern "C" entry points declared in include/xshare.h;
 * probe.hip -- the streaming-read probe (measurement of the HBM read ceiling).
-Every HIP compile disables packed-fp32 instruction selection.
+Every HIP compile disables packed-fp32 instruction selection.  The same sources built with
+XS_BLOCK_TIMES=1 give libxshare_timeline.so, the profiling build whose expert GEMMs stamp
+every block's start and end (xshare_block_times); nothing but the profiling driver loads it.
 """
 from __future__ import annotations
 
@@ -22,6 +24,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libxshare.so")
+# the profiling build: the same sources with the GEMMs' block timeline (XS_BLOCK_TIMES=1)
+TIMELINE_LIB = os.path.join(PKG, "libxshare_timeline.so")
 ARCH = "gfx950"
 
 COMMON = [
@@ -45,21 +49,52 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found: install ROCm or put hipcc on PATH")
 
 
-def build(verbose: bool = False) -> str:
-    """Compiles every translation unit and links libxshare.so; returns its path."""
+def build(verbose: bool = False, timeline: bool = True) -> str:
+    """Compiles every translation unit and links libxshare.so (and, with `timeline`, the
+    profiling build libxshare_timeline.so); returns the product library's path.  The
+    compiles run in parallel."""
+    jobs = [(LIB, "_build", [])]
+    if timeline:
+        jobs.append((TIMELINE_LIB, "_build_timeline", ["-DXS_BLOCK_TIMES=1"]))
     cc = hipcc()
-    objdir = os.path.join(PKG, "_build")
-    os.makedirs(objdir, exist_ok=True)
-    objs = []
-    for unit, flags in UNITS.items():
-        obj = os.path.join(objdir, unit.replace(".hip", ".o"))
-        cmd = [cc, *COMMON, *flags, "-c", os.path.join(CSRC, unit), "-o", obj]
-        _run(cmd, verbose)
-        objs.append(obj)
-    tmp = LIB + ".tmp"
-    _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs], verbose)
-    os.replace(tmp, LIB)
+    compiles, links = [], []
+    for lib, objname, defines in jobs:
+        objdir = os.path.join(PKG, objname)
+        os.makedirs(objdir, exist_ok=True)
+        objs = []
+        for unit, flags in UNITS.items():
+            obj = os.path.join(objdir, unit.replace(".hip", ".o"))
+            compiles.append([cc, *COMMON, *flags, *defines, "-c", os.path.join(CSRC, unit),
+                             "-o", obj])
+            objs.append(obj)
+        links.append((lib, objs))
+    _run_all(compiles, verbose)
+    for lib, objs in links:
+        tmp = lib + ".tmp"
+        _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs], verbose)
+        os.replace(tmp, lib)
     return LIB
+
+
+def _run_all(cmds, verbose, parallel: int = min(8, os.cpu_count() or 1)):
+    """Runs the commands, `parallel` at a time; raises on the first failure."""
+    pending = list(cmds)
+    running = []
+    while pending or running:
+        while pending and len(running) < parallel:
+            cmd = pending.pop(0)
+            if verbose:
+                print(" ".join(cmd), flush=True)
+            running.append((cmd, subprocess.Popen(cmd, stdout=subprocess.PIPE,
+                                                  stderr=subprocess.STDOUT, text=True)))
+        cmd, proc = running.pop(0)
+        out, _ = proc.communicate()
+        if proc.returncode != 0:
+            for _, p in running:
+                p.wait()
+            sys.stderr.write(out)
+            raise RuntimeError(f"build step failed ({proc.returncode}): {' '.join(cmd)}")
+        _report(out, verbose)
 
 
 def _run(cmd, verbose):
@@ -69,8 +104,12 @@ def _run(cmd, verbose):
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
         raise RuntimeError(f"build step failed ({res.returncode}): {' '.join(cmd)}")
+    _report(res.stdout + res.stderr, verbose)
+
+
+def _report(out, verbose):
     # the host pass does not know the packed-fp32 target feature; that warning is expected
-    noise = [ln for ln in (res.stdout + res.stderr).splitlines()
+    noise = [ln for ln in out.splitlines()
              if ln.strip() and "packed-fp32-ops" not in ln and "not a recognized feature" not in ln]
     if verbose and noise:
         sys.stderr.write("\n".join(noise) + "\n")

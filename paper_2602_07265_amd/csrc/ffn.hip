@@ -29,6 +29,7 @@
 #include <type_traits>
 
 #include "internal.h"
+#include "xshare.h"
 
 namespace xs {
 namespace {
@@ -40,6 +41,34 @@ constexpr int kBlock = 256;       // 4 waves
 constexpr int kWaves = kBlock / 64;
 constexpr int kCols = 16;         // weight rows (output columns) per wave
 constexpr int kTiles = 2;         // 16-token tiles per pass over the weights
+
+// Block timeline of the expert GEMMs, in a profiling build only (XS_BLOCK_TIMES 1, the
+// library libxshare_timeline.so): thread 0 of every block of a gate/up and a down launch
+// stamps its start and end, and every block of a persistent down launch its start and the
+// end of each unit, from the 100 MHz global clock (s_memrealtime), by block id; each launch
+// overwrites the entries of its blocks.  xshare_block_times copies them out.
+#ifndef XS_BLOCK_TIMES
+#define XS_BLOCK_TIMES 0
+#endif
+constexpr int kTimeSeqStride = XSHARE_TIME_SEQ_STRIDE;  // a block's start, then 32 unit ends
+#if XS_BLOCK_TIMES
+constexpr int kTimeBlocks = XSHARE_TIME_BLOCKS;         // stamped blocks of a grid launch
+constexpr int kTimeSeqBlocks = XSHARE_TIME_SEQ_BLOCKS;  // stamped persistent down blocks
+__device__ unsigned long long xs_times_gu[2 * kTimeBlocks];
+__device__ unsigned long long xs_times_dn[2 * kTimeBlocks];
+__device__ unsigned long long xs_times_seq[kTimeSeqBlocks * kTimeSeqStride];
+__device__ __forceinline__ unsigned block_id3() {
+  return (blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x;
+}
+#define XS_TIME(arr, idx, lim)                                                          \
+  do {                                                                                  \
+    if (threadIdx.x == 0 && (idx) < (lim)) arr[idx] = __builtin_amdgcn_s_memrealtime(); \
+  } while (0)
+#else
+#define XS_TIME(arr, idx, lim) \
+  do {                         \
+  } while (0)
+#endif
 
 __device__ __forceinline__ bf16x8 load8(const uint16_t* p) {
   return *reinterpret_cast<const bf16x8*>(p);
@@ -784,6 +813,7 @@ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
   constexpr int NM = 2 * CT;                   // weight tiles: W1 and W3 of each column tile
   SlotWork sw;
   if (!slot_work(a, a.slot_base + blockIdx.y, sw)) return;
+  XS_TIME(xs_times_gu, 2 * block_id3(), 2u * kTimeBlocks);
   const int p0 = sw.p0, te = sw.te;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int j0 = (blockIdx.x * kWaves + wave) * kCols * CT;
@@ -908,6 +938,7 @@ __launch_bounds__(kBlock) void gate_up_kernel(FfnArgs a) {
       }
     }
   }
+  XS_TIME(xs_times_gu, 2 * block_id3() + 1, 2u * kTimeBlocks);
 }
 
 // NM: 16-row W2 tiles per wave (the launch picks it per weight format and batch shape).
@@ -936,6 +967,7 @@ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
   }
   SlotWork sw;
   if (!slot_work(a, slot, sw)) return;
+  XS_TIME(xs_times_dn, 2 * block_id3(), 2u * kTimeBlocks);
   const int p0 = sw.p0, te = sw.te;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int n0 = (bx * kWaves + wave) * kCols * NM;
@@ -1044,6 +1076,7 @@ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
       }
     }
   }
+  XS_TIME(xs_times_dn, 2 * block_id3() + 1, 2u * kTimeBlocks);
 }
 
 // ---- Persistent down GEMM, for launches of whole rounds with one block per CU (the
@@ -1060,6 +1093,7 @@ __launch_bounds__(kBlock) void down_kernel(FfnArgs a) {
 // grid, so with G a multiple of 8 every unit of a slot below 8 * (live / 8) runs on the XCD
 // of that slot.  Blocks share nothing: no counters, no flags, no block waits for another.
 constexpr int kSeqUnits = 32;     // units per block of a persistent launch, at most
+static_assert(kTimeSeqStride == 1 + kSeqUnits, "a stamp per unit of a persistent block");
 
 __device__ __forceinline__ void down_unit(int L, int CB, int live, bool xcd, int& slot, int& bx) {
   if (xcd && L < CB * (live & ~7)) {
@@ -1135,6 +1169,7 @@ __launch_bounds__(kBlock) void down_seq_kernel(FfnArgs a) {
   const int G = (int)gridDim.x;
   const int nu = (int)blockIdx.x < units ? min((units - (int)blockIdx.x + G - 1) / G, kSeqUnits) : 0;
   if (nu == 0) return;   // uniform: the whole block leaves before any barrier
+  XS_TIME(xs_times_seq, blockIdx.x * kTimeSeqStride, (unsigned)(kTimeSeqBlocks * kTimeSeqStride));
   const bool xcd = a.max_active + a.n_shared >= XS_DOWN_XCD_SLOTS;
   const int nsteps = f / KB;                    // unsplit: the launch takes one K part
   const int rot = kW == kBf16 ? XS_DOWN_ROT : XS_Q8_DOWN_ROT;
@@ -1282,6 +1317,9 @@ __launch_bounds__(kBlock) void down_seq_kernel(FfnArgs a) {
     for (int m = 0; m < NM; ++m) b[m] = nb[m];
     __syncthreads();
     buf ^= 1;
+    if (jn != j)
+      XS_TIME(xs_times_seq, blockIdx.x * kTimeSeqStride + 1 + j,
+              (unsigned)(kTimeSeqBlocks * kTimeSeqStride));
     if (!has_nxt) break;
     cur = nxt;
     j = jn;
@@ -1790,3 +1828,35 @@ hipError_t launch_combine(const FfnArgs& a, hipStream_t stream) {
 }
 
 }  // namespace xs
+
+// The block timeline of the last gate/up, down and persistent down launches (a profiling
+// build); XSHARE_EUNSUPPORTED in the product build.  With `clear` the stamps are zeroed after
+// the copy (hipMemsetAsync: a measurement call, not for graph capture).
+extern "C" xshare_status xshare_block_times(uint64_t* gate_up, uint64_t* down,
+                                            uint64_t* down_units, int32_t clear,
+                                            hipStream_t stream) {
+#if XS_BLOCK_TIMES
+  if (!gate_up || !down || !down_units) return XSHARE_EINVAL;
+  void* src[3] = {nullptr, nullptr, nullptr};
+  if (hipGetSymbolAddress(&src[0], HIP_SYMBOL(xs::xs_times_gu)) != hipSuccess ||
+      hipGetSymbolAddress(&src[1], HIP_SYMBOL(xs::xs_times_dn)) != hipSuccess ||
+      hipGetSymbolAddress(&src[2], HIP_SYMBOL(xs::xs_times_seq)) != hipSuccess)
+    return XSHARE_EHIP;
+  uint64_t* dst[3] = {gate_up, down, down_units};
+  const size_t bytes[3] = {sizeof(xs::xs_times_gu), sizeof(xs::xs_times_dn),
+                           sizeof(xs::xs_times_seq)};
+  for (int i = 0; i < 3; ++i) {
+    if (hipMemcpyAsync(dst[i], src[i], bytes[i], hipMemcpyDeviceToDevice, stream) != hipSuccess)
+      return XSHARE_EHIP;
+    if (clear && hipMemsetAsync(src[i], 0, bytes[i], stream) != hipSuccess) return XSHARE_EHIP;
+  }
+  return XSHARE_OK;
+#else
+  (void)gate_up;
+  (void)down;
+  (void)down_units;
+  (void)clear;
+  (void)stream;
+  return XSHARE_EUNSUPPORTED;
+#endif
+}

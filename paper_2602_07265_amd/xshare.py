@@ -14,6 +14,9 @@ import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libxshare.so")
+# the profiling build (block timeline of the expert GEMMs, xshare_block_times)
+TIMELINE_LIB_PATH = os.path.join(_HERE, "libxshare_timeline.so")
+TIME_BLOCKS, TIME_SEQ_BLOCKS, TIME_SEQ_STRIDE = 16384, 1024, 33   # XSHARE_TIME_*
 
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP = 0, 1, 2, 3, 4
 BUDGET = {"total": 0, "extra": 1, "per_group": 2, "threshold": 3}
@@ -162,6 +165,8 @@ def lib() -> ctypes.CDLL:
         L.xshare_moe_forward_v2_workspace_bytes.restype = _SZ
         L.xshare_probe_stream_read.argtypes = [_P, _SZ, _I32, _I32, _P, _P]
         L.xshare_probe_stream_read.restype = ctypes.c_int
+        L.xshare_block_times.argtypes = [_P, _P, _P, _I32, _P]
+        L.xshare_block_times.restype = ctypes.c_int
         L.xshare_status_string.argtypes = [_I32]
         L.xshare_status_string.restype = ctypes.c_char_p
         L.xshare_version.argtypes = []
@@ -848,3 +853,30 @@ def probe_stream_read(buf: torch.Tensor, blocks: int = 2048, mode: int = 0, sink
                                           _stream(stream)),
            "xshare_probe_stream_read")
     return sink
+
+
+def use_timeline_library() -> None:
+    """Makes this process load the profiling build (libxshare_timeline.so) instead of the
+    product library; call before the first call into the library."""
+    global LIB_PATH
+    if _lib is not None:
+        raise RuntimeError("the library is already loaded")
+    LIB_PATH = TIMELINE_LIB_PATH
+
+
+def block_times(clear: bool = True, stream=None) -> dict:
+    """The block timeline of the last expert-GEMM launches (xshare_block_times; the profiling
+    build only): uint64 arrays of 100 MHz clock stamps, "gate_up" and "down" [blocks, 2]
+    (start, end) and "down_units" [blocks, 33] (start, then unit ends); 0 = not stamped.
+    ``clear`` zeroes the stamps afterwards, so the next read holds only later launches."""
+    dev = torch.device("cuda", torch.cuda.current_device())
+    gu = torch.zeros(2 * TIME_BLOCKS, dtype=torch.int64, device=dev)
+    dn = torch.zeros(2 * TIME_BLOCKS, dtype=torch.int64, device=dev)
+    units = torch.zeros(TIME_SEQ_BLOCKS * TIME_SEQ_STRIDE, dtype=torch.int64, device=dev)
+    _check(lib().xshare_block_times(_ptr(gu), _ptr(dn), _ptr(units), int(bool(clear)),
+                                    _stream(stream)),
+           "xshare_block_times")
+    (stream or torch.cuda.current_stream()).synchronize()
+    return {"gate_up": gu.cpu().numpy().view("uint64").reshape(-1, 2),
+            "down": dn.cpu().numpy().view("uint64").reshape(-1, 2),
+            "down_units": units.cpu().numpy().view("uint64").reshape(-1, TIME_SEQ_STRIDE)}

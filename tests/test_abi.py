@@ -377,3 +377,11 @@ def test_stream_probe_validation():
     assert call(blocks=0) == X.EINVAL
     assert call(sink=None) == X.EINVAL
     assert call(mode=4) == X.EINVAL
+
+
+def test_block_times_only_in_the_profiling_build():
+    """The product library exports xshare_block_times but has no timeline: it returns
+    EUNSUPPORTED before touching anything (so it can be called here, without a GPU)."""
+    L = X.lib()
+    assert L.xshare_block_times(FAKE, FAKE, FAKE, 0, None) == X.EUNSUPPORTED
+    assert L.xshare_block_times(None, None, None, 1, None) == X.EUNSUPPORTED
