@@ -81,3 +81,48 @@ def test_moe_layer_graph_replays_match_eager():
                               logits_out=False)["y"]
             torch.cuda.synchronize()
             assert torch.equal(got, _bits(ref)), f"replay {rep}, input {s}"
+
+
+def test_concurrent_calls_on_two_streams_match_serial():
+    """Calls are stateless: two layers in flight at once, on two streams (default priority)
+    with their own workspaces, enqueued from one host thread and then from two, give the
+    same bits as the same calls one after the other."""
+    import threading
+
+    from paper_2602_07265_amd import xshare as X
+    T, N, k, d, f, M = 32, 64, 8, 256, 512, 16
+    cfg = dict(N=N, k=k, d=d, f=f, T=T, logits="domains", Q=4)
+    w1, w3, w2 = W.expert_weights(N, d, f, 2, DEV)
+    inputs = [(W.activations(T, d, s, DEV), torch.from_numpy(W.make_logits(cfg, s)[0]).to(DEV))
+              for s in range(2)]
+    p = X.params(N, k, 1, M)
+    nws = X.moe_workspace_bytes(T, d, f, p)
+    say("concurrency case: serial reference")
+    ref = [_bits(X.moe_forward(x, h, w1, w3, w2, k, 1, M, routing_out=False)["y"])
+           for x, h in inputs]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    wss = [torch.empty(nws, dtype=torch.uint8, device=DEV) for _ in range(2)]
+    ys = [torch.empty((T, d), dtype=torch.bfloat16, device=DEV) for _ in range(2)]
+
+    def run(i, reps):
+        for _ in range(reps):
+            X.moe_forward(inputs[i][0], inputs[i][1], w1, w3, w2, k, 1, M, y=ys[i],
+                          workspace=wss[i], routing_out=False, stream=streams[i])
+
+    say("concurrency case: two streams, one thread")
+    for _ in range(3):
+        run(0, 2)
+        run(1, 2)
+    torch.cuda.synchronize()
+    assert all(torch.equal(_bits(ys[i]), ref[i]) for i in range(2))
+    say("concurrency case: two streams, two threads")
+    for y in ys:
+        y.zero_()
+    threads = [threading.Thread(target=run, args=(i, 4)) for i in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    torch.cuda.synchronize()
+    assert all(torch.equal(_bits(ys[i]), ref[i]) for i in range(2))
